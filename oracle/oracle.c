@@ -1,0 +1,620 @@
+/*
+ * oracle.c -- plain, slow, CPU reference of KV-aware routing-cost evaluation,
+ * routing episodes and the PoA-hat estimator.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  The routing product
+ * never calls it, and it shares no code, header, table or constant generator
+ * with the HIP implementation.
+ *
+ * Every function follows the plain definition of what it computes:
+ *
+ *  - Block hash chain: the router identifies cached KV blocks by hashes of
+ *    token blocks (Section 2.2, "The Smart Router": a radix tree of blocks per
+ *    worker).  Block i of a prompt is tokens [16i, 16i+16); its hash is
+ *    h_i = splitmix64(h_{i-1} XOR FNV-1a64(64 little-endian bytes of the 16
+ *    int32 tokens)), with h_{-1} = 0.  A hash equal to 0 (the empty-slot
+ *    sentinel) is replaced by 0x9E3779B97F4A7C15 both as the key and as the
+ *    next chain input.
+ *  - Overlap o_ij: the number of leading chain blocks of request i that are
+ *    cached on worker j (first-miss scan; Section 2.2, Eq. router-cost, where
+ *    the prefill blocks are the blocks not covered by the cached prefix).
+ *  - Cost: Eq. router-cost (omega * prefill blocks + active blocks) with an
+ *    overload term after Eq. latency-superlinear (Section 5.1), in fp32 with a
+ *    fixed operation order and no fused multiply-add:
+ *        t1 = w_ov * (float)(P - o)
+ *        t2 = w_act * (float)A_j
+ *        r  = (float)(A_j + P) / (float)cap
+ *        x  = max(r - 1, 0)
+ *        cost = (t1 + t2) + w_sat * (x * x)
+ *  - Selection: argmin with temperature 0 (Section 2.2, Eq. router-softmax in
+ *    the tau -> 0 limit; Section 4.3), lowest worker index on ties.
+ *  - Sequential greedy routing = best-response dynamics (Section 4.3): each
+ *    request is routed given the loads and caches left by earlier ones.  The
+ *    chosen worker's LRU cache touches the prompt's blocks from last to first
+ *    (block 0 becomes most recent), inserts the missing ones and evicts least
+ *    recently used blocks until it holds at most cache_blocks.
+ *  - Steps: a step routes up to C/H requests from the ready queue; a request
+ *    stays active (its blocks count in A_j) for H steps, so C requests are in
+ *    flight once the ramp is over (the semaphore-held concurrency of
+ *    Section 7.4).  A conversation's next turn joins the queue when its
+ *    previous turn is released.
+ *  - Controller: a route uses min(w_ov, ctrl_w_ov) when the mean, over the
+ *    last ctrl_window routes, of sum_j A_j / (W * cap) exceeds num/den
+ *    (integer test), in the spirit of the regime switch of Section 6.3.
+ *  - PoA-hat (Section 6.4, Eq. poa-estimate): per window of consecutive
+ *    routes, a frozen cost matrix c_ij = a n_j + b + d / (C_j - n_j)^beta
+ *    - w_c o_ij / P_i, where n_j is the window's request count on worker j;
+ *    the selfish sum evaluates it at the greedy assignment, and OPT is the
+ *    Hungarian optimum on the matrix whose worker columns are replicated
+ *    K = ceil(m/W) times (padded to square with zero-cost dummy rows).
+ *
+ * Floating point: fp32 exactly as written above (build with
+ * -ffp-contract=off and no fast-math); sums of costs in fp64, in row order.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+#define ORC_OK 0
+#define ORC_EINVAL -1
+#define ORC_ENOMEM -2
+
+static const uint64_t ZERO_REMAP = 0x9E3779B97F4A7C15ULL;
+
+/* ------------------------------------------------------------------ hash */
+
+uint64_t orc_fnv1a64(const uint8_t* p, int64_t n)
+{
+    uint64_t h = 0xcbf29ce484222325ULL;           /* FNV-1a 64-bit offset basis */
+    for (int64_t i = 0; i < n; ++i) {
+        h ^= (uint64_t)p[i];
+        h *= 0x100000001b3ULL;                     /* FNV 64-bit prime */
+    }
+    return h;
+}
+
+uint64_t orc_splitmix64(uint64_t x)
+{
+    /* Vigna's splitmix64 generator step applied to state x. */
+    uint64_t z = x + 0x9E3779B97F4A7C15ULL;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+uint64_t orc_block_fnv(const int32_t* tok16)
+{
+    uint8_t bytes[64];
+    for (int t = 0; t < 16; ++t) {
+        uint32_t v = (uint32_t)tok16[t];
+        bytes[4 * t + 0] = (uint8_t)(v & 0xffu);
+        bytes[4 * t + 1] = (uint8_t)((v >> 8) & 0xffu);
+        bytes[4 * t + 2] = (uint8_t)((v >> 16) & 0xffu);
+        bytes[4 * t + 3] = (uint8_t)((v >> 24) & 0xffu);
+    }
+    return orc_fnv1a64(bytes, 64);
+}
+
+uint64_t orc_chain_step(uint64_t prev, uint64_t block_fnv)
+{
+    uint64_t h = orc_splitmix64(prev ^ block_fnv);
+    return h == 0 ? ZERO_REMAP : h;
+}
+
+/* Hash n_seq token sequences.  Sequence s contributes nblocks[s] blocks read
+ * from tokens[tok_off[s] ...]; its chain is written to chains[chain_off[s] ...]. */
+int orc_hash_chains(int64_t n_seq, const int32_t* tokens, const int64_t* tok_off,
+                    const int32_t* nblocks, const int64_t* chain_off, uint64_t* chains)
+{
+    for (int64_t s = 0; s < n_seq; ++s) {
+        if (nblocks[s] < 0 || (int64_t)nblocks[s] * 16 > tok_off[s + 1] - tok_off[s])
+            return ORC_EINVAL;
+        if (chain_off[s + 1] - chain_off[s] != nblocks[s])
+            return ORC_EINVAL;
+        uint64_t h = 0;
+        for (int32_t i = 0; i < nblocks[s]; ++i) {
+            uint64_t f = orc_block_fnv(tokens + tok_off[s] + 16 * (int64_t)i);
+            h = orc_chain_step(h, f);
+            chains[chain_off[s] + i] = h;
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------ cost */
+
+float orc_route_cost(float w_ov, float w_act, float w_sat, int32_t cap,
+                     int32_t P, int32_t o, int64_t A)
+{
+    float t1 = w_ov * (float)(P - o);
+    float t2 = w_act * (float)A;
+    float r = (float)(A + (int64_t)P) / (float)cap;
+    float x = fmaxf(r - 1.0f, 0.0f);
+    float t3 = w_sat * (x * x);
+    return (t1 + t2) + t3;
+}
+
+/* ------------------------------------------------- snapshot scoring (sets) */
+
+static int cmp_u64(const void* a, const void* b)
+{
+    uint64_t x = *(const uint64_t*)a, y = *(const uint64_t*)b;
+    return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+static int sorted_has(const uint64_t* s, int64_t n, uint64_t key)
+{
+    int64_t lo = 0, hi = n;            /* binary search in a sorted key array */
+    while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (s[mid] < key) lo = mid + 1; else hi = mid;
+    }
+    return lo < n && s[lo] == key;
+}
+
+/* Score B requests against W fixed key sets: overlap and cost per pair
+ * (row-major, W contiguous) and the argmin worker per request. */
+int orc_score_batch(int32_t B, int32_t W, const uint64_t* chains, const int64_t* chain_off,
+                    const uint64_t* keys, const int64_t* key_off, const int32_t* active,
+                    float w_ov, float w_act, float w_sat, int32_t cap,
+                    int32_t* overlap, float* cost, int32_t* argmin)
+{
+    if (B < 0 || W < 1 || cap < 1) return ORC_EINVAL;
+    uint64_t** sets = (uint64_t**)calloc((size_t)W, sizeof(uint64_t*));
+    if (!sets) return ORC_ENOMEM;
+    for (int32_t j = 0; j < W; ++j) {
+        int64_t n = key_off[j + 1] - key_off[j];
+        sets[j] = (uint64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(uint64_t));
+        if (!sets[j]) return ORC_ENOMEM;
+        memcpy(sets[j], keys + key_off[j], (size_t)n * sizeof(uint64_t));
+        qsort(sets[j], (size_t)n, sizeof(uint64_t), cmp_u64);
+    }
+    for (int32_t i = 0; i < B; ++i) {
+        const uint64_t* h = chains + chain_off[i];
+        int32_t P = (int32_t)(chain_off[i + 1] - chain_off[i]);
+        float best = 0.0f;
+        int32_t bj = -1;
+        for (int32_t j = 0; j < W; ++j) {
+            int64_t n = key_off[j + 1] - key_off[j];
+            int32_t o = 0;
+            while (o < P && sorted_has(sets[j], n, h[o])) ++o;
+            float c = orc_route_cost(w_ov, w_act, w_sat, cap, P, o, active[j]);
+            overlap[(int64_t)i * W + j] = o;
+            cost[(int64_t)i * W + j] = c;
+            if (bj < 0 || c < best) { best = c; bj = j; }
+        }
+        argmin[i] = bj;
+    }
+    for (int32_t j = 0; j < W; ++j) free(sets[j]);
+    free(sets);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------ LRU cache of one worker
+ * Textbook LRU: a chained hash map from key to node plus a doubly linked
+ * recency list (oldest at the head, newest at the tail). */
+
+typedef struct {
+    uint64_t key;
+    int32_t prev, next;   /* recency list */
+    int32_t hnext;        /* bucket chain */
+} lru_node;
+
+typedef struct {
+    int32_t* bucket;
+    uint64_t mask;
+    lru_node* node;
+    int32_t free_head;
+    int32_t oldest, newest;
+    int32_t size;
+} lru_t;
+
+static int lru_init(lru_t* c, int32_t max_nodes)
+{
+    uint64_t nb = 1;
+    while (nb < (uint64_t)max_nodes * 2) nb <<= 1;
+    c->bucket = (int32_t*)malloc(nb * sizeof(int32_t));
+    c->node = (lru_node*)malloc((size_t)max_nodes * sizeof(lru_node));
+    if (!c->bucket || !c->node) return ORC_ENOMEM;
+    for (uint64_t b = 0; b < nb; ++b) c->bucket[b] = -1;
+    c->mask = nb - 1;
+    for (int32_t i = 0; i < max_nodes; ++i) c->node[i].hnext = i + 1 < max_nodes ? i + 1 : -1;
+    c->free_head = max_nodes > 0 ? 0 : -1;
+    c->oldest = c->newest = -1;
+    c->size = 0;
+    return ORC_OK;
+}
+
+static void lru_free(lru_t* c)
+{
+    free(c->bucket);
+    free(c->node);
+}
+
+static int32_t lru_find(const lru_t* c, uint64_t key)
+{
+    int32_t i = c->bucket[key & c->mask];
+    while (i >= 0 && c->node[i].key != key) i = c->node[i].hnext;
+    return i;
+}
+
+static void list_unlink(lru_t* c, int32_t i)
+{
+    int32_t p = c->node[i].prev, n = c->node[i].next;
+    if (p >= 0) c->node[p].next = n; else c->oldest = n;
+    if (n >= 0) c->node[n].prev = p; else c->newest = p;
+}
+
+static void list_append(lru_t* c, int32_t i)
+{
+    c->node[i].prev = c->newest;
+    c->node[i].next = -1;
+    if (c->newest >= 0) c->node[c->newest].next = i; else c->oldest = i;
+    c->newest = i;
+}
+
+/* Make key the most recently used entry; returns 1 if it was inserted. */
+static int lru_touch(lru_t* c, uint64_t key, int* err)
+{
+    int32_t i = lru_find(c, key);
+    if (i >= 0) {
+        list_unlink(c, i);
+        list_append(c, i);
+        return 0;
+    }
+    if (c->free_head < 0) { *err = 1; return 0; }
+    i = c->free_head;
+    c->free_head = c->node[i].hnext;
+    c->node[i].key = key;
+    c->node[i].hnext = c->bucket[key & c->mask];
+    c->bucket[key & c->mask] = i;
+    list_append(c, i);
+    c->size += 1;
+    return 1;
+}
+
+/* Remove the least recently used entry and return its key. */
+static uint64_t lru_evict_oldest(lru_t* c)
+{
+    int32_t i = c->oldest;
+    uint64_t key = c->node[i].key;
+    list_unlink(c, i);
+    int32_t* pp = &c->bucket[key & c->mask];
+    while (*pp != i) pp = &c->node[*pp].hnext;
+    *pp = c->node[i].hnext;
+    c->node[i].hnext = c->free_head;
+    c->free_head = i;
+    c->size -= 1;
+    return key;
+}
+
+static int32_t lru_overlap(const lru_t* c, const uint64_t* h, int32_t P)
+{
+    int32_t o = 0;
+    while (o < P && lru_find(c, h[o]) >= 0) ++o;
+    return o;
+}
+
+/* ------------------------------------------------------ routing episode
+ * Turn indices and chain offsets are relative to this episode's arrays:
+ * turn_off[0] == 0 and chain_off[0] == 0.  n_routes = turn_off[n_conv].
+ *
+ * totals[0] sum over routes of (P - o) on the chosen worker (recomputed blocks)
+ * totals[1] evicted blocks
+ * totals[2] sum of P
+ * totals[3] routes that used the controller's overlap weight
+ * totals[4] controller activations (inactive -> active transitions)
+ * totals[5] routing steps (index of the last step that routed, plus one)
+ * totals[6] sum over routes of o on the chosen worker
+ * totals[7] final sum of cached blocks over workers
+ *
+ * Optional outputs (NULL to skip): final_keys [W * cache_blocks] holds each
+ * worker's cached keys from least to most recently used, final_count [W] their
+ * number; evicted_keys [evicted_cap] lists evicted keys in eviction order and
+ * *n_evicted counts all evictions.
+ */
+int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t routes_per_step,
+                         float w_ov, float w_act, float w_sat, int32_t cap,
+                         int32_t controller, float ctrl_w_ov, int32_t ctrl_window,
+                         int32_t ctrl_num, int32_t ctrl_den,
+                         int32_t n_conv, const int64_t* turn_off, const int32_t* turn_blocks,
+                         const int64_t* chain_off, const uint64_t* chains,
+                         int32_t* route_turn, int32_t* route_worker, int32_t* route_step,
+                         int32_t* route_blocks, int32_t* overlap, float* cost,
+                         int32_t* evict_count, uint64_t* evict_digest, uint64_t* last_hash,
+                         int64_t* totals,
+                         uint64_t* final_keys, int32_t* final_count,
+                         uint64_t* evicted_keys, int64_t evicted_cap, int64_t* n_evicted)
+{
+    if (W < 1 || cache_blocks < 1 || H < 1 || routes_per_step < 1 || cap < 1 || n_conv < 0)
+        return ORC_EINVAL;
+    if (controller && (ctrl_window < 1 || ctrl_den < 1 || ctrl_num < 0)) return ORC_EINVAL;
+    const int64_t n_routes = turn_off[n_conv];
+    int32_t max_P = 0;
+    for (int32_t c = 0; c < n_conv; ++c) {
+        int64_t len = chain_off[c + 1] - chain_off[c];
+        for (int64_t t = turn_off[c]; t < turn_off[c + 1]; ++t) {
+            if (turn_blocks[t] < 0 || turn_blocks[t] > len) return ORC_EINVAL;
+            if (turn_blocks[t] > max_P) max_P = turn_blocks[t];
+        }
+    }
+
+    int rc = ORC_OK;
+    lru_t* lru = (lru_t*)calloc((size_t)W, sizeof(lru_t));
+    int64_t* A = (int64_t*)calloc((size_t)W, sizeof(int64_t));
+    int32_t* o_row = (int32_t*)malloc((size_t)W * sizeof(int32_t));
+    int32_t* queue = (int32_t*)malloc((size_t)(n_conv + 1) * sizeof(int32_t));
+    int64_t* next_turn = (int64_t*)malloc((size_t)(n_conv + 1) * sizeof(int64_t));
+    int32_t* route_conv = (int32_t*)malloc((size_t)(n_routes + 1) * sizeof(int32_t));
+    int64_t* step_first = (int64_t*)calloc((size_t)H, sizeof(int64_t));
+    int64_t* step_count = (int64_t*)calloc((size_t)H, sizeof(int64_t));
+    int64_t* u_ring = (int64_t*)calloc((size_t)(ctrl_window > 0 ? ctrl_window : 1), sizeof(int64_t));
+    if (!lru || !A || !o_row || !queue || !next_turn || !route_conv || !step_first ||
+        !step_count || !u_ring) { rc = ORC_ENOMEM; goto done; }
+    for (int32_t j = 0; j < W; ++j)
+        if (lru_init(&lru[j], cache_blocks + max_P + 1) != ORC_OK) { rc = ORC_ENOMEM; goto done; }
+
+    for (int k = 0; k < 8; ++k) totals[k] = 0;
+    int64_t q_head = 0, q_size = 0;
+    const int64_t q_cap = n_conv + 1;
+    for (int32_t c = 0; c < n_conv; ++c) {
+        next_turn[c] = turn_off[c];
+        if (turn_off[c + 1] > turn_off[c]) { queue[(q_head + q_size) % q_cap] = c; ++q_size; }
+    }
+    int64_t t = 0;            /* routes done */
+    int64_t u_sum = 0;        /* sum of the last ctrl_window load samples */
+    int prev_active = 0;
+
+    for (int64_t s = 0;; ++s) {
+        const int64_t slot = s % H;
+        if (s >= H) {                               /* release the routes of step s-H */
+            for (int64_t r = step_first[slot]; r < step_first[slot] + step_count[slot]; ++r) {
+                A[route_worker[r]] -= route_blocks[r];
+                int32_t c = route_conv[r];
+                if (next_turn[c] < turn_off[c + 1]) { queue[(q_head + q_size) % q_cap] = c; ++q_size; }
+            }
+        }
+        step_count[slot] = 0;
+        int64_t inflight = 0;
+        for (int64_t k = 1; k < H && k <= s; ++k) inflight += step_count[(s - k) % H];
+        if (q_size == 0 && inflight == 0) break;
+        int64_t n = q_size < routes_per_step ? q_size : routes_per_step;
+        step_first[slot] = t;
+        step_count[slot] = n;
+        if (n > 0) totals[5] = s + 1;
+
+        for (int64_t k = 0; k < n; ++k, ++t) {
+            int32_t c = queue[q_head];
+            q_head = (q_head + 1) % q_cap;
+            --q_size;
+            int64_t turn = next_turn[c]++;
+            int32_t P = turn_blocks[turn];
+            const uint64_t* h = chains + chain_off[c];
+
+            float w_eff = w_ov;
+            int active = 0;
+            if (controller && t >= ctrl_window &&
+                (int64_t)ctrl_den * u_sum > (int64_t)ctrl_num * ctrl_window * W * (int64_t)cap)
+                active = 1;
+            if (active) {
+                w_eff = fminf(w_ov, ctrl_w_ov);
+                totals[3] += 1;
+                if (!prev_active) totals[4] += 1;
+            }
+            prev_active = active;
+
+            float best = 0.0f;
+            int32_t sigma = -1;
+            for (int32_t j = 0; j < W; ++j) {
+                int32_t o = lru_overlap(&lru[j], h, P);
+                float cj = orc_route_cost(w_eff, w_act, w_sat, cap, P, o, A[j]);
+                o_row[j] = o;
+                overlap[t * W + j] = o;
+                cost[t * W + j] = cj;
+                if (sigma < 0 || cj < best) { best = cj; sigma = j; }
+            }
+
+            int err = 0;
+            for (int32_t k2 = P - 1; k2 >= 0; --k2) lru_touch(&lru[sigma], h[k2], &err);
+            if (err) { rc = ORC_ENOMEM; goto done; }
+            int32_t ev = 0;
+            uint64_t dig = 0;
+            while (lru[sigma].size > cache_blocks) {
+                uint64_t key = lru_evict_oldest(&lru[sigma]);
+                ev += 1;
+                dig += orc_splitmix64(key);
+                if (evicted_keys && totals[1] + ev - 1 < evicted_cap)
+                    evicted_keys[totals[1] + ev - 1] = key;
+            }
+            A[sigma] += P;
+
+            int64_t u = 0;
+            for (int32_t j = 0; j < W; ++j) u += A[j];
+            if (controller) {
+                int64_t pos = t % ctrl_window;
+                if (t >= ctrl_window) u_sum -= u_ring[pos];
+                u_ring[pos] = u;
+                u_sum += u;
+            }
+
+            route_turn[t] = (int32_t)turn;
+            route_worker[t] = sigma;
+            route_step[t] = (int32_t)s;
+            route_blocks[t] = P;
+            route_conv[t] = c;
+            evict_count[t] = ev;
+            evict_digest[t] = dig;
+            last_hash[t] = P > 0 ? h[P - 1] : 0;
+            totals[0] += P - o_row[sigma];
+            totals[1] += ev;
+            totals[2] += P;
+            totals[6] += o_row[sigma];
+        }
+    }
+    for (int32_t j = 0; j < W; ++j) {
+        totals[7] += lru[j].size;
+        if (final_keys && final_count) {
+            int32_t n = 0;
+            for (int32_t i = lru[j].oldest; i >= 0; i = lru[j].node[i].next)
+                final_keys[(int64_t)j * cache_blocks + n++] = lru[j].node[i].key;
+            final_count[j] = n;
+        }
+    }
+    if (n_evicted) *n_evicted = totals[1];
+
+done:
+    if (lru)
+        for (int32_t j = 0; j < W; ++j) lru_free(&lru[j]);
+    free(lru); free(A); free(o_row); free(queue); free(next_turn); free(route_conv);
+    free(step_first); free(step_count); free(u_ring);
+    return rc;
+}
+
+/* ----------------------------------------------------------------- PoA-hat */
+
+/* Hungarian algorithm (Kuhn-Munkres with row/column potentials), minimising
+ * the total cost of a one-to-one assignment of n rows to n columns.
+ * cost(i, j) is supplied by the callback; rows and columns are 0-based.
+ * On return col_of_row[i] is the column assigned to row i. */
+typedef double (*cost_fn)(const void* ctx, int32_t i, int32_t j);
+
+static int hungarian(int32_t n, cost_fn f, const void* ctx, int32_t* col_of_row)
+{
+    const double INF = 1e300;
+    double* u = (double*)calloc((size_t)n + 1, sizeof(double));
+    double* v = (double*)calloc((size_t)n + 1, sizeof(double));
+    double* minv = (double*)malloc(((size_t)n + 1) * sizeof(double));
+    int32_t* p = (int32_t*)calloc((size_t)n + 1, sizeof(int32_t));     /* p[col] = row (1-based) */
+    int32_t* way = (int32_t*)calloc((size_t)n + 1, sizeof(int32_t));
+    char* used = (char*)malloc((size_t)n + 1);
+    if (!u || !v || !minv || !p || !way || !used) {
+        free(u); free(v); free(minv); free(p); free(way); free(used);
+        return ORC_ENOMEM;
+    }
+    for (int32_t i = 1; i <= n; ++i) {
+        p[0] = i;
+        int32_t j0 = 0;
+        for (int32_t j = 0; j <= n; ++j) { minv[j] = INF; used[j] = 0; }
+        do {
+            used[j0] = 1;
+            int32_t i0 = p[j0], j1 = 0;
+            double delta = INF;
+            for (int32_t j = 1; j <= n; ++j) {
+                if (used[j]) continue;
+                double cur = f(ctx, i0 - 1, j - 1) - u[i0] - v[j];
+                if (cur < minv[j]) { minv[j] = cur; way[j] = j0; }
+                if (minv[j] < delta) { delta = minv[j]; j1 = j; }
+            }
+            for (int32_t j = 0; j <= n; ++j) {
+                if (used[j]) { u[p[j]] += delta; v[j] -= delta; }
+                else minv[j] -= delta;
+            }
+            j0 = j1;
+        } while (p[j0] != 0);
+        do {
+            int32_t j1 = way[j0];
+            p[j0] = p[j1];
+            j0 = j1;
+        } while (j0 != 0);
+    }
+    for (int32_t j = 1; j <= n; ++j)
+        if (p[j] > 0) col_of_row[p[j] - 1] = j - 1;
+    free(u); free(v); free(minv); free(p); free(way); free(used);
+    return ORC_OK;
+}
+
+typedef struct {
+    const float* c;      /* m x W */
+    int32_t m, W, K;
+} rep_ctx;
+
+static double rep_cost(const void* vctx, int32_t i, int32_t j)
+{
+    const rep_ctx* x = (const rep_ctx*)vctx;
+    if (i >= x->m) return 0.0;                       /* dummy row */
+    return (double)x->c[(int64_t)i * x->W + j / x->K];  /* column j is a replica of worker j/K */
+}
+
+/* Frozen cost matrix of one window (fp32, fixed op order). */
+int orc_poa_matrix(int32_t m, int32_t W, const int32_t* worker, const int32_t* overlap,
+                   const int32_t* blocks, float a, float b, float d, int32_t beta,
+                   int32_t C_cap, float w_c, float* c_out, int32_t* n_out)
+{
+    if (m < 0 || W < 1 || beta < 1) return ORC_EINVAL;
+    for (int32_t j = 0; j < W; ++j) n_out[j] = 0;
+    for (int32_t i = 0; i < m; ++i) {
+        if (worker[i] < 0 || worker[i] >= W) return ORC_EINVAL;
+        n_out[worker[i]] += 1;
+    }
+    for (int32_t j = 0; j < W; ++j) {
+        int32_t gap = C_cap - n_out[j];
+        float g = (float)(gap > 1 ? gap : 1);
+        float gb = g;
+        for (int32_t k = 1; k < beta; ++k) gb = gb * g;
+        float base = (a * (float)n_out[j] + b) + d / gb;
+        for (int32_t i = 0; i < m; ++i) {
+            float oh = blocks[i] > 0 ? (float)overlap[(int64_t)i * W + j] / (float)blocks[i] : 0.0f;
+            c_out[(int64_t)i * W + j] = base - w_c * oh;
+        }
+    }
+    return ORC_OK;
+}
+
+/* One window: selfish sum at the greedy assignment and the Hungarian OPT with
+ * every worker column replicated K times (K <= 0 means ceil(m/W)). */
+int orc_poa_window(int32_t m, int32_t W, const int32_t* worker, const int32_t* overlap,
+                   const int32_t* blocks, float a, float b, float d, int32_t beta,
+                   int32_t C_cap, float w_c, int32_t K, double* selfish, double* coordinated,
+                   int32_t* opt_worker)
+{
+    if (m < 0 || W < 1) return ORC_EINVAL;
+    if (K <= 0) K = (m + W - 1) / W;
+    if ((int64_t)K * W < m) return ORC_EINVAL;
+    *selfish = 0.0;
+    *coordinated = 0.0;
+    if (m == 0) return ORC_OK;
+    float* c = (float*)malloc((size_t)m * (size_t)W * sizeof(float));
+    int32_t* n = (int32_t*)malloc((size_t)W * sizeof(int32_t));
+    int32_t N = K * W;
+    int32_t* col = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+    if (!c || !n || !col) { free(c); free(n); free(col); return ORC_ENOMEM; }
+    int rc = orc_poa_matrix(m, W, worker, overlap, blocks, a, b, d, beta, C_cap, w_c, c, n);
+    if (rc == ORC_OK) {
+        double s = 0.0;
+        for (int32_t i = 0; i < m; ++i) s += (double)c[(int64_t)i * W + worker[i]];
+        *selfish = s;
+        rep_ctx ctx = { c, m, W, K };
+        rc = hungarian(N, rep_cost, &ctx, col);
+        if (rc == ORC_OK) {
+            double o = 0.0;
+            for (int32_t i = 0; i < m; ++i) {
+                int32_t j = col[i] / K;
+                if (opt_worker) opt_worker[i] = j;
+                o += (double)c[(int64_t)i * W + j];
+            }
+            *coordinated = o;
+        }
+    }
+    free(c); free(n); free(col);
+    return rc;
+}
+
+/* Windows of `window` consecutive routes (the last one may be shorter). */
+int orc_poa_windows(int64_t n_routes, int32_t W, int32_t window, const int32_t* worker,
+                    const int32_t* overlap, const int32_t* blocks, float a, float b, float d,
+                    int32_t beta, int32_t C_cap, float w_c, int32_t K,
+                    double* selfish_out, double* coord_out)
+{
+    if (window < 1) return ORC_EINVAL;
+    int64_t nw = (n_routes + window - 1) / window;
+    for (int64_t w = 0; w < nw; ++w) {
+        int64_t r0 = w * window;
+        int32_t m = (int32_t)(n_routes - r0 < window ? n_routes - r0 : window);
+        int rc = orc_poa_window(m, W, worker + r0, overlap + r0 * W, blocks + r0, a, b, d, beta,
+                                C_cap, w_c, K, &selfish_out[w], &coord_out[w], NULL);
+        if (rc != ORC_OK) return rc;
+    }
+    return ORC_OK;
+}

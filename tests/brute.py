@@ -1,0 +1,108 @@
+"""Pure-Python brute-force twins used to pin the C oracle on tiny inputs.
+
+These use different data structures from the oracle (Python sets and an
+OrderedDict LRU instead of a chained hash map with a linked recency list;
+exhaustive enumeration instead of the Hungarian method) so that a mistake in
+either implementation shows up as a disagreement.
+"""
+from __future__ import annotations
+
+import itertools
+from collections import OrderedDict
+
+import numpy as np
+
+f32 = np.float32
+
+
+def cost_f32(w_ov, w_act, w_sat, cap, P, o, A):
+    """Router cost in fp32, one IEEE operation at a time (numpy scalars do not fuse)."""
+    t1 = f32(w_ov) * f32(P - o)
+    t2 = f32(w_act) * f32(A)
+    r = f32(A + P) / f32(cap)
+    x = max(r - f32(1.0), f32(0.0))
+    t3 = f32(w_sat) * (x * x)
+    return f32(f32(t1 + t2) + t3)
+
+
+def overlap_set(chain, cached: set) -> int:
+    o = 0
+    while o < len(chain) and int(chain[o]) in cached:
+        o += 1
+    return o
+
+
+def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blocks, chains_per_conv,
+            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10):
+    """Sequential greedy routing episode with OrderedDict LRU caches."""
+    n_conv = len(turn_off) - 1
+    caches = [OrderedDict() for _ in range(W)]   # key -> None, oldest first
+    A = [0] * W
+    queue = [c for c in range(n_conv) if turn_off[c + 1] > turn_off[c]]
+    next_turn = [turn_off[c] for c in range(n_conv)]
+    steps = {}                                    # step -> list of (worker, P, conv)
+    routes = []
+    us = []
+    prev_active = False
+    s = 0
+    while True:
+        if s - H in steps:
+            for (j, P, c) in steps.pop(s - H):
+                A[j] -= P
+                if next_turn[c] < turn_off[c + 1]:
+                    queue.append(c)
+        inflight = sum(len(v) for k, v in steps.items() if s - H < k < s)
+        if not queue and inflight == 0:
+            break
+        take, queue = queue[:rps], queue[rps:]
+        steps[s] = []
+        for c in take:
+            turn = next_turn[c]
+            next_turn[c] += 1
+            P = int(turn_blocks[turn])
+            h = [int(x) for x in chains_per_conv[c][:P]]
+            w_eff = f32(w_ov)
+            active = (controller and len(us) >= ctrl_window and
+                      ctrl_den * sum(us[-ctrl_window:]) > ctrl_num * ctrl_window * W * cap)
+            if active:
+                w_eff = min(f32(w_ov), f32(ctrl_w_ov))
+            ovl = [overlap_set(h, caches[j].keys()) for j in range(W)]
+            costs = [cost_f32(w_eff, w_act, w_sat, cap, P, ovl[j], A[j]) for j in range(W)]
+            sigma = 0
+            for j in range(1, W):
+                if costs[j] < costs[sigma]:
+                    sigma = j
+            cache = caches[sigma]
+            for k in range(P - 1, -1, -1):
+                if h[k] in cache:
+                    cache.move_to_end(h[k])
+                else:
+                    cache[h[k]] = None
+            evicted = []
+            while len(cache) > cache_blocks:
+                key, _ = cache.popitem(last=False)
+                evicted.append(key)
+            A[sigma] += P
+            us.append(sum(A))
+            routes.append(dict(turn=turn, worker=sigma, step=s, P=P, overlap=ovl, cost=costs,
+                               evicted=evicted, active=bool(active),
+                               first_active=bool(active and not prev_active)))
+            prev_active = bool(active)
+            steps[s].append((sigma, P, c))
+        s += 1
+    final = [list(c.keys()) for c in caches]
+    return routes, final
+
+
+def opt_bruteforce(c: np.ndarray, K: int) -> float:
+    """Min over assignments of m rows to W columns with at most K rows per column."""
+    m, W = c.shape
+    best = None
+    for assign in itertools.product(range(W), repeat=m):
+        counts = np.bincount(np.asarray(assign, dtype=np.int64), minlength=W)
+        if counts.max(initial=0) > K:
+            continue
+        v = sum(float(c[i, assign[i]]) for i in range(m))
+        if best is None or v < best:
+            best = v
+    return best
