@@ -1,0 +1,311 @@
+"""Benchmark of the KV-aware routing hot path on one MI355X.
+
+One step = one pass of the whole path over the 1P/5D-shaped sweep: block-hash
+chains of 64 traces of 4,096 requests, 320 routing episodes (W = 6 workers,
+C in {32, 64, 128, 256, 512} x 64 seeds), and the PoA-hat windows and ratios.
+Inputs (tokens, offsets, parameters) are resident in HBM before timing.
+
+Also measured in the same run: the batched scoring kernel on 65,536 requests x
+64 workers with 2^20-slot tables, and the CPU oracle on a bounded sample of
+the sweep (reported as cpu_baseline).
+
+Prints one JSON line.  Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "request×worker route scorings/sec + routing episodes/sec; % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = {
+    "episode_kernel": ["paper_2606_17081_amd/csrc/episode.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
+    "score_kernel": ["paper_2606_17081_amd/csrc/score.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
+    "poa_window_kernel": ["paper_2606_17081_amd/csrc/poa.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
+    "block_fnv_kernel": ["paper_2606_17081_amd/csrc/abi.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_digest(kernel: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(PROFILE_DIR, f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha256_16") != source_digest(kernel):
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+# ---------------------------------------------------------------- algorithmic bytes
+
+def episode_algorithmic_bytes(runner) -> float:
+    """Bytes the episode kernel must move per launch, each access counted once
+    at its natural width (no cache-line rounding):
+      per episode: clearing W tables of S slots (8 B each);
+      per route:   chain 8P; per worker the probed keys, 8 B each, where the
+                   64-way search probes min(P, 64) positions when P <= 64 and
+                   64 + ceil(P/64) otherwise; the chosen worker's touch of P
+                   blocks (key read 8, stamp write 4, log write 4) and insert of
+                   P - o keys (8 each); 12 B of outputs per worker, 28 B per route;
+      per eviction: log read 4, stamp read 4 and write 4, key read 8."""
+    W = runner.W
+    n = runner.n_rows
+    P = runner.route_blocks[:n].cpu().numpy().astype(np.float64)
+    sig = runner.route_worker[:n].cpu().numpy()
+    ov = runner.overlap[:n].cpu().numpy()
+    o_sig = ov[np.arange(n), sig].astype(np.float64)
+    ev = runner.evict_count[:n].cpu().numpy().astype(np.float64)
+    probes = np.where(P <= 64, P, 64 + np.ceil(P / 64.0))
+    live_max = runner.cache_blocks + runner.max_blocks      # table slots: next power of two >= 2 * live_max
+    S = 1 << int(np.ceil(np.log2(2 * live_max)))
+    b = len(runner.episodes) * W * S * 8.0
+    b += np.sum(8 * P + 8 * W * probes + 16 * P + 8 * (P - o_sig) + 12 * W + 28)
+    b += np.sum(20 * ev)
+    return float(b)
+
+
+def score_algorithmic_bytes(inst) -> float:
+    """Compulsory bytes of one batched-scoring launch: every table slot once,
+    every chain hash once, the offsets, and the outputs (overlap and cost per
+    pair, argmin per request)."""
+    B, W = inst.B, inst.W
+    tables = W * (1 << inst.log2_slots) * 8
+    chains = inst.chains.size * 8
+    offs = (B + 1) * 8 + W * 4
+    outs = B * W * (4 + 4) + B * 4
+    return float(tables + chains + offs + outs)
+
+
+# ---------------------------------------------------------------- timing helpers
+
+class KernelTimer:
+    """HIP events around one stage, recorded on the stream the stage runs on."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream, self.pairs = torch, stream, []
+
+    def __enter__(self):
+        self.a = self.torch.cuda.Event(enable_timing=True)
+        self.b = self.torch.cuda.Event(enable_timing=True)
+        self.a.record(self.stream)
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record(self.stream)
+        self.pairs.append((self.a, self.b))
+
+    def mean_ms(self):
+        self.torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
+
+
+def cpu_baseline(workload, seeds, threads):
+    """The CPU oracle on a bounded sample: hash the sampled traces, run every
+    episode of those seeds (all five concurrency levels) and its PoA-hat."""
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import oracle as O
+    from paper_2606_17081_amd.workload import POA_PARAMS
+    specs = [e for e in workload.episodes if e.seed in seeds]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        chains = dict(zip(seeds, ex.map(lambda s: O.trace_chains(workload.traces[s]), seeds)))
+
+        def one(sp):
+            out = O.simulate_trace(workload.W, workload.cache_blocks, sp, workload.traces[sp.seed], chains[sp.seed])
+            O.episode_poa(out, workload.W, sp.concurrency, POA_PARAMS)
+            return len(out["route_worker"])
+        routes = sum(ex.map(one, specs))
+    dt = time.perf_counter() - t0
+    return dict(value=routes * workload.W / dt, unit="scorings/s", cores=threads, kind="oracle",
+                sample=f"{len(specs)} episodes (seeds {min(seeds)}..{max(seeds)} x C in 32..512) of the "
+                       f"1P/5D-shaped sweep incl. hashing and PoA-hat; {routes} routes in {dt:.2f} s",
+                episodes_per_s=len(specs) / dt, seconds=dt)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-scoring", action="store_true")
+    ap.add_argument("--cpu-seeds", type=int, default=8)
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device copy of this size (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the episode batch shards by episode with no exchange; "
+              "multi-GPU runs are not part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_17081_amd import rkroute as rk
+    from paper_2606_17081_amd import workload as wl
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {n} bytes 5 times")
+        return
+
+    log("generating the sweep (64 traces of 4,096 requests)")
+    w = wl.sweep70b_workload()
+    runner = EpisodeRunner(w, keep_cost=True)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    log(f"{len(runner.episodes)} episodes, {runner.n_rows} routes, {runner.n_windows} PoA windows; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        runner.step()
+    torch.cuda.synchronize()
+    assert rk.device_status(reset=True) == 0
+
+    t_hash, t_sim, t_poa = KernelTimer(torch, stream), KernelTimer(torch, stream), KernelTimer(torch, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        with t_hash:
+            runner.hash()
+        with t_sim:
+            runner.simulate()
+        with t_poa:
+            runner.poa()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert rk.device_status(reset=True) == 0
+    ms_step = wall * 1e3 / args.steps
+    E = len(runner.episodes)
+    scorings = runner.n_rows * runner.W
+    stage_ms = dict(hash=t_hash.mean_ms(), simulate=t_sim.mean_ms(), poa=t_poa.mean_ms())
+    log(f"step {ms_step:.3f} ms; stages {stage_ms}")
+    poa_hat = runner.poa_hat[:E].cpu().numpy()
+    per_C = {}
+    for C in wl.SWEEP70B_C:
+        v = np.array([poa_hat[e] for e, sp in enumerate(runner.episodes) if sp.concurrency == C])
+        per_C[str(C)] = [round(float(v.mean()), 6), round(float(v.std()), 6)]
+
+    dom = max(stage_ms, key=stage_ms.get)
+    dom_kernel = {"hash": "block_fnv_kernel", "simulate": "episode_kernel", "poa": "poa_window_kernel"}[dom]
+    if dom_kernel == "episode_kernel":
+        alg = episode_algorithmic_bytes(runner)
+    else:
+        alg = None
+    roofline = None
+    if alg is not None:
+        achieved = alg / (stage_ms[dom] * 1e-3) / 1e9
+        traffic = measured_traffic(dom_kernel, "sweep70b")
+        roofline = {"kernel": dom_kernel, "bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
+                    "traffic": traffic, "algorithmic_bytes": alg, "avg_ms": round(stage_ms[dom], 4)}
+    else:
+        roofline = {"kernel": dom_kernel, "bound": "alu", "achieved": None, "peak": None, "unit": None,
+                    "frac": None, "traffic": None, "avg_ms": round(stage_ms[dom], 4)}
+
+    score = None
+    if not args.no_scoring:
+        del runner
+        torch.cuda.empty_cache()
+        log("generating the 65,536 x 64 scoring instance")
+        inst = wl.scoring_instance(seed=0)
+        up = rk.to_device
+        tables = rk.table_build(up(inst.keys), inst.key_off, inst.log2_slots)
+        chains, chain_off, active = up(inst.chains), up(inst.chain_off), up(inst.active)
+        ov = torch.empty((inst.B, inst.W), dtype=torch.int32, device="cuda")
+        co = torch.empty((inst.B, inst.W), dtype=torch.float32, device="cuda")
+        am = torch.empty(inst.B, dtype=torch.int32, device="cuda")
+        for _ in range(3):
+            rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co, argmin=am)
+        ts = KernelTimer(torch, stream)
+        for _ in range(max(args.steps, 10)):
+            with ts:
+                rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co,
+                                     argmin=am)
+        ms = ts.mean_ms()
+        assert rk.device_status(reset=True) == 0
+        salg = score_algorithmic_bytes(inst)
+        ach = salg / (ms * 1e-3) / 1e9
+        score = {"workload": "scoring 65536 requests x 64 workers, 2^20-slot tables at load 0.5, chains of 16..512",
+                 "scorings_per_s": inst.B * inst.W / (ms * 1e-3), "avg_ms": round(ms, 4),
+                 "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": round(ach, 3),
+                              "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 6),
+                              "traffic": measured_traffic("score_kernel", "scoring"),
+                              "algorithmic_bytes": salg}}
+        log(f"scoring: {ms:.4f} ms, {score['scorings_per_s']:.4g} scorings/s, {ach:.1f} GB/s algorithmic")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        threads = max(1, min(16, os.cpu_count() or 1))
+        log(f"oracle on {args.cpu_seeds} seeds x 5 concurrency levels with {threads} threads")
+        cpu = cpu_baseline(w, list(range(args.cpu_seeds)), threads)
+        log(f"oracle: {cpu['value']:.4g} scorings/s in {cpu['seconds']:.2f} s")
+
+    line = {
+        "metric": METRIC,
+        "value": scorings / (ms_step * 1e-3),
+        "unit": "scorings/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64/i32 hashing and probes, f32 cost, f64 PoA sums",
+        "data": "synthetic",
+        "config": {"workload": "sweep70b: 70B-1P/5D-shaped sweep, W=6 workers, 4096 requests per episode, "
+                               "C in {32,64,128,256,512} x 64 seeds = 320 episodes; hash + episodes + PoA-hat",
+                   "episodes": E, "routes": runner_rows(scorings, w.W), "scorings_per_step": scorings},
+        "episodes_per_s": E / (ms_step * 1e-3),
+        "routes_per_s": scorings / w.W / (ms_step * 1e-3),
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "poa_hat_by_C": per_C,
+        "roofline": roofline,
+        "score_batch": score,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def runner_rows(scorings, W):
+    return scorings // W
+
+
+if __name__ == "__main__":
+    main()

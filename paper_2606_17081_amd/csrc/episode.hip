@@ -1,0 +1,583 @@
+// episode.hip -- independent sequential routing episodes, one workgroup each.
+//
+// Per episode the workgroup (256 threads, 4 wavefronts) keeps in LDS the
+// worker loads A_j, the LRU bookkeeping of every worker, the in-flight routes
+// of the last H steps, the controller's load window and the current prompt's
+// chain.  Each worker's cached blocks live in HBM as an open-addressing table
+// (key, stamp) plus a ring log of touches:
+//   - a touch of a block at stamp p writes stamps[slot] = p and log[p] = slot,
+//     so stamps are log positions and recency order is log order;
+//   - a log record p is live iff stamps[log[p]] == p; eviction pops the log
+//     head, skipping stale records, and tombstones the slot (stamp kTomb);
+//   - when tombstones or the log fill up, the live records are compacted,
+//     re-stamped in order and re-inserted into a cleared table.
+// A route: stage the chain in LDS; every worker's longest cached prefix by a
+// wavefront-wide search (lanes probe 64 positions per round); fp32 cost per
+// worker; argmin by a wavefront min over packed (cost, worker) keys; then the
+// chosen worker inserts/touches all P blocks in parallel (stamps assigned in
+// reverse block order) and evicts the oldest live records.
+#include <hip/hip_runtime.h>
+
+#include "rk_internal.h"
+
+namespace rk {
+
+constexpr int NT = 256;
+constexpr int NW = NT / 64;
+
+struct EpArgs {
+    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode;
+    const rk_episode_params* params;
+    const int64_t* turn_off;
+    const int32_t* turn_blocks;
+    const int64_t* chain_off;
+    const uint64_t* chains;
+    rk_episode_outputs out;
+    unsigned char* ws;
+    EpisodeLayout L;
+    int32_t* status;
+    uint32_t lds_chain, lds_w, lds_inflight, lds_step, lds_u;
+};
+
+struct EpShared {
+    int32_t n_route, done, sigma, P, rebuild, ins, remaining, ev, qhead, qsize, pop_base;
+    uint32_t new_head;
+    float w_eff;
+    int64_t cbase;
+    unsigned long long digest;
+    int32_t wtot[NW];
+};
+
+// Exclusive rank of `flag` among the workgroup's threads (thread order) and the
+// total count.  Every thread of the workgroup must call it.
+__device__ __forceinline__ int32_t block_scan(bool flag, int32_t* wtot, int32_t& total)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const unsigned long long b = __ballot(flag);
+    const int32_t rank = __popcll(b & ((1ull << lane) - 1ull));
+    if (lane == 0) wtot[w] = __popcll(b);
+    __syncthreads();
+    int32_t off = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+        const int32_t v = wtot[k];
+        off += k < w ? v : 0;
+        tot += v;
+    }
+    __syncthreads();
+    total = tot;
+    return off + rank;
+}
+
+// Barrier after global-memory writes of the workgroup.  All waves of a
+// workgroup share one CU, so the workgroup-scope release/acquire of the
+// barrier is enough for them to see each other's stores and atomics.
+__device__ __forceinline__ void block_sync_global()
+{
+    __syncthreads();
+}
+
+__device__ __forceinline__ bool cached(const uint64_t* __restrict__ tk, const uint32_t* __restrict__ ts,
+                                       uint64_t smask, uint64_t h)
+{
+    uint64_t s = h & smask;
+    for (uint64_t n = 0; n <= smask; ++n) {
+        const uint64_t k = tk[s];
+        if (k == kEmpty) return false;
+        if (k == h && ts[s] != kTomb) return true;
+        s = (s + 1) & smask;
+    }
+    return false;
+}
+
+// Longest cached prefix with every worker's cache prefix-closed along the
+// chain: a round probes 64 evenly spread positions of the open interval
+// (lo, hi) and keeps the sub-interval where the first miss lies; the last
+// round probes every remaining position.  Wavefront-uniform result.
+__device__ int32_t wave_prefix_search(const uint64_t* s_chain, int32_t P, const uint64_t* tk,
+                                      const uint32_t* ts, uint64_t smask)
+{
+    const int lane = threadIdx.x & 63;
+    int32_t lo = 0, hi = P;   // blocks < lo are cached; block hi is not (or hi == P)
+    while (hi - lo > 64) {
+        const int64_t span = hi - lo;
+        const int32_t q = lo + (int32_t)(((int64_t)(lane + 1) * span) / 64) - 1;
+        const bool hit = cached(tk, ts, smask, s_chain[q]);
+        const unsigned long long miss = __ballot(!hit);
+        if (miss == 0ull) return hi;
+        const int t = __ffsll((unsigned long long)miss) - 1;
+        const int32_t qt = lo + (int32_t)(((int64_t)(t + 1) * span) / 64) - 1;
+        const int32_t qp = t == 0 ? lo - 1 : lo + (int32_t)(((int64_t)t * span) / 64) - 1;
+        lo = qp + 1;
+        hi = qt;
+    }
+    const int32_t n = hi - lo;
+    const bool valid = lane < n;
+    const bool hit = valid ? cached(tk, ts, smask, s_chain[lo + lane]) : true;
+    const unsigned long long miss = __ballot(valid && !hit);
+    return miss ? lo + __ffsll((unsigned long long)miss) - 1 : hi;
+}
+
+// Longest cached prefix for arbitrary caches: scan from block 0, 64 per round.
+__device__ int32_t wave_prefix_scan(const uint64_t* s_chain, int32_t P, const uint64_t* tk,
+                                    const uint32_t* ts, uint64_t smask)
+{
+    const int lane = threadIdx.x & 63;
+    for (int32_t lo = 0; lo < P; lo += 64) {
+        const int32_t n = min(64, P - lo);
+        const bool valid = lane < n;
+        const bool hit = valid ? cached(tk, ts, smask, s_chain[lo + lane]) : true;
+        const unsigned long long miss = __ballot(valid && !hit);
+        if (miss) return lo + __ffsll((unsigned long long)miss) - 1;
+    }
+    return P;
+}
+
+// Find the live slot of h, or claim an empty slot for it.  Concurrent callers
+// insert distinct keys; a failed claim moves on along the probe sequence.
+__device__ __forceinline__ uint64_t insert_or_touch(uint64_t* __restrict__ tk, const uint32_t* __restrict__ ts,
+                                                   uint64_t smask, uint64_t h, int& inserted, int32_t* status)
+{
+    inserted = 0;
+    uint64_t s = h & smask;
+    for (uint64_t n = 0; n <= smask; ++n) {
+        const uint64_t k = __hip_atomic_load(&tk[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (k == h) {
+            if (ts[s] != kTomb) return s;
+        } else if (k == kEmpty) {
+            uint64_t prev = kEmpty;
+            if (__hip_atomic_compare_exchange_strong(&tk[s], &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                inserted = 1;
+                return s;
+            }
+            if (prev == h) return s;
+        }
+        s = (s + 1) & smask;
+    }
+    atomicOr(status, RK_DEV_TABLE_FULL);
+    return ~0ull;
+}
+
+__global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ EpShared sh;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int e = blockIdx.x;
+    const rk_episode_params prm = a.params[e];
+    const int32_t W = a.W;
+
+    uint64_t* s_chain = (uint64_t*)(smem + a.lds_chain);
+    int32_t* s_A = (int32_t*)(smem + a.lds_w);
+    uint32_t* s_head = (uint32_t*)(s_A + W);
+    uint32_t* s_tail = s_head + W;
+    int32_t* s_live = (int32_t*)(s_tail + W);
+    int32_t* s_used = s_live + W;
+    int32_t* s_ov = s_used + W;
+    float* s_cost = (float*)(s_ov + W);
+    int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // in-flight routes: worker
+    int32_t* s_stP = s_stw + a.max_inflight;               //                   prompt blocks
+    int32_t* s_stc = s_stP + a.max_inflight;               //                   conversation
+    int32_t* s_stepn = s_stc + a.max_inflight;             // routes per step slot
+    int64_t* s_stcb = (int64_t*)(smem + a.lds_step);       // this step: chain base
+    int32_t* s_stt = (int32_t*)(s_stcb + a.max_rps);       //            global turn
+    int64_t* s_u = (int64_t*)(smem + a.lds_u);             // controller load samples
+
+    const int32_t H = prm.hold_steps, rps = prm.routes_per_step, n_conv = prm.n_conv;
+    const bool bad = H < 1 || rps < 1 || rps > a.max_rps || (int64_t)H * rps > a.max_inflight ||
+                     n_conv < 0 || n_conv > a.max_conv || prm.cap_blocks < 1 ||
+                     (prm.controller && (prm.ctrl_window < 1 || prm.ctrl_window > a.max_ctrl_window ||
+                                         prm.ctrl_den < 1 || prm.ctrl_num < 0));
+    if (bad) {
+        if (tid == 0) atomicOr(a.status, RK_DEV_TOO_LARGE);
+        return;
+    }
+    const int64_t gc0 = prm.conv_begin;
+
+    unsigned char* ws = a.ws + (size_t)e * a.L.per_episode;
+    uint64_t* g_keys = (uint64_t*)(ws + a.L.off_keys);
+    uint32_t* g_stamps = (uint32_t*)(ws + a.L.off_stamps);
+    uint32_t* g_log = (uint32_t*)(ws + a.L.off_log);
+    uint64_t* g_scratch = (uint64_t*)(ws + a.L.off_scratch);
+    int32_t* g_queue = (int32_t*)(ws + a.L.off_queue);
+    int32_t* g_next = (int32_t*)(ws + a.L.off_next);
+    const uint64_t S = a.L.slots, smask = S - 1, R = a.L.ring, rmask = R - 1;
+    const uint64_t used_limit = S - S / 4;
+    const uint64_t scratch_cap = (uint64_t)a.cache + (uint64_t)a.max_blocks;
+
+    // ---- initial state: empty caches, idle workers, every first turn queued
+    for (uint64_t i = tid; i < (uint64_t)W * S; i += NT) g_keys[i] = kEmpty;
+    if (tid < W) {
+        s_A[tid] = 0;
+        s_head[tid] = 0;
+        s_tail[tid] = 0;
+        s_live[tid] = 0;
+        s_used[tid] = 0;
+    }
+    for (int32_t i = tid; i < a.max_inflight; i += NT) s_stepn[i] = 0;
+    int32_t qn = 0;
+    for (int32_t base = 0; base < n_conv; base += NT) {
+        const int32_t c = base + tid;
+        bool has = false;
+        if (c < n_conv) {
+            g_next[c] = 0;
+            has = a.turn_off[gc0 + c + 1] > a.turn_off[gc0 + c];
+        }
+        int32_t total;
+        const int32_t rank = block_scan(has, sh.wtot, total);
+        if (has) g_queue[qn + rank] = c;
+        qn += total;
+    }
+    if (tid == 0) {
+        sh.qhead = 0;
+        sh.qsize = qn;
+        sh.ins = 0;
+        sh.digest = 0;
+    }
+    block_sync_global();
+
+    const int32_t qcap = n_conv + 1;
+    int64_t t = 0;                       // routes done (uniform)
+    int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};   // thread 0
+    int64_t u_sum = 0;                   // thread 0
+    bool prev_active = false;            // thread 0
+
+    for (int64_t s = 0;; ++s) {
+        const int32_t slot = (int32_t)(s % H);
+        const int32_t sb = slot * rps;
+        // ---- release the routes of step s - H; queue their conversations' next turns
+        if (s >= H) {
+            const int32_t nprev = s_stepn[slot];
+            const int32_t qend = sh.qhead + sh.qsize;
+            int32_t pushed = 0;
+            for (int32_t base = 0; base < nprev; base += NT) {
+                const int32_t r = base + tid;
+                bool more = false;
+                int32_t c = 0;
+                if (r < nprev) {
+                    c = s_stc[sb + r];
+                    atomicSub(&s_A[s_stw[sb + r]], s_stP[sb + r]);
+                    more = g_next[c] < (int32_t)(a.turn_off[gc0 + c + 1] - a.turn_off[gc0 + c]);
+                }
+                int32_t total;
+                const int32_t rank = block_scan(more, sh.wtot, total);
+                if (more) g_queue[(qend + pushed + rank) % qcap] = c;
+                pushed += total;
+            }
+            if (tid == 0 && pushed) sh.qsize += pushed;
+            block_sync_global();
+        }
+        // ---- how many requests this step routes
+        if (tid == 0) {
+            int64_t inflight = 0;
+            for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[(int32_t)((s - k) % H)];
+            sh.done = sh.qsize == 0 && inflight == 0;
+            sh.n_route = sh.done ? 0 : min(rps, sh.qsize);
+            s_stepn[slot] = sh.n_route;
+            if (sh.n_route > 0) tot[5] = s + 1;
+            sh.pop_base = sh.qhead;
+            sh.qhead = (sh.qhead + sh.n_route) % (n_conv + 1);
+            sh.qsize -= sh.n_route;
+        }
+        __syncthreads();
+        if (sh.done) break;
+        const int32_t n = sh.n_route;
+        // ---- pop the step's requests from the queue head (in parallel)
+        for (int32_t r = tid; r < n; r += NT) {
+            const int32_t c = g_queue[(sh.pop_base + r) % qcap];
+            const int32_t k = g_next[c];
+            g_next[c] = k + 1;
+            const int64_t g = gc0 + c;
+            const int64_t turn = a.turn_off[g] + k;
+            int32_t P = a.turn_blocks[turn];
+            const int64_t cb = a.chain_off[g], ce = a.chain_off[g + 1];
+            if (P < 0 || (int64_t)P > ce - cb) {
+                atomicOr(a.status, RK_DEV_SHORT_INPUT);
+                P = P < 0 ? 0 : (int32_t)max((int64_t)0, ce - cb);
+            }
+            if (P > a.max_blocks) {
+                atomicOr(a.status, RK_DEV_TOO_LARGE);
+                P = a.max_blocks;
+            }
+            s_stc[sb + r] = c;
+            s_stP[sb + r] = P;
+            s_stt[r] = (int32_t)turn;
+            s_stcb[r] = cb;
+        }
+        block_sync_global();
+
+        for (int32_t r = 0; r < n; ++r) {
+            // ---- route setup: prompt, controller
+            if (tid == 0) {
+                bool active = false;
+                if (prm.controller && t >= prm.ctrl_window)
+                    active = (int64_t)prm.ctrl_den * u_sum >
+                             (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
+                float w = prm.w_ov;
+                if (active) {
+                    w = fminf(prm.w_ov, prm.ctrl_w_ov);
+                    tot[3] += 1;
+                    if (!prev_active) tot[4] += 1;
+                }
+                prev_active = active;
+                sh.w_eff = w;
+                sh.P = s_stP[sb + r];
+                sh.cbase = s_stcb[r];
+            }
+            __syncthreads();
+            const int32_t P = sh.P;
+            {
+                const uint64_t* gch = a.chains + sh.cbase;
+                for (int32_t k = tid; k < P; k += NT) s_chain[k] = gch[k];
+            }
+            __syncthreads();
+            // ---- longest cached prefix on every worker
+            for (int32_t j = wave; j < W; j += NW) {
+                const uint64_t* tk = g_keys + (uint64_t)j * S;
+                const uint32_t* ts = g_stamps + (uint64_t)j * S;
+                const int32_t o = a.probe_mode == RK_PROBE_SCAN ? wave_prefix_scan(s_chain, P, tk, ts, smask)
+                                                                : wave_prefix_search(s_chain, P, tk, ts, smask);
+                if (lane == 0) s_ov[j] = o;
+            }
+            __syncthreads();
+            // ---- cost of every worker, then argmin
+            const int64_t row = prm.out_base + t;
+            if (tid < W) {
+                const float c = route_cost(sh.w_eff, prm.w_act, prm.w_sat, prm.cap_blocks, P, s_ov[tid], s_A[tid]);
+                s_cost[tid] = c;
+                if (a.out.overlap) a.out.overlap[row * W + tid] = s_ov[tid];
+                if (a.out.cost) a.out.cost[row * W + tid] = c;
+            }
+            __syncthreads();
+            if (wave == 0) {
+                uint64_t key = lane < W ? argmin_key(s_cost[lane], lane) : ~0ull;
+                key = wave_min_u64(key);
+                if (lane == 0) {
+                    const int32_t sg = (int32_t)(uint32_t)(key & 0xffffffffu);
+                    sh.sigma = sg;
+                    const uint64_t ins_max = (uint64_t)(P - s_ov[sg]);
+                    sh.rebuild = ((uint64_t)s_used[sg] + ins_max > used_limit) ||
+                                 ((uint64_t)(s_tail[sg] - s_head[sg]) + (uint64_t)P > R) ||
+                                 (s_tail[sg] > 0x40000000u);
+                }
+            }
+            __syncthreads();
+            const int32_t sg = sh.sigma;
+            uint64_t* tk = g_keys + (uint64_t)sg * S;
+            uint32_t* ts = g_stamps + (uint64_t)sg * S;
+            uint32_t* tl = g_log + (uint64_t)sg * R;
+
+            // ---- compaction: re-stamp the live records in order into a cleared table
+            if (sh.rebuild) {
+                const uint32_t head = s_head[sg], tail = s_tail[sg];
+                int32_t cnt = 0;
+                for (uint32_t base = head; base < tail; base += NT) {
+                    const uint32_t pos = base + (uint32_t)tid;
+                    bool live = false;
+                    uint64_t key = 0;
+                    if (pos < tail) {
+                        const uint32_t sl = tl[pos & rmask];
+                        live = sl < S && ts[sl] == pos;
+                        if (live) key = tk[sl];
+                    }
+                    int32_t total;
+                    const int32_t rank = block_scan(live, sh.wtot, total);
+                    if (live && (uint64_t)(cnt + rank) < scratch_cap) g_scratch[cnt + rank] = key;
+                    cnt += total;
+                }
+                if ((uint64_t)cnt > scratch_cap) {
+                    if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
+                    cnt = (int32_t)scratch_cap;
+                }
+                block_sync_global();
+                for (uint64_t i = tid; i < S; i += NT) tk[i] = kEmpty;
+                block_sync_global();
+                for (int32_t q = tid; q < cnt; q += NT) {
+                    int ins;
+                    const uint64_t sl = insert_or_touch(tk, ts, smask, g_scratch[q], ins, a.status);
+                    if (sl != ~0ull) ts[sl] = (uint32_t)q;
+                    tl[(uint32_t)q & rmask] = (uint32_t)sl;
+                }
+                block_sync_global();
+                if (tid == 0) {
+                    s_head[sg] = 0;
+                    s_tail[sg] = (uint32_t)cnt;
+                    s_live[sg] = cnt;
+                    s_used[sg] = cnt;
+                }
+                __syncthreads();
+            }
+
+            // ---- touch the prompt's blocks (block k gets stamp tail + P-1-k), inserting misses
+            {
+                const uint32_t tail = s_tail[sg];
+                int my_ins = 0;
+                for (int32_t k = tid; k < P; k += NT) {
+                    int ins;
+                    const uint32_t stamp = tail + (uint32_t)(P - 1 - k);
+                    const uint64_t sl = insert_or_touch(tk, ts, smask, s_chain[k], ins, a.status);
+                    if (sl != ~0ull) ts[sl] = stamp;
+                    tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
+                    my_ins += ins;
+                }
+                if (my_ins) atomicAdd(&sh.ins, my_ins);
+            }
+            block_sync_global();
+            if (tid == 0) {
+                s_tail[sg] += (uint32_t)P;
+                s_live[sg] += sh.ins;
+                s_used[sg] += sh.ins;
+                sh.remaining = max(0, s_live[sg] - a.cache);
+                sh.ins = 0;
+                sh.ev = 0;
+                sh.digest = 0ull;
+            }
+            __syncthreads();
+            // ---- evict least recently used blocks down to the capacity
+            while (sh.remaining > 0) {
+                const uint32_t head = s_head[sg], tail = s_tail[sg];
+                const int32_t rem = sh.remaining;
+                if (head >= tail) {
+                    if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
+                    break;
+                }
+                const uint32_t pos = head + (uint32_t)tid;
+                uint32_t sl = 0;
+                bool live = false;
+                if (pos < tail) {
+                    sl = tl[pos & rmask];
+                    live = sl < S && ts[sl] == pos;
+                }
+                int32_t total;
+                const int32_t rank = block_scan(live, sh.wtot, total);
+                if (live && rank < rem) {
+                    const uint64_t key = tk[sl];
+                    ts[sl] = kTomb;
+                    atomicAdd(&sh.digest, (unsigned long long)mix64(key));
+                    if (rank == rem - 1) sh.new_head = pos + 1;
+                }
+                block_sync_global();
+                if (tid == 0) {
+                    if (total >= rem) {
+                        s_head[sg] = sh.new_head;
+                        sh.ev += rem;
+                        s_live[sg] -= rem;
+                        sh.remaining = 0;
+                    } else {
+                        s_head[sg] = min(head + (uint32_t)NT, tail);
+                        sh.ev += total;
+                        s_live[sg] -= total;
+                        sh.remaining = rem - total;
+                    }
+                }
+                __syncthreads();
+            }
+            // ---- load, controller sample, outputs
+            if (tid == 0) {
+                s_A[sg] += P;
+                s_stw[sb + r] = sg;
+                if (prm.controller) {
+                    int64_t u = 0;
+                    for (int32_t j = 0; j < W; ++j) u += s_A[j];
+                    const int32_t pos = (int32_t)(t % prm.ctrl_window);
+                    if (t >= prm.ctrl_window) u_sum -= s_u[pos];
+                    s_u[pos] = u;
+                    u_sum += u;
+                }
+                if (a.out.route_turn) a.out.route_turn[row] = s_stt[r];
+                if (a.out.route_worker) a.out.route_worker[row] = sg;
+                if (a.out.route_step) a.out.route_step[row] = (int32_t)s;
+                if (a.out.route_blocks) a.out.route_blocks[row] = P;
+                if (a.out.evict_count) a.out.evict_count[row] = sh.ev;
+                if (a.out.evict_digest) a.out.evict_digest[row] = sh.digest;
+                if (a.out.last_hash) a.out.last_hash[row] = P > 0 ? s_chain[P - 1] : 0ull;
+                tot[0] += P - s_ov[sg];
+                tot[1] += sh.ev;
+                tot[2] += P;
+                tot[6] += s_ov[sg];
+            }
+            ++t;
+            __syncthreads();
+        }
+    }
+    if (tid == 0 && a.out.totals) {
+        int64_t cachedsum = 0;
+        for (int32_t j = 0; j < W; ++j) cachedsum += s_live[j];
+        tot[7] = cachedsum;
+        for (int k = 0; k < 8; ++k) a.out.totals[(int64_t)e * 8 + k] = tot[k];
+    }
+}
+
+}  // namespace rk
+
+using namespace rk;
+
+extern "C" size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache_blocks, int32_t max_blocks,
+                                             int32_t max_conv)
+{
+    if (E < 0 || W < 1 || cache_blocks < 1 || max_blocks < 1 || max_conv < 0) return 0;
+    const EpisodeLayout L = episode_layout(W, cache_blocks, max_blocks, max_conv);
+    return L.per_episode * (size_t)E;
+}
+
+extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_outputs* out, void* workspace,
+                                    size_t ws_bytes, void* stream)
+{
+    if (!b || !out) return fail(RK_EINVAL, "rk_simulate_episodes: NULL batch or outputs");
+    if (b->E < 0) return fail(RK_EINVAL, "rk_simulate_episodes: E < 0");
+    if (b->W < 1 || b->W > 64) return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: W outside 1..64");
+    if (b->cache_blocks < 1) return fail(RK_EINVAL, "rk_simulate_episodes: cache_blocks < 1");
+    if (b->max_blocks < 1 || b->max_blocks > 8192)
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: max_blocks outside 1..8192");
+    if (b->max_conv < 0 || b->max_conv > (1 << 28)) return fail(RK_EINVAL, "rk_simulate_episodes: max_conv");
+    if (b->max_inflight < 1 || b->max_inflight > 8192)
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: max_inflight outside 1..8192");
+    if (b->max_routes_per_step < 1 || b->max_routes_per_step > b->max_inflight)
+        return fail(RK_EINVAL, "rk_simulate_episodes: max_routes_per_step outside 1..max_inflight");
+    if (b->max_ctrl_window < 1 || b->max_ctrl_window > 4096)
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: max_ctrl_window outside 1..4096");
+    if (b->probe_mode != RK_PROBE_PREFIX && b->probe_mode != RK_PROBE_SCAN)
+        return fail(RK_EINVAL, "rk_simulate_episodes: unknown probe_mode");
+    if ((int64_t)b->cache_blocks + b->max_blocks > (1ll << 29))
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: cache too large");
+    if (b->E == 0) return RK_OK;
+    if (!b->params || !b->turn_off || !b->turn_blocks || !b->chain_off || !b->chains || !workspace)
+        return fail(RK_EINVAL, "rk_simulate_episodes: NULL array");
+    const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv);
+    const size_t need = L.per_episode * (size_t)b->E;
+    if (ws_bytes < need)
+        return fail(RK_ENOMEM, "rk_simulate_episodes: workspace %zu bytes < %zu needed", ws_bytes, need);
+    int32_t* st = status_word();
+    if (!st) return fail(RK_EHIP, "rk_simulate_episodes: no status word");
+
+    EpArgs a;
+    a.E = b->E;
+    a.W = b->W;
+    a.cache = b->cache_blocks;
+    a.max_blocks = b->max_blocks;
+    a.max_conv = b->max_conv;
+    a.max_inflight = b->max_inflight;
+    a.max_rps = b->max_routes_per_step;
+    a.max_ctrl_window = b->max_ctrl_window;
+    a.probe_mode = b->probe_mode;
+    a.params = b->params;
+    a.turn_off = b->turn_off;
+    a.turn_blocks = b->turn_blocks;
+    a.chain_off = b->chain_off;
+    a.chains = b->chains;
+    a.out = *out;
+    a.ws = (unsigned char*)workspace;
+    a.L = L;
+    a.status = st;
+    size_t o = 0;
+    a.lds_chain = (uint32_t)o;    o = align_up(o + (size_t)b->max_blocks * 8, 16);
+    a.lds_w = (uint32_t)o;        o = align_up(o + (size_t)b->W * 7 * 4, 16);
+    a.lds_inflight = (uint32_t)o; o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
+    a.lds_step = (uint32_t)o;     o = align_up(o + (size_t)b->max_routes_per_step * 12, 16);
+    a.lds_u = (uint32_t)o;        o = align_up(o + (size_t)b->max_ctrl_window * 8, 16);
+    if (o > 60 * 1024)
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 60 KiB", o);
+    hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), o, (hipStream_t)stream, a);
+    return hip_check(hipGetLastError(), "rk_simulate_episodes launch");
+}

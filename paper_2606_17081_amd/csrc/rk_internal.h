@@ -1,0 +1,111 @@
+// rk_internal.h -- shared device helpers and host plumbing of the routing library.
+// Internal to the library (not part of the C ABI in include/rkroute.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rkroute.h"
+
+namespace rk {
+
+constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;  // splitmix64 increment; also the zero remap
+constexpr uint64_t kEmpty = 0;                       // empty table slot
+constexpr uint32_t kTomb = 0xFFFFFFFFu;              // stamp of an evicted (tombstoned) slot
+
+// ------------------------------------------------------------------ hashing
+
+// One splitmix64 generator step applied to state x (Vigna, splitmix64.c).
+__device__ __forceinline__ uint64_t mix64(uint64_t x)
+{
+    uint64_t z = x + kGolden;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// FNV-1a 64 over the four little-endian bytes of one int32 token.
+__device__ __forceinline__ uint64_t fnv_word(uint64_t h, uint32_t v)
+{
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        h ^= (uint64_t)((v >> (8 * b)) & 0xffu);
+        h *= 0x100000001b3ull;
+    }
+    return h;
+}
+
+__device__ __forceinline__ uint64_t chain_next(uint64_t prev, uint64_t f)
+{
+    uint64_t h = mix64(prev ^ f);
+    return h == 0 ? kGolden : h;
+}
+
+// -------------------------------------------------------------------- cost
+
+// Router cost in fp32 with the fixed operation order of the ABI; explicit
+// round-to-nearest intrinsics keep every product and sum separately rounded.
+__device__ __forceinline__ float route_cost(float w_ov, float w_act, float w_sat, int32_t cap,
+                                            int32_t P, int32_t o, int32_t A)
+{
+    float t1 = __fmul_rn(w_ov, (float)(P - o));
+    float t2 = __fmul_rn(w_act, (float)A);
+    float r = __fdiv_rn((float)((int64_t)A + (int64_t)P), (float)cap);
+    float x = fmaxf(__fsub_rn(r, 1.0f), 0.0f);
+    float t3 = __fmul_rn(w_sat, __fmul_rn(x, x));
+    return __fadd_rn(__fadd_rn(t1, t2), t3);
+}
+
+// Key whose unsigned order is (cost, worker) lexicographic for cost >= 0.
+__device__ __forceinline__ uint64_t argmin_key(float c, int32_t j)
+{
+    return ((uint64_t)__float_as_uint(__fadd_rn(c, 0.0f)) << 32) | (uint32_t)j;
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        uint64_t o = __shfl_xor(v, off, 64);
+        v = o < v ? o : v;
+    }
+    return v;
+}
+
+// ------------------------------------------------- read-only table probes
+// Open addressing, home slot key & mask, linear probing; 0 is empty.
+__device__ __forceinline__ bool table_has(const uint64_t* __restrict__ t, uint64_t mask, uint64_t key)
+{
+    uint64_t s = key & mask;
+    for (uint64_t n = 0; n <= mask; ++n) {
+        uint64_t k = t[s];
+        if (k == key) return true;
+        if (k == kEmpty) return false;
+        s = (s + 1) & mask;
+    }
+    return false;
+}
+
+// ------------------------------------------------------------ host plumbing
+int fail(int status, const char* fmt, ...);                  // records rk_last_error
+int hip_check(hipError_t e, const char* what);
+int32_t* status_word();                                      // device address for the current device
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline uint64_t next_pow2(uint64_t x)
+{
+    uint64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// Episode workspace layout (bytes), shared by the size query and the launch.
+struct EpisodeLayout {
+    uint64_t slots;        // table slots per worker (power of two)
+    uint64_t ring;         // LRU log records per worker (power of two)
+    size_t off_keys, off_stamps, off_log, off_scratch, off_queue, off_next;
+    size_t per_episode;
+};
+EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv);
+
+}  // namespace rk

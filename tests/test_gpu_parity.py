@@ -1,0 +1,404 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Integer results (hashes, overlaps, routes, steps, evictions, digests, argmins)
+must match bit for bit; fp32 costs must match bit for bit as well (both sides
+evaluate the same IEEE operations in the same order, which is tighter than the
+1e-5 relative bound the method needs); PoA sums use a 1e-9 relative bound
+(fp64 sums of identical fp32 terms, possibly of a different optimal
+assignment).  Large workloads run at their full per-episode sizes in the same
+launch configuration as the benchmark and are checked on sampled episodes.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2606_17081_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+REL = 1e-9
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "episode_hand.json")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_2606_17081_amd import rkroute as rk
+    rk.lib()
+    assert rk.device_status(reset=True) == 0
+    return torch, rk
+
+
+def _status_clean(rk):
+    bits = rk.device_status(reset=True)
+    assert bits == 0, [v for k, v in rk.DEV_BITS.items() if bits & k]
+
+
+def _compare_episode(g, o, W, poa_params=wl.POA_PARAMS, window=None, label=""):
+    n = len(o["route_worker"])
+    assert len(g["route_worker"]) == n, label
+    for k in ("route_turn", "route_worker", "route_step", "route_blocks", "evict_count", "evict_digest",
+              "last_hash"):
+        bad = np.nonzero(np.asarray(g[k]) != np.asarray(o[k]))[0]
+        assert bad.size == 0, f"{label} {k} differs first at route {bad[:5]}"
+    assert np.array_equal(g["overlap"], o["overlap"]), label
+    if "cost" in g:
+        assert np.array_equal(g["cost"].view(np.uint32), o["cost"].view(np.uint32)), label
+    assert np.array_equal(g["totals"], o["totals"]), (label, g["totals"], o["totals"])
+    if window is not None:
+        from oracle import oracle as O
+        ref = O.episode_poa(o, W, window, poa_params)
+        np.testing.assert_allclose(g["selfish"], ref["selfish"], rtol=REL)
+        np.testing.assert_allclose(g["coordinated"], ref["coordinated"], rtol=REL)
+        assert g["poa_hat"] == pytest.approx(ref["poa_hat"], rel=REL)
+
+
+# ------------------------------------------------------------------ hashing
+
+def test_hash_chains_parity(gpu, orc):
+    torch, rk = gpu
+    traces = [wl.tiny_trace(0), wl.sweep70b_trace(5), wl.multiturn_trace(2, n_conv=64)]
+    for tr in traces:
+        say("hash parity, seed", tr.seed, "sequences", tr.n_conv, "blocks", tr.n_blocks)
+        up = rk.to_device
+        ch = rk.hash_chains(up(tr.tokens), up(tr.tok_off), up(tr.chain_off))
+        torch.cuda.synchronize()
+        got = rk.to_host_u64(ch[: tr.n_blocks])
+        assert np.array_equal(got, orc.trace_chains(tr))
+    # empty sequences, a trailing partial block, zero sequences
+    toks = np.arange(16 * 3 + 5, dtype=np.int32)
+    tok_off = np.array([0, 0, 16 * 3 + 5], np.int64)
+    chain_off = np.array([0, 0, 3], np.int64)
+    ch = rk.hash_chains(torch.from_numpy(toks).cuda(), torch.from_numpy(tok_off).cuda(),
+                        torch.from_numpy(chain_off).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(rk.to_host_u64(ch[:3]), orc.hash_chains(toks, tok_off, [0, 3], chain_off))
+    _status_clean(rk)
+
+
+def test_hash_short_tokens_flagged(gpu):
+    torch, rk = gpu
+    toks = torch.zeros(20, dtype=torch.int32, device="cuda")
+    ch = rk.hash_chains(toks, torch.tensor([0, 20], device="cuda"), torch.tensor([0, 2], device="cuda"))
+    torch.cuda.synchronize()
+    assert rk.device_status(reset=True) & 0x2
+    assert int(rk.to_host_u64(ch[1:2])[0]) == 0
+
+
+# ------------------------------------------------------------------ snapshot scoring
+
+def _score(rk, torch, inst, mode, tables=None):
+    up = rk.to_device
+    if tables is None:
+        tables = rk.table_build(up(inst.keys), inst.key_off, inst.log2_slots)
+    ov, co, am = rk.route_score_batch(up(inst.chains), up(inst.chain_off), tables, inst.log2_slots,
+                                      up(inst.active), inst.w_ov, inst.w_act, inst.w_sat, inst.cap,
+                                      probe_mode=mode)
+    torch.cuda.synchronize()
+    return ov.cpu().numpy(), co.cpu().numpy(), am.cpu().numpy(), tables
+
+
+@pytest.mark.parametrize("W", [64, 5, 70])
+def test_score_small_both_modes(gpu, orc, W):
+    torch, rk = gpu
+    inst = wl.scoring_instance(seed=W, B=1500, W=W, log2_slots=11, len_lo=1, len_hi=70)
+    ref = orc.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                          inst.w_ov, inst.w_act, inst.w_sat, inst.cap)
+    for mode in (rk.RK_PROBE_PREFIX, rk.RK_PROBE_SCAN):
+        say("score small W", W, "mode", mode)
+        ov, co, am, _ = _score(rk, torch, inst, mode)
+        assert np.array_equal(ov, ref[0])
+        assert np.array_equal(co.view(np.uint32), ref[1].view(np.uint32))
+        assert np.array_equal(am, ref[2])
+    _status_clean(rk)
+
+
+def test_score_scan_mode_arbitrary_tables(gpu, orc):
+    # keys from a tiny alphabet: tables are not prefix-closed along chains
+    torch, rk = gpu
+    rng = np.random.default_rng(3)
+    W, B = 9, 800
+    L = rng.integers(0, 40, size=B)
+    chain_off = np.zeros(B + 1, np.int64)
+    np.cumsum(L, out=chain_off[1:])
+    chains = rng.integers(1, 30, size=int(chain_off[-1])).astype(np.uint64)
+    keys = [np.unique(rng.integers(1, 30, size=int(rng.integers(0, 25)))).astype(np.uint64) for _ in range(W)]
+    key_off = np.zeros(W + 1, np.int64)
+    np.cumsum([k.size for k in keys], out=key_off[1:])
+    inst = wl.ScoringInstance(W=W, B=B, keys=np.concatenate(keys), key_off=key_off, chains=chains,
+                              chain_off=chain_off, active=rng.integers(0, 50, W).astype(np.int32), cap=16,
+                              log2_slots=6)
+    ref = orc.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                          inst.w_ov, inst.w_act, inst.w_sat, inst.cap)
+    ov, co, am, _ = _score(rk, torch, inst, rk.RK_PROBE_SCAN)
+    assert np.array_equal(ov, ref[0]) and np.array_equal(am, ref[2])
+    assert np.array_equal(co.view(np.uint32), ref[1].view(np.uint32))
+    _status_clean(rk)
+
+
+def test_score_full_size_sampled(gpu, orc):
+    """65,536 requests x 64 workers, 2^20-slot tables; 300 sampled requests vs the oracle."""
+    torch, rk = gpu
+    say("generating the 65,536 x 64 scoring instance")
+    inst = wl.scoring_instance(seed=0)
+    say("scoring on the GPU")
+    ov, co, am, tables = _score(rk, torch, inst, rk.RK_PROBE_PREFIX)
+    _status_clean(rk)
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([[0, inst.B - 1], rng.integers(0, inst.B, 298)]))
+    say("oracle on", rows.size, "sampled requests")
+    r_ov, r_co, r_am = orc.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                                       inst.w_ov, inst.w_act, inst.w_sat, inst.cap, rows=rows)
+    assert np.array_equal(ov[rows], r_ov)
+    assert np.array_equal(co[rows].view(np.uint32), r_co.view(np.uint32))
+    assert np.array_equal(am[rows], r_am)
+    # properties over every request: overlap within the prompt, argmin is the first minimum
+    P = np.diff(inst.chain_off)
+    assert np.all(ov >= 0) and np.all(ov <= P[:, None])
+    assert np.array_equal(am, np.argmin(co, axis=1))
+    # the scan mode agrees on the same tables (prefix-closed by construction)
+    ov2, _, am2, _ = _score(rk, torch, inst, rk.RK_PROBE_SCAN, tables=tables)
+    assert np.array_equal(ov2, ov) and np.array_equal(am2, am)
+    _status_clean(rk)
+
+
+def test_score_empty_and_degenerate(gpu, orc):
+    torch, rk = gpu
+    inst = wl.scoring_instance(seed=9, B=40, W=3, log2_slots=6, len_lo=1, len_hi=8)
+    n4 = int(inst.chain_off[5] - inst.chain_off[4])                       # make request 4 empty
+    inst.chains = np.delete(inst.chains, np.s_[inst.chain_off[4]:inst.chain_off[5]])
+    inst.chain_off[5:] -= n4
+    ref = orc.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                          inst.w_ov, inst.w_act, inst.w_sat, inst.cap)
+    ov, co, am, _ = _score(rk, torch, inst, rk.RK_PROBE_PREFIX)
+    assert np.array_equal(ov, ref[0]) and np.array_equal(am, ref[2])
+    assert np.array_equal(co.view(np.uint32), ref[1].view(np.uint32))
+    z = torch.zeros(1, dtype=torch.int64, device="cuda")
+    o, c, a = rk.route_score_batch(torch.zeros(1, dtype=torch.int64, device="cuda"), z,
+                                   torch.zeros(3 << 6, dtype=torch.int64, device="cuda"), 6,
+                                   torch.zeros(3, dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+    assert a.numel() == 0
+    _status_clean(rk)
+
+
+# ------------------------------------------------------------------ episodes
+
+def _run(gpu, workload, episodes=None, mode=0, chains=None):
+    torch, rk = gpu
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    r = EpisodeRunner(workload, episodes, probe_mode=mode, chains=chains)
+    r.step()
+    torch.cuda.synchronize()
+    _status_clean(rk)
+    return r
+
+
+def _oracle_episode(orc, workload, spec, chains_cache):
+    tr = workload.traces[spec.seed]
+    if spec.seed not in chains_cache:
+        chains_cache[spec.seed] = orc.trace_chains(tr)
+    return orc.simulate_trace(workload.W, workload.cache_blocks, spec, tr, chains_cache[spec.seed])
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_tiny_episode_parity(gpu, orc, mode):
+    w = wl.tiny_workload()
+    say("tiny episode, probe mode", mode)
+    r = _run(gpu, w, mode=mode)
+    o = _oracle_episode(orc, w, w.episodes[0], {})
+    _compare_episode(r.episode_results(0), o, w.W, window=w.episodes[0].concurrency, label="tiny")
+
+
+def test_hand_fixtures_gpu(gpu):
+    with open(GOLD) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
+        say("hand fixture", case["name"])
+        chains = case["chains"]
+        n = len(chains)
+        lens = np.array([len(c) for c in chains], np.int32)
+        chain_off = np.zeros(n + 1, np.int64)
+        np.cumsum(lens, out=chain_off[1:])
+        tok_off = chain_off * 16
+        tr = wl.Trace(seed=0, tokens=np.zeros(int(tok_off[-1]) or 16, np.int32), tok_off=tok_off,
+                      chain_blocks=lens, chain_off=chain_off, turn_off=np.array(case["turn_off"], np.int64),
+                      turn_blocks=np.array(case["turn_blocks"], np.int32), group=np.zeros(n, np.int32),
+                      shared=np.zeros(n, np.int32))
+        spec = wl.EpisodeSpec(seed=0, concurrency=case["routes_per_step"] * case["H"], hold_steps=case["H"],
+                              w_ov=case["w_ov"], w_act=case["w_act"], w_sat=case["w_sat"], cap=case["cap"],
+                              controller=case["controller"], ctrl_w_ov=case.get("ctrl_w_ov", 0.25),
+                              ctrl_window=case.get("ctrl_window", 128), ctrl_num=case.get("ctrl_num", 9),
+                              ctrl_den=case.get("ctrl_den", 10))
+        work = wl.Workload("hand", W=case["W"], cache_blocks=case["cache_blocks"], traces={0: tr}, episodes=[spec])
+        flat_chains = np.array([k for c in chains for k in c], np.uint64)
+        for mode in (0, 1):
+            g = _run(gpu, work, mode=mode, chains=flat_chains).episode_results(0)
+            ex = case["expect"]
+            assert g["route_turn"].tolist() == ex["route_turn"]
+            assert g["route_worker"].tolist() == ex["route_worker"]
+            assert g["route_step"].tolist() == ex["route_step"]
+            assert g["overlap"].tolist() == ex["overlap"]
+            assert g["cost"].tolist() == ex["cost"]
+            assert g["evict_count"].tolist() == ex["evict_count"]
+            assert g["last_hash"].tolist() == ex["last_hash"]
+            t = g["totals"]
+            assert t[0] == ex["totals"]["prefill"] and t[1] == ex["totals"]["evicted"]
+            assert t[5] == ex["totals"]["steps"] and t[7] == ex["totals"]["cached"]
+
+
+def _prefix_closed_case(rng, W, cache, multiturn):
+    n_conv = int(rng.integers(1, 40))
+    chains, turn_blocks, turn_off = [], [], [0]
+    prefix_id = {}
+    for _ in range(n_conv):
+        L = int(rng.integers(1, 150))
+        path = tuple(int(x) for x in rng.integers(0, 2 if L < 20 else 4, size=L))
+        chains.append([prefix_id.setdefault(path[:k], len(prefix_id) + 1) for k in range(1, L + 1)])
+        tb = sorted(int(x) for x in rng.integers(0, L + 1, size=int(rng.integers(1, 4)))) if multiturn else [L]
+        turn_blocks.extend(tb)
+        turn_off.append(len(turn_blocks))
+    return chains, np.array(turn_off, np.int64), np.array(turn_blocks, np.int32)
+
+
+def test_random_small_episodes_batched(gpu, orc):
+    """60 small episodes (prefix-closed keys, heavy eviction, controller, multi-turn) in one launch."""
+    torch, rk = gpu
+    rng = np.random.default_rng(77)
+    W, cache = 3, 24
+    traces, specs, all_chains = {}, [], {}
+    for seed in range(60):
+        chains, turn_off, turn_blocks = _prefix_closed_case(rng, W, cache, multiturn=seed % 2 == 1)
+        lens = np.array([len(c) for c in chains], np.int32)
+        chain_off = np.zeros(len(chains) + 1, np.int64)
+        np.cumsum(lens, out=chain_off[1:])
+        traces[seed] = wl.Trace(seed=seed, tokens=np.zeros(16, np.int32), tok_off=chain_off * 0,
+                                chain_blocks=lens, chain_off=chain_off, turn_off=turn_off,
+                                turn_blocks=turn_blocks, group=np.zeros(len(chains), np.int32),
+                                shared=np.zeros(len(chains), np.int32))
+        all_chains[seed] = np.array([k for c in chains for k in c], np.uint64)
+        H = int(rng.integers(1, 5))
+        rps = int(rng.integers(1, 6))
+        specs.append(wl.EpisodeSpec(seed=seed, concurrency=H * rps, hold_steps=H,
+                                    w_ov=float(rng.choice([0.0, 0.25, 1.0, 2.0])),
+                                    w_act=float(rng.choice([0.0, 0.5, 1.0])), w_sat=float(rng.choice([0.0, 4.0])),
+                                    cap=int(rng.integers(1, 200)), controller=int(rng.integers(0, 2)),
+                                    ctrl_window=int(rng.integers(1, 6)), ctrl_num=int(rng.integers(0, 10))))
+    work = wl.Workload("random", W=W, cache_blocks=cache, traces=traces, episodes=specs)
+    flat = np.concatenate([all_chains[s] for s in sorted(traces)])
+    for mode in (0, 1):
+        say("60 random episodes, probe mode", mode)
+        r = _run(gpu, work, mode=mode, chains=flat)
+        for e, sp in enumerate(specs):
+            tr = traces[sp.seed]
+            o = orc.simulate_episode(W, cache, sp, tr.turn_off, tr.turn_blocks, tr.chain_off, all_chains[sp.seed])
+            _compare_episode(r.episode_results(e), o, W, window=sp.concurrency, label=f"episode {e}")
+
+
+def test_sweep70b_full_launch_sampled(gpu, orc):
+    """All 320 episodes of the 1P/5D-shaped sweep in one launch; 3 sampled episodes vs the oracle."""
+    say("generating 64 traces of 4,096 requests")
+    w = wl.sweep70b_workload()
+    say("running 320 episodes on the GPU")
+    r = _run(gpu, w)
+    cache = {}
+    for e in (0, 64 * 2 + 17, 64 * 5 - 1):
+        sp = r.episodes[e]
+        say("oracle episode", e, "seed", sp.seed, "C", sp.concurrency)
+        o = _oracle_episode(orc, w, sp, cache)
+        _compare_episode(r.episode_results(e), o, w.W, window=sp.concurrency, label=f"sweep70b e{e}")
+    poa = r.poa_hat.cpu().numpy()[: len(r.episodes)]
+    assert np.all(np.isfinite(poa)) and np.all(poa > 0)
+
+
+def test_saturation_subset(gpu, orc):
+    """8 seeds x 8 concurrency levels x 5 overlap weights with the controller; 5 sampled episodes."""
+    say("generating 8 saturation traces")
+    w = wl.saturation_workload(seeds=range(8))
+    say("running", len(w.episodes), "episodes on the GPU")
+    r = _run(gpu, w)
+    cache = {}
+    idx = {(sp.seed, sp.concurrency, sp.w_ov): e for e, sp in enumerate(r.episodes)}
+    for key in [(0, 8, 1.0), (1, 128, 1.0), (2, 256, 0.0), (3, 1024, 2.0), (7, 64, 0.25)]:
+        e = idx[key]
+        say("oracle episode", key)
+        o = _oracle_episode(orc, w, r.episodes[e], cache)
+        _compare_episode(r.episode_results(e), o, w.W, window=key[1], label=f"saturation {key}")
+    tot = r.totals.cpu().numpy()[: len(r.episodes)]
+    assert tot[:, 3].sum() > 0        # the controller fires somewhere in the sweep
+
+
+def test_multiturn_subset(gpu, orc):
+    """Long-context multi-turn episodes at full size (512 conversations, 16,384-block caches)."""
+    say("generating 12 multi-turn traces")
+    w = wl.multiturn_workload(seeds=range(12))
+    say("running 12 episodes on the GPU")
+    r = _run(gpu, w)
+    cache = {}
+    for e in (0, 11):
+        say("oracle episode", e)
+        o = _oracle_episode(orc, w, r.episodes[e], cache)
+        _compare_episode(r.episode_results(e), o, w.W, window=256, label=f"multiturn e{e}")
+        assert o["totals"][1] > 0
+
+
+def test_eviction_extremes(gpu, orc):
+    """Caches smaller than one prompt (a route evicts part of its own prompt), single worker."""
+    tr = wl.tiny_trace(4)
+    for W, cache in [(4, 1), (2, 7), (1, 40)]:
+        say("eviction extremes W", W, "cache", cache)
+        spec = wl.EpisodeSpec(seed=4, concurrency=8, cap=64)
+        work = wl.Workload("x", W=W, cache_blocks=cache, traces={4: tr}, episodes=[spec])
+        for mode in (0, 1):
+            r = _run(gpu, work, mode=mode)
+            o = orc.simulate_trace(W, cache, spec, tr)
+            _compare_episode(r.episode_results(0), o, W, window=8, label=f"W{W} cache{cache}")
+
+
+def test_determinism(gpu):
+    torch, rk = gpu
+    w = wl.sweep70b_workload(seeds=range(4), concurrency=(64, 256))
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    r = EpisodeRunner(w)
+    r.step()
+    a = [t.clone() for t in (r.route_worker, r.overlap, r.evict_digest, r.coord)]
+    r.step()
+    torch.cuda.synchronize()
+    b = (r.route_worker, r.overlap, r.evict_digest, r.coord)
+    for x, y in zip(a, b):
+        assert torch.equal(x.cpu(), y.cpu())
+    _status_clean(rk)
+
+
+def test_snapshot_poa(gpu, orc):
+    """PoA-hat of the snapshot workload: windows of 512 requests, K = 8 replicas per worker."""
+    torch, rk = gpu
+    inst = wl.scoring_instance(seed=2, B=4096, W=64, log2_slots=14, len_lo=16, len_hi=128)
+    ov, co, am, _ = _score(rk, torch, inst, rk.RK_PROBE_PREFIX)
+    P = np.diff(inst.chain_off).astype(np.int32)
+    win = np.arange(0, inst.B + 1, 512, dtype=np.int64)
+    up = rk.to_device
+    sel = torch.zeros(win.size - 1, dtype=torch.float64, device="cuda")
+    coo = torch.zeros_like(sel)
+    hat = torch.zeros(1, dtype=torch.float64, device="cuda")
+    pp = dict(wl.POA_PARAMS)
+    params = rk.PoaParams(pp["a"], pp["b"], pp["d"], pp["beta"], pp["C_cap"], pp["w_c"], 8)
+    ws = torch.empty(rk.poa_workspace_size(inst.B, 64), dtype=torch.uint8, device="cuda")
+    rk.poa_estimate(up(win), up(np.array([0, win.size - 1], np.int64)), inst.B, 512, 64, up(am), up(ov), up(P),
+                    params, sel, coo, hat, ws)
+    torch.cuda.synchronize()
+    _status_clean(rk)
+    sel, coo = sel.cpu().numpy(), coo.cpu().numpy()
+    for w in (0, 3, 7):
+        s, c, _ = orc.poa_window(am[512 * w:512 * (w + 1)], ov[512 * w:512 * (w + 1)], P[512 * w:512 * (w + 1)],
+                                 64, K=8, **pp)
+        assert sel[w] == pytest.approx(s, rel=REL) and coo[w] == pytest.approx(c, rel=REL)
+    assert float(hat[0]) == pytest.approx(sel.sum() / coo.sum(), rel=1e-12)
