@@ -154,6 +154,36 @@ def cpu_baseline(workload, seeds, threads):
                 episodes_per_s=len(specs) / dt, seconds=dt)
 
 
+def scoring_bench(torch, rk, wl, stream, steps):
+    """Time rk_route_score_batch on the 65,536 x 64 snapshot workload."""
+    log("generating the 65,536 x 64 scoring instance")
+    inst = wl.scoring_instance(seed=0)
+    up = rk.to_device
+    tables = rk.table_build(up(inst.keys), inst.key_off, inst.log2_slots)
+    chains, chain_off, active = up(inst.chains), up(inst.chain_off), up(inst.active)
+    ov = torch.empty((inst.B, inst.W), dtype=torch.int32, device="cuda")
+    co = torch.empty((inst.B, inst.W), dtype=torch.float32, device="cuda")
+    am = torch.empty(inst.B, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co, argmin=am)
+    ts = KernelTimer(torch, stream)
+    for _ in range(max(steps, 10)):
+        with ts:
+            rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co,
+                                 argmin=am)
+    ms = ts.mean_ms()
+    assert rk.device_status(reset=True) == 0
+    salg = score_algorithmic_bytes(inst)
+    ach = salg / (ms * 1e-3) / 1e9
+    log(f"scoring: {ms:.4f} ms, {inst.B * inst.W / (ms * 1e-3):.4g} scorings/s, {ach:.1f} GB/s algorithmic")
+    return {"workload": "scoring 65536 requests x 64 workers, 2^20-slot tables at load 0.5, chains of 16..512",
+            "scorings_per_s": inst.B * inst.W / (ms * 1e-3), "avg_ms": round(ms, 4),
+            "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": round(ach, 3),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 6),
+                         "traffic": measured_traffic("score_kernel", "scoring"),
+                         "algorithmic_bytes": salg}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,6 +192,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-scoring", action="store_true")
     ap.add_argument("--cpu-seeds", type=int, default=8)
+    ap.add_argument("--only", choices=("all", "sweep", "scoring"), default="all",
+                    help="profiling passes: run only the sweep step or only the scoring kernel")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this size (counter calibration)")
     args = ap.parse_args()
@@ -188,6 +220,10 @@ def main():
         log(f"copied {n} bytes 5 times")
         return
 
+    if args.only == "scoring":
+        score = scoring_bench(torch, rk, wl, torch.cuda.current_stream(), args.steps)
+        print(json.dumps({"score_batch": score}), flush=True)
+        return
     log("generating the sweep (64 traces of 4,096 requests)")
     w = wl.sweep70b_workload()
     runner = EpisodeRunner(w, keep_cost=True)
@@ -241,38 +277,13 @@ def main():
                     "frac": None, "traffic": None, "avg_ms": round(stage_ms[dom], 4)}
 
     score = None
-    if not args.no_scoring:
+    if not args.no_scoring and args.only == "all":
         del runner
         torch.cuda.empty_cache()
-        log("generating the 65,536 x 64 scoring instance")
-        inst = wl.scoring_instance(seed=0)
-        up = rk.to_device
-        tables = rk.table_build(up(inst.keys), inst.key_off, inst.log2_slots)
-        chains, chain_off, active = up(inst.chains), up(inst.chain_off), up(inst.active)
-        ov = torch.empty((inst.B, inst.W), dtype=torch.int32, device="cuda")
-        co = torch.empty((inst.B, inst.W), dtype=torch.float32, device="cuda")
-        am = torch.empty(inst.B, dtype=torch.int32, device="cuda")
-        for _ in range(3):
-            rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co, argmin=am)
-        ts = KernelTimer(torch, stream)
-        for _ in range(max(args.steps, 10)):
-            with ts:
-                rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co,
-                                     argmin=am)
-        ms = ts.mean_ms()
-        assert rk.device_status(reset=True) == 0
-        salg = score_algorithmic_bytes(inst)
-        ach = salg / (ms * 1e-3) / 1e9
-        score = {"workload": "scoring 65536 requests x 64 workers, 2^20-slot tables at load 0.5, chains of 16..512",
-                 "scorings_per_s": inst.B * inst.W / (ms * 1e-3), "avg_ms": round(ms, 4),
-                 "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": round(ach, 3),
-                              "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 6),
-                              "traffic": measured_traffic("score_kernel", "scoring"),
-                              "algorithmic_bytes": salg}}
-        log(f"scoring: {ms:.4f} ms, {score['scorings_per_s']:.4g} scorings/s, {ach:.1f} GB/s algorithmic")
+        score = scoring_bench(torch, rk, wl, stream, args.steps)
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.only == "all":
         threads = max(1, min(16, os.cpu_count() or 1))
         log(f"oracle on {args.cpu_seeds} seeds x 5 concurrency levels with {threads} threads")
         cpu = cpu_baseline(w, list(range(args.cpu_seeds)), threads)

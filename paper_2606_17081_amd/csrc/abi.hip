@@ -54,8 +54,7 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     L.slots = next_pow2(2 * live_max);
     L.ring = next_pow2(2 * live_max);
     size_t o = 0;
-    L.off_keys = o;    o = align_up(o + (size_t)W * L.slots * sizeof(uint64_t), 256);
-    L.off_stamps = o;  o = align_up(o + (size_t)W * L.slots * sizeof(uint32_t), 256);
+    L.off_slots = o;   o = align_up(o + (size_t)W * L.slots * sizeof(Slot), 256);
     L.off_log = o;     o = align_up(o + (size_t)W * L.ring * sizeof(uint32_t), 256);
     L.off_scratch = o; o = align_up(o + live_max * sizeof(uint64_t), 256);
     L.off_queue = o;   o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);

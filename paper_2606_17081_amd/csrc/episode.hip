@@ -2,20 +2,25 @@
 //
 // Per episode the workgroup (256 threads, 4 wavefronts) keeps in LDS the
 // worker loads A_j, the LRU bookkeeping of every worker, the in-flight routes
-// of the last H steps, the controller's load window and the current prompt's
-// chain.  Each worker's cached blocks live in HBM as an open-addressing table
-// (key, stamp) plus a ring log of touches:
-//   - a touch of a block at stamp p writes stamps[slot] = p and log[p] = slot,
+// of the last H steps, the controller's load window and the current and next
+// prompt chains.  Each worker's cached blocks live in HBM as an
+// open-addressing table of 16-byte slots (key, stamp) plus a ring log of
+// touches:
+//   - a touch of a block at stamp p writes slot.stamp = p and log[p] = slot,
 //     so stamps are log positions and recency order is log order;
-//   - a log record p is live iff stamps[log[p]] == p; eviction pops the log
-//     head, skipping stale records, and tombstones the slot (stamp kTomb);
+//   - a log record p is live iff the stamp of slot log[p] still equals p;
+//     eviction pops the log head, skipping stale records, and tombstones the
+//     slot (stamp kTomb);
 //   - when tombstones or the log fill up, the live records are compacted,
 //     re-stamped in order and re-inserted into a cleared table.
-// A route: stage the chain in LDS; every worker's longest cached prefix by a
-// wavefront-wide search (lanes probe 64 positions per round); fp32 cost per
-// worker; argmin by a wavefront min over packed (cost, worker) keys; then the
-// chosen worker inserts/touches all P blocks in parallel (stamps assigned in
-// reverse block order) and evicts the oldest live records.
+// A route: every wavefront finds the longest cached prefix of the chain on
+// its workers (all of its workers' probes in flight together; a round probes
+// 64 spread positions, the next round the sub-interval holding the first
+// miss); wavefront 0 turns the overlaps into fp32 costs and takes the min of
+// packed (cost, worker) keys; all threads touch/insert the chosen worker's P
+// blocks in parallel (stamps in reverse block order) and evict the oldest live
+// records.  The next route's chain is loaded into registers while the current
+// route runs.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -24,9 +29,10 @@ namespace rk {
 
 constexpr int NT = 256;
 constexpr int NW = NT / 64;
+constexpr int PF = 8;      // chain blocks per thread prefetched for the next route
 
 struct EpArgs {
-    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode;
+    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, prefetch;
     const rk_episode_params* params;
     const int64_t* turn_off;
     const int32_t* turn_blocks;
@@ -36,7 +42,7 @@ struct EpArgs {
     unsigned char* ws;
     EpisodeLayout L;
     int32_t* status;
-    uint32_t lds_chain, lds_w, lds_inflight, lds_step, lds_u;
+    uint32_t lds_chain0, lds_chain1, lds_w, lds_key, lds_inflight, lds_step, lds_u;
 };
 
 struct EpShared {
@@ -69,84 +75,155 @@ __device__ __forceinline__ int32_t block_scan(bool flag, int32_t* wtot, int32_t&
     return off + rank;
 }
 
-// Barrier after global-memory writes of the workgroup.  All waves of a
-// workgroup share one CU, so the workgroup-scope release/acquire of the
-// barrier is enough for them to see each other's stores and atomics.
-__device__ __forceinline__ void block_sync_global()
+__device__ __forceinline__ void load_slot(const Slot* p, uint64_t& key, uint32_t& stamp)
 {
-    __syncthreads();
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    key = (uint64_t)v.x | ((uint64_t)v.y << 32);
+    stamp = v.z;
 }
 
-__device__ __forceinline__ bool cached(const uint64_t* __restrict__ tk, const uint32_t* __restrict__ ts,
-                                       uint64_t smask, uint64_t h)
+// Membership test finishing a walk whose first two slots are already loaded.
+__device__ __forceinline__ bool finish_lookup(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
+                                              uint64_t k0, uint32_t st0, uint64_t k1, uint32_t st1)
 {
-    uint64_t s = h & smask;
-    for (uint64_t n = 0; n <= smask; ++n) {
-        const uint64_t k = tk[s];
+    if (k0 == kEmpty) return false;
+    if (k0 == h && st0 != kTomb) return true;
+    if (k1 == kEmpty) return false;
+    if (k1 == h && st1 != kTomb) return true;
+    s = (s + 2) & smask;
+    for (uint64_t n = 2; n <= smask; ++n) {
+        uint64_t k;
+        uint32_t st;
+        load_slot(t + s, k, st);
         if (k == kEmpty) return false;
-        if (k == h && ts[s] != kTomb) return true;
+        if (k == h && st != kTomb) return true;
         s = (s + 1) & smask;
     }
     return false;
 }
 
-// Longest cached prefix with every worker's cache prefix-closed along the
-// chain: a round probes 64 evenly spread positions of the open interval
-// (lo, hi) and keeps the sub-interval where the first miss lies; the last
-// round probes every remaining position.  Wavefront-uniform result.
-__device__ int32_t wave_prefix_search(const uint64_t* s_chain, int32_t P, const uint64_t* tk,
-                                      const uint32_t* ts, uint64_t smask)
+#ifndef RK_FULL_PROBE
+#define RK_FULL_PROBE 64
+#endif
+#ifndef RK_FANOUT_SQRT
+#define RK_FANOUT_SQRT 0
+#endif
+constexpr int32_t kFullProbe = RK_FULL_PROBE;   // intervals this wide are probed position by position
+
+// Positions sampled in a round over an interval of `span` > kFullProbe blocks,
+// at most 64 so that the next interval fits one round when span <= 64 * 64.
+__device__ __forceinline__ int32_t fanout(int32_t span)
 {
-    const int lane = threadIdx.x & 63;
-    int32_t lo = 0, hi = P;   // blocks < lo are cached; block hi is not (or hi == P)
-    while (hi - lo > 64) {
-        const int64_t span = hi - lo;
-        const int32_t q = lo + (int32_t)(((int64_t)(lane + 1) * span) / 64) - 1;
-        const bool hit = cached(tk, ts, smask, s_chain[q]);
-        const unsigned long long miss = __ballot(!hit);
-        if (miss == 0ull) return hi;
-        const int t = __ffsll((unsigned long long)miss) - 1;
-        const int32_t qt = lo + (int32_t)(((int64_t)(t + 1) * span) / 64) - 1;
-        const int32_t qp = t == 0 ? lo - 1 : lo + (int32_t)(((int64_t)t * span) / 64) - 1;
-        lo = qp + 1;
-        hi = qt;
+    if (RK_FANOUT_SQRT) {
+        int32_t f = (int32_t)ceilf(sqrtf((float)span));
+        f = f < 4 ? 4 : f;
+        f = f > 64 ? 64 : f;
+        return (span + f - 1) / f > 64 ? 64 : f;
     }
-    const int32_t n = hi - lo;
-    const bool valid = lane < n;
-    const bool hit = valid ? cached(tk, ts, smask, s_chain[lo + lane]) : true;
-    const unsigned long long miss = __ballot(valid && !hit);
-    return miss ? lo + __ffsll((unsigned long long)miss) - 1 : hi;
+    return 64;
 }
 
-// Longest cached prefix for arbitrary caches: scan from block 0, 64 per round.
-__device__ int32_t wave_prefix_scan(const uint64_t* s_chain, int32_t P, const uint64_t* tk,
-                                    const uint32_t* ts, uint64_t smask)
+// Longest cached prefix of the staged chain on the workers j = j0, j0 + NW, ...
+// handled by this wavefront.  Every round issues, per lane, one probe (two
+// adjacent slots) for each unresolved worker before any result is used, so
+// all of the wavefront's probes are in flight together.
+//   PREFIX mode (caches prefix-closed along the chain): while an interval is
+//   wider than 64 a round probes 64 evenly spread positions and keeps the
+//   sub-interval holding the first miss; the last round probes every position.
+//   SCAN mode: rounds probe blocks [lo, lo + 64) from block 0 on.
+template <int JPW>
+__device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, int32_t W, const Slot* slots,
+                              uint64_t S, int mode, int32_t* s_ov)
 {
     const int lane = threadIdx.x & 63;
-    for (int32_t lo = 0; lo < P; lo += 64) {
-        const int32_t n = min(64, P - lo);
-        const bool valid = lane < n;
-        const bool hit = valid ? cached(tk, ts, smask, s_chain[lo + lane]) : true;
-        const unsigned long long miss = __ballot(valid && !hit);
-        if (miss) return lo + __ffsll((unsigned long long)miss) - 1;
+    const uint64_t smask = S - 1;
+    int32_t lo[JPW], hi[JPW];
+    uint32_t open = 0;
+#pragma unroll
+    for (int jj = 0; jj < JPW; ++jj) {
+        lo[jj] = 0;
+        hi[jj] = P;
+        if (j0 + jj * NW < W) open |= 1u << jj;
     }
-    return P;
+    while (open) {
+        uint64_t hk[JPW], k0[JPW], k1[JPW], sh0[JPW];
+        uint32_t st0[JPW], st1[JPW];
+        int32_t q[JPW];
+        bool valid[JPW];
+#pragma unroll
+        for (int jj = 0; jj < JPW; ++jj) {
+            valid[jj] = false;
+            if (!((open >> jj) & 1u)) continue;
+            const int32_t span = hi[jj] - lo[jj];
+            if (mode == RK_PROBE_PREFIX && span > kFullProbe) {
+                const int32_t f = fanout(span);
+                q[jj] = lo[jj] + (int32_t)(((int64_t)(lane + 1) * span) / f) - 1;
+                valid[jj] = lane < f;
+            } else {
+                q[jj] = lo[jj] + lane;
+                valid[jj] = q[jj] < hi[jj];
+            }
+            if (valid[jj]) {
+                const Slot* t = slots + (uint64_t)(j0 + jj * NW) * S;
+                hk[jj] = s_chain[q[jj]];
+                sh0[jj] = hk[jj] & smask;
+                load_slot(t + sh0[jj], k0[jj], st0[jj]);
+                load_slot(t + ((sh0[jj] + 1) & smask), k1[jj], st1[jj]);
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < JPW; ++jj) {
+            if (!((open >> jj) & 1u)) continue;
+            bool hit = true;
+            if (valid[jj]) {
+                const Slot* t = slots + (uint64_t)(j0 + jj * NW) * S;
+                hit = finish_lookup(t, smask, hk[jj], sh0[jj], k0[jj], st0[jj], k1[jj], st1[jj]);
+            }
+            const unsigned long long miss = __ballot(valid[jj] && !hit);
+            const int32_t span = hi[jj] - lo[jj];
+            int32_t o = -1;
+            if (mode == RK_PROBE_PREFIX && span > kFullProbe) {
+                if (miss == 0ull) {
+                    o = hi[jj];
+                } else {
+                    const int32_t f = fanout(span);
+                    const int t = __ffsll(miss) - 1;
+                    const int32_t qt = lo[jj] + (int32_t)(((int64_t)(t + 1) * span) / f) - 1;
+                    const int32_t qp = t == 0 ? lo[jj] - 1 : lo[jj] + (int32_t)(((int64_t)t * span) / f) - 1;
+                    lo[jj] = qp + 1;
+                    hi[jj] = qt;
+                    if (hi[jj] == lo[jj]) o = lo[jj];
+                }
+            } else if (mode == RK_PROBE_PREFIX) {
+                o = miss ? lo[jj] + __ffsll(miss) - 1 : hi[jj];
+            } else {
+                if (miss) o = lo[jj] + __ffsll(miss) - 1;
+                else if (lo[jj] + 64 >= hi[jj]) o = hi[jj];
+                else lo[jj] += 64;
+            }
+            if (o >= 0) {
+                open &= ~(1u << jj);
+                if (lane == 0) s_ov[j0 + jj * NW] = o;
+            }
+        }
+    }
 }
 
 // Find the live slot of h, or claim an empty slot for it.  Concurrent callers
 // insert distinct keys; a failed claim moves on along the probe sequence.
-__device__ __forceinline__ uint64_t insert_or_touch(uint64_t* __restrict__ tk, const uint32_t* __restrict__ ts,
-                                                   uint64_t smask, uint64_t h, int& inserted, int32_t* status)
+__device__ __forceinline__ uint64_t insert_or_touch(Slot* __restrict__ t, uint64_t smask, uint64_t h, int& inserted,
+                                                   int32_t* status)
 {
     inserted = 0;
     uint64_t s = h & smask;
     for (uint64_t n = 0; n <= smask; ++n) {
-        const uint64_t k = __hip_atomic_load(&tk[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const uint64_t k = __hip_atomic_load(&t[s].key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const uint32_t st = t[s].stamp;
         if (k == h) {
-            if (ts[s] != kTomb) return s;
+            if (st != kTomb) return s;
         } else if (k == kEmpty) {
             uint64_t prev = kEmpty;
-            if (__hip_atomic_compare_exchange_strong(&tk[s], &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+            if (__hip_atomic_compare_exchange_strong(&t[s].key, &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                                      __HIP_MEMORY_SCOPE_WORKGROUP)) {
                 inserted = 1;
                 return s;
@@ -159,6 +236,35 @@ __device__ __forceinline__ uint64_t insert_or_touch(uint64_t* __restrict__ tk, c
     return ~0ull;
 }
 
+// Same result as insert_or_touch, with one memory round trip in the usual
+// case.  A block the overlap search found cached is looked up in its first
+// two slots.  A block past the overlap is claimed directly at its home slot:
+// slots never return to empty between compactions, so an empty home slot
+// proves the key is absent.  Anything else falls back to the full walk.
+__device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t smask, uint64_t h, bool cached_hint,
+                                                 int& inserted, int32_t* status)
+{
+    const uint64_t s = h & smask;
+    inserted = 0;
+    if (cached_hint) {
+        uint64_t k0, k1;
+        uint32_t st0, st1;
+        load_slot(t + s, k0, st0);
+        load_slot(t + ((s + 1) & smask), k1, st1);
+        if (k0 == h && st0 != kTomb) return s;
+        if (k1 == h && st1 != kTomb) return (s + 1) & smask;
+    } else {
+        uint64_t prev = kEmpty;
+        if (__hip_atomic_compare_exchange_strong(&t[s].key, &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP)) {
+            inserted = 1;
+            return s;
+        }
+    }
+    return insert_or_touch(t, smask, h, inserted, status);
+}
+
+template <int JPW>
 __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -168,14 +274,15 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     const rk_episode_params prm = a.params[e];
     const int32_t W = a.W;
 
-    uint64_t* s_chain = (uint64_t*)(smem + a.lds_chain);
+    uint64_t* s_cur = (uint64_t*)(smem + a.lds_chain0);     // chain of the current route
+    uint64_t* s_nxt = (uint64_t*)(smem + a.lds_chain1);     // chain of the next route (prefetched)
     int32_t* s_A = (int32_t*)(smem + a.lds_w);
     uint32_t* s_head = (uint32_t*)(s_A + W);
     uint32_t* s_tail = s_head + W;
     int32_t* s_live = (int32_t*)(s_tail + W);
     int32_t* s_used = s_live + W;
     int32_t* s_ov = s_used + W;
-    float* s_cost = (float*)(s_ov + W);
+    uint64_t* s_key = (uint64_t*)(smem + a.lds_key);       // packed (cost, worker) per worker
     int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // in-flight routes: worker
     int32_t* s_stP = s_stw + a.max_inflight;               //                   prompt blocks
     int32_t* s_stc = s_stP + a.max_inflight;               //                   conversation
@@ -196,8 +303,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     const int64_t gc0 = prm.conv_begin;
 
     unsigned char* ws = a.ws + (size_t)e * a.L.per_episode;
-    uint64_t* g_keys = (uint64_t*)(ws + a.L.off_keys);
-    uint32_t* g_stamps = (uint32_t*)(ws + a.L.off_stamps);
+    Slot* g_slots = (Slot*)(ws + a.L.off_slots);
     uint32_t* g_log = (uint32_t*)(ws + a.L.off_log);
     uint64_t* g_scratch = (uint64_t*)(ws + a.L.off_scratch);
     int32_t* g_queue = (int32_t*)(ws + a.L.off_queue);
@@ -207,7 +313,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     const uint64_t scratch_cap = (uint64_t)a.cache + (uint64_t)a.max_blocks;
 
     // ---- initial state: empty caches, idle workers, every first turn queued
-    for (uint64_t i = tid; i < (uint64_t)W * S; i += NT) g_keys[i] = kEmpty;
+    {
+        uint4* z = reinterpret_cast<uint4*>(g_slots);
+        const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+        for (uint64_t i = tid; i < (uint64_t)W * S; i += NT) z[i] = zero;
+    }
     if (tid < W) {
         s_A[tid] = 0;
         s_head[tid] = 0;
@@ -235,13 +345,31 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         sh.ins = 0;
         sh.digest = 0;
     }
-    block_sync_global();
+    __syncthreads();
 
     const int32_t qcap = n_conv + 1;
-    int64_t t = 0;                       // routes done (uniform)
-    int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};   // thread 0
-    int64_t u_sum = 0;                   // thread 0
-    bool prev_active = false;            // thread 0
+    int64_t t = 0;                                 // routes done (uniform)
+    int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};     // thread 0
+    int64_t u_sum = 0;                             // thread 0
+    bool prev_active = false;                      // thread 0
+
+    // thread 0: prompt, chain base and effective overlap weight of route r of the step
+    auto setup = [&](int32_t sbase, int32_t r) {
+        bool active = false;
+        if (prm.controller && t >= prm.ctrl_window)
+            active = (int64_t)prm.ctrl_den * u_sum >
+                     (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
+        float w = prm.w_ov;
+        if (active) {
+            w = fminf(prm.w_ov, prm.ctrl_w_ov);
+            tot[3] += 1;
+            if (!prev_active) tot[4] += 1;
+        }
+        prev_active = active;
+        sh.w_eff = w;
+        sh.P = s_stP[sbase + r];
+        sh.cbase = s_stcb[r];
+    };
 
     for (int64_t s = 0;; ++s) {
         const int32_t slot = (int32_t)(s % H);
@@ -266,7 +394,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 pushed += total;
             }
             if (tid == 0 && pushed) sh.qsize += pushed;
-            block_sync_global();
+            __syncthreads();
         }
         // ---- how many requests this step routes
         if (tid == 0) {
@@ -277,7 +405,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             s_stepn[slot] = sh.n_route;
             if (sh.n_route > 0) tot[5] = s + 1;
             sh.pop_base = sh.qhead;
-            sh.qhead = (sh.qhead + sh.n_route) % (n_conv + 1);
+            sh.qhead = (sh.qhead + sh.n_route) % qcap;
             sh.qsize -= sh.n_route;
         }
         __syncthreads();
@@ -305,55 +433,56 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             s_stt[r] = (int32_t)turn;
             s_stcb[r] = cb;
         }
-        block_sync_global();
+        __syncthreads();
+        if (tid == 0 && n > 0) setup(sb, 0);
+        __syncthreads();
+        bool staged = false;     // the current chain buffer already holds route r's chain (uniform)
 
         for (int32_t r = 0; r < n; ++r) {
-            // ---- route setup: prompt, controller
-            if (tid == 0) {
-                bool active = false;
-                if (prm.controller && t >= prm.ctrl_window)
-                    active = (int64_t)prm.ctrl_den * u_sum >
-                             (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
-                float w = prm.w_ov;
-                if (active) {
-                    w = fminf(prm.w_ov, prm.ctrl_w_ov);
-                    tot[3] += 1;
-                    if (!prev_active) tot[4] += 1;
-                }
-                prev_active = active;
-                sh.w_eff = w;
-                sh.P = s_stP[sb + r];
-                sh.cbase = s_stcb[r];
-            }
-            __syncthreads();
             const int32_t P = sh.P;
-            {
+            if (!staged) {
                 const uint64_t* gch = a.chains + sh.cbase;
-                for (int32_t k = tid; k < P; k += NT) s_chain[k] = gch[k];
+                for (int32_t k = tid; k < P; k += NT) s_cur[k] = gch[k];
+                __syncthreads();
             }
-            __syncthreads();
+            // ---- prefetch the next route's chain into registers
+            uint64_t pf[PF];
+            int32_t Pn = 0;
+            bool prefetch = false;
+            if (a.prefetch && r + 1 < n) {
+                Pn = s_stP[sb + r + 1];
+                prefetch = Pn <= NT * PF;
+                if (prefetch) {
+                    const uint64_t* gch = a.chains + s_stcb[r + 1];
+#pragma unroll
+                    for (int i = 0; i < PF; ++i) {
+                        const int32_t k = tid + i * NT;
+                        pf[i] = k < Pn ? gch[k] : 0ull;
+                    }
+                }
+            }
             // ---- longest cached prefix on every worker
-            for (int32_t j = wave; j < W; j += NW) {
-                const uint64_t* tk = g_keys + (uint64_t)j * S;
-                const uint32_t* ts = g_stamps + (uint64_t)j * S;
-                const int32_t o = a.probe_mode == RK_PROBE_SCAN ? wave_prefix_scan(s_chain, P, tk, ts, smask)
-                                                                : wave_prefix_search(s_chain, P, tk, ts, smask);
-                if (lane == 0) s_ov[j] = o;
-            }
+            wave_overlaps<JPW>(s_cur, P, wave, W, g_slots, S, a.probe_mode, s_ov);
             __syncthreads();
-            // ---- cost of every worker, then argmin
+            // ---- cost of every worker and argmin (wavefront 0)
             const int64_t row = prm.out_base + t;
-            if (tid < W) {
-                const float c = route_cost(sh.w_eff, prm.w_act, prm.w_sat, prm.cap_blocks, P, s_ov[tid], s_A[tid]);
-                s_cost[tid] = c;
-                if (a.out.overlap) a.out.overlap[row * W + tid] = s_ov[tid];
-                if (a.out.cost) a.out.cost[row * W + tid] = c;
-            }
-            __syncthreads();
             if (wave == 0) {
-                uint64_t key = lane < W ? argmin_key(s_cost[lane], lane) : ~0ull;
-                key = wave_min_u64(key);
+                if (lane < W) {
+                    const float c = route_cost(sh.w_eff, prm.w_act, prm.w_sat, prm.cap_blocks, P, s_ov[lane],
+                                               s_A[lane]);
+                    if (a.out.overlap) a.out.overlap[row * W + lane] = s_ov[lane];
+                    if (a.out.cost) a.out.cost[row * W + lane] = c;
+                    s_key[lane] = argmin_key(c, lane);
+                }
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
                 if (lane == 0) {
+                    uint64_t key = s_key[0];
+                    for (int32_t j = 1; j < W; ++j) {
+                        const uint64_t kj = s_key[j];
+                        key = kj < key ? kj : key;
+                    }
                     const int32_t sg = (int32_t)(uint32_t)(key & 0xffffffffu);
                     sh.sigma = sg;
                     const uint64_t ins_max = (uint64_t)(P - s_ov[sg]);
@@ -364,8 +493,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             }
             __syncthreads();
             const int32_t sg = sh.sigma;
-            uint64_t* tk = g_keys + (uint64_t)sg * S;
-            uint32_t* ts = g_stamps + (uint64_t)sg * S;
+            Slot* tk = g_slots + (uint64_t)sg * S;
             uint32_t* tl = g_log + (uint64_t)sg * R;
 
             // ---- compaction: re-stamp the live records in order into a cleared table
@@ -378,8 +506,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     uint64_t key = 0;
                     if (pos < tail) {
                         const uint32_t sl = tl[pos & rmask];
-                        live = sl < S && ts[sl] == pos;
-                        if (live) key = tk[sl];
+                        if (sl < S) {
+                            uint32_t st;
+                            load_slot(tk + sl, key, st);
+                            live = st == pos;
+                        }
                     }
                     int32_t total;
                     const int32_t rank = block_scan(live, sh.wtot, total);
@@ -390,16 +521,20 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
                     cnt = (int32_t)scratch_cap;
                 }
-                block_sync_global();
-                for (uint64_t i = tid; i < S; i += NT) tk[i] = kEmpty;
-                block_sync_global();
+                __syncthreads();
+                {
+                    uint4* z = reinterpret_cast<uint4*>(tk);
+                    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+                    for (uint64_t i = tid; i < S; i += NT) z[i] = zero;
+                }
+                __syncthreads();
                 for (int32_t q = tid; q < cnt; q += NT) {
                     int ins;
-                    const uint64_t sl = insert_or_touch(tk, ts, smask, g_scratch[q], ins, a.status);
-                    if (sl != ~0ull) ts[sl] = (uint32_t)q;
+                    const uint64_t sl = insert_or_touch(tk, smask, g_scratch[q], ins, a.status);
+                    if (sl != ~0ull) tk[sl].stamp = (uint32_t)q;
                     tl[(uint32_t)q & rmask] = (uint32_t)sl;
                 }
-                block_sync_global();
+                __syncthreads();
                 if (tid == 0) {
                     s_head[sg] = 0;
                     s_tail[sg] = (uint32_t)cnt;
@@ -413,17 +548,18 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             {
                 const uint32_t tail = s_tail[sg];
                 int my_ins = 0;
+                const int32_t o_sg = s_ov[sg];
                 for (int32_t k = tid; k < P; k += NT) {
                     int ins;
                     const uint32_t stamp = tail + (uint32_t)(P - 1 - k);
-                    const uint64_t sl = insert_or_touch(tk, ts, smask, s_chain[k], ins, a.status);
-                    if (sl != ~0ull) ts[sl] = stamp;
+                    const uint64_t sl = touch_hinted(tk, smask, s_cur[k], k < o_sg, ins, a.status);
+                    if (sl != ~0ull) tk[sl].stamp = stamp;
                     tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
                     my_ins += ins;
                 }
                 if (my_ins) atomicAdd(&sh.ins, my_ins);
             }
-            block_sync_global();
+            __syncthreads();
             if (tid == 0) {
                 s_tail[sg] += (uint32_t)P;
                 s_live[sg] += sh.ins;
@@ -445,19 +581,23 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 const uint32_t pos = head + (uint32_t)tid;
                 uint32_t sl = 0;
                 bool live = false;
+                uint64_t key = 0;
                 if (pos < tail) {
                     sl = tl[pos & rmask];
-                    live = sl < S && ts[sl] == pos;
+                    if (sl < S) {
+                        uint32_t st;
+                        load_slot(tk + sl, key, st);
+                        live = st == pos;
+                    }
                 }
                 int32_t total;
                 const int32_t rank = block_scan(live, sh.wtot, total);
                 if (live && rank < rem) {
-                    const uint64_t key = tk[sl];
-                    ts[sl] = kTomb;
+                    tk[sl].stamp = kTomb;
                     atomicAdd(&sh.digest, (unsigned long long)mix64(key));
                     if (rank == rem - 1) sh.new_head = pos + 1;
                 }
-                block_sync_global();
+                __syncthreads();
                 if (tid == 0) {
                     if (total >= rem) {
                         s_head[sg] = sh.new_head;
@@ -473,7 +613,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 }
                 __syncthreads();
             }
-            // ---- load, controller sample, outputs
+            // ---- load, controller sample, outputs; set up the next route
             if (tid == 0) {
                 s_A[sg] += P;
                 s_stw[sb + r] = sg;
@@ -491,13 +631,27 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 if (a.out.route_blocks) a.out.route_blocks[row] = P;
                 if (a.out.evict_count) a.out.evict_count[row] = sh.ev;
                 if (a.out.evict_digest) a.out.evict_digest[row] = sh.digest;
-                if (a.out.last_hash) a.out.last_hash[row] = P > 0 ? s_chain[P - 1] : 0ull;
+                if (a.out.last_hash) a.out.last_hash[row] = P > 0 ? s_cur[P - 1] : 0ull;
                 tot[0] += P - s_ov[sg];
                 tot[1] += sh.ev;
                 tot[2] += P;
                 tot[6] += s_ov[sg];
+                ++t;
+                if (r + 1 < n) setup(sb, r + 1);
+            } else {
+                ++t;
             }
-            ++t;
+            if (prefetch) {
+#pragma unroll
+                for (int i = 0; i < PF; ++i) {
+                    const int32_t k = tid + i * NT;
+                    if (k < Pn) s_nxt[k] = pf[i];
+                }
+                uint64_t* x = s_cur;
+                s_cur = s_nxt;
+                s_nxt = x;
+            }
+            staged = prefetch;
             __syncthreads();
         }
     }
@@ -570,14 +724,37 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.ws = (unsigned char*)workspace;
     a.L = L;
     a.status = st;
-    size_t o = 0;
-    a.lds_chain = (uint32_t)o;    o = align_up(o + (size_t)b->max_blocks * 8, 16);
-    a.lds_w = (uint32_t)o;        o = align_up(o + (size_t)b->W * 7 * 4, 16);
-    a.lds_inflight = (uint32_t)o; o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
-    a.lds_step = (uint32_t)o;     o = align_up(o + (size_t)b->max_routes_per_step * 12, 16);
-    a.lds_u = (uint32_t)o;        o = align_up(o + (size_t)b->max_ctrl_window * 8, 16);
-    if (o > 60 * 1024)
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 60 KiB", o);
-    hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), o, (hipStream_t)stream, a);
+    const size_t chain_bytes = align_up((size_t)b->max_blocks * 8, 16);
+    size_t rest = 0;
+    rest = align_up(rest + (size_t)b->W * 6 * 4, 16);
+    const size_t off_key = rest;
+    rest = align_up(rest + (size_t)b->W * 8, 16);
+    const size_t off_inflight = rest;
+    rest = align_up(rest + (size_t)b->max_inflight * 4 * 4, 16);
+    const size_t off_step = rest;
+    rest = align_up(rest + (size_t)b->max_routes_per_step * 12, 16);
+    const size_t off_u = rest;
+    rest = align_up(rest + (size_t)b->max_ctrl_window * 8, 16);
+    const size_t limit = 60 * 1024;
+    a.prefetch = 2 * chain_bytes + rest <= limit;
+    const size_t chains_total = (a.prefetch ? 2 : 1) * chain_bytes;
+    if (chains_total + rest > limit)
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 60 KiB",
+                    chains_total + rest);
+    a.lds_chain0 = 0;
+    a.lds_chain1 = a.prefetch ? (uint32_t)chain_bytes : 0;
+    a.lds_w = (uint32_t)chains_total;
+    a.lds_key = (uint32_t)(chains_total + off_key);
+    a.lds_inflight = (uint32_t)(chains_total + off_inflight);
+    a.lds_step = (uint32_t)(chains_total + off_step);
+    a.lds_u = (uint32_t)(chains_total + off_u);
+    const size_t lds = chains_total + rest;
+    const int jpw = (b->W + NW - 1) / NW;
+    hipStream_t s = (hipStream_t)stream;
+    if (jpw <= 1) hipLaunchKernelGGL(episode_kernel<1>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
+    else if (jpw <= 2) hipLaunchKernelGGL(episode_kernel<2>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
+    else if (jpw <= 4) hipLaunchKernelGGL(episode_kernel<4>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
+    else if (jpw <= 8) hipLaunchKernelGGL(episode_kernel<8>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
+    else hipLaunchKernelGGL(episode_kernel<16>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
     return hip_check(hipGetLastError(), "rk_simulate_episodes launch");
 }

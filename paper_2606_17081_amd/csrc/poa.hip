@@ -9,7 +9,9 @@
 // weighs the minimum of that over rows on a.  A path starts with the new row
 // on some worker and ends on a worker with spare capacity; Bellman-Ford over
 // the W nodes finds it (no negative cycles, since the partial assignment is
-// optimal).  One wavefront solves one window.
+// optimal).  Edge minima are kept across rows and recomputed only for workers
+// whose rows changed on the last path.  One wavefront solves one window; the
+// window's matrix lives in LDS when it fits, else in the workspace.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -28,15 +30,19 @@ struct PoaArgs {
     rk_poa_params p;
     double* selfish;
     double* coord;
-    float* cm;            // workspace: frozen matrix, row-major by route row
+    float* cm;            // workspace: frozen matrix, row-major by route row (when not in LDS)
     int32_t* status;
-    uint32_t lds_int, lds_dbl;
+    uint32_t lds_int, lds_dbl, lds_mat;
 };
 
+__device__ __forceinline__ double dinf() { return __longlong_as_double(0x7ff0000000000000ll); }
+
+template <bool LDSMAT>
 __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ int32_t sh_bad;
+    __shared__ int32_t sh_hops;
     const int tid = threadIdx.x;
     const int32_t W = a.W;
     int32_t* s_n = (int32_t*)(smem + a.lds_int);   // [W] window counts of the greedy assignment
@@ -46,9 +52,12 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
     float* s_base = (float*)(s_np + W);              // [W]
     int32_t* s_mem = (int32_t*)(s_base + W);         // [W * kmax] rows held by each worker
     int32_t* s_assign = s_mem + W * a.kmax;          // [max_window]
-    double* s_dist = (double*)(smem + a.lds_dbl);    // [W]
-    double* s_nd = s_dist + W;                       // [W]
-    double* s_e = s_nd + W;                          // [W * W] edge weights a -> b
+    int32_t* s_pos = s_assign + a.max_window;        // [max_window] index of a row in its worker's list
+    int32_t* s_er = s_pos + a.max_window;            // [W * W] row realising each edge weight
+    int32_t* s_hx = s_er + W * W;                    // [W + 2] path moves: losing worker
+    int32_t* s_hy = s_hx + W + 2;                    // [W + 2]                gaining worker
+    int32_t* s_hr = s_hy + W + 2;                    // [W + 2]                row
+    double* s_e = (double*)(smem + a.lds_dbl);       // [W * W] edge weights a -> b
 
     for (int32_t w = blockIdx.x; w < a.n_windows; w += gridDim.x) {
         const int64_t r0 = a.win_off[w], r1 = a.win_off[w + 1];
@@ -79,11 +88,13 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             }
             continue;
         }
+        float* cm = LDSMAT ? (float*)(smem + a.lds_mat) : a.cm + r0 * W;
         // ---- frozen matrix
         for (int32_t j = tid; j < W; j += PT) {
             s_n[j] = 0;
             s_cnt[j] = 0;
         }
+        for (int32_t pq = tid; pq < W * W; pq += PT) s_e[pq] = dinf();
         if (tid == 0) sh_bad = 0;
         __syncthreads();
         for (int32_t i = tid; i < m; i += PT) {
@@ -100,7 +111,6 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             s_base[j] = __fadd_rn(__fadd_rn(__fmul_rn(a.p.a, (float)s_n[j]), a.p.b), __fdiv_rn(a.p.d, gb));
         }
         __syncthreads();
-        float* cm = a.cm + r0 * W;
         for (int64_t idx = tid; idx < (int64_t)m * W; idx += PT) {
             const int64_t i = idx / W;
             const int32_t j = (int32_t)(idx - i * W);
@@ -124,88 +134,137 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             for (int32_t i = 0; i < m; ++i) s += (double)cm[(int64_t)i * W + a.route_worker[r0 + i]];
             a.selfish[w] = s;
         }
-        // ---- successive shortest paths
+        // ---- successive shortest paths (lane y < W stands for worker y)
+        for (int32_t pq = tid; pq < W * W; pq += PT) s_er[pq] = -1;
+        __syncthreads();
         for (int32_t i = 0; i < m; ++i) {
-            for (int32_t pq = tid; pq < W * W; pq += PT) {
-                const int32_t x = pq / W, y = pq - x * W;
-                double best = __longlong_as_double(0x7ff0000000000000ll);   // +inf
-                if (x != y) {
-                    for (int32_t k = 0; k < s_cnt[x]; ++k) {
-                        const int64_t r = s_mem[x * a.kmax + k];
-                        const double v = (double)cm[r * W + y] - (double)cm[r * W + x];
-                        best = v < best ? v : best;
-                    }
-                }
-                s_e[pq] = best;
-            }
-            for (int32_t j = tid; j < W; j += PT) {
-                s_dist[j] = (double)cm[(int64_t)i * W + j];
-                s_pred[j] = -1;
-            }
-            __syncthreads();
+            // Bellman-Ford over the workers, wavefront-synchronous: lane y keeps
+            // dist[y] and pred[y] in registers and reads the others by shuffles
+            double dist = tid < W ? (double)cm[(int64_t)i * W + tid] : dinf();
+            int32_t pred = -1;
             for (int32_t round = 0;; ++round) {
-                for (int32_t y = tid; y < W; y += PT) {
-                    double nd = s_dist[y];
-                    int32_t pb = s_pred[y];
-                    for (int32_t x = 0; x < W; ++x) {
-                        const double v = s_dist[x] + s_e[x * W + y];
+                double nd = dist;
+                int32_t pb = pred;
+                for (int32_t x = 0; x < W; ++x) {
+                    const double dx = __shfl(dist, x, 64);
+                    if (tid < W) {
+                        const double v = dx + s_e[x * W + tid];
                         if (v < nd) {
                             nd = v;
                             pb = x;
                         }
                     }
-                    s_nd[y] = nd;
-                    s_np[y] = pb;
                 }
-                __syncthreads();
-                bool changed = false;   // identical in every thread
-                for (int32_t y = 0; y < W; ++y) changed |= s_nd[y] != s_dist[y] || s_np[y] != s_pred[y];
-                __syncthreads();
-                for (int32_t y = tid; y < W; y += PT) {
-                    s_dist[y] = s_nd[y];
-                    s_pred[y] = s_np[y];
-                }
-                __syncthreads();
+                const bool changed = __ballot(nd != dist || pb != pred) != 0ull;
+                dist = nd;
+                pred = pb;
                 if (!changed) break;
                 if (round > W + 1) {
                     if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
                     break;
                 }
             }
+            // target: least distance among workers with spare capacity (lowest index on ties)
+            int32_t t = -1;
+            {
+                double bd = tid < W && s_cnt[tid] < K ? dist : dinf();
+                int32_t bj = tid < W && s_cnt[tid] < K ? tid : 0x7fffffff;
+                for (int off = 32; off > 0; off >>= 1) {
+                    const double od = __shfl_xor(bd, off, 64);
+                    const int32_t oj = __shfl_xor(bj, off, 64);
+                    if (od < bd || (od == bd && oj < bj)) {
+                        bd = od;
+                        bj = oj;
+                    }
+                }
+                t = bj;
+            }
+            if (tid < W) s_pred[tid] = pred;
+            __syncthreads();
             if (tid == 0) {
-                int32_t t = -1;
-                for (int32_t j = 0; j < W; ++j)
-                    if (s_cnt[j] < K && (t < 0 || s_dist[j] < s_dist[t])) t = j;
                 // walk the path back from the target, moving one row per edge
                 int32_t y = t, hops = 0;
                 while (s_pred[y] >= 0 && hops <= W) {
                     const int32_t x = s_pred[y];
-                    const double ew = s_e[x * W + y];
-                    int32_t kk = 0;
-                    for (; kk < s_cnt[x]; ++kk) {
-                        const int64_t r = s_mem[x * a.kmax + kk];
-                        if ((double)cm[r * W + y] - (double)cm[r * W + x] == ew) break;
+                    const int32_t r = s_er[x * W + y];
+                    int32_t kk = r >= 0 ? s_pos[r] : -1;
+                    if (kk < 0 || kk >= s_cnt[x] || s_mem[x * a.kmax + kk] != r || s_cnt[y] >= a.kmax) {
+                        atomicOr(a.status, RK_DEV_NO_CONVERGE);
+                        break;
                     }
-                    if (kk == s_cnt[x]) { atomicOr(a.status, RK_DEV_NO_CONVERGE); break; }
-                    if (s_cnt[y] >= a.kmax) { atomicOr(a.status, RK_DEV_NO_CONVERGE); break; }
-                    const int32_t r = s_mem[x * a.kmax + kk];
-                    s_mem[x * a.kmax + kk] = s_mem[x * a.kmax + s_cnt[x] - 1];
+                    const int32_t last = s_mem[x * a.kmax + s_cnt[x] - 1];
+                    s_mem[x * a.kmax + kk] = last;
+                    s_pos[last] = kk;
                     s_cnt[x] -= 1;
                     s_mem[y * a.kmax + s_cnt[y]] = r;
+                    s_pos[r] = s_cnt[y];
                     s_cnt[y] += 1;
                     s_assign[r] = y;
+                    s_hx[hops] = x;        // x lost r ...
+                    s_hy[hops] = y;        // ... and y gained it
+                    s_hr[hops] = r;
                     y = x;
                     ++hops;
                 }
                 if (s_cnt[y] < a.kmax) {
                     s_mem[y * a.kmax + s_cnt[y]] = i;
+                    s_pos[i] = s_cnt[y];
                     s_cnt[y] += 1;
                 } else {
                     atomicOr(a.status, RK_DEV_NO_CONVERGE);
                 }
                 s_assign[i] = y;
+                s_hx[hops] = -1;           // no loss
+                s_hy[hops] = y;            // the new row's worker gained row i
+                s_hr[hops] = i;
+                sh_hops = hops + 1;
             }
             __syncthreads();
+            // ---- edge maintenance, e[x][z] = min over rows r on x of c[r][z] - c[r][x]:
+            // an edge whose argmin row left x is recomputed over x's rows (all
+            // lanes scan, then a wavefront min); a gained row is folded in.
+            const int32_t nev = sh_hops;
+            for (int32_t h = 0; h < nev; ++h) {
+                const int32_t x = s_hx[h], r = s_hr[h];
+                if (x < 0) continue;
+                for (int32_t z = 0; z < W; ++z) {
+                    if (z == x || s_er[x * W + z] != r) continue;
+                    double best = dinf();
+                    int32_t brow = 0x7fffffff;
+                    for (int32_t k = tid; k < s_cnt[x]; k += PT) {
+                        const int32_t q = s_mem[x * a.kmax + k];
+                        const double v = (double)cm[(int64_t)q * W + z] - (double)cm[(int64_t)q * W + x];
+                        if (v < best || (v == best && q < brow)) {
+                            best = v;
+                            brow = q;
+                        }
+                    }
+                    for (int off = 32; off > 0; off >>= 1) {
+                        const double ob = __shfl_xor(best, off, 64);
+                        const int32_t orow = __shfl_xor(brow, off, 64);
+                        if (ob < best || (ob == best && orow < brow)) {
+                            best = ob;
+                            brow = orow;
+                        }
+                    }
+                    if (tid == 0) {
+                        s_e[x * W + z] = best;
+                        s_er[x * W + z] = brow == 0x7fffffff ? -1 : brow;
+                    }
+                    __syncthreads();
+                }
+            }
+            for (int32_t h = 0; h < nev; ++h) {
+                const int32_t y = s_hy[h], r = s_hr[h];
+                if (tid < W && tid != y) {
+                    const double v = (double)cm[(int64_t)r * W + tid] - (double)cm[(int64_t)r * W + y];
+                    if (v < s_e[y * W + tid]) {
+                        s_e[y * W + tid] = v;
+                        s_er[y * W + tid] = r;
+                    }
+                }
+                __syncthreads();
+            }
         }
         if (tid == 0 && a.coord) {
             double s = 0.0;
@@ -290,13 +349,20 @@ extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_
         a.status = st;
         size_t o = 0;
         a.lds_int = 0;
-        o = align_up(((size_t)W * 5 + (size_t)W * a.kmax + (size_t)max_window) * 4, 16);
+        o = align_up(((size_t)W * 5 + (size_t)W * a.kmax + 2 * (size_t)max_window + (size_t)W * W +
+                      3 * ((size_t)W + 2)) * 4, 16);
         a.lds_dbl = (uint32_t)o;
-        o += ((size_t)W * 2 + (size_t)W * W) * 8;
-        if (o > 60 * 1024)
+        o = align_up(o + (size_t)W * W * 8, 16);
+        const size_t limit = 60 * 1024;
+        if (o > limit)
             return fail(RK_EUNSUPPORTED, "rk_poa_estimate: %zu bytes of LDS per window exceed 60 KiB", o);
+        const size_t mat = (size_t)max_window * (size_t)W * sizeof(float);
+        const bool lds_mat = o + mat <= limit;
+        a.lds_mat = (uint32_t)o;
+        if (lds_mat) o += mat;
         unsigned grid = (unsigned)(n_windows < 65536 ? n_windows : 65536);
-        hipLaunchKernelGGL(poa_window_kernel, dim3(grid), dim3(PT), o, s, a);
+        if (lds_mat) hipLaunchKernelGGL(poa_window_kernel<true>, dim3(grid), dim3(PT), o, s, a);
+        else hipLaunchKernelGGL(poa_window_kernel<false>, dim3(grid), dim3(PT), o, s, a);
         int rc = hip_check(hipGetLastError(), "rk_poa_estimate window launch");
         if (rc) return rc;
     }
