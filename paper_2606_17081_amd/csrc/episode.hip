@@ -46,7 +46,7 @@ struct EpArgs {
 };
 
 struct EpShared {
-    int32_t n_route, done, sigma, P, rebuild, ins, remaining, ev, qhead, qsize, pop_base;
+    int32_t n_route, done, sigma, P, rebuild, ins, remaining, ev, qhead, qsize, pop_base, lcp;
     uint32_t new_head;
     float w_eff;
     int64_t cbase;
@@ -82,58 +82,56 @@ __device__ __forceinline__ void load_slot(const Slot* p, uint64_t& key, uint32_t
     stamp = v.z;
 }
 
-// Membership test finishing a walk whose first two slots are already loaded.
+constexpr int kWin = 4;    // slots read by one lookup (a run of this length is rare at load <= 0.5)
+
+// Membership test finishing a walk whose first kWin slots (from s) are loaded.
 __device__ __forceinline__ bool finish_lookup(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
-                                              uint64_t k0, uint32_t st0, uint64_t k1, uint32_t st1)
+                                              const uint64_t* k, const uint32_t* st)
 {
-    if (k0 == kEmpty) return false;
-    if (k0 == h && st0 != kTomb) return true;
-    if (k1 == kEmpty) return false;
-    if (k1 == h && st1 != kTomb) return true;
-    s = (s + 2) & smask;
-    for (uint64_t n = 2; n <= smask; ++n) {
-        uint64_t k;
-        uint32_t st;
-        load_slot(t + s, k, st);
-        if (k == kEmpty) return false;
-        if (k == h && st != kTomb) return true;
+#pragma unroll
+    for (int i = 0; i < kWin; ++i) {
+        if (k[i] == kEmpty) return false;
+        if (k[i] == h && st[i] != kTomb) return true;
+    }
+    s = (s + kWin) & smask;
+    for (uint64_t n = kWin; n <= smask; ++n) {
+        uint64_t kk;
+        uint32_t ss;
+        load_slot(t + s, kk, ss);
+        if (kk == kEmpty) return false;
+        if (kk == h && ss != kTomb) return true;
         s = (s + 1) & smask;
     }
     return false;
 }
 
-#ifndef RK_FULL_PROBE
-#define RK_FULL_PROBE 64
-#endif
-#ifndef RK_FANOUT_SQRT
-#define RK_FANOUT_SQRT 0
-#endif
-constexpr int32_t kFullProbe = RK_FULL_PROBE;   // intervals this wide are probed position by position
+constexpr int32_t kFullProbe = 64;   // intervals this wide are probed position by position
 
-// Positions sampled in a round over an interval of `span` > kFullProbe blocks,
-// at most 64 so that the next interval fits one round when span <= 64 * 64.
+// Positions sampled in a round over an interval of `span` > kFullProbe blocks:
+// about sqrt(span), so two rounds cover span with few probes, and at most 64
+// so that the next interval fits one round when span <= 64 * 64.
 __device__ __forceinline__ int32_t fanout(int32_t span)
 {
-    if (RK_FANOUT_SQRT) {
-        int32_t f = (int32_t)ceilf(sqrtf((float)span));
-        f = f < 4 ? 4 : f;
-        f = f > 64 ? 64 : f;
-        return (span + f - 1) / f > 64 ? 64 : f;
-    }
-    return 64;
+    int32_t f = (int32_t)ceilf(sqrtf((float)span));
+    f = f < 4 ? 4 : f;
+    f = f > 64 ? 64 : f;
+    return span > 64 * f ? 64 : f;     // the next interval, at most ceil(span / f) wide, fits 64
 }
 
-// Longest cached prefix of the staged chain on the workers j = j0, j0 + NW, ...
-// handled by this wavefront.  Every round issues, per lane, one probe (two
-// adjacent slots) for each unresolved worker before any result is used, so
-// all of the wavefront's probes are in flight together.
+// Longest cached prefix of the staged chain on the workers j = jfirst,
+// jfirst + jstride, ... (< W) handled by this wavefront; worker jspecial's
+// search starts at block lo_special (its blocks below are known cached).
+// Every round issues, per lane, one probe (two adjacent slots) for each
+// unresolved worker before any result is used, so all of the wavefront's
+// probes are in flight together.
 //   PREFIX mode (caches prefix-closed along the chain): while an interval is
-//   wider than 64 a round probes 64 evenly spread positions and keeps the
+//   wider than kFullProbe a round probes spread positions and keeps the
 //   sub-interval holding the first miss; the last round probes every position.
 //   SCAN mode: rounds probe blocks [lo, lo + 64) from block 0 on.
 template <int JPW>
-__device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, int32_t W, const Slot* slots,
-                              uint64_t S, int mode, int32_t* s_ov)
+__device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t jfirst, int32_t jstride, int32_t W,
+                              const Slot* slots, uint64_t S, int mode, int32_t* s_ov, int32_t jspecial,
+                              int32_t lo_special)
 {
     const int lane = threadIdx.x & 63;
     const uint64_t smask = S - 1;
@@ -141,13 +139,14 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, in
     uint32_t open = 0;
 #pragma unroll
     for (int jj = 0; jj < JPW; ++jj) {
-        lo[jj] = 0;
+        const int32_t j = jfirst + jj * jstride;
+        lo[jj] = j == jspecial ? lo_special : 0;
         hi[jj] = P;
-        if (j0 + jj * NW < W) open |= 1u << jj;
+        if (j < W) open |= 1u << jj;
     }
     while (open) {
-        uint64_t hk[JPW], k0[JPW], k1[JPW], sh0[JPW];
-        uint32_t st0[JPW], st1[JPW];
+        uint64_t hk[JPW], kw[JPW][kWin], sh0[JPW];
+        uint32_t sw[JPW][kWin];
         int32_t q[JPW];
         bool valid[JPW];
 #pragma unroll
@@ -156,19 +155,19 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, in
             if (!((open >> jj) & 1u)) continue;
             const int32_t span = hi[jj] - lo[jj];
             if (mode == RK_PROBE_PREFIX && span > kFullProbe) {
-                const int32_t f = fanout(span);
-                q[jj] = lo[jj] + (int32_t)(((int64_t)(lane + 1) * span) / f) - 1;
-                valid[jj] = lane < f;
+                const uint32_t f = (uint32_t)fanout(span);
+                q[jj] = lo[jj] + (int32_t)(((uint32_t)(lane + 1) * (uint32_t)span) / f) - 1;
+                valid[jj] = (uint32_t)lane < f;
             } else {
                 q[jj] = lo[jj] + lane;
                 valid[jj] = q[jj] < hi[jj];
             }
             if (valid[jj]) {
-                const Slot* t = slots + (uint64_t)(j0 + jj * NW) * S;
+                const Slot* t = slots + (uint64_t)(jfirst + jj * jstride) * S;
                 hk[jj] = s_chain[q[jj]];
                 sh0[jj] = hk[jj] & smask;
-                load_slot(t + sh0[jj], k0[jj], st0[jj]);
-                load_slot(t + ((sh0[jj] + 1) & smask), k1[jj], st1[jj]);
+#pragma unroll
+                for (int i = 0; i < kWin; ++i) load_slot(t + ((sh0[jj] + i) & smask), kw[jj][i], sw[jj][i]);
             }
         }
 #pragma unroll
@@ -176,8 +175,8 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, in
             if (!((open >> jj) & 1u)) continue;
             bool hit = true;
             if (valid[jj]) {
-                const Slot* t = slots + (uint64_t)(j0 + jj * NW) * S;
-                hit = finish_lookup(t, smask, hk[jj], sh0[jj], k0[jj], st0[jj], k1[jj], st1[jj]);
+                const Slot* t = slots + (uint64_t)(jfirst + jj * jstride) * S;
+                hit = finish_lookup(t, smask, hk[jj], sh0[jj], kw[jj], sw[jj]);
             }
             const unsigned long long miss = __ballot(valid[jj] && !hit);
             const int32_t span = hi[jj] - lo[jj];
@@ -186,10 +185,11 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, in
                 if (miss == 0ull) {
                     o = hi[jj];
                 } else {
-                    const int32_t f = fanout(span);
+                    // lane t holds the first missing sample; lanes t and t-1 computed its bounds
                     const int t = __ffsll(miss) - 1;
-                    const int32_t qt = lo[jj] + (int32_t)(((int64_t)(t + 1) * span) / f) - 1;
-                    const int32_t qp = t == 0 ? lo[jj] - 1 : lo[jj] + (int32_t)(((int64_t)t * span) / f) - 1;
+                    const int32_t qt = __shfl(q[jj], t, 64);
+                    const int32_t qprev = __shfl(q[jj], t > 0 ? t - 1 : 0, 64);
+                    const int32_t qp = t == 0 ? lo[jj] - 1 : qprev;
                     lo[jj] = qp + 1;
                     hi[jj] = qt;
                     if (hi[jj] == lo[jj]) o = lo[jj];
@@ -203,7 +203,7 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t j0, in
             }
             if (o >= 0) {
                 open &= ~(1u << jj);
-                if (lane == 0) s_ov[j0 + jj * NW] = o;
+                if (lane == 0) s_ov[jfirst + jj * jstride] = o;
             }
         }
     }
@@ -236,29 +236,53 @@ __device__ __forceinline__ uint64_t insert_or_touch(Slot* __restrict__ t, uint64
     return ~0ull;
 }
 
-// Same result as insert_or_touch, with one memory round trip in the usual
-// case.  A block the overlap search found cached is looked up in its first
-// two slots.  A block past the overlap is claimed directly at its home slot:
-// slots never return to empty between compactions, so an empty home slot
-// proves the key is absent.  Anything else falls back to the full walk.
+// Same result as insert_or_touch, in one memory round trip in the usual
+// case.  A block the overlap search found cached is looked up in a window of
+// kWin slots.  For a block past the overlap, the claim of its home slot is
+// issued together with the loads of the next kWin-1 slots: slots never return
+// to empty between compactions, so an empty home slot proves the key absent,
+// and an occupied one usually leaves a free slot in the window.  Anything else
+// falls back to the full walk.
 __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t smask, uint64_t h, bool cached_hint,
                                                  int& inserted, int32_t* status)
 {
     const uint64_t s = h & smask;
     inserted = 0;
+    uint64_t k[kWin];
+    uint32_t st[kWin];
     if (cached_hint) {
-        uint64_t k0, k1;
-        uint32_t st0, st1;
-        load_slot(t + s, k0, st0);
-        load_slot(t + ((s + 1) & smask), k1, st1);
-        if (k0 == h && st0 != kTomb) return s;
-        if (k1 == h && st1 != kTomb) return (s + 1) & smask;
+#pragma unroll
+        for (int i = 0; i < kWin; ++i) load_slot(t + ((s + i) & smask), k[i], st[i]);
+#pragma unroll
+        for (int i = 0; i < kWin; ++i)
+            if (k[i] == h && st[i] != kTomb) return (s + i) & smask;
     } else {
         uint64_t prev = kEmpty;
-        if (__hip_atomic_compare_exchange_strong(&t[s].key, &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_WORKGROUP)) {
+        const bool won = __hip_atomic_compare_exchange_strong(&t[s].key, &prev, h, __ATOMIC_RELAXED,
+                                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+        for (int i = 1; i < kWin; ++i) load_slot(t + ((s + i) & smask), k[i], st[i]);
+        if (won) {
             inserted = 1;
             return s;
+        }
+        if (prev != h) {           // home holds another key: look further in the window
+#pragma unroll
+            for (int i = 1; i < kWin; ++i) {
+                const uint64_t si = (s + i) & smask;
+                if (k[i] == h) {
+                    if (st[i] != kTomb) return si;
+                    continue;
+                }
+                if (k[i] != kEmpty) continue;
+                uint64_t pi = kEmpty;
+                if (__hip_atomic_compare_exchange_strong(&t[si].key, &pi, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                    inserted = 1;
+                    return si;
+                }
+                break;             // lost a race for the slot: walk from the start
+            }
         }
     }
     return insert_or_touch(t, smask, h, inserted, status);
@@ -267,6 +291,7 @@ __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t 
 template <int JPW>
 __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
 {
+    constexpr bool kPipe = JPW <= 4;      // two wavefronts then search up to 8 workers each
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ EpShared sh;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -281,7 +306,8 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     uint32_t* s_tail = s_head + W;
     int32_t* s_live = (int32_t*)(s_tail + W);
     int32_t* s_used = s_live + W;
-    int32_t* s_ov = s_used + W;
+    int32_t* s_ovc = s_used + W;                          // overlaps of the current route
+    int32_t* s_ovn = s_ovc + W;                            // overlaps of the next route (lookahead)
     uint64_t* s_key = (uint64_t*)(smem + a.lds_key);       // packed (cost, worker) per worker
     int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // in-flight routes: worker
     int32_t* s_stP = s_stw + a.max_inflight;               //                   prompt blocks
@@ -348,7 +374,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     __syncthreads();
 
     const int32_t qcap = n_conv + 1;
-    int64_t t = 0;                                 // routes done (uniform)
+    int32_t t = 0;                                 // routes done (uniform)
     int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};     // thread 0
     int64_t u_sum = 0;                             // thread 0
     bool prev_active = false;                      // thread 0
@@ -371,8 +397,8 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         sh.cbase = s_stcb[r];
     };
 
-    for (int64_t s = 0;; ++s) {
-        const int32_t slot = (int32_t)(s % H);
+    for (int32_t s = 0;; ++s) {
+        const int32_t slot = s % H;
         const int32_t sb = slot * rps;
         // ---- release the routes of step s - H; queue their conversations' next turns
         if (s >= H) {
@@ -399,7 +425,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         // ---- how many requests this step routes
         if (tid == 0) {
             int64_t inflight = 0;
-            for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[(int32_t)((s - k) % H)];
+            for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[(s - k) % H];
             sh.done = sh.qsize == 0 && inflight == 0;
             sh.n_route = sh.done ? 0 : min(rps, sh.qsize);
             s_stepn[slot] = sh.n_route;
@@ -436,41 +462,59 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         __syncthreads();
         if (tid == 0 && n > 0) setup(sb, 0);
         __syncthreads();
-        bool staged = false;     // the current chain buffer already holds route r's chain (uniform)
+        // Pipelining: while worker sigma_r absorbs route r's blocks, waves 2-3
+        // already search route r+1's cached prefixes.  Workers other than
+        // sigma_r are unchanged by route r.  On sigma_r, route r+1's blocks
+        // shared with route r's chain (their common prefix) are cached after
+        // the update, and its later blocks are chained hashes route r cannot
+        // insert, so a search over those positions only is exact while the
+        // update runs.  Evictions by route r are corrected by a new search.
+        const bool can_pipe = kPipe && a.probe_mode == RK_PROBE_PREFIX;
+        bool nxt_ready = false;    // s_nxt holds route r+1's chain (uniform)
+        bool have_ov = false;      // s_ovc holds route r's overlaps (uniform)
+        {
+            const uint64_t* gch = a.chains + sh.cbase;
+            for (int32_t k = tid; k < sh.P; k += NT) s_cur[k] = gch[k];
+            __syncthreads();
+        }
 
         for (int32_t r = 0; r < n; ++r) {
             const int32_t P = sh.P;
-            if (!staged) {
-                const uint64_t* gch = a.chains + sh.cbase;
-                for (int32_t k = tid; k < P; k += NT) s_cur[k] = gch[k];
-                __syncthreads();
+            const int32_t Pn = r + 1 < n ? s_stP[sb + r + 1] : 0;
+            uint64_t last_h = 0;    // thread 0: h_{P-1} of route r
+            if (r + 1 < n && !nxt_ready) {
+                const uint64_t* gch = a.chains + s_stcb[r + 1];
+                for (int32_t k = tid; k < Pn; k += NT) s_nxt[k] = gch[k];
             }
-            // ---- prefetch the next route's chain into registers
+            // ---- prefetch the chain of route r+2 into registers
             uint64_t pf[PF];
-            int32_t Pn = 0;
+            int32_t P2 = 0;
             bool prefetch = false;
-            if (a.prefetch && r + 1 < n) {
-                Pn = s_stP[sb + r + 1];
-                prefetch = Pn <= NT * PF;
+            if (a.prefetch && r + 2 < n) {
+                P2 = s_stP[sb + r + 2];
+                prefetch = P2 <= NT * PF;
                 if (prefetch) {
-                    const uint64_t* gch = a.chains + s_stcb[r + 1];
+                    const uint64_t* gch = a.chains + s_stcb[r + 2];
 #pragma unroll
                     for (int i = 0; i < PF; ++i) {
                         const int32_t k = tid + i * NT;
-                        pf[i] = k < Pn ? gch[k] : 0ull;
+                        pf[i] = k < P2 ? gch[k] : 0ull;
                     }
                 }
             }
-            // ---- longest cached prefix on every worker
-            wave_overlaps<JPW>(s_cur, P, wave, W, g_slots, S, a.probe_mode, s_ov);
+            // ---- longest cached prefix of route r on every worker (unless already known)
+            if (!have_ov) {
+                wave_overlaps<JPW>(s_cur, P, wave, NW, W, g_slots, S, a.probe_mode, s_ovc, -1, 0);
+            }
             __syncthreads();
-            // ---- cost of every worker and argmin (wavefront 0)
-            const int64_t row = prm.out_base + t;
+            const bool pipe = can_pipe && r + 1 < n;
+            // ---- cost of every worker and argmin (wavefront 0); common prefix with route r+1 (wavefront 1)
+            const int64_t row = prm.out_base + (int64_t)t;
             if (wave == 0) {
                 if (lane < W) {
-                    const float c = route_cost(sh.w_eff, prm.w_act, prm.w_sat, prm.cap_blocks, P, s_ov[lane],
+                    const float c = route_cost(sh.w_eff, prm.w_act, prm.w_sat, prm.cap_blocks, P, s_ovc[lane],
                                                s_A[lane]);
-                    if (a.out.overlap) a.out.overlap[row * W + lane] = s_ov[lane];
+                    if (a.out.overlap) a.out.overlap[row * W + lane] = s_ovc[lane];
                     if (a.out.cost) a.out.cost[row * W + lane] = c;
                     s_key[lane] = argmin_key(c, lane);
                 }
@@ -485,11 +529,24 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     }
                     const int32_t sg = (int32_t)(uint32_t)(key & 0xffffffffu);
                     sh.sigma = sg;
-                    const uint64_t ins_max = (uint64_t)(P - s_ov[sg]);
+                    last_h = P > 0 ? s_cur[P - 1] : 0ull;   // read before the buffer is reused
+                    const uint64_t ins_max = (uint64_t)(P - s_ovc[sg]);
                     sh.rebuild = ((uint64_t)s_used[sg] + ins_max > used_limit) ||
                                  ((uint64_t)(s_tail[sg] - s_head[sg]) + (uint64_t)P > R) ||
                                  (s_tail[sg] > 0x40000000u);
                 }
+            } else if (wave == 1 && pipe) {
+                const int32_t m = min(P, Pn);
+                int32_t l = m;
+                for (int32_t base = 0; base < m; base += 64) {
+                    const int32_t k = base + lane;
+                    const unsigned long long d = __ballot(k < m && s_cur[k] != s_nxt[k]);
+                    if (d) {
+                        l = base + __ffsll(d) - 1;
+                        break;
+                    }
+                }
+                if (lane == 0) sh.lcp = l;
             }
             __syncthreads();
             const int32_t sg = sh.sigma;
@@ -544,20 +601,27 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 __syncthreads();
             }
 
-            // ---- touch the prompt's blocks (block k gets stamp tail + P-1-k), inserting misses
+            // ---- touch route r's blocks (block k gets stamp tail + P-1-k), inserting misses;
+            //      with pipelining, waves 2-3 meanwhile search route r+1's overlaps
             {
-                const uint32_t tail = s_tail[sg];
-                int my_ins = 0;
-                const int32_t o_sg = s_ov[sg];
-                for (int32_t k = tid; k < P; k += NT) {
-                    int ins;
-                    const uint32_t stamp = tail + (uint32_t)(P - 1 - k);
-                    const uint64_t sl = touch_hinted(tk, smask, s_cur[k], k < o_sg, ins, a.status);
-                    if (sl != ~0ull) tk[sl].stamp = stamp;
-                    tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
-                    my_ins += ins;
+                const int32_t nupd = pipe ? NT / 2 : NT;
+                if (tid < nupd) {
+                    const uint32_t tail = s_tail[sg];
+                    const int32_t o_sg = s_ovc[sg];
+                    int my_ins = 0;
+                    for (int32_t k = tid; k < P; k += nupd) {
+                        int ins;
+                        const uint32_t stamp = tail + (uint32_t)(P - 1 - k);
+                        const uint64_t sl = touch_hinted(tk, smask, s_cur[k], k < o_sg, ins, a.status);
+                        if (sl != ~0ull) tk[sl].stamp = stamp;
+                        tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
+                        my_ins += ins;
+                    }
+                    if (my_ins) atomicAdd(&sh.ins, my_ins);
+                } else if constexpr (kPipe) {
+                    wave_overlaps<2 * JPW>(s_nxt, Pn, wave - NW / 2, NW / 2, W, g_slots, S, RK_PROBE_PREFIX, s_ovn,
+                                           sg, sh.lcp);
                 }
-                if (my_ins) atomicAdd(&sh.ins, my_ins);
             }
             __syncthreads();
             if (tid == 0) {
@@ -613,6 +677,12 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 }
                 __syncthreads();
             }
+            // ---- the lookahead search of sigma_r is void if route r evicted: search again
+            if (pipe && sh.ev > 0) {
+                if (wave == 0)
+                    wave_overlaps<1>(s_nxt, Pn, sg, 1, sg + 1, g_slots, S, RK_PROBE_PREFIX, s_ovn, -1, 0);
+                __syncthreads();
+            }
             // ---- load, controller sample, outputs; set up the next route
             if (tid == 0) {
                 s_A[sg] += P;
@@ -620,7 +690,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 if (prm.controller) {
                     int64_t u = 0;
                     for (int32_t j = 0; j < W; ++j) u += s_A[j];
-                    const int32_t pos = (int32_t)(t % prm.ctrl_window);
+                    const int32_t pos = t % prm.ctrl_window;
                     if (t >= prm.ctrl_window) u_sum -= s_u[pos];
                     s_u[pos] = u;
                     u_sum += u;
@@ -631,27 +701,34 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 if (a.out.route_blocks) a.out.route_blocks[row] = P;
                 if (a.out.evict_count) a.out.evict_count[row] = sh.ev;
                 if (a.out.evict_digest) a.out.evict_digest[row] = sh.digest;
-                if (a.out.last_hash) a.out.last_hash[row] = P > 0 ? s_cur[P - 1] : 0ull;
-                tot[0] += P - s_ov[sg];
+                if (a.out.last_hash) a.out.last_hash[row] = last_h;
+                tot[0] += P - s_ovc[sg];
                 tot[1] += sh.ev;
                 tot[2] += P;
-                tot[6] += s_ov[sg];
+                tot[6] += s_ovc[sg];
                 ++t;
                 if (r + 1 < n) setup(sb, r + 1);
             } else {
                 ++t;
             }
+            // route r's chain buffer now takes route r+2's chain; rotate the buffers
             if (prefetch) {
 #pragma unroll
                 for (int i = 0; i < PF; ++i) {
                     const int32_t k = tid + i * NT;
-                    if (k < Pn) s_nxt[k] = pf[i];
+                    if (k < P2) s_cur[k] = pf[i];
                 }
+            }
+            {
                 uint64_t* x = s_cur;
                 s_cur = s_nxt;
                 s_nxt = x;
+                int32_t* y = s_ovc;
+                s_ovc = s_ovn;
+                s_ovn = y;
             }
-            staged = prefetch;
+            nxt_ready = prefetch;
+            have_ov = pipe;
             __syncthreads();
         }
     }
@@ -726,7 +803,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.status = st;
     const size_t chain_bytes = align_up((size_t)b->max_blocks * 8, 16);
     size_t rest = 0;
-    rest = align_up(rest + (size_t)b->W * 6 * 4, 16);
+    rest = align_up(rest + (size_t)b->W * 7 * 4, 16);
     const size_t off_key = rest;
     rest = align_up(rest + (size_t)b->W * 8, 16);
     const size_t off_inflight = rest;
