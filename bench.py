@@ -31,6 +31,7 @@ PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
     "episode_kernel": ["paper_2606_17081_amd/csrc/episode.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
     "score_kernel": ["paper_2606_17081_amd/csrc/score.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
+    "score_index_kernel": ["paper_2606_17081_amd/csrc/index.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
     "poa_window_kernel": ["paper_2606_17081_amd/csrc/poa.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
     "block_fnv_kernel": ["paper_2606_17081_amd/csrc/abi.hip", "paper_2606_17081_amd/csrc/rk_internal.h"],
 }
@@ -108,6 +109,22 @@ def score_algorithmic_bytes(inst) -> float:
     return float(tables + chains + offs + outs)
 
 
+def score_index_algorithmic_bytes(inst, overlap: np.ndarray) -> float:
+    """Bytes the global-index scorer needs per launch, each access counted once
+    at its natural width: every chain hash once, the offsets and loads, the
+    outputs, and one 16-byte index slot per position a first-miss scan of the
+    union must see: M_i + [M_i < P_i] positions, M_i = max_j o_ij (positions
+    past M_i are cached nowhere, one all-miss probe closes the scan)."""
+    B, W = inst.B, inst.W
+    P = np.diff(inst.chain_off).astype(np.float64)
+    M = overlap.max(axis=1).astype(np.float64) if W > 0 else np.zeros(B)
+    index = 16.0 * np.sum(M + (M < P))
+    chains = inst.chains.size * 8
+    offs = (B + 1) * 8 + W * 4
+    outs = B * W * (4 + 4) + B * 4
+    return float(index + chains + offs + outs)
+
+
 # ---------------------------------------------------------------- timing helpers
 
 class KernelTimer:
@@ -154,12 +171,22 @@ def cpu_baseline(workload, seeds, threads):
                 episodes_per_s=len(specs) / dt, seconds=dt)
 
 
+def index_log2_slots(n_keys: int) -> int:
+    b = 4
+    while (1 << b) < 2 * n_keys:
+        b += 1
+    return b
+
+
 def scoring_bench(torch, rk, wl, stream, steps):
-    """Time rk_route_score_batch on the 65,536 x 64 snapshot workload."""
+    """Time the 65,536 x 64 snapshot scoring on the per-worker tables
+    (rk_route_score_batch) and on the global block index
+    (rk_route_score_index) built from the same key sets."""
     log("generating the 65,536 x 64 scoring instance")
     inst = wl.scoring_instance(seed=0)
     up = rk.to_device
-    tables = rk.table_build(up(inst.keys), inst.key_off, inst.log2_slots)
+    keys = up(inst.keys)
+    tables = rk.table_build(keys, inst.key_off, inst.log2_slots)
     chains, chain_off, active = up(inst.chains), up(inst.chain_off), up(inst.active)
     ov = torch.empty((inst.B, inst.W), dtype=torch.int32, device="cuda")
     co = torch.empty((inst.B, inst.W), dtype=torch.float32, device="cuda")
@@ -175,13 +202,46 @@ def scoring_bench(torch, rk, wl, stream, steps):
     assert rk.device_status(reset=True) == 0
     salg = score_algorithmic_bytes(inst)
     ach = salg / (ms * 1e-3) / 1e9
-    log(f"scoring: {ms:.4f} ms, {inst.B * inst.W / (ms * 1e-3):.4g} scorings/s, {ach:.1f} GB/s algorithmic")
-    return {"workload": "scoring 65536 requests x 64 workers, 2^20-slot tables at load 0.5, chains of 16..512",
+    log(f"scoring (tables): {ms:.4f} ms, {inst.B * inst.W / (ms * 1e-3):.4g} scorings/s, {ach:.1f} GB/s algorithmic")
+    ov_ref = ov.cpu().numpy()
+    del tables
+    torch.cuda.empty_cache()
+
+    lg = index_log2_slots(int(inst.key_off[-1]))
+    tb = KernelTimer(torch, stream)
+    index = torch.empty(2 << lg, dtype=torch.int64, device="cuda")
+    for _ in range(3):
+        with tb:
+            rk.index_build(keys, inst.key_off, lg, index=index)
+    for _ in range(3):
+        rk.route_score_index(chains, chain_off, index, lg, active, overlap=ov, cost=co, argmin=am)
+    ti = KernelTimer(torch, stream)
+    for _ in range(max(steps, 10)):
+        with ti:
+            rk.route_score_index(chains, chain_off, index, lg, active, overlap=ov, cost=co, argmin=am)
+    ms_i = ti.mean_ms()
+    assert rk.device_status(reset=True) == 0
+    ov_i = ov.cpu().numpy()
+    assert np.array_equal(ov_i, ov_ref), "index and table scorers disagree"
+    ialg = score_index_algorithmic_bytes(inst, ov_i)
+    ach_i = ialg / (ms_i * 1e-3) / 1e9
+    log(f"scoring (index): {ms_i:.4f} ms, {inst.B * inst.W / (ms_i * 1e-3):.4g} scorings/s, "
+        f"{ach_i:.1f} GB/s algorithmic; index build {tb.mean_ms():.3f} ms")
+    wl_name = "scoring 65536 requests x 64 workers, 2^20-slot tables at load 0.5, chains of 16..512"
+    return {"workload": wl_name,
             "scorings_per_s": inst.B * inst.W / (ms * 1e-3), "avg_ms": round(ms, 4),
             "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": round(ach, 3),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 6),
                          "traffic": measured_traffic("score_kernel", "scoring"),
-                         "algorithmic_bytes": salg}}
+                         "algorithmic_bytes": salg},
+            "index": {"workload": wl_name + "; the same key sets in one global block index of "
+                                            f"2^{lg} 16-byte slots",
+                      "scorings_per_s": inst.B * inst.W / (ms_i * 1e-3), "avg_ms": round(ms_i, 4),
+                      "index_build_ms": round(tb.mean_ms(), 4),
+                      "roofline": {"kernel": "score_index_kernel", "bound": "hbm", "achieved": round(ach_i, 3),
+                                   "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach_i / HBM_PEAK_GBS, 6),
+                                   "traffic": measured_traffic("score_index_kernel", "scoring"),
+                                   "algorithmic_bytes": ialg}}}
 
 
 def main():

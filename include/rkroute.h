@@ -155,6 +155,44 @@ int rk_route_score_batch(int32_t B, int32_t W, const uint64_t* chains, const int
                          int32_t* overlap_out, float* cost_out, int32_t* argmin_out,
                          void* stream);
 
+/* ------------------------------------------------------------ global block index
+ * The router's index over all workers (the global radix tree of the Smart
+ * Router, background section on the Dynamo architecture; best_worker in
+ * Alg. adaptive-router).  A chained hash names a whole prefix, so the tree is
+ * held as one open-addressing table of 2^log2_slots 16-byte slots
+ *   struct { uint64_t key; uint64_t mask; }   (key 0 = empty slot)
+ * where bit j of mask is set when worker j caches the block.  A key's home
+ * slot is (key & (2^log2_slots - 1)); collisions probe linearly upward with
+ * wrap-around.  Worker count is limited to 64 by the mask.
+ *
+ * rk_index_build -- clear the index and insert worker j's keys
+ * keys[key_off[j] .. key_off[j+1]) for j < W (the same key sets as
+ * rk_table_build; duplicates once, zero keys skipped with RK_DEV_ZERO_KEY).
+ *   W          1..64 (else RK_EUNSUPPORTED)
+ *   keys       uint64 [key_off[W]], device
+ *   key_off    int64 [W+1], HOST pointer, non-decreasing
+ *   index      device buffer of 16 << log2_slots bytes, 16-byte aligned, owned by the caller
+ *   log2_slots 4..31
+ * Returns RK_ETABLEFULL when key_off[W] - key_off[0] exceeds half the slots.
+ */
+int rk_index_build(int32_t W, const uint64_t* keys, const int64_t* key_off /* host */,
+                   void* index, int32_t log2_slots, void* stream);
+
+/*
+ * rk_route_score_index -- rk_route_score_batch against the global index
+ * instead of per-worker tables: same o_ij, cost_ij and argmin_i definitions,
+ * same output layouts, same probe modes (RK_PROBE_PREFIX requires every
+ * worker's set to be prefix-closed along every chain; RK_PROBE_SCAN takes
+ * any sets).  The index is read-only.
+ *   B, W          requests (>= 0) and workers (1..64, else RK_EUNSUPPORTED)
+ *   chains, chain_off, active_blocks, params, outputs as in rk_route_score_batch
+ *   index         rk_index_build's layout, 2^log2_slots slots
+ */
+int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains, const int64_t* chain_off,
+                         const void* index, int32_t log2_slots, const int32_t* active_blocks,
+                         rk_cost_params params, int32_t probe_mode,
+                         int32_t* overlap_out, float* cost_out, int32_t* argmin_out, void* stream);
+
 /* ------------------------------------------------------------ routing episodes
  * One episode is a sequential greedy routing run (best-response dynamics,
  * Section 4.3) over the conversations conv_begin .. conv_begin+n_conv-1 of the

@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librkroute.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["abi.hip", "score.hip", "episode.hip", "poa.hip"]
+SOURCES = ["abi.hip", "score.hip", "index.hip", "episode.hip", "poa.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

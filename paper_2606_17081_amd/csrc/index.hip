@@ -1,0 +1,348 @@
+// index.hip -- the router's global block index (block hash -> set of workers
+// caching that block) and batched routing-cost evaluation against it.
+//
+// The router the paper studies answers "which workers hold this prefix" from
+// one index over all workers (the global radix tree of the Smart Router in the
+// Dynamo architecture background section, queried by best_worker in
+// Alg. adaptive-router).  Chained block hashes name prefixes uniquely, so the radix tree
+// becomes one open-addressing table of 16-byte slots (key, worker mask) and a
+// single probe answers membership on all W <= 64 workers at once.  Scoring a
+// request then costs a few lane-parallel probe rounds per request instead of
+// a search per (request, worker) pair:
+//   - PREFIX mode (every worker's set is prefix-closed along the chains):
+//     worker masks along a chain only lose bits.  A coarse round (16
+//     samples) bounds the region [0, U) where any worker may still hold the
+//     chain, a second round samples it with 64 lanes (every position when
+//     U <= 64), and a third probes the inside of the sample intervals where
+//     some worker's bit disappears.  Worker j's overlap is the first
+//     position whose mask lacks bit j.
+//   - SCAN mode (any sets): positions from block 0 in rounds of 64; a
+//     running AND of the masks gives each worker's first miss exactly, and
+//     the scan stops once no worker is left.
+// One wavefront scores one request; lane j owns worker j's overlap and cost.
+#include <hip/hip_runtime.h>
+
+#include "rk_internal.h"
+
+namespace rk {
+
+struct __align__(16) IndexSlot {
+    uint64_t key;
+    uint64_t mask;
+};
+
+__device__ __forceinline__ void load_slot(const IndexSlot* t, uint64_t s, uint64_t& k, uint64_t& m)
+{
+    const uint4 v = *reinterpret_cast<const uint4*>(t + s);
+    k = (uint64_t)v.x | ((uint64_t)v.y << 32);
+    m = (uint64_t)v.z | ((uint64_t)v.w << 32);
+}
+
+// Worker mask of block hash h (0 when no worker holds it).  The first two
+// slots are read together; the walk continues one slot at a time.
+__device__ __forceinline__ uint64_t index_lookup(const IndexSlot* __restrict__ t, uint64_t smask, uint64_t h)
+{
+    uint64_t s = h & smask;
+    uint64_t k0, m0, k1, m1;
+    load_slot(t, s, k0, m0);
+    load_slot(t, (s + 1) & smask, k1, m1);
+    if (k0 == h) return m0;
+    if (k0 == kEmpty) return 0ull;
+    if (k1 == h) return m1;
+    if (k1 == kEmpty) return 0ull;
+    s = (s + 2) & smask;
+    for (uint64_t n = 2; n <= smask; ++n) {
+        uint64_t k, m;
+        load_slot(t, s, k, m);
+        if (k == h) return m;
+        if (k == kEmpty) return 0ull;
+        s = (s + 1) & smask;
+    }
+    return 0ull;
+}
+
+// Inclusive prefix AND of a 64-bit value across the wavefront's lanes.
+__device__ __forceinline__ uint64_t wave_prefix_and(uint64_t v)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t o = __shfl_up(v, off, 64);
+        if (lane >= off) v &= o;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_or_u64(uint64_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v |= __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Exclusive prefix sum across the wavefront; total receives the full sum.
+__device__ __forceinline__ int32_t wave_excl_sum(int32_t v, int32_t& total)
+{
+    const int lane = threadIdx.x & 63;
+    int32_t x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t o = __shfl_up(x, off, 64);
+        if (lane >= off) x += o;
+    }
+    total = __shfl(x, 63, 64);
+    return x - v;
+}
+
+// First index in [lo, hi) whose mask lacks bit j, for masks in which bit j
+// never comes back once cleared; hi if none.
+__device__ __forceinline__ int32_t first_clear(const uint64_t* m, int32_t lo, int32_t hi, int32_t j)
+{
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if ((m[mid] >> j) & 1ull) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// LDS writes of one wavefront made visible to the other lanes of that wavefront.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+constexpr int IWAVES = 4;    // wavefronts per workgroup
+
+struct IdxLds {
+    uint64_t m[64];          // masks of the current round (prefix ANDs in rounds 1-2)
+    int32_t q[64];           // second-round sample positions
+    int32_t ioff[65];        // start of each sample interval's positions in the third round
+};
+
+template <int MODE>
+__global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
+    int32_t B, int32_t W, const uint64_t* __restrict__ chains, const int64_t* __restrict__ chain_off,
+    const IndexSlot* __restrict__ index, int32_t log2_slots, const int32_t* __restrict__ active, rk_cost_params p,
+    int32_t* __restrict__ ov_out, float* __restrict__ cost_out, int32_t* __restrict__ am_out, int32_t* status)
+{
+    __shared__ IdxLds lds_all[IWAVES];
+    IdxLds& L = lds_all[threadIdx.x >> 6];
+    const int32_t lane = threadIdx.x & 63;
+    const int64_t nwaves = (int64_t)gridDim.x * IWAVES;
+    const uint64_t smask = (1ull << log2_slots) - 1;
+    const int32_t A = lane < W ? active[lane] : 0;
+    const uint64_t all = W == 64 ? ~0ull : ((1ull << W) - 1ull);
+
+    for (int64_t i = (int64_t)blockIdx.x * IWAVES + (threadIdx.x >> 6); i < B; i += nwaves) {
+        const int64_t c0 = chain_off[i], c1 = chain_off[i + 1];
+        int32_t P = 0;
+        if (c1 < c0 || c1 - c0 > 0x7fffffff) {
+            if (lane == 0) atomicOr(status, RK_DEV_BAD_OFFSETS);
+        } else {
+            P = (int32_t)(c1 - c0);
+        }
+        const uint64_t* h = chains + c0;
+        int32_t o = 0;   // lane j: overlap on worker j
+
+        if (MODE == RK_PROBE_SCAN) {
+            uint64_t carry = all;
+            bool done = false;
+            for (int32_t base = 0; base < P && carry != 0ull; base += 64) {
+                const int32_t n = min(64, P - base);
+                const uint64_t m = lane < n ? index_lookup(index, smask, h[base + lane]) : 0ull;
+                const uint64_t pa = wave_prefix_and(m) & carry;
+                L.m[lane] = pa;
+                wave_sync();
+                if (lane < W && !done) {
+                    const int32_t f = first_clear(L.m, 0, n, lane);
+                    o += f;
+                    done = f < n;
+                }
+                carry = __shfl(pa, n - 1, 64);
+                wave_sync();
+            }
+        } else {
+            // ---- round 1: every worker's first miss lies in [0, U)
+            int32_t U = P;
+            if (P > 64) {
+                const int32_t q1 = (int32_t)(((uint64_t)(lane + 1) * (uint64_t)P) >> 4) - 1;
+                const uint64_t m = lane < 16 ? index_lookup(index, smask, h[q1]) : all;
+                const uint64_t pa = wave_prefix_and(m & all);
+                const uint64_t z = __ballot(lane < 16 && pa == 0ull);
+                if (z) U = __shfl(q1, __ffsll((unsigned long long)z) - 1, 64) + 1;
+            }
+            // ---- round 2: every position of [0, U) when U <= 64, else 64 samples
+            const bool exact = U <= 64;
+            const int32_t nq = exact ? U : 64;
+            const int32_t q = exact ? lane : (int32_t)(((uint64_t)(lane + 1) * (uint64_t)U) >> 6) - 1;
+            const uint64_t m = lane < nq ? index_lookup(index, smask, h[q]) : 0ull;
+            L.m[lane] = wave_prefix_and(m & all);
+            L.q[lane] = q;
+            wave_sync();
+            const int32_t t = lane < W ? first_clear(L.m, 0, nq, lane) : nq;
+            if (exact) {
+                o = t;   // t == U only when U == P: every position is cached
+            } else {
+                // ---- round 3: worker j's first miss is in (q[t-1], q[t]]; probe the inside
+                const uint64_t need = wave_or_u64(lane < W && t < 64 ? 1ull << t : 0ull);
+                const int32_t qprev = lane == 0 ? -1 : L.q[lane - 1];
+                const int32_t width = ((need >> lane) & 1ull) ? q - qprev - 1 : 0;
+                int32_t total;
+                const int32_t off = wave_excl_sum(width, total);
+                L.ioff[lane] = off;
+                if (lane == 63) L.ioff[64] = total;
+                wave_sync();
+                const bool mine = lane < W && t < 64;
+                o = mine ? L.q[t] : P;
+                const int32_t a0 = mine ? L.ioff[t] : 0, a1 = mine ? L.ioff[t + 1] : 0;
+                const int32_t pbase = mine ? (t == 0 ? 0 : L.q[t - 1] + 1) : 0;
+                bool found = !mine;
+                for (int32_t b3 = 0; b3 < total; b3 += 64) {
+                    const int32_t idx = b3 + lane;
+                    uint64_t mm = 0ull;
+                    if (idx < total) {
+                        int32_t lo = 0, hi = 63;   // largest k with ioff[k] <= idx
+                        while (lo < hi) {
+                            const int32_t mid = (lo + hi + 1) >> 1;
+                            if (L.ioff[mid] <= idx) lo = mid;
+                            else hi = mid - 1;
+                        }
+                        const int32_t pos = (lo == 0 ? 0 : L.q[lo - 1] + 1) + (idx - L.ioff[lo]);
+                        mm = index_lookup(index, smask, h[pos]);
+                    }
+                    wave_sync();   // the previous chunk's masks have been read
+                    L.m[lane] = mm;
+                    wave_sync();
+                    if (!found) {
+                        const int32_t lo = max(a0, b3), hi = min(a1, b3 + 64);
+                        if (lo < hi) {
+                            const int32_t x = first_clear(L.m, lo - b3, hi - b3, lane) + b3;
+                            if (x < hi) {
+                                o = pbase + (x - a0);
+                                found = true;
+                            }
+                        }
+                    }
+                }
+            }
+            wave_sync();
+        }
+
+        uint64_t best = ~0ull;
+        if (lane < W) {
+            const float c = route_cost(p.w_ov, p.w_act, p.w_sat, p.cap_blocks, P, o, A);
+            if (ov_out) ov_out[i * W + lane] = o;
+            if (cost_out) cost_out[i * W + lane] = c;
+            best = argmin_key(c, lane);
+        }
+        best = wave_min_u64(best);
+        if (lane == 0 && am_out) am_out[i] = (int32_t)(uint32_t)(best & 0xffffffffu);
+    }
+}
+
+__global__ __launch_bounds__(256) void index_clear_kernel(IndexSlot* __restrict__ t, uint64_t n)
+{
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+        *reinterpret_cast<uint4*>(t + i) = zero;
+}
+
+__global__ __launch_bounds__(256) void index_insert_kernel(const uint64_t* __restrict__ keys, int64_t n, int32_t j,
+                                                           IndexSlot* __restrict__ t, uint64_t smask, int32_t* status)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const uint64_t key = keys[i];
+        if (key == kEmpty) {
+            atomicOr(status, RK_DEV_ZERO_KEY);
+            continue;
+        }
+        uint64_t s = key & smask;
+        bool done = false;
+        for (uint64_t probe = 0; probe <= smask; ++probe) {
+            const unsigned long long prev = atomicCAS((unsigned long long*)&t[s].key, (unsigned long long)kEmpty,
+                                                      (unsigned long long)key);
+            if (prev == kEmpty || prev == key) {
+                atomicOr((unsigned long long*)&t[s].mask, 1ull << j);
+                done = true;
+                break;
+            }
+            s = (s + 1) & smask;
+        }
+        if (!done) atomicOr(status, RK_DEV_TABLE_FULL);
+    }
+}
+
+}  // namespace rk
+
+using namespace rk;
+
+extern "C" int rk_index_build(int32_t W, const uint64_t* keys, const int64_t* key_off, void* index,
+                              int32_t log2_slots, void* stream)
+{
+    if (W < 1 || W > 64) return fail(RK_EUNSUPPORTED, "rk_index_build: W outside 1..64");
+    if (log2_slots < 4 || log2_slots > 31) return fail(RK_EINVAL, "rk_index_build: log2_slots outside 4..31");
+    if (!key_off || !index) return fail(RK_EINVAL, "rk_index_build: NULL array");
+    const uint64_t slots = 1ull << log2_slots;
+    for (int32_t j = 0; j < W; ++j)
+        if (key_off[j + 1] < key_off[j]) return fail(RK_EINVAL, "rk_index_build: key_off not monotone at %d", j);
+    const int64_t total = key_off[W] - key_off[0];
+    if ((uint64_t)total > slots / 2)
+        return fail(RK_ETABLEFULL, "rk_index_build: %lld keys for %llu slots (load above 0.5)", (long long)total,
+                    (unsigned long long)slots);
+    if (total > 0 && !keys) return fail(RK_EINVAL, "rk_index_build: keys is NULL");
+    int32_t* st = status_word();
+    if (!st) return fail(RK_EHIP, "rk_index_build: no status word");
+    hipStream_t s = (hipStream_t)stream;
+    IndexSlot* t = (IndexSlot*)index;
+    uint64_t blocks = (slots + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(index_clear_kernel, dim3((unsigned)blocks), dim3(256), 0, s, t, slots);
+    int rc = hip_check(hipGetLastError(), "rk_index_build clear launch");
+    if (rc) return rc;
+    for (int32_t j = 0; j < W; ++j) {
+        const int64_t n = key_off[j + 1] - key_off[j];
+        if (n == 0) continue;
+        int64_t b = (n + 255) / 256;
+        if (b > 65536) b = 65536;
+        hipLaunchKernelGGL(index_insert_kernel, dim3((unsigned)b), dim3(256), 0, s, keys + key_off[j], n, j, t,
+                           slots - 1, st);
+        rc = hip_check(hipGetLastError(), "rk_index_build insert launch");
+        if (rc) return rc;
+    }
+    return RK_OK;
+}
+
+extern "C" int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains, const int64_t* chain_off,
+                                    const void* index, int32_t log2_slots, const int32_t* active_blocks,
+                                    rk_cost_params params, int32_t probe_mode, int32_t* overlap_out, float* cost_out,
+                                    int32_t* argmin_out, void* stream)
+{
+    if (B < 0) return fail(RK_EINVAL, "rk_route_score_index: B < 0");
+    if (W < 1 || W > 64) return fail(RK_EUNSUPPORTED, "rk_route_score_index: W outside 1..64");
+    if (log2_slots < 4 || log2_slots > 31) return fail(RK_EINVAL, "rk_route_score_index: log2_slots outside 4..31");
+    if (!(params.w_ov >= 0.0f) || !(params.w_act >= 0.0f) || !(params.w_sat >= 0.0f))
+        return fail(RK_EINVAL, "rk_route_score_index: weights must be >= 0");
+    if (params.cap_blocks < 1) return fail(RK_EINVAL, "rk_route_score_index: cap_blocks < 1");
+    if (probe_mode != RK_PROBE_PREFIX && probe_mode != RK_PROBE_SCAN)
+        return fail(RK_EINVAL, "rk_route_score_index: unknown probe_mode");
+    if (B == 0) return RK_OK;
+    if (!chain_off || !index || !active_blocks) return fail(RK_EINVAL, "rk_route_score_index: NULL array");
+    int32_t* st = status_word();
+    if (!st) return fail(RK_EHIP, "rk_route_score_index: no status word");
+    hipStream_t s = (hipStream_t)stream;
+    int64_t blocks = ((int64_t)B + IWAVES - 1) / IWAVES;
+    if (blocks > 1 << 20) blocks = 1 << 20;
+    const IndexSlot* t = (const IndexSlot*)index;
+    if (probe_mode == RK_PROBE_SCAN)
+        hipLaunchKernelGGL(score_index_kernel<RK_PROBE_SCAN>, dim3((unsigned)blocks), dim3(64 * IWAVES), 0, s, B, W,
+                           chains, chain_off, t, log2_slots, active_blocks, params, overlap_out, cost_out, argmin_out,
+                           st);
+    else
+        hipLaunchKernelGGL(score_index_kernel<RK_PROBE_PREFIX>, dim3((unsigned)blocks), dim3(64 * IWAVES), 0, s, B,
+                           W, chains, chain_off, t, log2_slots, active_blocks, params, overlap_out, cost_out,
+                           argmin_out, st);
+    return hip_check(hipGetLastError(), "rk_route_score_index launch");
+}

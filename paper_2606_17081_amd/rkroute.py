@@ -23,7 +23,8 @@ DEV_BITS = {0x1: "bad offsets", 0x2: "short input", 0x4: "zero key", 0x8: "table
             0x10: "too large", 0x20: "no convergence"}
 
 EXPORTED = ("rk_status_string", "rk_last_error", "rk_device_status", "rk_hash_chains",
-            "rk_table_build", "rk_route_score_batch", "rk_simulate_workspace_size",
+            "rk_table_build", "rk_route_score_batch", "rk_index_build", "rk_route_score_index",
+            "rk_simulate_workspace_size",
             "rk_simulate_episodes", "rk_poa_workspace_size", "rk_poa_estimate")
 
 
@@ -93,6 +94,10 @@ def lib():
             L.rk_table_build.argtypes = [i32, vp, vp, vp, i32, vp]
             L.rk_route_score_batch.restype = C.c_int
             L.rk_route_score_batch.argtypes = [i32, i32, vp, vp, vp, i32, vp, CostParams, i32, vp, vp, vp, vp]
+            L.rk_index_build.restype = C.c_int
+            L.rk_index_build.argtypes = [i32, vp, vp, vp, i32, vp]
+            L.rk_route_score_index.restype = C.c_int
+            L.rk_route_score_index.argtypes = [i32, i32, vp, vp, vp, i32, vp, CostParams, i32, vp, vp, vp, vp]
             L.rk_simulate_workspace_size.restype = sz
             L.rk_simulate_workspace_size.argtypes = [i32, i32, i32, i32, i32]
             L.rk_simulate_episodes.restype = C.c_int
@@ -138,9 +143,15 @@ def _need(t, dtype, name):
         raise RkError(f"{name} must be a contiguous CUDA tensor of {dtype}")
 
 
+def _outputs_fit(B, W, overlap, cost, argmin):
+    for t, n, name in ((overlap, B * W, "overlap"), (cost, B * W, "cost"), (argmin, B, "argmin")):
+        if t is not None and t.numel() < n:
+            raise RkError(f"{name} holds {t.numel()} elements, {n} needed")
+
+
 # 64-bit block hashes may live in int64 tensors (same bits; PyTorch supports
 # more int64 operations than uint64 ones).
-_HASH_ARGS = ("chains", "keys", "tables", "evict_digest", "last_hash")
+_HASH_ARGS = ("chains", "keys", "tables", "index", "evict_digest", "last_hash")
 
 
 def to_device(a: np.ndarray, device="cuda"):
@@ -217,10 +228,59 @@ def route_score_batch(chains, chain_off, tables, log2_slots: int, active_blocks,
     _need(overlap, torch.int32, "overlap")
     _need(cost, torch.float32, "cost")
     _need(argmin, torch.int32, "argmin")
+    _outputs_fit(B, W, overlap, cost, argmin)
     p = CostParams(w_ov, w_act, w_sat, cap_blocks)
     _check(lib().rk_route_score_batch(B, W, _ptr(chains), _ptr(chain_off), _ptr(tables), log2_slots,
                                       _ptr(active_blocks), p, probe_mode, _ptr(overlap), _ptr(cost),
                                       _ptr(argmin), _stream(stream)), "rk_route_score_batch")
+    return overlap, cost, argmin
+
+
+def index_build(keys, key_off: np.ndarray, log2_slots: int, index=None, stream=None):
+    """The global block index (key, worker mask) over W workers' key lists
+    (key_off is a host array); 16-byte slots held as int64 pairs."""
+    torch = _torch()
+    _need(keys, torch.uint64, "keys")
+    key_off = np.ascontiguousarray(key_off, dtype=np.int64)
+    W = key_off.shape[0] - 1
+    if index is None:
+        index = torch.empty(2 << log2_slots, dtype=torch.int64, device=keys.device)
+    _need(index, torch.uint64, "index")
+    if index.numel() < (2 << log2_slots):
+        raise RkError("index holds fewer than 2^log2_slots 16-byte slots")
+    _check(lib().rk_index_build(W, _ptr(keys), C.c_void_p(key_off.ctypes.data), _ptr(index), log2_slots,
+                                _stream(stream)), "rk_index_build")
+    return index
+
+
+def route_score_index(chains, chain_off, index, log2_slots: int, active_blocks, w_ov=1.0, w_act=0.5,
+                      w_sat=4.0, cap_blocks=32768, probe_mode=RK_PROBE_PREFIX, overlap=None, cost=None,
+                      argmin=None, want_overlap=True, want_cost=True, stream=None):
+    """route_score_batch against the global block index (rk_route_score_index)."""
+    torch = _torch()
+    _need(chains, torch.uint64, "chains")
+    _need(chain_off, torch.int64, "chain_off")
+    _need(index, torch.uint64, "index")
+    _need(active_blocks, torch.int32, "active_blocks")
+    B = chain_off.numel() - 1
+    W = active_blocks.numel()
+    if index.numel() < (2 << log2_slots):
+        raise RkError("index holds fewer than 2^log2_slots 16-byte slots")
+    dev = chains.device
+    if overlap is None and want_overlap:
+        overlap = torch.empty((B, W), dtype=torch.int32, device=dev)
+    if cost is None and want_cost:
+        cost = torch.empty((B, W), dtype=torch.float32, device=dev)
+    if argmin is None:
+        argmin = torch.empty(B, dtype=torch.int32, device=dev)
+    _need(overlap, torch.int32, "overlap")
+    _need(cost, torch.float32, "cost")
+    _need(argmin, torch.int32, "argmin")
+    _outputs_fit(B, W, overlap, cost, argmin)
+    p = CostParams(w_ov, w_act, w_sat, cap_blocks)
+    _check(lib().rk_route_score_index(B, W, _ptr(chains), _ptr(chain_off), _ptr(index), log2_slots,
+                                      _ptr(active_blocks), p, probe_mode, _ptr(overlap), _ptr(cost),
+                                      _ptr(argmin), _stream(stream)), "rk_route_score_index")
     return overlap, cost, argmin
 
 

@@ -79,3 +79,26 @@ def test_episode_and_poa_host_validation():
     bad = rk.PoaParams(0.005, 0.02, 0.01, 0, 64, 0.015, 0)
     assert L.rk_poa_estimate(1, None, 0, None, 8, 8, 4, None, None, None, bad, None, None, None, None, 0,
                              None) == rk.RK_EINVAL
+
+
+def test_index_host_validation():
+    if not rk.library_available():
+        pytest.skip("librkroute.so not built")
+    import numpy as np
+    L = rk.lib()
+    p = rk.CostParams(1.0, 0.5, 4.0, 512)
+    koff = np.zeros(66, np.int64)
+    assert L.rk_index_build(65, None, C.c_void_p(koff.ctypes.data), C.c_void_p(16), 8, None) == rk.RK_EUNSUPPORTED
+    assert L.rk_index_build(2, None, C.c_void_p(koff.ctypes.data), C.c_void_p(16), 3, None) == rk.RK_EINVAL
+    koff = np.array([0, 10, 5], np.int64)
+    assert L.rk_index_build(2, None, C.c_void_p(koff.ctypes.data), C.c_void_p(16), 8, None) == rk.RK_EINVAL
+    koff = np.array([0, 100, 129], np.int64)     # 129 keys for 256 slots: above load 0.5
+    assert L.rk_index_build(2, None, C.c_void_p(koff.ctypes.data), C.c_void_p(16), 8, None) == rk.RK_ETABLEFULL
+    assert L.rk_route_score_index(4, 65, None, None, None, 12, None, p, 0, None, None, None,
+                                  None) == rk.RK_EUNSUPPORTED
+    assert L.rk_route_score_index(4, 2, None, None, None, 32, None, p, 0, None, None, None, None) == rk.RK_EINVAL
+    assert L.rk_route_score_index(4, 2, None, None, None, 12, None, p, 5, None, None, None, None) == rk.RK_EINVAL
+    bad = rk.CostParams(1.0, 0.5, 4.0, 0)
+    assert L.rk_route_score_index(4, 2, None, None, None, 12, None, bad, 0, None, None, None, None) == rk.RK_EINVAL
+    assert L.rk_route_score_index(0, 2, None, None, None, 12, None, p, 0, None, None, None, None) == rk.RK_OK
+    assert L.rk_route_score_index(3, 2, None, None, None, 12, None, p, 0, None, None, None, None) == rk.RK_EINVAL
