@@ -38,27 +38,32 @@ __device__ __forceinline__ void load_slot(const IndexSlot* t, uint64_t s, uint64
     m = (uint64_t)v.z | ((uint64_t)v.w << 32);
 }
 
-// Worker mask of block hash h (0 when no worker holds it).  The first two
-// slots are read together; the walk continues one slot at a time.
-__device__ __forceinline__ uint64_t index_lookup(const IndexSlot* __restrict__ t, uint64_t smask, uint64_t h)
+constexpr uint64_t kGroup = 4;   // slots per 64-byte group: a key's probe walk starts at its group's first slot
+
+__device__ __forceinline__ uint64_t home_group(uint64_t h, uint64_t smask) { return h & smask & ~(kGroup - 1); }
+
+// Worker mask of block hash h (0 when no worker holds it), walking whole
+// aligned 64-byte groups from slot s (a group's first slot): the first group
+// resolves almost every lookup in one round trip.
+__device__ __forceinline__ uint64_t index_walk(const IndexSlot* __restrict__ t, uint64_t smask, uint64_t h, uint64_t s)
 {
-    uint64_t s = h & smask;
-    uint64_t k0, m0, k1, m1;
-    load_slot(t, s, k0, m0);
-    load_slot(t, (s + 1) & smask, k1, m1);
-    if (k0 == h) return m0;
-    if (k0 == kEmpty) return 0ull;
-    if (k1 == h) return m1;
-    if (k1 == kEmpty) return 0ull;
-    s = (s + 2) & smask;
-    for (uint64_t n = 2; n <= smask; ++n) {
-        uint64_t k, m;
-        load_slot(t, s, k, m);
-        if (k == h) return m;
-        if (k == kEmpty) return 0ull;
-        s = (s + 1) & smask;
+    for (uint64_t n = 0; n <= smask; n += kGroup) {
+        uint64_t k[kGroup], m[kGroup];
+#pragma unroll
+        for (uint64_t x = 0; x < kGroup; ++x) load_slot(t, s + x, k[x], m[x]);
+#pragma unroll
+        for (uint64_t x = 0; x < kGroup; ++x) {
+            if (k[x] == h) return m[x];
+            if (k[x] == kEmpty) return 0ull;
+        }
+        s = (s + kGroup) & smask;
     }
     return 0ull;
+}
+
+__device__ __forceinline__ uint64_t index_lookup(const IndexSlot* __restrict__ t, uint64_t smask, uint64_t h)
+{
+    return index_walk(t, smask, h, home_group(h, smask));
 }
 
 // Inclusive prefix AND of a 64-bit value across the wavefront's lanes.
@@ -106,6 +111,11 @@ __device__ __forceinline__ int32_t first_clear(const uint64_t* m, int32_t lo, in
     return lo;
 }
 
+__device__ __forceinline__ uint32_t next_pow2_dev(uint32_t x)
+{
+    return x <= 1u ? 1u : 1u << (32 - __clz((int)(x - 1u)));
+}
+
 // LDS writes of one wavefront made visible to the other lanes of that wavefront.
 __device__ __forceinline__ void wave_sync()
 {
@@ -114,9 +124,13 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-constexpr int IWAVES = 4;    // wavefronts per workgroup
+constexpr int IWAVES = 1;         // wavefronts per workgroup: a finished request frees its slot at once
+constexpr int kRound1Min = 64;    // chains longer than this get the coarse first round
+constexpr int kStage = 256;       // leading chain blocks staged in LDS, read in one coalesced pass
+constexpr int kStageRegs = kStage / 64;
 
 struct IdxLds {
+    uint64_t ch[kStage];     // the request's first kStage chain hashes
     uint64_t m[64];          // masks of the current round (prefix ANDs in rounds 1-2)
     int32_t q[64];           // second-round sample positions
     int32_t ioff[65];        // start of each sample interval's positions in the third round
@@ -136,7 +150,11 @@ __global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
     const int32_t A = lane < W ? active[lane] : 0;
     const uint64_t all = W == 64 ? ~0ull : ((1ull << W) - 1ull);
 
-    for (int64_t i = (int64_t)blockIdx.x * IWAVES + (threadIdx.x >> 6); i < B; i += nwaves) {
+    // Workgroups are handed to the 8 XCDs round-robin; renumber them so each
+    // XCD walks one contiguous range of requests (gridDim.x is a multiple of 8).
+    const uint32_t nb8 = gridDim.x >> 3;
+    const uint32_t lb = (blockIdx.x & 7u) * nb8 + (blockIdx.x >> 3);
+    for (int64_t i = (int64_t)lb * IWAVES + (threadIdx.x >> 6); i < B; i += nwaves) {
         const int64_t c0 = chain_off[i], c1 = chain_off[i + 1];
         int32_t P = 0;
         if (c1 < c0 || c1 - c0 > 0x7fffffff) {
@@ -144,7 +162,18 @@ __global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
         } else {
             P = (int32_t)(c1 - c0);
         }
-        const uint64_t* h = chains + c0;
+        const uint64_t* __restrict__ hg = chains + c0;
+        wave_sync();   // the previous request's reads of L.ch are done
+        {
+            const int32_t n = min(P, kStage);
+            uint64_t v[kStageRegs];
+#pragma unroll
+            for (int k = 0; k < kStageRegs; ++k) v[k] = lane + 64 * k < n ? hg[lane + 64 * k] : 0ull;
+#pragma unroll
+            for (int k = 0; k < kStageRegs; ++k) L.ch[lane + 64 * k] = v[k];
+        }
+        wave_sync();
+        auto h = [&](int32_t x) -> uint64_t { return x < kStage ? L.ch[x] : hg[x]; };
         int32_t o = 0;   // lane j: overlap on worker j
 
         if (MODE == RK_PROBE_SCAN) {
@@ -152,7 +181,7 @@ __global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
             bool done = false;
             for (int32_t base = 0; base < P && carry != 0ull; base += 64) {
                 const int32_t n = min(64, P - base);
-                const uint64_t m = lane < n ? index_lookup(index, smask, h[base + lane]) : 0ull;
+                const uint64_t m = lane < n ? index_lookup(index, smask, h(base + lane)) : 0ull;
                 const uint64_t pa = wave_prefix_and(m) & carry;
                 L.m[lane] = pa;
                 wave_sync();
@@ -165,20 +194,25 @@ __global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
                 wave_sync();
             }
         } else {
-            // ---- round 1: every worker's first miss lies in [0, U)
+            // ---- round 1: every worker's first miss lies in [0, U).  Sample
+            // positions sit on a power-of-two grid (clamped to the chain's end)
+            // so requests of one prefix group probe the same index slots.
             int32_t U = P;
-            if (P > 64) {
-                const int32_t q1 = (int32_t)(((uint64_t)(lane + 1) * (uint64_t)P) >> 4) - 1;
-                const uint64_t m = lane < 16 ? index_lookup(index, smask, h[q1]) : all;
+            if (P > kRound1Min) {
+                const int64_t st1 = (int64_t)next_pow2_dev((uint32_t)P) >> 4;
+                const int32_t q1 = (int32_t)min((int64_t)(lane + 1) * st1, (int64_t)P) - 1;
+                const uint64_t m = lane < 16 ? index_lookup(index, smask, h(q1)) : all;
                 const uint64_t pa = wave_prefix_and(m & all);
                 const uint64_t z = __ballot(lane < 16 && pa == 0ull);
                 if (z) U = __shfl(q1, __ffsll((unsigned long long)z) - 1, 64) + 1;
             }
             // ---- round 2: every position of [0, U) when U <= 64, else 64 samples
+            // on the power-of-two grid of step next_pow2(U) / 64, clamped to U - 1
             const bool exact = U <= 64;
             const int32_t nq = exact ? U : 64;
-            const int32_t q = exact ? lane : (int32_t)(((uint64_t)(lane + 1) * (uint64_t)U) >> 6) - 1;
-            const uint64_t m = lane < nq ? index_lookup(index, smask, h[q]) : 0ull;
+            const int64_t st2 = (int64_t)next_pow2_dev((uint32_t)U) >> 6;
+            const int32_t q = exact ? lane : (int32_t)min((int64_t)(lane + 1) * st2, (int64_t)U) - 1;
+            const uint64_t m = lane < nq ? index_lookup(index, smask, h(q)) : 0ull;
             L.m[lane] = wave_prefix_and(m & all);
             L.q[lane] = q;
             wave_sync();
@@ -189,7 +223,7 @@ __global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
                 // ---- round 3: worker j's first miss is in (q[t-1], q[t]]; probe the inside
                 const uint64_t need = wave_or_u64(lane < W && t < 64 ? 1ull << t : 0ull);
                 const int32_t qprev = lane == 0 ? -1 : L.q[lane - 1];
-                const int32_t width = ((need >> lane) & 1ull) ? q - qprev - 1 : 0;
+                const int32_t width = ((need >> lane) & 1ull) ? max(q - qprev - 1, 0) : 0;
                 int32_t total;
                 const int32_t off = wave_excl_sum(width, total);
                 L.ioff[lane] = off;
@@ -211,7 +245,7 @@ __global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
                             else hi = mid - 1;
                         }
                         const int32_t pos = (lo == 0 ? 0 : L.q[lo - 1] + 1) + (idx - L.ioff[lo]);
-                        mm = index_lookup(index, smask, h[pos]);
+                        mm = index_lookup(index, smask, h(pos));
                     }
                     wave_sync();   // the previous chunk's masks have been read
                     L.m[lane] = mm;
@@ -259,7 +293,7 @@ __global__ __launch_bounds__(256) void index_insert_kernel(const uint64_t* __res
             atomicOr(status, RK_DEV_ZERO_KEY);
             continue;
         }
-        uint64_t s = key & smask;
+        uint64_t s = home_group(key, smask);
         bool done = false;
         for (uint64_t probe = 0; probe <= smask; ++probe) {
             const unsigned long long prev = atomicCAS((unsigned long long*)&t[s].key, (unsigned long long)kEmpty,
@@ -335,6 +369,7 @@ extern "C" int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains
     hipStream_t s = (hipStream_t)stream;
     int64_t blocks = ((int64_t)B + IWAVES - 1) / IWAVES;
     if (blocks > 1 << 20) blocks = 1 << 20;
+    blocks = (blocks + 7) / 8 * 8;
     const IndexSlot* t = (const IndexSlot*)index;
     if (probe_mode == RK_PROBE_SCAN)
         hipLaunchKernelGGL(score_index_kernel<RK_PROBE_SCAN>, dim3((unsigned)blocks), dim3(64 * IWAVES), 0, s, B, W,

@@ -121,14 +121,15 @@ def test_index_scan_mode_arbitrary_sets(gpu, orc):
     _status_clean(rk)
 
 
-def test_index_full_size_sampled(gpu, orc):
-    """65,536 requests x 64 workers on the benchmark's key sets: 300 sampled
-    requests against the oracle; every request against the per-worker-table
-    scorer."""
+@pytest.mark.parametrize("spare", [0, 1])
+def test_index_full_size_sampled(gpu, orc, spare):
+    """65,536 requests x 64 workers on the benchmark's key sets, index at load
+    <= 0.5 and (as benchmarked) <= 0.25: 300 sampled requests against the
+    oracle; every request against the per-worker-table scorer."""
     torch, rk = gpu
     say("generating the 65,536 x 64 scoring instance")
     inst = wl.scoring_instance(seed=0)
-    lg = index_log2(int(inst.key_off[-1]))
+    lg = index_log2(int(inst.key_off[-1])) + spare
     say("index scoring, log2 slots", lg)
     got = _score_index(rk, torch, inst, rk.RK_PROBE_PREFIX, lg=lg)
     _status_clean(rk)
