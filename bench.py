@@ -253,7 +253,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-scoring", action="store_true")
-    ap.add_argument("--cpu-seeds", type=int, default=8)
+    ap.add_argument("--cpu-seeds", type=int, default=64)
     ap.add_argument("--only", choices=("all", "sweep", "scoring"), default="all",
                     help="profiling passes: run only the sweep step or only the scoring kernel")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
