@@ -2,25 +2,35 @@
 //
 // Per episode the workgroup (256 threads, 4 wavefronts) keeps in LDS the
 // worker loads A_j, the LRU bookkeeping of every worker, the in-flight routes
-// of the last H steps, the controller's load window and the current and next
-// prompt chains.  Each worker's cached blocks live in HBM as an
-// open-addressing table of 16-byte slots (key, stamp) plus a ring log of
-// touches:
-//   - a touch of a block at stamp p writes slot.stamp = p and log[p] = slot,
-//     so stamps are log positions and recency order is log order;
+// of the last H steps and the controller's load window.  Each worker's cached
+// blocks live in HBM as an open-addressing table of 16-byte slots (key, stamp)
+// plus a ring log of touches:
+//   - a touch of a block at stamp p sets slot.stamp to p (the largest stamp
+//     wins) and writes log[p] = slot, so stamps are log positions and recency
+//     order is log order;
 //   - a log record p is live iff the stamp of slot log[p] still equals p;
 //     eviction pops the log head, skipping stale records, and tombstones the
 //     slot (stamp kTomb);
-//   - when tombstones or the log fill up, the live records are compacted,
-//     re-stamped in order and re-inserted into a cleared table.
-// A route: every wavefront finds the longest cached prefix of the chain on
-// its workers (all of its workers' probes in flight together; a round probes
-// 64 spread positions, the next round the sub-interval holding the first
-// miss); wavefront 0 turns the overlaps into fp32 costs and takes the min of
-// packed (cost, worker) keys; all threads touch/insert the chosen worker's P
-// blocks in parallel (stamps in reverse block order) and evict the oldest live
-// records.  The next route's chain is loaded into registers while the current
-// route runs.
+//   - when tombstones or the log would fill up, the live records are
+//     compacted, re-stamped in order and re-inserted into a cleared table.
+//
+// Routes are processed in batches of up to NB queued requests (the queue
+// order is the routing order, so the next requests are known in advance):
+//   A. every (request, worker) overlap of the batch is searched at once
+//      against the caches as they stand, and so is the longest common prefix
+//      of every pair of the batch's chains;
+//   B. one wavefront makes the routing decisions in order (releases, queue,
+//      controller, cost, argmin, loads).  Route b changes only the cache of
+//      its worker sigma, and only by adding its chain: with caches
+//      prefix-closed along the chains and chained hashes naming whole
+//      prefixes, a later request b'' then has overlap
+//      max(o[b''][sigma], lcp(b'', b)) on sigma and unchanged overlaps
+//      elsewhere.  The cache writes themselves are deferred;
+//   C. the deferred touches and inserts of the batch are applied in parallel.
+// A route that must evict (and every route in scan mode, where caches need
+// not be prefix-closed) stops phase B: its worker's deferred writes are
+// applied, the least recently used blocks evicted, and the pending requests
+// searched again on that worker.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -29,10 +39,13 @@ namespace rk {
 
 constexpr int NT = 256;
 constexpr int NW = NT / 64;
-constexpr int PF = 8;      // chain blocks per thread prefetched for the next route
+constexpr int kMaxBatch = 64;       // routes per batch (at most one wavefront of lanes)
+constexpr int32_t kMoreTurns = 0x40000000;   // flag on an in-flight conversation index: it has a next turn
+
+enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2 };
 
 struct EpArgs {
-    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, prefetch;
+    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB;
     const rk_episode_params* params;
     const int64_t* turn_off;
     const int32_t* turn_blocks;
@@ -42,15 +55,14 @@ struct EpArgs {
     unsigned char* ws;
     EpisodeLayout L;
     int32_t* status;
-    uint32_t lds_chain0, lds_chain1, lds_w, lds_key, lds_inflight, lds_step, lds_u;
+    uint32_t lds_w, lds_inflight, lds_u, lds_batch;
 };
 
 struct EpShared {
-    int32_t n_route, done, sigma, P, rebuild, ins, remaining, ev, qhead, qsize, pop_base, lcp;
+    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, seln;
     uint32_t new_head;
-    float w_eff;
-    int64_t cbase;
-    unsigned long long digest;
+    int64_t ev_row, ev_total;
+    unsigned long long digest, rb_mask;
     int32_t wtot[NW];
 };
 
@@ -288,34 +300,190 @@ __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t 
     return insert_or_touch(t, smask, h, inserted, status);
 }
 
-template <int JPW>
+
+static __device__ __forceinline__ void ep_wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+static __device__ __forceinline__ uint32_t ep_wave_min_u32(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(v, off, 64);
+        v = o < v ? o : v;
+    }
+    return v;
+}
+
+static __device__ __forceinline__ int32_t ep_wave_sum(int32_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Exclusive prefix sum across the wavefront; total receives the full sum.
+static __device__ __forceinline__ int32_t ep_wave_excl_sum(int32_t v, int32_t& total)
+{
+    const int lane = threadIdx.x & 63;
+    int32_t x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t o = __shfl_up(x, off, 64);
+        if (lane >= off) x += o;
+    }
+    total = __shfl(x, 63, 64);
+    return x - v;
+}
+
+constexpr int KI = 4;   // searches a thread keeps in flight together
+
+// Longest cached prefix for items i = threadIdx.x, + NT, ... < n: item i
+// names a chain, its length and a worker table (info), and receives the
+// first chain position missing from the table (put).  Binary search per
+// thread, exact for tables prefix-closed along the chain; KI searches of a
+// thread issue their loads together.
+template <class Info, class Put>
+__device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, const Put& put, const Slot* slots,
+                                                uint64_t S)
+{
+    const uint64_t smask = S - 1;
+    for (int32_t base = 0; base < n; base += NT * KI) {
+        int32_t lo[KI], hi[KI];
+        const uint64_t* ch[KI];
+        const Slot* tb[KI];
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            lo[u] = 0;
+            hi[u] = 0;
+            ch[u] = nullptr;
+            tb[u] = slots;
+            if (i < n) {
+                int32_t P, j;
+                info(i, ch[u], P, j);
+                hi[u] = P;
+                tb[u] = slots + (uint64_t)j * S;
+            }
+        }
+        for (;;) {
+            bool any = false;
+            int32_t mid[KI];
+            uint64_t hk[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                mid[u] = (lo[u] + hi[u]) >> 1;
+                hk[u] = 0ull;
+                if (lo[u] < hi[u]) {
+                    hk[u] = ch[u][mid[u]];
+                    any = true;
+                }
+            }
+            if (!any) break;
+            uint64_t kw[KI][kWin];
+            uint32_t sw[KI][kWin];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                if (lo[u] < hi[u]) {
+                    const uint64_t s0 = hk[u] & smask;
+#pragma unroll
+                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + ((s0 + x) & smask), kw[u][x], sw[u][x]);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                if (lo[u] < hi[u]) {
+                    if (finish_lookup(tb[u], smask, hk[u], hk[u] & smask, kw[u], sw[u])) lo[u] = mid[u] + 1;
+                    else hi[u] = mid[u];
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            if (i < n) put(i, lo[u]);
+        }
+    }
+}
+
+// Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
+struct BatchLayout {
+    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rflag, rstamp, sel, seloff, lcp, bytes;
+};
+
+__host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
+{
+    BatchLayout b;
+    uint32_t o = 0;
+    auto take = [&](uint32_t n, uint32_t al) {
+        o = (o + al - 1) / al * al;
+        const uint32_t r = o;
+        o += n;
+        return r;
+    };
+    const uint32_t nb = (uint32_t)NB, w = (uint32_t)W;
+    b.rcb = take(nb * 8, 8);
+    b.rlast = take(nb * 8, 8);
+    b.o_cur = take(nb * w * 4, 4);
+    b.o_tab = take(nb * w * 4, 4);
+    b.rc = take(nb * 4, 4);
+    b.rk = take(nb * 4, 4);
+    b.rturn = take(nb * 4, 4);
+    b.rP = take(nb * 4, 4);
+    b.rsig = take(nb * 4, 4);
+    b.rotab = take(nb * 4, 4);
+    b.rflag = take(nb * 4, 4);
+    b.rstamp = take(nb * 4, 4);
+    b.sel = take(nb * 4, 4);
+    b.seloff = take((nb + 1) * 4, 4);
+    b.lcp = take(nb * nb * 2, 4);
+    b.bytes = (o + 15) / 16 * 16;
+    return b;
+}
+
 __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
 {
-    constexpr bool kPipe = JPW <= 4;      // two wavefronts then search up to 8 workers each
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ EpShared sh;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int e = blockIdx.x;
     const rk_episode_params prm = a.params[e];
-    const int32_t W = a.W;
+    const int32_t W = a.W, NB = a.NB;
+    const bool scan = a.probe_mode == RK_PROBE_SCAN;
 
-    uint64_t* s_cur = (uint64_t*)(smem + a.lds_chain0);     // chain of the current route
-    uint64_t* s_nxt = (uint64_t*)(smem + a.lds_chain1);     // chain of the next route (prefetched)
+    // per-worker state
     int32_t* s_A = (int32_t*)(smem + a.lds_w);
     uint32_t* s_head = (uint32_t*)(s_A + W);
     uint32_t* s_tail = s_head + W;
     int32_t* s_live = (int32_t*)(s_tail + W);
     int32_t* s_used = s_live + W;
-    int32_t* s_ovc = s_used + W;                          // overlaps of the current route
-    int32_t* s_ovn = s_ovc + W;                            // overlaps of the next route (lookahead)
-    uint64_t* s_key = (uint64_t*)(smem + a.lds_key);       // packed (cost, worker) per worker
-    int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // in-flight routes: worker
-    int32_t* s_stP = s_stw + a.max_inflight;               //                   prompt blocks
-    int32_t* s_stc = s_stP + a.max_inflight;               //                   conversation
+    // in-flight routes of the last H steps, by step slot
+    int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // worker
+    int32_t* s_stP = s_stw + a.max_inflight;               // prompt blocks
+    int32_t* s_stc = s_stP + a.max_inflight;               // conversation (| kMoreTurns)
     int32_t* s_stepn = s_stc + a.max_inflight;             // routes per step slot
-    int64_t* s_stcb = (int64_t*)(smem + a.lds_step);       // this step: chain base
-    int32_t* s_stt = (int32_t*)(s_stcb + a.max_rps);       //            global turn
     int64_t* s_u = (int64_t*)(smem + a.lds_u);             // controller load samples
+    // the batch
+    const BatchLayout BL = batch_layout(NB, W);
+    unsigned char* bb = smem + a.lds_batch;
+    int64_t* r_cb = (int64_t*)(bb + BL.rcb);               // chain base
+    uint64_t* r_last = (uint64_t*)(bb + BL.rlast);         // h_{P-1}
+    int32_t* o_cur = (int32_t*)(bb + BL.o_cur);            // [b][j] overlap as of now
+    int32_t* o_tab = (int32_t*)(bb + BL.o_tab);            // [b][j] overlap found in the table
+    int32_t* r_c = (int32_t*)(bb + BL.rc);                 // conversation (| kMoreTurns)
+    int32_t* r_k = (int32_t*)(bb + BL.rk);                 // turn of the conversation
+    int32_t* r_turn = (int32_t*)(bb + BL.rturn);           // global turn index
+    int32_t* r_P = (int32_t*)(bb + BL.rP);                 // prompt blocks
+    int32_t* r_sig = (int32_t*)(bb + BL.rsig);             // chosen worker
+    int32_t* r_otab = (int32_t*)(bb + BL.rotab);           // blocks known cached in sigma's table
+    int32_t* r_flag = (int32_t*)(bb + BL.rflag);           // cache writes applied
+    uint32_t* r_stamp = (uint32_t*)(bb + BL.rstamp);       // stamp of the last block
+    int32_t* l_sel = (int32_t*)(bb + BL.sel);              // routes selected for application
+    int32_t* l_seloff = (int32_t*)(bb + BL.seloff);        //   and their block offsets
+    uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
 
     const int32_t H = prm.hold_steps, rps = prm.routes_per_step, n_conv = prm.n_conv;
     const bool bad = H < 1 || rps < 1 || rps > a.max_rps || (int64_t)H * rps > a.max_inflight ||
@@ -369,81 +537,220 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         sh.qhead = 0;
         sh.qsize = qn;
         sh.ins = 0;
-        sh.digest = 0;
+        sh.ev_total = 0;
     }
     __syncthreads();
-
     const int32_t qcap = n_conv + 1;
-    int32_t t = 0;                                 // routes done (uniform)
-    int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};     // thread 0
-    int64_t u_sum = 0;                             // thread 0
-    bool prev_active = false;                      // thread 0
 
-    // thread 0: prompt, chain base and effective overlap weight of route r of the step
-    auto setup = [&](int32_t sbase, int32_t r) {
-        bool active = false;
-        if (prm.controller && t >= prm.ctrl_window)
-            active = (int64_t)prm.ctrl_den * u_sum >
-                     (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
-        float w = prm.w_ov;
-        if (active) {
-            w = fminf(prm.w_ov, prm.ctrl_w_ov);
-            tot[3] += 1;
-            if (!prev_active) tot[4] += 1;
-        }
-        prev_active = active;
-        sh.w_eff = w;
-        sh.P = s_stP[sbase + r];
-        sh.cbase = s_stcb[r];
-    };
-
-    for (int32_t s = 0;; ++s) {
-        const int32_t slot = s % H;
-        const int32_t sb = slot * rps;
-        // ---- release the routes of step s - H; queue their conversations' next turns
-        if (s >= H) {
-            const int32_t nprev = s_stepn[slot];
-            const int32_t qend = sh.qhead + sh.qsize;
-            int32_t pushed = 0;
-            for (int32_t base = 0; base < nprev; base += NT) {
-                const int32_t r = base + tid;
-                bool more = false;
-                int32_t c = 0;
-                if (r < nprev) {
-                    c = s_stc[sb + r];
-                    atomicSub(&s_A[s_stw[sb + r]], s_stP[sb + r]);
-                    more = g_next[c] < (int32_t)(a.turn_off[gc0 + c + 1] - a.turn_off[gc0 + c]);
+    // ---- compaction of worker j: re-stamp its live records in order into a cleared table (all threads)
+    auto rebuild = [&](int32_t j) {
+        Slot* tk = g_slots + (uint64_t)j * S;
+        uint32_t* tl = g_log + (uint64_t)j * R;
+        const uint32_t head = s_head[j], tail = s_tail[j];
+        int32_t cnt = 0;
+        for (uint32_t base = head; base < tail; base += NT) {
+            const uint32_t pos = base + (uint32_t)tid;
+            bool live = false;
+            uint64_t key = 0;
+            if (pos < tail) {
+                const uint32_t sl = tl[pos & rmask];
+                if (sl < S) {
+                    uint32_t st;
+                    load_slot(tk + sl, key, st);
+                    live = st == pos;
                 }
-                int32_t total;
-                const int32_t rank = block_scan(more, sh.wtot, total);
-                if (more) g_queue[(qend + pushed + rank) % qcap] = c;
-                pushed += total;
             }
-            if (tid == 0 && pushed) sh.qsize += pushed;
-            __syncthreads();
+            int32_t total;
+            const int32_t rank = block_scan(live, sh.wtot, total);
+            if (live && (uint64_t)(cnt + rank) < scratch_cap) g_scratch[cnt + rank] = key;
+            cnt += total;
         }
-        // ---- how many requests this step routes
-        if (tid == 0) {
-            int64_t inflight = 0;
-            for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[(s - k) % H];
-            sh.done = sh.qsize == 0 && inflight == 0;
-            sh.n_route = sh.done ? 0 : min(rps, sh.qsize);
-            s_stepn[slot] = sh.n_route;
-            if (sh.n_route > 0) tot[5] = s + 1;
-            sh.pop_base = sh.qhead;
-            sh.qhead = (sh.qhead + sh.n_route) % qcap;
-            sh.qsize -= sh.n_route;
+        if ((uint64_t)cnt > scratch_cap) {
+            if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
+            cnt = (int32_t)scratch_cap;
         }
         __syncthreads();
-        if (sh.done) break;
-        const int32_t n = sh.n_route;
-        // ---- pop the step's requests from the queue head (in parallel)
-        for (int32_t r = tid; r < n; r += NT) {
-            const int32_t c = g_queue[(sh.pop_base + r) % qcap];
+        {
+            uint4* z = reinterpret_cast<uint4*>(tk);
+            const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+            for (uint64_t i = tid; i < S; i += NT) z[i] = zero;
+        }
+        __syncthreads();
+        for (int32_t q = tid; q < cnt; q += NT) {
+            int ins;
+            const uint64_t sl = insert_or_touch(tk, smask, g_scratch[q], ins, a.status);
+            if (sl != ~0ull) tk[sl].stamp = (uint32_t)q;
+            tl[(uint32_t)q & rmask] = (uint32_t)sl;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            s_head[j] = 0;
+            s_tail[j] = (uint32_t)cnt;
+            s_live[j] = cnt;
+            s_used[j] = cnt;
+        }
+        __syncthreads();
+    };
+
+    // ---- apply the deferred cache writes of batch routes b < bhi not applied yet,
+    //      only those of worker `only` when only >= 0 (all threads)
+    auto apply = [&](int32_t bhi, int32_t only) {
+        if (wave == 0) {
+            const int32_t b = lane;
+            const bool sel = b < bhi && !r_flag[b] && (only < 0 || r_sig[b] == only);
+            const unsigned long long mb = __ballot(sel);
+            const int32_t rank = __popcll(mb & ((1ull << lane) - 1ull));
+            int32_t total;
+            const int32_t off = ep_wave_excl_sum(sel ? r_P[b] : 0, total);
+            if (sel) {
+                l_sel[rank] = b;
+                l_seloff[rank] = off;
+                r_flag[b] = 1;
+            }
+            if (lane == 0) {
+                sh.seln = __popcll(mb);
+                l_seloff[__popcll(mb)] = total;
+            }
+        }
+        __syncthreads();
+        const int32_t n = sh.seln, total = l_seloff[n];
+        int my_ins = 0;
+        for (int32_t i = tid; i < total; i += NT) {
+            int32_t lo = 0, hi = n - 1;     // last selected route with l_seloff <= i
+            while (lo < hi) {
+                const int32_t mid = (lo + hi + 1) >> 1;
+                if (l_seloff[mid] <= i) lo = mid;
+                else hi = mid - 1;
+            }
+            const int32_t b = l_sel[lo];
+            const int32_t k = i - l_seloff[lo];
+            const int32_t P = r_P[b], sg = r_sig[b];
+            Slot* tk = g_slots + (uint64_t)sg * S;
+            uint32_t* tl = g_log + (uint64_t)sg * R;
+            const uint64_t h = a.chains[r_cb[b] + k];
+            const uint32_t stamp = r_stamp[b] + (uint32_t)(P - 1 - k);
+            int ins;
+            const uint64_t sl = touch_hinted(tk, smask, h, k < r_otab[b], ins, a.status);
+            if (sl != ~0ull)
+                __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
+            my_ins += ins;
+        }
+        if (my_ins) atomicAdd(&sh.ins, my_ins);
+        __syncthreads();
+    };
+
+    // ---- evict least recently used blocks of worker sg down to the capacity (all threads)
+    auto evict = [&](int32_t sg) {
+        Slot* tk = g_slots + (uint64_t)sg * S;
+        uint32_t* tl = g_log + (uint64_t)sg * R;
+        while (sh.remaining > 0) {
+            const uint32_t head = s_head[sg], tail = s_tail[sg];
+            const int32_t rem = sh.remaining;
+            if (head >= tail) {
+                __syncthreads();
+                if (tid == 0) {
+                    atomicOr(a.status, RK_DEV_TABLE_FULL);
+                    sh.remaining = 0;
+                }
+                __syncthreads();
+                break;
+            }
+            const uint32_t pos = head + (uint32_t)tid;
+            uint32_t sl = 0;
+            bool live = false;
+            uint64_t key = 0;
+            if (pos < tail) {
+                sl = tl[pos & rmask];
+                if (sl < S) {
+                    uint32_t st;
+                    load_slot(tk + sl, key, st);
+                    live = st == pos;
+                }
+            }
+            int32_t total;
+            const int32_t rank = block_scan(live, sh.wtot, total);
+            if (live && rank < rem) {
+                tk[sl].stamp = kTomb;
+                atomicAdd(&sh.digest, (unsigned long long)mix64(key));
+                if (rank == rem - 1) sh.new_head = pos + 1;
+            }
+            __syncthreads();
+            if (tid == 0) {
+                if (total >= rem) {
+                    s_head[sg] = sh.new_head;
+                    sh.ev += rem;
+                    s_live[sg] -= rem;
+                    sh.remaining = 0;
+                } else {
+                    s_head[sg] = min(head + (uint32_t)NT, tail);
+                    sh.ev += total;
+                    s_live[sg] -= total;
+                    sh.remaining = rem - total;
+                }
+            }
+            __syncthreads();
+        }
+    };
+
+    // overlaps of batch routes b in [b_lo, nb) on worker j (j < 0: every worker), into o_tab and o_cur
+    auto search = [&](int32_t b_lo, int32_t nb, int32_t j) {
+        if (!scan) {
+            const int32_t per = j < 0 ? W : 1;
+            const int32_t n = (nb - b_lo) * per;
+            prefix_searches(
+                n,
+                [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj) {
+                    const int32_t b = b_lo + i / per;
+                    jj = j < 0 ? i % per : j;
+                    ch = a.chains + r_cb[b];
+                    P = r_P[b];
+                },
+                [&](int32_t i, int32_t o) {
+                    const int32_t b = b_lo + i / per;
+                    const int32_t jj = j < 0 ? i % per : j;
+                    o_tab[b * W + jj] = o;
+                    o_cur[b * W + jj] = o;
+                },
+                g_slots, S);
+        } else {
+            for (int32_t b = b_lo + wave; b < nb; b += NW) {
+                const uint64_t* ch = a.chains + r_cb[b];
+                if (j < 0) {
+                    for (int32_t jb = 0; jb < W; jb += 4)
+                        wave_overlaps<4>(ch, r_P[b], jb, 1, min(W, jb + 4), g_slots, S, RK_PROBE_SCAN, o_tab + b * W,
+                                         -1, 0);
+                } else {
+                    wave_overlaps<1>(ch, r_P[b], j, 1, j + 1, g_slots, S, RK_PROBE_SCAN, o_tab + b * W, -1, 0);
+                }
+            }
+            __syncthreads();
+            const int32_t per = j < 0 ? W : 1;
+            for (int32_t i = tid; i < (nb - b_lo) * per; i += NT) {
+                const int32_t b = b_lo + i / per;
+                const int32_t jj = j < 0 ? i % per : j;
+                o_cur[b * W + jj] = o_tab[b * W + jj];
+            }
+        }
+        __syncthreads();
+    };
+
+    // state of the routing sequence, kept by wavefront 0
+    int32_t t = 0, s = 0, r_in_step = 0, n_step = 0;
+    bool step_open = false, prev_active = false;
+    int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int64_t u_sum = 0, u_tot = 0;
+
+    for (;;) {
+        // ---- A. the batch: the next nb queued requests (queue order is routing order)
+        const int32_t qh0 = sh.qhead;
+        int32_t nb = min(NB, sh.qsize);
+        for (int32_t b = tid; b < nb; b += NT) {
+            const int32_t c = g_queue[(qh0 + b) % qcap];
             const int32_t k = g_next[c];
-            g_next[c] = k + 1;
             const int64_t g = gc0 + c;
-            const int64_t turn = a.turn_off[g] + k;
+            const int64_t tb0 = a.turn_off[g], tb1 = a.turn_off[g + 1];
+            const int64_t turn = tb0 + k;
             int32_t P = a.turn_blocks[turn];
             const int64_t cb = a.chain_off[g], ce = a.chain_off[g + 1];
             if (P < 0 || (int64_t)P > ce - cb) {
@@ -454,287 +761,259 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 atomicOr(a.status, RK_DEV_TOO_LARGE);
                 P = a.max_blocks;
             }
-            s_stc[sb + r] = c;
-            s_stP[sb + r] = P;
-            s_stt[r] = (int32_t)turn;
-            s_stcb[r] = cb;
+            r_c[b] = c | ((int64_t)k + 1 < tb1 - tb0 ? kMoreTurns : 0);
+            r_k[b] = k;
+            r_turn[b] = (int32_t)turn;
+            r_P[b] = P;
+            r_cb[b] = cb;
+            r_flag[b] = 0;
+            r_last[b] = P > 0 ? a.chains[cb + P - 1] : 0ull;
         }
         __syncthreads();
-        if (tid == 0 && n > 0) setup(sb, 0);
+        // workers without room for every block of the batch are compacted first; the batch is cut to
+        // what the tightest worker can take (at least one request always fits after compaction)
+        if (tid == 0) {
+            int64_t T = 0;
+            for (int32_t b = 0; b < nb; ++b) T += r_P[b];
+            unsigned long long m = 0;
+            for (int32_t j = 0; j < W; ++j)
+                if ((uint64_t)s_used[j] + (uint64_t)T > used_limit ||
+                    (uint64_t)(s_tail[j] - s_head[j]) + (uint64_t)T > R || (uint64_t)s_tail[j] + (uint64_t)T > 0x40000000u)
+                    m |= 1ull << j;
+            sh.rb_mask = m;
+        }
         __syncthreads();
-        // Pipelining: while worker sigma_r absorbs route r's blocks, waves 2-3
-        // already search route r+1's cached prefixes.  Workers other than
-        // sigma_r are unchanged by route r.  On sigma_r, route r+1's blocks
-        // shared with route r's chain (their common prefix) are cached after
-        // the update, and its later blocks are chained hashes route r cannot
-        // insert, so a search over those positions only is exact while the
-        // update runs.  Evictions by route r are corrected by a new search.
-        const bool can_pipe = kPipe && a.probe_mode == RK_PROBE_PREFIX;
-        bool nxt_ready = false;    // s_nxt holds route r+1's chain (uniform)
-        bool have_ov = false;      // s_ovc holds route r's overlaps (uniform)
-        {
-            const uint64_t* gch = a.chains + sh.cbase;
-            for (int32_t k = tid; k < sh.P; k += NT) s_cur[k] = gch[k];
+        for (unsigned long long m = sh.rb_mask; m; m &= m - 1ull) rebuild(__ffsll(m) - 1);
+        if (tid == 0) {
+            int64_t margin = INT64_MAX;
+            for (int32_t j = 0; j < W; ++j) {
+                margin = min(margin, (int64_t)used_limit - (int64_t)s_used[j]);
+                margin = min(margin, (int64_t)R - (int64_t)(s_tail[j] - s_head[j]));
+                margin = min(margin, (int64_t)0x40000000 - (int64_t)s_tail[j]);
+            }
+            int64_t acc = 0;
+            int32_t n2 = 0;
+            while (n2 < nb && acc + r_P[n2] <= margin) acc += r_P[n2++];
+            if (n2 == 0 && nb > 0) {
+                atomicOr(a.status, RK_DEV_TABLE_FULL);
+                n2 = 1;
+            }
+            sh.nb = n2;
+        }
+        __syncthreads();
+        nb = sh.nb;
+        // every (request, worker) overlap against the caches as they stand
+        search(0, nb, -1);
+        // common prefix of every pair of the batch's chains (prefix mode)
+        if (!scan) {
+            const int32_t npair = nb * (nb - 1) / 2;
+            for (int32_t q = tid; q < npair; q += NT) {
+                int32_t b = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
+                while (b > 1 && b * (b - 1) / 2 > q) --b;
+                while ((b + 1) * b / 2 <= q) ++b;
+                const int32_t b2 = q - b * (b - 1) / 2;
+                const int32_t m = min(r_P[b], r_P[b2]);
+                const uint64_t* ca = a.chains + r_cb[b];
+                const uint64_t* cc = a.chains + r_cb[b2];
+                int32_t lo = 0;
+                if (m > 0 && ca[0] == cc[0]) {
+                    int32_t hi = m;
+                    lo = 1;
+                    while (lo < hi) {
+                        const int32_t mid = (lo + hi) >> 1;
+                        if (ca[mid] == cc[mid]) lo = mid + 1;
+                        else hi = mid;
+                    }
+                }
+                l_lcp[b * NB + b2] = (uint16_t)lo;
+            }
             __syncthreads();
         }
 
-        for (int32_t r = 0; r < n; ++r) {
-            const int32_t P = sh.P;
-            const int32_t Pn = r + 1 < n ? s_stP[sb + r + 1] : 0;
-            uint64_t last_h = 0;    // thread 0: h_{P-1} of route r
-            if (r + 1 < n && !nxt_ready) {
-                const uint64_t* gch = a.chains + s_stcb[r + 1];
-                for (int32_t k = tid; k < Pn; k += NT) s_nxt[k] = gch[k];
-            }
-            // ---- prefetch the chain of route r+2 into registers
-            uint64_t pf[PF];
-            int32_t P2 = 0;
-            bool prefetch = false;
-            if (a.prefetch && r + 2 < n) {
-                P2 = s_stP[sb + r + 2];
-                prefetch = P2 <= NT * PF;
-                if (prefetch) {
-                    const uint64_t* gch = a.chains + s_stcb[r + 2];
-#pragma unroll
-                    for (int i = 0; i < PF; ++i) {
-                        const int32_t k = tid + i * NT;
-                        pf[i] = k < P2 ? gch[k] : 0ull;
-                    }
-                }
-            }
-            // ---- longest cached prefix of route r on every worker (unless already known)
-            if (!have_ov) {
-                wave_overlaps<JPW>(s_cur, P, wave, NW, W, g_slots, S, a.probe_mode, s_ovc, -1, 0);
-            }
-            __syncthreads();
-            const bool pipe = can_pipe && r + 1 < n;
-            // ---- cost of every worker and argmin (wavefront 0); common prefix with route r+1 (wavefront 1)
-            const int64_t row = prm.out_base + (int64_t)t;
+        // ---- B. routing decisions in order (wavefront 0); stops for a flush, a new batch or the end
+        const int32_t t0 = t;
+        int32_t event = EV_BATCH;
+        for (;;) {
             if (wave == 0) {
-                if (lane < W) {
-                    const float c = route_cost(sh.w_eff, prm.w_act, prm.w_sat, prm.cap_blocks, P, s_ovc[lane],
-                                               s_A[lane]);
-                    if (a.out.overlap) a.out.overlap[row * W + lane] = s_ovc[lane];
-                    if (a.out.cost) a.out.cost[row * W + lane] = c;
-                    s_key[lane] = argmin_key(c, lane);
-                }
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-                if (lane == 0) {
-                    uint64_t key = s_key[0];
-                    for (int32_t j = 1; j < W; ++j) {
-                        const uint64_t kj = s_key[j];
-                        key = kj < key ? kj : key;
+                event = EV_BATCH;
+                for (;;) {
+                    if (!step_open) {
+                        // release the routes of step s - H; queue their conversations' next turns
+                        const int32_t slot = s % H, sb = slot * rps;
+                        if (s >= H) {
+                            const int32_t nprev = s_stepn[slot];
+                            const int32_t qtail = sh.qhead + sh.qsize;
+                            int32_t pushed = 0, rel = 0;
+                            for (int32_t base = 0; base < nprev; base += 64) {
+                                const int32_t r = base + lane;
+                                bool more = false;
+                                int32_t c = 0;
+                                if (r < nprev) {
+                                    const int32_t cc = s_stc[sb + r];
+                                    c = cc & ~kMoreTurns;
+                                    more = (cc & kMoreTurns) != 0;
+                                    rel += s_stP[sb + r];
+                                    atomicSub(&s_A[s_stw[sb + r]], s_stP[sb + r]);
+                                }
+                                const unsigned long long mb = __ballot(more);
+                                if (more) g_queue[(qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull))) % qcap] = c;
+                                pushed += __popcll(mb);
+                            }
+                            u_tot -= ep_wave_sum(rel);
+                            ep_wave_sync();
+                            if (lane == 0) sh.qsize += pushed;
+                            ep_wave_sync();
+                        }
+                        int32_t inflight = 0;
+                        for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[(s - k) % H];
+                        const int32_t qs = sh.qsize;
+                        if (qs == 0 && inflight == 0) {
+                            event = EV_DONE;
+                            break;
+                        }
+                        n_step = min(rps, qs);
+                        if (lane == 0) s_stepn[slot] = n_step;
+                        if (n_step > 0) tot[5] = s + 1;
+                        r_in_step = 0;
+                        step_open = true;
+                        ep_wave_sync();
                     }
-                    const int32_t sg = (int32_t)(uint32_t)(key & 0xffffffffu);
-                    sh.sigma = sg;
-                    last_h = P > 0 ? s_cur[P - 1] : 0ull;   // read before the buffer is reused
-                    const uint64_t ins_max = (uint64_t)(P - s_ovc[sg]);
-                    sh.rebuild = ((uint64_t)s_used[sg] + ins_max > used_limit) ||
-                                 ((uint64_t)(s_tail[sg] - s_head[sg]) + (uint64_t)P > R) ||
-                                 (s_tail[sg] > 0x40000000u);
-                }
-            } else if (wave == 1 && pipe) {
-                const int32_t m = min(P, Pn);
-                int32_t l = m;
-                for (int32_t base = 0; base < m; base += 64) {
-                    const int32_t k = base + lane;
-                    const unsigned long long d = __ballot(k < m && s_cur[k] != s_nxt[k]);
-                    if (d) {
-                        l = base + __ffsll(d) - 1;
+                    if (r_in_step >= n_step) {
+                        ++s;
+                        step_open = false;
+                        continue;
+                    }
+                    const int32_t b = t - t0;
+                    if (b >= nb) break;
+                    // one route: controller, cost of every worker, argmin
+                    const int32_t slot = s % H, sb = slot * rps;
+                    bool active = false;
+                    if (prm.controller && t >= prm.ctrl_window)
+                        active = (int64_t)prm.ctrl_den * u_sum >
+                                 (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
+                    float w = prm.w_ov;
+                    if (active) {
+                        w = fminf(prm.w_ov, prm.ctrl_w_ov);
+                        tot[3] += 1;
+                        if (!prev_active) tot[4] += 1;
+                    }
+                    prev_active = active;
+                    const int32_t P = r_P[b];
+                    const int64_t row = prm.out_base + (int64_t)t;
+                    uint32_t bits = 0xFFFFFFFFu;
+                    int32_t oj = 0;
+                    if (lane < W) {
+                        oj = o_cur[b * W + lane];
+                        const float c = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, s_A[lane]);
+                        if (a.out.overlap) a.out.overlap[row * W + lane] = oj;
+                        if (a.out.cost) a.out.cost[row * W + lane] = c;
+                        bits = __float_as_uint(__fadd_rn(c, 0.0f));
+                    }
+                    const uint32_t mn = ep_wave_min_u32(bits);
+                    const int32_t sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
+                    const int32_t osg = __shfl(oj, sg, 64);
+                    const int32_t live_after = s_live[sg] + (scan ? 0 : P - osg);
+                    const bool flush = scan || live_after > a.cache;
+                    const int32_t rc = r_c[b];
+                    if (lane == 0) {
+                        s_A[sg] += P;
+                        const uint32_t base = s_tail[sg];
+                        s_tail[sg] = base + (uint32_t)P;
+                        if (!scan) {
+                            s_live[sg] = live_after;
+                            s_used[sg] += P - osg;
+                        }
+                        r_sig[b] = sg;
+                        r_stamp[b] = base;
+                        r_otab[b] = o_tab[b * W + sg];
+                        s_stw[sb + r_in_step] = sg;
+                        s_stP[sb + r_in_step] = P;
+                        s_stc[sb + r_in_step] = rc;
+                        g_next[rc & ~kMoreTurns] = r_k[b] + 1;
+                        sh.qhead = (sh.qhead + 1) % qcap;
+                        sh.qsize -= 1;
+                        if (a.out.route_turn) a.out.route_turn[row] = r_turn[b];
+                        if (a.out.route_worker) a.out.route_worker[row] = sg;
+                        if (a.out.route_step) a.out.route_step[row] = (int32_t)s;
+                        if (a.out.route_blocks) a.out.route_blocks[row] = P;
+                        if (a.out.last_hash) a.out.last_hash[row] = r_last[b];
+                        if (!flush) {
+                            if (a.out.evict_count) a.out.evict_count[row] = 0;
+                            if (a.out.evict_digest) a.out.evict_digest[row] = 0ull;
+                        } else {
+                            sh.ev_b = b;
+                            sh.ev_row = row;
+                        }
+                    }
+                    u_tot += P;
+                    if (prm.controller) {
+                        const int32_t pos = t % prm.ctrl_window;
+                        if (t >= prm.ctrl_window) u_sum -= s_u[pos];
+                        ep_wave_sync();
+                        if (lane == 0) s_u[pos] = u_tot;
+                        u_sum += u_tot;
+                    }
+                    tot[0] += P - osg;
+                    tot[2] += P;
+                    tot[6] += osg;
+                    // later requests of the batch now find this chain on sg
+                    if (!scan) {
+                        const int32_t b2 = b + 1 + lane;
+                        if (b2 < nb) {
+                            const int32_t l = l_lcp[b2 * NB + b];
+                            if (l > o_cur[b2 * W + sg]) o_cur[b2 * W + sg] = l;
+                        }
+                    }
+                    ++t;
+                    ++r_in_step;
+                    ep_wave_sync();
+                    if (flush) {
+                        event = EV_FLUSH;
                         break;
                     }
                 }
-                if (lane == 0) sh.lcp = l;
+                if (lane == 0) sh.event = event;
             }
             __syncthreads();
-            const int32_t sg = sh.sigma;
-            Slot* tk = g_slots + (uint64_t)sg * S;
-            uint32_t* tl = g_log + (uint64_t)sg * R;
-
-            // ---- compaction: re-stamp the live records in order into a cleared table
-            if (sh.rebuild) {
-                const uint32_t head = s_head[sg], tail = s_tail[sg];
-                int32_t cnt = 0;
-                for (uint32_t base = head; base < tail; base += NT) {
-                    const uint32_t pos = base + (uint32_t)tid;
-                    bool live = false;
-                    uint64_t key = 0;
-                    if (pos < tail) {
-                        const uint32_t sl = tl[pos & rmask];
-                        if (sl < S) {
-                            uint32_t st;
-                            load_slot(tk + sl, key, st);
-                            live = st == pos;
-                        }
-                    }
-                    int32_t total;
-                    const int32_t rank = block_scan(live, sh.wtot, total);
-                    if (live && (uint64_t)(cnt + rank) < scratch_cap) g_scratch[cnt + rank] = key;
-                    cnt += total;
-                }
-                if ((uint64_t)cnt > scratch_cap) {
-                    if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
-                    cnt = (int32_t)scratch_cap;
-                }
-                __syncthreads();
-                {
-                    uint4* z = reinterpret_cast<uint4*>(tk);
-                    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-                    for (uint64_t i = tid; i < S; i += NT) z[i] = zero;
-                }
-                __syncthreads();
-                for (int32_t q = tid; q < cnt; q += NT) {
-                    int ins;
-                    const uint64_t sl = insert_or_touch(tk, smask, g_scratch[q], ins, a.status);
-                    if (sl != ~0ull) tk[sl].stamp = (uint32_t)q;
-                    tl[(uint32_t)q & rmask] = (uint32_t)sl;
-                }
-                __syncthreads();
-                if (tid == 0) {
-                    s_head[sg] = 0;
-                    s_tail[sg] = (uint32_t)cnt;
-                    s_live[sg] = cnt;
-                    s_used[sg] = cnt;
-                }
-                __syncthreads();
-            }
-
-            // ---- touch route r's blocks (block k gets stamp tail + P-1-k), inserting misses;
-            //      with pipelining, waves 2-3 meanwhile search route r+1's overlaps
-            {
-                const int32_t nupd = pipe ? NT / 2 : NT;
-                if (tid < nupd) {
-                    const uint32_t tail = s_tail[sg];
-                    const int32_t o_sg = s_ovc[sg];
-                    int my_ins = 0;
-                    for (int32_t k = tid; k < P; k += nupd) {
-                        int ins;
-                        const uint32_t stamp = tail + (uint32_t)(P - 1 - k);
-                        const uint64_t sl = touch_hinted(tk, smask, s_cur[k], k < o_sg, ins, a.status);
-                        if (sl != ~0ull) tk[sl].stamp = stamp;
-                        tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
-                        my_ins += ins;
-                    }
-                    if (my_ins) atomicAdd(&sh.ins, my_ins);
-                } else if constexpr (kPipe) {
-                    wave_overlaps<2 * JPW>(s_nxt, Pn, wave - NW / 2, NW / 2, W, g_slots, S, RK_PROBE_PREFIX, s_ovn,
-                                           sg, sh.lcp);
-                }
-            }
-            __syncthreads();
+            event = sh.event;
+            if (event != EV_FLUSH) break;
+            // the route's worker: apply its deferred writes, evict, search the pending requests again
+            const int32_t b = sh.ev_b;
+            const int32_t sg = r_sig[b];
+            apply(b + 1, sg);
             if (tid == 0) {
-                s_tail[sg] += (uint32_t)P;
-                s_live[sg] += sh.ins;
-                s_used[sg] += sh.ins;
-                sh.remaining = max(0, s_live[sg] - a.cache);
+                if (scan) {
+                    s_live[sg] += sh.ins;
+                    s_used[sg] += sh.ins;
+                }
                 sh.ins = 0;
+                sh.remaining = max(0, s_live[sg] - a.cache);
                 sh.ev = 0;
                 sh.digest = 0ull;
             }
             __syncthreads();
-            // ---- evict least recently used blocks down to the capacity
-            while (sh.remaining > 0) {
-                const uint32_t head = s_head[sg], tail = s_tail[sg];
-                const int32_t rem = sh.remaining;
-                if (head >= tail) {
-                    if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
-                    break;
-                }
-                const uint32_t pos = head + (uint32_t)tid;
-                uint32_t sl = 0;
-                bool live = false;
-                uint64_t key = 0;
-                if (pos < tail) {
-                    sl = tl[pos & rmask];
-                    if (sl < S) {
-                        uint32_t st;
-                        load_slot(tk + sl, key, st);
-                        live = st == pos;
-                    }
-                }
-                int32_t total;
-                const int32_t rank = block_scan(live, sh.wtot, total);
-                if (live && rank < rem) {
-                    tk[sl].stamp = kTomb;
-                    atomicAdd(&sh.digest, (unsigned long long)mix64(key));
-                    if (rank == rem - 1) sh.new_head = pos + 1;
-                }
-                __syncthreads();
-                if (tid == 0) {
-                    if (total >= rem) {
-                        s_head[sg] = sh.new_head;
-                        sh.ev += rem;
-                        s_live[sg] -= rem;
-                        sh.remaining = 0;
-                    } else {
-                        s_head[sg] = min(head + (uint32_t)NT, tail);
-                        sh.ev += total;
-                        s_live[sg] -= total;
-                        sh.remaining = rem - total;
-                    }
-                }
-                __syncthreads();
-            }
-            // ---- the lookahead search of sigma_r is void if route r evicted: search again
-            if (pipe && sh.ev > 0) {
-                if (wave == 0)
-                    wave_overlaps<1>(s_nxt, Pn, sg, 1, sg + 1, g_slots, S, RK_PROBE_PREFIX, s_ovn, -1, 0);
-                __syncthreads();
-            }
-            // ---- load, controller sample, outputs; set up the next route
+            evict(sg);
+            search(b + 1, nb, sg);
             if (tid == 0) {
-                s_A[sg] += P;
-                s_stw[sb + r] = sg;
-                if (prm.controller) {
-                    int64_t u = 0;
-                    for (int32_t j = 0; j < W; ++j) u += s_A[j];
-                    const int32_t pos = t % prm.ctrl_window;
-                    if (t >= prm.ctrl_window) u_sum -= s_u[pos];
-                    s_u[pos] = u;
-                    u_sum += u;
-                }
-                if (a.out.route_turn) a.out.route_turn[row] = s_stt[r];
-                if (a.out.route_worker) a.out.route_worker[row] = sg;
-                if (a.out.route_step) a.out.route_step[row] = (int32_t)s;
-                if (a.out.route_blocks) a.out.route_blocks[row] = P;
-                if (a.out.evict_count) a.out.evict_count[row] = sh.ev;
-                if (a.out.evict_digest) a.out.evict_digest[row] = sh.digest;
-                if (a.out.last_hash) a.out.last_hash[row] = last_h;
-                tot[0] += P - s_ovc[sg];
-                tot[1] += sh.ev;
-                tot[2] += P;
-                tot[6] += s_ovc[sg];
-                ++t;
-                if (r + 1 < n) setup(sb, r + 1);
-            } else {
-                ++t;
+                if (a.out.evict_count) a.out.evict_count[sh.ev_row] = sh.ev;
+                if (a.out.evict_digest) a.out.evict_digest[sh.ev_row] = sh.digest;
+                sh.ev_total += sh.ev;
             }
-            // route r's chain buffer now takes route r+2's chain; rotate the buffers
-            if (prefetch) {
-#pragma unroll
-                for (int i = 0; i < PF; ++i) {
-                    const int32_t k = tid + i * NT;
-                    if (k < P2) s_cur[k] = pf[i];
-                }
-            }
-            {
-                uint64_t* x = s_cur;
-                s_cur = s_nxt;
-                s_nxt = x;
-                int32_t* y = s_ovc;
-                s_ovc = s_ovn;
-                s_ovn = y;
-            }
-            nxt_ready = prefetch;
-            have_ov = pipe;
             __syncthreads();
         }
+
+        // ---- C. the batch's remaining cache writes
+        if (tid == 0) sh.nb = t - t0;
+        __syncthreads();
+        apply(sh.nb, -1);
+        if (tid == 0) sh.ins = 0;
+        __syncthreads();
+        if (event == EV_DONE) break;
     }
     if (tid == 0 && a.out.totals) {
         int64_t cachedsum = 0;
         for (int32_t j = 0; j < W; ++j) cachedsum += s_live[j];
+        tot[1] = sh.ev_total;
         tot[7] = cachedsum;
         for (int k = 0; k < 8; ++k) a.out.totals[(int64_t)e * 8 + k] = tot[k];
     }
@@ -801,37 +1080,25 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.ws = (unsigned char*)workspace;
     a.L = L;
     a.status = st;
-    const size_t chain_bytes = align_up((size_t)b->max_blocks * 8, 16);
-    size_t rest = 0;
-    rest = align_up(rest + (size_t)b->W * 7 * 4, 16);
-    const size_t off_key = rest;
-    rest = align_up(rest + (size_t)b->W * 8, 16);
-    const size_t off_inflight = rest;
-    rest = align_up(rest + (size_t)b->max_inflight * 4 * 4, 16);
-    const size_t off_step = rest;
-    rest = align_up(rest + (size_t)b->max_routes_per_step * 12, 16);
-    const size_t off_u = rest;
-    rest = align_up(rest + (size_t)b->max_ctrl_window * 8, 16);
+    // LDS: worker state, in-flight routes, controller window, then the batch arrays of the largest
+    // batch that fits in 60 KiB (two episodes can then share a CU)
+    size_t o = 0;
+    a.lds_w = 0;
+    o = align_up(o + (size_t)b->W * 5 * 4, 16);
+    a.lds_inflight = (uint32_t)o;
+    o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
+    a.lds_u = (uint32_t)o;
+    o = align_up(o + (size_t)b->max_ctrl_window * 8, 16);
+    a.lds_batch = (uint32_t)o;
     const size_t limit = 60 * 1024;
-    a.prefetch = 2 * chain_bytes + rest <= limit;
-    const size_t chains_total = (a.prefetch ? 2 : 1) * chain_bytes;
-    if (chains_total + rest > limit)
+    int32_t NB = kMaxBatch;
+    while (NB > 1 && o + batch_layout(NB, b->W).bytes > limit) NB /= 2;
+    if (o + batch_layout(NB, b->W).bytes > limit)
         return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 60 KiB",
-                    chains_total + rest);
-    a.lds_chain0 = 0;
-    a.lds_chain1 = a.prefetch ? (uint32_t)chain_bytes : 0;
-    a.lds_w = (uint32_t)chains_total;
-    a.lds_key = (uint32_t)(chains_total + off_key);
-    a.lds_inflight = (uint32_t)(chains_total + off_inflight);
-    a.lds_step = (uint32_t)(chains_total + off_step);
-    a.lds_u = (uint32_t)(chains_total + off_u);
-    const size_t lds = chains_total + rest;
-    const int jpw = (b->W + NW - 1) / NW;
+                    o + (size_t)batch_layout(NB, b->W).bytes);
+    a.NB = NB;
+    const size_t lds = o + batch_layout(NB, b->W).bytes;
     hipStream_t s = (hipStream_t)stream;
-    if (jpw <= 1) hipLaunchKernelGGL(episode_kernel<1>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
-    else if (jpw <= 2) hipLaunchKernelGGL(episode_kernel<2>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
-    else if (jpw <= 4) hipLaunchKernelGGL(episode_kernel<4>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
-    else if (jpw <= 8) hipLaunchKernelGGL(episode_kernel<8>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
-    else hipLaunchKernelGGL(episode_kernel<16>, dim3((unsigned)b->E), dim3(NT), lds, s, a);
+    hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), lds, s, a);
     return hip_check(hipGetLastError(), "rk_simulate_episodes launch");
 }
