@@ -26,10 +26,11 @@
 //      prefixes, a later request b'' then has overlap
 //      max(o[b''][sigma], lcp(b'', b)) on sigma and unchanged overlaps
 //      elsewhere.  The cache writes themselves are deferred;
-//   C. the deferred touches and inserts of the batch are applied in parallel.
+//   C. meanwhile the other three wavefronts apply the touches and inserts of
+//      the decided routes, a few routes per claim.
 // A route that must evict (and every route in scan mode, where caches need
-// not be prefix-closed) stops phase B: its worker's deferred writes are
-// applied, the least recently used blocks evicted, and the pending requests
+// not be prefix-closed) stops phase B: once every decided route's writes are
+// in, the least recently used blocks are evicted and the pending requests
 // searched again on that worker.
 #include <hip/hip_runtime.h>
 
@@ -58,8 +59,11 @@ struct EpArgs {
     uint32_t lds_w, lds_inflight, lds_u, lds_batch;
 };
 
+constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
+
 struct EpShared {
-    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, seln;
+    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop;
+    int32_t woff[NW][KR + 1];
     uint32_t new_head;
     int64_t ev_row, ev_total;
     unsigned long long digest, rb_mask;
@@ -95,6 +99,13 @@ __device__ __forceinline__ void load_slot(const Slot* p, uint64_t& key, uint32_t
 }
 
 constexpr int kWin = 4;    // slots read by one lookup (a run of this length is rare at load <= 0.5)
+
+// A key's probe walk starts at the first slot of its aligned group of kWin
+// slots (64 bytes), so a lookup's window is one aligned group.
+__device__ __forceinline__ uint64_t home_slot(uint64_t h, uint64_t smask)
+{
+    return h & smask & ~(uint64_t)(kWin - 1);
+}
 
 // Membership test finishing a walk whose first kWin slots (from s) are loaded.
 __device__ __forceinline__ bool finish_lookup(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
@@ -177,7 +188,7 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t jfirst
             if (valid[jj]) {
                 const Slot* t = slots + (uint64_t)(jfirst + jj * jstride) * S;
                 hk[jj] = s_chain[q[jj]];
-                sh0[jj] = hk[jj] & smask;
+                sh0[jj] = home_slot(hk[jj], smask);
 #pragma unroll
                 for (int i = 0; i < kWin; ++i) load_slot(t + ((sh0[jj] + i) & smask), kw[jj][i], sw[jj][i]);
             }
@@ -227,7 +238,7 @@ __device__ __forceinline__ uint64_t insert_or_touch(Slot* __restrict__ t, uint64
                                                    int32_t* status)
 {
     inserted = 0;
-    uint64_t s = h & smask;
+    uint64_t s = home_slot(h, smask);
     for (uint64_t n = 0; n <= smask; ++n) {
         const uint64_t k = __hip_atomic_load(&t[s].key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         const uint32_t st = t[s].stamp;
@@ -258,7 +269,7 @@ __device__ __forceinline__ uint64_t insert_or_touch(Slot* __restrict__ t, uint64
 __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t smask, uint64_t h, bool cached_hint,
                                                  int& inserted, int32_t* status)
 {
-    const uint64_t s = h & smask;
+    const uint64_t s = home_slot(h, smask);
     inserted = 0;
     uint64_t k[kWin];
     uint32_t st[kWin];
@@ -308,14 +319,19 @@ static __device__ __forceinline__ void ep_wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Minimum over the wavefront: DPP moves within each row of 16 lanes (pair
+// swap, quad swap, half-row mirror, row mirror), then the four row minima.
 static __device__ __forceinline__ uint32_t ep_wave_min_u32(uint32_t v)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint32_t o = __shfl_xor(v, off, 64);
-        v = o < v ? o : v;
-    }
-    return v;
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false));
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false));
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    return min(min(r0, r1), min(r2, r3));
 }
 
 static __device__ __forceinline__ int32_t ep_wave_sum(int32_t v)
@@ -388,7 +404,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
                 if (lo[u] < hi[u]) {
-                    const uint64_t s0 = hk[u] & smask;
+                    const uint64_t s0 = home_slot(hk[u], smask);
 #pragma unroll
                     for (int x = 0; x < kWin; ++x) load_slot(tb[u] + ((s0 + x) & smask), kw[u][x], sw[u][x]);
                 }
@@ -396,7 +412,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
                 if (lo[u] < hi[u]) {
-                    if (finish_lookup(tb[u], smask, hk[u], hk[u] & smask, kw[u], sw[u])) lo[u] = mid[u] + 1;
+                    if (finish_lookup(tb[u], smask, hk[u], home_slot(hk[u], smask), kw[u], sw[u])) lo[u] = mid[u] + 1;
                     else hi[u] = mid[u];
                 }
             }
@@ -411,7 +427,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
-    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rflag, rstamp, sel, seloff, lcp, bytes;
+    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, lcp, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
@@ -435,10 +451,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
     b.rP = take(nb * 4, 4);
     b.rsig = take(nb * 4, 4);
     b.rotab = take(nb * 4, 4);
-    b.rflag = take(nb * 4, 4);
     b.rstamp = take(nb * 4, 4);
-    b.sel = take(nb * 4, 4);
-    b.seloff = take((nb + 1) * 4, 4);
     b.lcp = take(nb * nb * 2, 4);
     b.bytes = (o + 15) / 16 * 16;
     return b;
@@ -479,10 +492,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     int32_t* r_P = (int32_t*)(bb + BL.rP);                 // prompt blocks
     int32_t* r_sig = (int32_t*)(bb + BL.rsig);             // chosen worker
     int32_t* r_otab = (int32_t*)(bb + BL.rotab);           // blocks known cached in sigma's table
-    int32_t* r_flag = (int32_t*)(bb + BL.rflag);           // cache writes applied
     uint32_t* r_stamp = (uint32_t*)(bb + BL.rstamp);       // stamp of the last block
-    int32_t* l_sel = (int32_t*)(bb + BL.sel);              // routes selected for application
-    int32_t* l_seloff = (int32_t*)(bb + BL.seloff);        //   and their block offsets
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
 
     const int32_t H = prm.hold_steps, rps = prm.routes_per_step, n_conv = prm.n_conv;
@@ -592,52 +602,69 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         __syncthreads();
     };
 
-    // ---- apply the deferred cache writes of batch routes b < bhi not applied yet,
-    //      only those of worker `only` when only >= 0 (all threads)
-    auto apply = [&](int32_t bhi, int32_t only) {
-        if (wave == 0) {
-            const int32_t b = lane;
-            const bool sel = b < bhi && !r_flag[b] && (only < 0 || r_sig[b] == only);
-            const unsigned long long mb = __ballot(sel);
-            const int32_t rank = __popcll(mb & ((1ull << lane) - 1ull));
-            int32_t total;
-            const int32_t off = ep_wave_excl_sum(sel ? r_P[b] : 0, total);
-            if (sel) {
-                l_sel[rank] = b;
-                l_seloff[rank] = off;
-                r_flag[b] = 1;
-            }
-            if (lane == 0) {
-                sh.seln = __popcll(mb);
-                l_seloff[__popcll(mb)] = total;
-            }
-        }
-        __syncthreads();
-        const int32_t n = sh.seln, total = l_seloff[n];
+    // ---- waves 1-3 while wavefront 0 decides: claim up to KR decided routes at a time (sh.claimed,
+    //      compare-and-swap) and apply their cache writes with the wave's 64 lanes, the claimed
+    //      routes' blocks numbered consecutively; stop once wavefront 0 has stopped and every
+    //      decided route is claimed.  sh.decided and sh.claimed only grow until the workgroup
+    //      synchronizes.
+    auto writer = [&]() {
+        int32_t* woff = sh.woff[wave];
         int my_ins = 0;
-        for (int32_t i = tid; i < total; i += NT) {
-            int32_t lo = 0, hi = n - 1;     // last selected route with l_seloff <= i
-            while (lo < hi) {
-                const int32_t mid = (lo + hi + 1) >> 1;
-                if (l_seloff[mid] <= i) lo = mid;
-                else hi = mid - 1;
+        for (;;) {
+            const int32_t c = __builtin_amdgcn_readfirstlane(
+                __hip_atomic_load(&sh.claimed, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
+            const int32_t d = __builtin_amdgcn_readfirstlane(
+                __hip_atomic_load(&sh.decided, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
+            if (c < d) {
+                const int32_t hi = min(d, c + KR);
+                int32_t won = 0;
+                if (lane == 0) {
+                    int32_t expect = c;
+                    won = __hip_atomic_compare_exchange_strong(&sh.claimed, &expect, hi, __ATOMIC_ACQ_REL,
+                                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                }
+                if (!__builtin_amdgcn_readfirstlane(won)) continue;
+                // routes [c, hi): their blocks numbered consecutively
+                const int32_t nr = hi - c;
+                int32_t tot = 0;
+                const int32_t pr = lane < nr ? r_P[c + lane] : 0;
+                const int32_t off = ep_wave_excl_sum(pr, tot);
+                if (lane < nr) woff[lane] = off;
+                if (lane == 0) woff[nr] = tot;
+                ep_wave_sync();
+                for (int32_t i = lane; i < tot; i += 64) {
+                    int32_t r = 0;
+                    while (r + 1 < nr && woff[r + 1] <= i) ++r;
+                    const int32_t b = c + r;
+                    const int32_t k = i - woff[r];
+                    const int32_t P = r_P[b], sg = r_sig[b];
+                    Slot* tk = g_slots + (uint64_t)sg * S;
+                    uint32_t* tl = g_log + (uint64_t)sg * R;
+                    const uint64_t h = a.chains[r_cb[b] + k];
+                    const uint32_t stamp = r_stamp[b] + (uint32_t)(P - 1 - k);
+                    int ins;
+                    const uint64_t sl = touch_hinted(tk, smask, h, k < r_otab[b], ins, a.status);
+                    // routes of one worker that share a block touch it concurrently: the latest stamp wins
+                    if (sl != ~0ull)
+                        __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
+                    my_ins += ins;
+                }
+                ep_wave_sync();
+                continue;
             }
-            const int32_t b = l_sel[lo];
-            const int32_t k = i - l_seloff[lo];
-            const int32_t P = r_P[b], sg = r_sig[b];
-            Slot* tk = g_slots + (uint64_t)sg * S;
-            uint32_t* tl = g_log + (uint64_t)sg * R;
-            const uint64_t h = a.chains[r_cb[b] + k];
-            const uint32_t stamp = r_stamp[b] + (uint32_t)(P - 1 - k);
-            int ins;
-            const uint64_t sl = touch_hinted(tk, smask, h, k < r_otab[b], ins, a.status);
-            if (sl != ~0ull)
-                __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
-            my_ins += ins;
+            if (__builtin_amdgcn_readfirstlane(
+                    __hip_atomic_load(&sh.stop, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP))) {
+                const int32_t c2 = __builtin_amdgcn_readfirstlane(
+                    __hip_atomic_load(&sh.claimed, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
+                const int32_t d2 = __builtin_amdgcn_readfirstlane(
+                    __hip_atomic_load(&sh.decided, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
+                if (c2 >= d2) break;
+                continue;
+            }
+            __builtin_amdgcn_s_sleep(2);
         }
         if (my_ins) atomicAdd(&sh.ins, my_ins);
-        __syncthreads();
     };
 
     // ---- evict least recently used blocks of worker sg down to the capacity (all threads)
@@ -766,7 +793,6 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             r_turn[b] = (int32_t)turn;
             r_P[b] = P;
             r_cb[b] = cb;
-            r_flag[b] = 0;
             r_last[b] = P > 0 ? a.chains[cb + P - 1] : 0ull;
         }
         __syncthreads();
@@ -799,6 +825,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 n2 = 1;
             }
             sh.nb = n2;
+        }
+        if (tid == 0) {
+            sh.decided = 0;
+            sh.claimed = 0;
+            sh.stop = 0;
         }
         __syncthreads();
         nb = sh.nb;
@@ -836,11 +867,22 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         for (;;) {
             if (wave == 0) {
                 event = EV_BATCH;
+                // lane j < W keeps worker j's load, log tail and block counts in registers
+                int32_t rA = 0, rlive = 0, rused = 0;
+                uint32_t rtail = 0;
+                if (lane < W) {
+                    rA = s_A[lane];
+                    rtail = s_tail[lane];
+                    rlive = s_live[lane];
+                    rused = s_used[lane];
+                }
                 for (;;) {
                     if (!step_open) {
                         // release the routes of step s - H; queue their conversations' next turns
                         const int32_t slot = s % H, sb = slot * rps;
                         if (s >= H) {
+                            if (lane < W) s_A[lane] = rA;
+                            ep_wave_sync();
                             const int32_t nprev = s_stepn[slot];
                             const int32_t qtail = sh.qhead + sh.qsize;
                             int32_t pushed = 0, rel = 0;
@@ -862,6 +904,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                             u_tot -= ep_wave_sum(rel);
                             ep_wave_sync();
                             if (lane == 0) sh.qsize += pushed;
+                            if (lane < W) rA = s_A[lane];
                             ep_wave_sync();
                         }
                         int32_t inflight = 0;
@@ -904,25 +947,27 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     int32_t oj = 0;
                     if (lane < W) {
                         oj = o_cur[b * W + lane];
-                        const float c = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, s_A[lane]);
+                        const float c = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
                         if (a.out.overlap) a.out.overlap[row * W + lane] = oj;
                         if (a.out.cost) a.out.cost[row * W + lane] = c;
                         bits = __float_as_uint(__fadd_rn(c, 0.0f));
                     }
                     const uint32_t mn = ep_wave_min_u32(bits);
                     const int32_t sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
-                    const int32_t osg = __shfl(oj, sg, 64);
-                    const int32_t live_after = s_live[sg] + (scan ? 0 : P - osg);
+                    const int32_t osg = __builtin_amdgcn_readlane(oj, sg);
+                    const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + (scan ? 0 : P - osg);
+                    const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
                     const bool flush = scan || live_after > a.cache;
                     const int32_t rc = r_c[b];
-                    if (lane == 0) {
-                        s_A[sg] += P;
-                        const uint32_t base = s_tail[sg];
-                        s_tail[sg] = base + (uint32_t)P;
+                    if (lane == sg) {
+                        rA += P;
+                        rtail = base + (uint32_t)P;
                         if (!scan) {
-                            s_live[sg] = live_after;
-                            s_used[sg] += P - osg;
+                            rlive = live_after;
+                            rused += P - osg;
                         }
+                    }
+                    if (lane == 0) {
                         r_sig[b] = sg;
                         r_stamp[b] = base;
                         r_otab[b] = o_tab[b * W + sg];
@@ -967,21 +1012,35 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     ++t;
                     ++r_in_step;
                     ep_wave_sync();
+                    if (lane == 0)
+                        __hip_atomic_store(&sh.decided, b + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
                     if (flush) {
                         event = EV_FLUSH;
                         break;
                     }
                 }
-                if (lane == 0) sh.event = event;
+                if (lane < W) {
+                    s_A[lane] = rA;
+                    s_tail[lane] = rtail;
+                    s_live[lane] = rlive;
+                    s_used[lane] = rused;
+                }
+                if (lane == 0) {
+                    sh.event = event;
+                    __hip_atomic_store(&sh.stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                }
+            } else {
+                writer();
             }
             __syncthreads();
             event = sh.event;
             if (event != EV_FLUSH) break;
-            // the route's worker: apply its deferred writes, evict, search the pending requests again
+            // the route's worker (every decided route's writes are in): evict, search the pending
+            // requests again
             const int32_t b = sh.ev_b;
             const int32_t sg = r_sig[b];
-            apply(b + 1, sg);
             if (tid == 0) {
+                sh.stop = 0;
                 if (scan) {
                     s_live[sg] += sh.ins;
                     s_used[sg] += sh.ins;
@@ -1002,10 +1061,6 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             __syncthreads();
         }
 
-        // ---- C. the batch's remaining cache writes
-        if (tid == 0) sh.nb = t - t0;
-        __syncthreads();
-        apply(sh.nb, -1);
         if (tid == 0) sh.ins = 0;
         __syncthreads();
         if (event == EV_DONE) break;
