@@ -74,12 +74,14 @@ def measured_traffic(kernel: str, workload: str):
 def episode_algorithmic_bytes(runner) -> float:
     """Bytes the episode kernel must move per launch, each access counted once
     at its natural width (no cache-line rounding):
-      per episode: clearing W tables of S slots (8 B each);
-      per route:   chain 8P; per worker the probed keys, 8 B each, where the
-                   64-way search probes min(P, 64) positions when P <= 64 and
-                   64 + ceil(P/64) otherwise; the chosen worker's touch of P
-                   blocks (key read 8, stamp write 4, log write 4) and insert of
-                   P - o keys (8 each); 12 B of outputs per worker, 28 B per route;
+      per episode: clearing W tables of S slots (key 8 + stamp 4);
+      per route:   per worker the keys a binary search for the first miss
+                   reads, ceil(log2(P + 1)) probes of 8 B; the chosen worker's
+                   touch of P blocks (chain hash read 8, key read 8, stamp
+                   write 4, log write 4) and insert of P - o keys (8 each);
+                   8 B of outputs per worker (overlap, cost) and 28 B per route;
+                   the first chain hash of the route compared with those of
+                   the other routes of its batch of 64 (8 B each);
       per eviction: log read 4, stamp read 4 and write 4, key read 8."""
     W = runner.W
     n = runner.n_rows
@@ -88,11 +90,11 @@ def episode_algorithmic_bytes(runner) -> float:
     ov = runner.overlap[:n].cpu().numpy()
     o_sig = ov[np.arange(n), sig].astype(np.float64)
     ev = runner.evict_count[:n].cpu().numpy().astype(np.float64)
-    probes = np.where(P <= 64, P, 64 + np.ceil(P / 64.0))
+    probes = np.ceil(np.log2(P + 1.0))
     live_max = runner.cache_blocks + runner.max_blocks      # table slots: next power of two >= 2 * live_max
     S = 1 << int(np.ceil(np.log2(2 * live_max)))
-    b = len(runner.episodes) * W * S * 8.0
-    b += np.sum(8 * P + 8 * W * probes + 16 * P + 8 * (P - o_sig) + 12 * W + 28)
+    b = len(runner.episodes) * W * S * 12.0
+    b += np.sum(8 * W * probes + 28 * P + 8 * (P - o_sig) + 8 * W + 28 + 8 * 63)
     b += np.sum(20 * ev)
     return float(b)
 
