@@ -28,7 +28,10 @@
  *        x  = max(r - 1, 0)
  *        cost = (t1 + t2) + w_sat * (x * x)
  *  - Selection: argmin with temperature 0 (Section 2.2, Eq. router-softmax in
- *    the tau -> 0 limit; Section 4.3), lowest worker index on ties.
+ *    the tau -> 0 limit; Section 4.3), lowest worker index on ties; or, per
+ *    episode, a softmax sample at temperature tau > 0 (Eq. router-softmax), or
+ *    one of the static counterfactual policies of the discussion section
+ *    (round robin, uniform random, power of two choices under the same cost).
  *  - Sequential greedy routing = best-response dynamics (Section 4.3): each
  *    request is routed given the loads and caches left by earlier ones.  The
  *    chosen worker's LRU cache touches the prompt's blocks from last to first
@@ -134,6 +137,98 @@ float orc_route_cost(float w_ov, float w_act, float w_sat, int32_t cap,
     float x = fmaxf(r - 1.0f, 0.0f);
     float t3 = w_sat * (x * x);
     return (t1 + t2) + t3;
+}
+
+/* ------------------------------------------------- worker selection policies
+ * Random draws are inputs: two uniform 32-bit words (r0, r1) per route.
+ */
+#define ORC_POLICY_ARGMIN 0
+#define ORC_POLICY_SOFTMAX 1
+#define ORC_POLICY_ROUND_ROBIN 2
+#define ORC_POLICY_RANDOM 3
+#define ORC_POLICY_P2C 4
+
+/* exp(x) for x <= 0 in float arithmetic (Cody and Waite's argument
+ * reduction): x = n ln2 + r with n = floor(x log2(e) + 1/2), ln2 split into a
+ * part exact in float times n and a small correction, so |r| <= ln2 / 2;
+ * exp(r) by its Taylor series to degree 7 in Horner form (truncation error
+ * below 3e-9 relative); times 2^n built in the exponent field.  Below -87 the
+ * result is 0; x > 0 or NaN gives 1 (not used by the router). */
+float orc_exp_neg(float x)
+{
+    if (!(x <= 0.0f)) return 1.0f;
+    if (x < -87.0f) return 0.0f;
+    const float log2e = 1.44269504088896341f;
+    const float ln2_hi = 0.693145751953125f;          /* 0x3f317200: 9 low mantissa bits clear */
+    const float ln2_lo = 1.42860682030941723212e-6f;  /* ln2 - ln2_hi */
+    const float fn = floorf(x * log2e + 0.5f);
+    const float r = (x - fn * ln2_hi) - fn * ln2_lo;
+    float p = 1.98412698412698412698e-4f;             /* 1/7! */
+    p = p * r + 1.38888888888888888889e-3f;           /* 1/6! */
+    p = p * r + 8.33333333333333333333e-3f;           /* 1/5! */
+    p = p * r + 4.16666666666666666667e-2f;           /* 1/4! */
+    p = p * r + 1.66666666666666666667e-1f;           /* 1/3! */
+    p = p * r + 0.5f;
+    p = p * r + 1.0f;
+    p = p * r + 1.0f;
+    const int32_t n = (int32_t)fn;                    /* -125 .. 0 */
+    union { uint32_t u; float f; } sc;
+    sc.u = (uint32_t)(n + 127) << 23;
+    return p * sc.f;
+}
+
+/* Worker chosen for route t (its index in the episode) from the costs of its
+ * W workers:
+ *   ARGMIN      least cost, lowest index on ties;
+ *   SOFTMAX     with e_j = exp((min_k c_k - c_j) / tau) (Eq. router-softmax
+ *               shifted by the minimum cost, the same distribution), the first
+ *               j whose running sum e_0 + ... + e_j (float, in worker order)
+ *               exceeds u * sum_k e_k, u = (r0 >> 8) / 2^24 in [0, 1); if
+ *               rounding leaves none, the last j with e_j > 0;
+ *   ROUND_ROBIN t mod W;
+ *   RANDOM      floor(r0 * W / 2^32);
+ *   P2C         a = floor(r0 * W / 2^32) and b = floor(r1 * (W-1) / 2^32),
+ *               moved past a (b >= a: b + 1), two distinct uniform workers;
+ *               the cheaper one, the lower index on equal cost.
+ * Returns -1 for an unknown policy. */
+int32_t orc_select(int32_t policy, float tau, int32_t W, const float* cost, int64_t t, uint32_t r0,
+                   uint32_t r1)
+{
+    if (W < 1) return -1;
+    if (policy == ORC_POLICY_ARGMIN) {
+        int32_t s = 0;
+        for (int32_t j = 1; j < W; ++j)
+            if (cost[j] < cost[s]) s = j;
+        return s;
+    }
+    if (policy == ORC_POLICY_SOFTMAX) {
+        float cmin = cost[0];
+        for (int32_t j = 1; j < W; ++j)
+            if (cost[j] < cmin) cmin = cost[j];
+        float total = 0.0f;
+        for (int32_t j = 0; j < W; ++j) total = total + orc_exp_neg((cmin - cost[j]) / tau);
+        const float u = (float)(r0 >> 8) * 5.9604644775390625e-8f;    /* 2^-24 */
+        const float thr = u * total;
+        float run = 0.0f;
+        int32_t last = 0;
+        for (int32_t j = 0; j < W; ++j) {
+            const float e = orc_exp_neg((cmin - cost[j]) / tau);
+            run = run + e;
+            if (e > 0.0f) last = j;
+            if (run > thr) return j;
+        }
+        return last;
+    }
+    if (policy == ORC_POLICY_ROUND_ROBIN) return (int32_t)(t % W);
+    if (policy == ORC_POLICY_RANDOM) return (int32_t)(((uint64_t)r0 * (uint64_t)W) >> 32);
+    if (policy == ORC_POLICY_P2C) {
+        const int32_t a = (int32_t)(((uint64_t)r0 * (uint64_t)W) >> 32);
+        if (W == 1) return 0;
+        int32_t b = (int32_t)(((uint64_t)r1 * (uint64_t)(W - 1)) >> 32);
+        if (b >= a) ++b;
+        return (cost[b] < cost[a] || (cost[b] == cost[a] && b < a)) ? b : a;
+    }
+    return -1;
 }
 
 /* ------------------------------------------------- snapshot scoring (sets) */
@@ -319,6 +414,7 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
                          float w_ov, float w_act, float w_sat, int32_t cap,
                          int32_t controller, float ctrl_w_ov, int32_t ctrl_window,
                          int32_t ctrl_num, int32_t ctrl_den,
+                         int32_t policy, float tau, const uint32_t* rand,
                          int32_t n_conv, const int64_t* turn_off, const int32_t* turn_blocks,
                          const int64_t* chain_off, const uint64_t* chains,
                          int32_t* route_turn, int32_t* route_worker, int32_t* route_step,
@@ -331,6 +427,10 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
     if (W < 1 || cache_blocks < 1 || H < 1 || routes_per_step < 1 || cap < 1 || n_conv < 0)
         return ORC_EINVAL;
     if (controller && (ctrl_window < 1 || ctrl_den < 1 || ctrl_num < 0)) return ORC_EINVAL;
+    if (policy < ORC_POLICY_ARGMIN || policy > ORC_POLICY_P2C) return ORC_EINVAL;
+    if (policy == ORC_POLICY_SOFTMAX && !(tau > 0.0f)) return ORC_EINVAL;
+    if (!rand && (policy == ORC_POLICY_SOFTMAX || policy == ORC_POLICY_RANDOM || policy == ORC_POLICY_P2C))
+        return ORC_EINVAL;
     const int64_t n_routes = turn_off[n_conv];
     int32_t max_P = 0;
     for (int32_t c = 0; c < n_conv; ++c) {
@@ -405,16 +505,15 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
             }
             prev_active = active;
 
-            float best = 0.0f;
-            int32_t sigma = -1;
             for (int32_t j = 0; j < W; ++j) {
                 int32_t o = lru_overlap(&lru[j], h, P);
                 float cj = orc_route_cost(w_eff, w_act, w_sat, cap, P, o, A[j]);
                 o_row[j] = o;
                 overlap[t * W + j] = o;
                 cost[t * W + j] = cj;
-                if (sigma < 0 || cj < best) { best = cj; sigma = j; }
             }
+            const int32_t sigma = orc_select(policy, tau, W, cost + t * W, t, rand ? rand[2 * t] : 0u,
+                                             rand ? rand[2 * t + 1] : 0u);
 
             int err = 0;
             for (int32_t k2 = P - 1; k2 >= 0; --k2) lru_touch(&lru[sigma], h[k2], &err);

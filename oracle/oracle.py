@@ -64,9 +64,14 @@ def lib():
             L.orc_simulate_episode.restype = C.c_int
             L.orc_simulate_episode.argtypes = [
                 i32, i32, i32, i32, f32, f32, f32, i32, i32, f32, i32, i32, i32,
+                i32, f32, p,
                 i32, p, p, p, p,
                 p, p, p, p, p, p, p, p, p, p,
                 p, p, p, i64, p]
+            L.orc_exp_neg.restype = f32
+            L.orc_exp_neg.argtypes = [f32]
+            L.orc_select.restype = i32
+            L.orc_select.argtypes = [i32, f32, i32, p, i64, C.c_uint32, C.c_uint32]
             L.orc_poa_matrix.restype = C.c_int
             L.orc_poa_matrix.argtypes = [i32, i32, p, p, p, f32, f32, f32, i32, i32, f32, p, p]
             L.orc_poa_window.restype = C.c_int
@@ -174,9 +179,22 @@ def score_batch(chains, chain_off, keys, key_off, active, w_ov=1.0, w_act=0.5, w
 
 # ------------------------------------------------------------------ episodes
 
+def exp_neg(x: float) -> float:
+    """The oracle's float exp for x <= 0 (Cody-Waite reduction, Taylor degree 7)."""
+    return float(lib().orc_exp_neg(float(x)))
+
+
+def select(policy: int, tau: float, costs, t: int = 0, r0: int = 0, r1: int = 0) -> int:
+    """Worker a route with these float costs is sent to under a selection policy."""
+    c = _c(costs, np.float32)
+    return int(lib().orc_select(int(policy), float(tau), int(c.shape[0]), _ptr(c), int(t), int(r0), int(r1)))
+
+
 def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, chains,
-                     dump: bool = False, evicted_cap: int = 0) -> Dict[str, np.ndarray]:
-    """One routing episode; arrays must be rebased (turn_off[0] == chain_off[0] == 0)."""
+                     dump: bool = False, evicted_cap: int = 0, rand=None) -> Dict[str, np.ndarray]:
+    """One routing episode; arrays must be rebased (turn_off[0] == chain_off[0] == 0).
+    rand: two uint32 words per route (the stochastic policies' draws); drawn by
+    workload.route_rand when not given."""
     turn_off = _c(turn_off, np.int64)
     turn_blocks = _c(turn_blocks, np.int32)
     chain_off = _c(chain_off, np.int64)
@@ -190,6 +208,16 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         overlap=np.zeros((n, W), np.int32), cost=np.zeros((n, W), np.float32),
         evict_count=np.zeros(n, np.int32), evict_digest=np.zeros(n, np.uint64),
         last_hash=np.zeros(n, np.uint64), totals=np.zeros(8, np.int64))
+    policy = int(getattr(spec, "policy", 0))
+    tau = float(getattr(spec, "tau", 0.0))
+    if rand is None:
+        if policy in (1, 3, 4):         # softmax, random, power of two choices draw per route
+            from paper_2606_17081_amd.workload import route_rand
+            rand = route_rand(spec, n)
+        else:
+            rand = np.zeros(2 * n, np.uint32)
+    rand = _c(rand, np.uint32)
+    assert rand.shape[0] >= 2 * n
     fk = np.zeros((W, cache_blocks), np.uint64) if dump else None
     fc = np.zeros(W, np.int32) if dump else None
     ek = np.zeros(max(evicted_cap, 1), np.uint64) if evicted_cap > 0 else None
@@ -199,6 +227,7 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         W, cache_blocks, spec.hold_steps, spec.routes_per_step,
         spec.w_ov, spec.w_act, spec.w_sat, spec.cap,
         spec.controller, spec.ctrl_w_ov, spec.ctrl_window, spec.ctrl_num, spec.ctrl_den,
+        policy, tau, g(rand),
         n_conv, _ptr(turn_off), g(turn_blocks), _ptr(chain_off), g(chains),
         g(out["route_turn"]), g(out["route_worker"]), g(out["route_step"]),
         g(out["route_blocks"]), g(out["overlap"]), g(out["cost"]),

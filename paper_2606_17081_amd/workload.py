@@ -224,10 +224,31 @@ class EpisodeSpec:
     ctrl_window: int = 128
     ctrl_num: int = 9         # threshold num/den of mean load per unit capacity
     ctrl_den: int = 10
+    policy: int = 0           # POLICY_ARGMIN, POLICY_SOFTMAX, POLICY_ROUND_ROBIN, POLICY_RANDOM, POLICY_P2C
+    tau: float = 0.0          # softmax temperature (> 0 with POLICY_SOFTMAX), in cost units
 
     @property
     def routes_per_step(self) -> int:
         return self.concurrency // self.hold_steps
+
+
+# Worker-selection policies of an episode (the routing library's RK_POLICY_* codes).
+POLICY_ARGMIN = 0        # least cost, lowest index on ties (temperature 0)
+POLICY_SOFTMAX = 1       # sample by exp(-cost / tau)
+POLICY_ROUND_ROBIN = 2   # route t goes to worker t mod W
+POLICY_RANDOM = 3        # uniform worker
+POLICY_P2C = 4           # two distinct uniform candidates, the cheaper one
+POLICY_NAMES = {POLICY_ARGMIN: "argmin", POLICY_SOFTMAX: "softmax", POLICY_ROUND_ROBIN: "round-robin",
+                POLICY_RANDOM: "random", POLICY_P2C: "power-of-two"}
+
+
+def route_rand(spec: "EpisodeSpec", n_routes: int) -> np.ndarray:
+    """Two uniform 32-bit words per route of an episode, in routing order (the
+    random draws of the stochastic policies, passed to the router as inputs)."""
+    ss = np.random.SeedSequence([0x5EED, int(spec.seed), int(spec.concurrency), int(spec.policy),
+                                 int(round(float(spec.tau) * 1e6))])
+    return np.random.Generator(np.random.PCG64(ss)).integers(0, 1 << 32, size=2 * n_routes,
+                                                             dtype=np.uint64).astype(np.uint32)
 
 
 @dataclass
@@ -261,6 +282,21 @@ def sweep70b_workload(seeds: Sequence[int] = range(64), concurrency: Sequence[in
     eps = [EpisodeSpec(seed=int(s), concurrency=int(C), cap=32768)
            for C in concurrency for s in seeds]
     return Workload("sweep70b", W=6, cache_blocks=65536, traces=traces, episodes=eps)
+
+
+# The static counterfactual policies next to the router's own (argmin and a
+# softmax whose temperature is in cost units, i.e. blocks).
+POLICY_SWEEP = ((POLICY_ARGMIN, 0.0), (POLICY_SOFTMAX, 16.0), (POLICY_ROUND_ROBIN, 0.0),
+                (POLICY_RANDOM, 0.0), (POLICY_P2C, 0.0))
+
+
+def policy_workload(seeds: Sequence[int] = range(16), concurrency: Sequence[int] = SWEEP70B_C,
+                    policies: Sequence = POLICY_SWEEP, n_req: int = 4096) -> Workload:
+    """The 1P/5D-shaped sweep traces routed by each selection policy."""
+    traces = {int(s): sweep70b_trace(int(s), n_req) for s in seeds}
+    eps = [EpisodeSpec(seed=int(s), concurrency=int(C), cap=32768, policy=int(p), tau=float(tau))
+           for p, tau in policies for C in concurrency for s in seeds]
+    return Workload("policies", W=6, cache_blocks=65536, traces=traces, episodes=eps)
 
 
 def saturation_workload(seeds: Sequence[int] = range(256), concurrency: Sequence[int] = SATURATION_C,

@@ -33,8 +33,9 @@ def overlap_set(chain, cached: set) -> int:
 
 
 def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blocks, chains_per_conv,
-            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10):
-    """Sequential greedy routing episode with OrderedDict LRU caches."""
+            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10, select=None):
+    """Sequential routing episode with OrderedDict LRU caches; select(costs, t)
+    picks the worker of route t (default: least cost, lowest index)."""
     n_conv = len(turn_off) - 1
     caches = [OrderedDict() for _ in range(W)]   # key -> None, oldest first
     A = [0] * W
@@ -68,10 +69,13 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
                 w_eff = min(f32(w_ov), f32(ctrl_w_ov))
             ovl = [overlap_set(h, caches[j].keys()) for j in range(W)]
             costs = [cost_f32(w_eff, w_act, w_sat, cap, P, ovl[j], A[j]) for j in range(W)]
-            sigma = 0
-            for j in range(1, W):
-                if costs[j] < costs[sigma]:
-                    sigma = j
+            if select is None:
+                sigma = 0
+                for j in range(1, W):
+                    if costs[j] < costs[sigma]:
+                        sigma = j
+            else:
+                sigma = int(select(costs, len(routes)))
             cache = caches[sigma]
             for k in range(P - 1, -1, -1):
                 if h[k] in cache:
