@@ -65,6 +65,7 @@ typedef enum {
 #define RK_DEV_TABLE_FULL    0x8   /* an insert found no empty slot                      */
 #define RK_DEV_TOO_LARGE     0x10  /* a window or prompt exceeded the launch's maximum   */
 #define RK_DEV_NO_CONVERGE   0x20  /* the assignment solver hit its iteration bound      */
+#define RK_DEV_BAD_PARAMS    0x40  /* an episode's policy parameters were invalid       */
 
 /* Static message for a status code. */
 const char* rk_status_string(int status);
@@ -214,6 +215,26 @@ int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains, const int
  *     (a sample is taken after every route; at least ctrl_window samples are
  *     needed), a load-triggered switch of the overlap weight in the spirit of
  *     Section 6.3;
+ *   - the worker sigma is chosen by the episode's policy from the W costs of
+ *     route t (its index in the episode) and the two random words r0, r1 of
+ *     its output row (route_rand[2 * row], route_rand[2 * row + 1]):
+ *       RK_POLICY_ARGMIN      least cost, lowest index on ties (temperature 0,
+ *                             Section 2.2 and Section 4.3);
+ *       RK_POLICY_SOFTMAX     a sample of Eq. router-softmax at temperature
+ *                             tau > 0 (cost units): with e_j = exp((min_k c_k
+ *                             - c_j) / tau) in float (exp by Cody-Waite
+ *                             reduction and a degree-7 Taylor series, each
+ *                             operation rounded), the first j whose running
+ *                             sum e_0 + ... + e_j exceeds u * sum_k e_k,
+ *                             u = (r0 >> 8) / 2^24, else the last j with
+ *                             e_j > 0;
+ *       RK_POLICY_ROUND_ROBIN t mod W;
+ *       RK_POLICY_RANDOM      floor(r0 * W / 2^32);
+ *       RK_POLICY_P2C         the cheaper of a = floor(r0 * W / 2^32) and
+ *                             b = floor(r1 * (W-1) / 2^32) (+1 when b >= a),
+ *                             lower index on equal cost;
+ *     the last three are the static counterfactual policies of the
+ *     discussion section, under the same cost;
  *   - the chosen worker sigma touches the prompt's blocks from last to first
  *     (block 0 ends most recent), inserting those it lacks, then evicts least
  *     recently used blocks until it holds at most cache_blocks; A_sigma += P.
@@ -233,7 +254,16 @@ typedef struct {
     float   w_ov, w_act, w_sat;   /* >= 0                                              */
     float   ctrl_w_ov;       /* weight used while the controller is active, >= 0       */
     int64_t out_base;        /* first output row of this episode                       */
-} rk_episode_params;         /* 64 bytes */
+    int32_t policy;          /* RK_POLICY_*                                            */
+    float   tau;             /* softmax temperature, > 0 with RK_POLICY_SOFTMAX        */
+} rk_episode_params;         /* 72 bytes; invalid policy fields set RK_DEV_BAD_PARAMS and
+                                leave the episode's outputs unwritten                 */
+
+#define RK_POLICY_ARGMIN      0
+#define RK_POLICY_SOFTMAX     1
+#define RK_POLICY_ROUND_ROBIN 2
+#define RK_POLICY_RANDOM      3
+#define RK_POLICY_P2C         4
 
 typedef struct {
     int32_t E;                       /* episodes (>= 0)                                 */
@@ -256,6 +286,9 @@ typedef struct {
                                         first P blocks of its conversation's chain       */
     const int64_t* chain_off;        /* chain of conversation c: chains[chain_off[c] .. chain_off[c+1]) */
     const uint64_t* chains;          /* block-hash chains (rk_hash_chains)              */
+    const uint32_t* route_rand;      /* 2 uniform 32-bit words per output row, read by the
+                                        SOFTMAX, RANDOM and P2C policies; may be NULL when
+                                        no episode uses them                             */
 } rk_episode_batch;
 
 /* Outputs, one row per route in routing order, written at out_base + t of the

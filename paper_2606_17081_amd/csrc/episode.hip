@@ -52,6 +52,7 @@ struct EpArgs {
     const int32_t* turn_blocks;
     const int64_t* chain_off;
     const uint64_t* chains;
+    const uint32_t* route_rand;
     rk_episode_outputs out;
     unsigned char* ws;
     EpisodeLayout L;
@@ -62,7 +63,7 @@ struct EpArgs {
 constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 
 struct EpShared {
-    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop;
+    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone;
     int32_t woff[NW][KR + 1];
     uint32_t new_head;
     int64_t ev_row, ev_total;
@@ -427,7 +428,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
-    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, lcp, bytes;
+    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rrnd, lcp, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
@@ -452,6 +453,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
     b.rsig = take(nb * 4, 4);
     b.rotab = take(nb * 4, 4);
     b.rstamp = take(nb * 4, 4);
+    b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
     b.bytes = (o + 15) / 16 * 16;
     return b;
@@ -493,6 +495,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     int32_t* r_sig = (int32_t*)(bb + BL.rsig);             // chosen worker
     int32_t* r_otab = (int32_t*)(bb + BL.rotab);           // blocks known cached in sigma's table
     uint32_t* r_stamp = (uint32_t*)(bb + BL.rstamp);       // stamp of the last block
+    uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
 
     const int32_t H = prm.hold_steps, rps = prm.routes_per_step, n_conv = prm.n_conv;
@@ -502,6 +505,14 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                                          prm.ctrl_den < 1 || prm.ctrl_num < 0));
     if (bad) {
         if (tid == 0) atomicOr(a.status, RK_DEV_TOO_LARGE);
+        return;
+    }
+    const int32_t policy = prm.policy;
+    const float tau = prm.tau;
+    const bool draws = policy == RK_POLICY_SOFTMAX || policy == RK_POLICY_RANDOM || policy == RK_POLICY_P2C;
+    if (policy < RK_POLICY_ARGMIN || policy > RK_POLICY_P2C || (policy == RK_POLICY_SOFTMAX && !(tau > 0.0f)) ||
+        (draws && !a.route_rand)) {
+        if (tid == 0) atomicOr(a.status, RK_DEV_BAD_PARAMS);
         return;
     }
     const int64_t gc0 = prm.conv_begin;
@@ -548,6 +559,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         sh.qsize = qn;
         sh.ins = 0;
         sh.ev_total = 0;
+        sh.tdone = 0;
     }
     __syncthreads();
     const int32_t qcap = n_conv + 1;
@@ -794,6 +806,9 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             r_P[b] = P;
             r_cb[b] = cb;
             r_last[b] = P > 0 ? a.chains[cb + P - 1] : 0ull;
+            const int64_t row = prm.out_base + (int64_t)sh.tdone + b;
+            r_rnd[2 * b] = draws ? a.route_rand[2 * row] : 0u;
+            r_rnd[2 * b + 1] = draws ? a.route_rand[2 * row + 1] : 0u;
         }
         __syncthreads();
         // workers without room for every block of the batch are compacted first; the batch is cut to
@@ -945,15 +960,50 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     const int64_t row = prm.out_base + (int64_t)t;
                     uint32_t bits = 0xFFFFFFFFu;
                     int32_t oj = 0;
+                    float cj = 0.0f;
                     if (lane < W) {
                         oj = o_cur[b * W + lane];
-                        const float c = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
+                        cj = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
                         if (a.out.overlap) a.out.overlap[row * W + lane] = oj;
-                        if (a.out.cost) a.out.cost[row * W + lane] = c;
-                        bits = __float_as_uint(__fadd_rn(c, 0.0f));
+                        if (a.out.cost) a.out.cost[row * W + lane] = cj;
+                        bits = __float_as_uint(__fadd_rn(cj, 0.0f));
                     }
-                    const uint32_t mn = ep_wave_min_u32(bits);
-                    const int32_t sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
+                    int32_t sg;
+                    if (policy == RK_POLICY_ARGMIN) {
+                        const uint32_t mn = ep_wave_min_u32(bits);
+                        sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
+                    } else if (policy == RK_POLICY_SOFTMAX) {
+                        // weights exp((c_min - c_j) / tau); running sums in worker order
+                        const float cmin = __uint_as_float(ep_wave_min_u32(bits));
+                        const float ej = lane < W ? exp_neg_f32(__fdiv_rn(__fsub_rn(cmin, cj), tau)) : 0.0f;
+                        float total = 0.0f;
+                        for (int32_t j = 0; j < W; ++j)
+                            total = __fadd_rn(total, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j)));
+                        const float u = __fmul_rn((float)(r_rnd[2 * b] >> 8), 5.9604644775390625e-8f);
+                        const float thr = __fmul_rn(u, total);
+                        float run = 0.0f;
+                        int32_t last = 0;
+                        sg = -1;
+                        for (int32_t j = 0; j < W && sg < 0; ++j) {
+                            const float e = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j));
+                            run = __fadd_rn(run, e);
+                            if (e > 0.0f) last = j;
+                            if (run > thr) sg = j;
+                        }
+                        if (sg < 0) sg = last;
+                    } else if (policy == RK_POLICY_ROUND_ROBIN) {
+                        sg = t % W;
+                    } else {
+                        const int32_t ca = (int32_t)(((uint64_t)r_rnd[2 * b] * (uint64_t)W) >> 32);
+                        sg = ca;
+                        if (policy == RK_POLICY_P2C && W > 1) {
+                            int32_t cb2 = (int32_t)(((uint64_t)r_rnd[2 * b + 1] * (uint64_t)(W - 1)) >> 32);
+                            if (cb2 >= ca) ++cb2;
+                            const float fa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), ca));
+                            const float fb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), cb2));
+                            if (fb < fa || (fb == fa && cb2 < ca)) sg = cb2;
+                        }
+                    }
                     const int32_t osg = __builtin_amdgcn_readlane(oj, sg);
                     const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + (scan ? 0 : P - osg);
                     const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
@@ -1027,6 +1077,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 }
                 if (lane == 0) {
                     sh.event = event;
+                    sh.tdone = t;
                     __hip_atomic_store(&sh.stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
                 }
             } else {
@@ -1131,6 +1182,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.turn_blocks = b->turn_blocks;
     a.chain_off = b->chain_off;
     a.chains = b->chains;
+    a.route_rand = b->route_rand;
     a.out = *out;
     a.ws = (unsigned char*)workspace;
     a.L = L;

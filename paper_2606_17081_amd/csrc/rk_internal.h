@@ -57,6 +57,29 @@ __device__ __forceinline__ float route_cost(float w_ov, float w_act, float w_sat
     return __fadd_rn(__fadd_rn(t1, t2), t3);
 }
 
+// exp(x) for x <= 0 in float, Cody and Waite's method: x = n ln2 + r with
+// n = floor(x log2(e) + 1/2) and ln2 split into a part exact in float and a
+// correction, |r| <= ln2/2; exp(r) by its Taylor series to degree 7 (Horner);
+// times 2^n through the exponent field.  Every operation is rounded on its
+// own.  Below -87 the result is 0; x > 0 or NaN gives 1.
+__device__ __forceinline__ float exp_neg_f32(float x)
+{
+    if (!(x <= 0.0f)) return 1.0f;
+    if (x < -87.0f) return 0.0f;
+    const float n = floorf(__fadd_rn(__fmul_rn(x, 1.44269504088896341f), 0.5f));
+    const float r = __fsub_rn(__fsub_rn(x, __fmul_rn(n, 0.693145751953125f)),
+                              __fmul_rn(n, 1.42860682030941723212e-6f));
+    float p = 1.98412698412698412698e-4f;                      // 1/7!
+    p = __fadd_rn(__fmul_rn(p, r), 1.38888888888888888889e-3f);   // 1/6!
+    p = __fadd_rn(__fmul_rn(p, r), 8.33333333333333333333e-3f);   // 1/5!
+    p = __fadd_rn(__fmul_rn(p, r), 4.16666666666666666667e-2f);   // 1/4!
+    p = __fadd_rn(__fmul_rn(p, r), 1.66666666666666666667e-1f);   // 1/3!
+    p = __fadd_rn(__fmul_rn(p, r), 0.5f);
+    p = __fadd_rn(__fmul_rn(p, r), 1.0f);
+    p = __fadd_rn(__fmul_rn(p, r), 1.0f);
+    return __fmul_rn(p, __uint_as_float((uint32_t)((int32_t)n + 127) << 23));
+}
+
 // Key whose unsigned order is (cost, worker) lexicographic for cost >= 0.
 __device__ __forceinline__ uint64_t argmin_key(float c, int32_t j)
 {

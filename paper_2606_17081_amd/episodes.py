@@ -14,7 +14,7 @@ from typing import Dict, List, Optional, Sequence
 import numpy as np
 
 from . import rkroute as rk
-from .workload import POA_PARAMS, EpisodeSpec, Workload, flatten_traces
+from .workload import POA_PARAMS, EpisodeSpec, Workload, flatten_traces, route_rand
 
 
 class EpisodeRunner:
@@ -55,7 +55,8 @@ class EpisodeRunner:
             tb = int(flat.turn_off[cb])
             n_routes = int(flat.turn_off[cb + nc]) - tb
             prm[e] = (cb, nc, sp.hold_steps, sp.routes_per_step, sp.controller, sp.ctrl_window,
-                      sp.ctrl_num, sp.ctrl_den, sp.cap, sp.w_ov, sp.w_act, sp.w_sat, sp.ctrl_w_ov, out_base)
+                      sp.ctrl_num, sp.ctrl_den, sp.cap, sp.w_ov, sp.w_act, sp.w_sat, sp.ctrl_w_ov, out_base,
+                      sp.policy, sp.tau)
             self.rows.append((out_base, n_routes, cb, tb))
             for k in range(0, n_routes, sp.concurrency):
                 win_off.append(out_base + min(k + sp.concurrency, n_routes))
@@ -63,6 +64,14 @@ class EpisodeRunner:
             out_base += n_routes
         self.n_rows = out_base
         self.params_host = prm
+        # the stochastic policies' draws: two words per output row (inputs, seeded per episode)
+        self.route_rand = None
+        if any(sp.policy in (rk.RK_POLICY_SOFTMAX, rk.RK_POLICY_RANDOM, rk.RK_POLICY_P2C)
+               for sp in self.episodes):
+            rr = np.zeros(2 * max(out_base, 1), np.uint32)
+            for sp, (b0, n_routes, _, _) in zip(self.episodes, self.rows):
+                rr[2 * b0: 2 * (b0 + n_routes)] = route_rand(sp, n_routes)
+            self.route_rand = up(rr.view(np.int32), torch.int32)
         self.params = up(prm.view(np.uint8), torch.uint8)
         self.max_blocks = max(int(flat.turn_blocks.max()) if flat.turn_blocks.size else 1, 1)
         self.max_conv = max((flat.conv_count[sp.seed] for sp in self.episodes), default=0)
@@ -102,7 +111,7 @@ class EpisodeRunner:
         self.batch = rk.EpisodeBatch(E, W, self.cache_blocks, self.max_blocks, self.max_conv,
                                      self.max_inflight, self.max_rps, self.max_ctrl_window, probe_mode, 0,
                                      P(self.params), P(self.turn_off), P(self.turn_blocks), P(self.chain_off),
-                                     P(self.chains))
+                                     P(self.chains), P(self.route_rand))
         self.outputs = rk.EpisodeOutputs(P(self.route_turn), P(self.route_worker), P(self.route_step),
                                          P(self.route_blocks), P(self.overlap), P(self.cost),
                                          P(self.evict_count), P(self.evict_digest), P(self.last_hash),

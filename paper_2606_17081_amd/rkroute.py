@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(HERE, "librkroute.so")
 
 RK_OK, RK_EINVAL, RK_ENOMEM, RK_EHIP, RK_ETABLEFULL, RK_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 RK_PROBE_PREFIX, RK_PROBE_SCAN = 0, 1
+RK_POLICY_ARGMIN, RK_POLICY_SOFTMAX, RK_POLICY_ROUND_ROBIN, RK_POLICY_RANDOM, RK_POLICY_P2C = range(5)
 DEV_BITS = {0x1: "bad offsets", 0x2: "short input", 0x4: "zero key", 0x8: "table full",
-            0x10: "too large", 0x20: "no convergence"}
+            0x10: "too large", 0x20: "no convergence", 0x40: "bad policy parameters"}
 
 EXPORTED = ("rk_status_string", "rk_last_error", "rk_device_status", "rk_hash_chains",
             "rk_table_build", "rk_route_score_batch", "rk_index_build", "rk_route_score_index",
@@ -48,7 +49,7 @@ class EpisodeBatch(C.Structure):
                 ("max_routes_per_step", C.c_int32), ("max_ctrl_window", C.c_int32),
                 ("probe_mode", C.c_int32), ("reserved", C.c_int32),
                 ("params", C.c_void_p), ("turn_off", C.c_void_p), ("turn_blocks", C.c_void_p),
-                ("chain_off", C.c_void_p), ("chains", C.c_void_p)]
+                ("chain_off", C.c_void_p), ("chains", C.c_void_p), ("route_rand", C.c_void_p)]
 
 
 class EpisodeOutputs(C.Structure):
@@ -62,8 +63,8 @@ EPISODE_PARAMS_DTYPE = np.dtype([
     ("conv_begin", "<i8"), ("n_conv", "<i4"), ("hold_steps", "<i4"), ("routes_per_step", "<i4"),
     ("controller", "<i4"), ("ctrl_window", "<i4"), ("ctrl_num", "<i4"), ("ctrl_den", "<i4"),
     ("cap_blocks", "<i4"), ("w_ov", "<f4"), ("w_act", "<f4"), ("w_sat", "<f4"),
-    ("ctrl_w_ov", "<f4"), ("out_base", "<i8")])
-assert EPISODE_PARAMS_DTYPE.itemsize == 64
+    ("ctrl_w_ov", "<f4"), ("out_base", "<i8"), ("policy", "<i4"), ("tau", "<f4")])
+assert EPISODE_PARAMS_DTYPE.itemsize == 72
 
 _lock = threading.Lock()
 _lib = None

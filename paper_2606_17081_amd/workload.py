@@ -245,8 +245,8 @@ POLICY_NAMES = {POLICY_ARGMIN: "argmin", POLICY_SOFTMAX: "softmax", POLICY_ROUND
 def route_rand(spec: "EpisodeSpec", n_routes: int) -> np.ndarray:
     """Two uniform 32-bit words per route of an episode, in routing order (the
     random draws of the stochastic policies, passed to the router as inputs)."""
-    ss = np.random.SeedSequence([0x5EED, int(spec.seed), int(spec.concurrency), int(spec.policy),
-                                 int(round(float(spec.tau) * 1e6))])
+    ss = np.random.SeedSequence([0x5EED, int(spec.seed), int(spec.concurrency), int(spec.policy) & 0xFFFFFFFF,
+                                 int(np.float32(spec.tau).view(np.uint32))])
     return np.random.Generator(np.random.PCG64(ss)).integers(0, 1 << 32, size=2 * n_routes,
                                                              dtype=np.uint64).astype(np.uint32)
 
