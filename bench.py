@@ -248,6 +248,43 @@ def scoring_bench(torch, rk, wl, stream, steps):
                                    "algorithmic_bytes": ialg}}}
 
 
+def policy_bench(torch, rk, wl, stream, steps):
+    """The 1P/5D-shaped traces under every selection policy (the router's
+    argmin and softmax, and the static round-robin, random and power-of-two
+    policies): 16 seeds x 5 concurrency levels x 5 policies in one launch;
+    PoA-hat per policy and concurrency level."""
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    log("generating the policy sweep (16 traces, 400 episodes)")
+    w = wl.policy_workload()
+    r = EpisodeRunner(w, keep_cost=False)
+    r.hash()
+    r.simulate()
+    r.poa()
+    torch.cuda.synchronize()
+    ts, tp = KernelTimer(torch, stream), KernelTimer(torch, stream)
+    for _ in range(max(1, steps // 2)):
+        with ts:
+            r.simulate()
+        with tp:
+            r.poa()
+    torch.cuda.synchronize()
+    assert rk.device_status(reset=True) == 0
+    poa = r.poa_hat[: len(r.episodes)].cpu().numpy()
+    out = {}
+    for p, tau in wl.POLICY_SWEEP:
+        name = wl.POLICY_NAMES[p] + (f" tau={tau:g}" if p == wl.POLICY_SOFTMAX else "")
+        by_c = {}
+        for C in wl.SWEEP70B_C:
+            v = np.array([poa[e] for e, sp in enumerate(r.episodes) if sp.policy == p and sp.concurrency == C])
+            by_c[str(C)] = [round(float(v.mean()), 6), round(float(v.std()), 6)]
+        out[name] = by_c
+    E = len(r.episodes)
+    log(f"policies: {E} episodes, simulate {ts.mean_ms():.3f} ms, PoA {tp.mean_ms():.3f} ms")
+    return {"workload": "1P/5D-shaped traces, W=6, 4096 requests, C in {32..512} x 16 seeds x 5 policies",
+            "episodes": E, "simulate_ms": round(ts.mean_ms(), 4), "poa_ms": round(tp.mean_ms(), 4),
+            "episodes_per_s": E / (ts.mean_ms() * 1e-3), "poa_hat_by_policy_and_C": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -256,7 +293,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-scoring", action="store_true")
     ap.add_argument("--cpu-seeds", type=int, default=64)
-    ap.add_argument("--only", choices=("all", "sweep", "scoring"), default="all",
+    ap.add_argument("--no-policies", action="store_true")
+    ap.add_argument("--only", choices=("all", "sweep", "scoring", "policies"), default="all",
                     help="profiling passes: run only the sweep step or only the scoring kernel")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this size (counter calibration)")
@@ -287,6 +325,10 @@ def main():
     if args.only == "scoring":
         score = scoring_bench(torch, rk, wl, torch.cuda.current_stream(), args.steps)
         print(json.dumps({"score_batch": score}), flush=True)
+        return
+    if args.only == "policies":
+        pol = policy_bench(torch, rk, wl, torch.cuda.current_stream(), args.steps)
+        print(json.dumps({"policies": pol}), flush=True)
         return
     log("generating the sweep (64 traces of 4,096 requests)")
     w = wl.sweep70b_workload()
@@ -346,6 +388,11 @@ def main():
         torch.cuda.empty_cache()
         score = scoring_bench(torch, rk, wl, stream, args.steps)
 
+    pol = None
+    if not args.no_policies and args.only == "all":
+        torch.cuda.empty_cache()
+        pol = policy_bench(torch, rk, wl, stream, args.steps)
+
     cpu = None
     if not args.no_cpu_baseline and args.only == "all":
         threads = max(1, min(16, os.cpu_count() or 1))
@@ -373,6 +420,7 @@ def main():
         "poa_hat_by_C": per_C,
         "roofline": roofline,
         "score_batch": score,
+        "policies": pol,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
