@@ -42,9 +42,17 @@
  *    flight once the ramp is over (the semaphore-held concurrency of
  *    Section 7.4).  A conversation's next turn joins the queue when its
  *    previous turn is released.
- *  - Controller: a route uses min(w_ov, ctrl_w_ov) when the mean, over the
+ *  - Controller 1: a route uses min(w_ov, ctrl_w_ov) when the mean, over the
  *    last ctrl_window routes, of sum_j A_j / (W * cap) exceeds num/den
  *    (integer test), in the spirit of the regime switch of Section 6.3.
+ *  - Controller 2, the regime controller of Sections 6.2-6.3: after every
+ *    route the chosen worker's latency f(n) = a n + b + d / max(n_sat - n,
+ *    1)^beta (Eq. latency-superlinear, n its requests in flight including the
+ *    new one) stands in for TTFT; its EWMA (Eq. saturation-signal, weight
+ *    alpha per route) sets the regime Below / Transition / Saturated
+ *    (Eq. saturation-state) with k-sample hysteresis and margin eps, and the
+ *    regime sets the next routes' temperature and overlap weight
+ *    (Tab. regime-params).  fp64.
  *  - PoA-hat (Section 6.4, Eq. poa-estimate): per window of consecutive
  *    routes, a frozen cost matrix c_ij = a n_j + b + d / (C_j - n_j)^beta
  *    - w_c o_ij / P_i, where n_j is the window's request count on worker j;
@@ -399,8 +407,10 @@ static int32_t lru_overlap(const lru_t* c, const uint64_t* h, int32_t P)
  * totals[0] sum over routes of (P - o) on the chosen worker (recomputed blocks)
  * totals[1] evicted blocks
  * totals[2] sum of P
- * totals[3] routes that used the controller's overlap weight
- * totals[4] controller activations (inactive -> active transitions)
+ * totals[3] routes that used the controller's overlap weight (controller 1), or
+ *           that were routed outside the Below regime (controller 2)
+ * totals[4] controller activations (inactive -> active transitions), or regime
+ *           moves up (controller 2)
  * totals[5] routing steps (index of the last step that routed, plus one)
  * totals[6] sum over routes of o on the chosen worker
  * totals[7] final sum of cached blocks over workers
@@ -410,11 +420,55 @@ static int32_t lru_overlap(const lru_t* c, const uint64_t* h, int32_t P)
  * number; evicted_keys [evicted_cap] lists evicted keys in eviction order and
  * *n_evicted counts all evictions.
  */
+/* Regime controller state after one sample of the latency signal (fp64):
+ * ewma = lat for the first sample, else alpha * lat + (1 - alpha) * ewma;
+ * Below -> Transition after k consecutive samples with ewma > theta1,
+ * Transition -> Saturated after k with ewma >= theta2,
+ * Transition -> Below after k with ewma < theta1 - eps,
+ * Saturated -> Transition after k with ewma < theta2 - eps;
+ * one regime step per sample, counters restart after a change.
+ * Returns 1 when the regime moved up. */
+int orc_regime_step(const double* rg_d, const int32_t* rg_i, double lat, int64_t sample, double* ewma,
+                    int32_t* regime, int32_t* up, int32_t* down)
+{
+    const double alpha = rg_d[0], theta1 = rg_d[1], theta2 = rg_d[2], eps = rg_d[3];
+    const int32_t k = rg_i[0];
+    *ewma = sample == 0 ? lat : alpha * lat + (1.0 - alpha) * *ewma;
+    const double e = *ewma;
+    int moved_up = 0;
+    if (*regime == 0) {
+        *up = e > theta1 ? *up + 1 : 0;
+        if (*up >= k) { *regime = 1; *up = 0; *down = 0; moved_up = 1; }
+    } else if (*regime == 1) {
+        *up = e >= theta2 ? *up + 1 : 0;
+        *down = e < theta1 - eps ? *down + 1 : 0;
+        if (*up >= k) { *regime = 2; *up = 0; *down = 0; moved_up = 1; }
+        else if (*down >= k) { *regime = 0; *up = 0; *down = 0; }
+    } else {
+        *down = e < theta2 - eps ? *down + 1 : 0;
+        if (*down >= k) { *regime = 1; *up = 0; *down = 0; }
+    }
+    return moved_up;
+}
+
+/* Latency model f(n) = a n + b + d / max(n_sat - n, 1)^beta in fp64. */
+double orc_latency(const double* rg_d, const int32_t* rg_i, int64_t n)
+{
+    const double a = rg_d[4], b = rg_d[5], d = rg_d[6];
+    const int32_t beta = rg_i[1], n_sat = rg_i[2];
+    double gap = (double)(n_sat - n);
+    if (gap < 1.0) gap = 1.0;
+    double pw = gap;
+    for (int32_t i = 1; i < beta; ++i) pw = pw * gap;
+    return (a * (double)n + b) + d / pw;
+}
+
 int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t routes_per_step,
                          float w_ov, float w_act, float w_sat, int32_t cap,
                          int32_t controller, float ctrl_w_ov, int32_t ctrl_window,
                          int32_t ctrl_num, int32_t ctrl_den,
                          int32_t policy, float tau, const uint32_t* rand,
+                         const double* rg_d, const int32_t* rg_i, const float* rg_f, int32_t* route_regime,
                          int32_t n_conv, const int64_t* turn_off, const int32_t* turn_blocks,
                          const int64_t* chain_off, const uint64_t* chains,
                          int32_t* route_turn, int32_t* route_worker, int32_t* route_step,
@@ -426,7 +480,17 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
 {
     if (W < 1 || cache_blocks < 1 || H < 1 || routes_per_step < 1 || cap < 1 || n_conv < 0)
         return ORC_EINVAL;
-    if (controller && (ctrl_window < 1 || ctrl_den < 1 || ctrl_num < 0)) return ORC_EINVAL;
+    if (controller < 0 || controller > 2) return ORC_EINVAL;
+    if (controller == 1 && (ctrl_window < 1 || ctrl_den < 1 || ctrl_num < 0)) return ORC_EINVAL;
+    if (controller == 2) {
+        if (!rg_d || !rg_i || !rg_f) return ORC_EINVAL;
+        if (!(rg_d[0] > 0.0 && rg_d[0] <= 1.0) || !(rg_d[1] <= rg_d[2]) || !(rg_d[3] >= 0.0)) return ORC_EINVAL;
+        if (rg_i[0] < 1 || rg_i[1] < 1 || rg_i[1] > 8 || rg_i[2] < 1) return ORC_EINVAL;
+        for (int r = 0; r < 3; ++r) {
+            if (!(rg_f[r] >= 0.0f) || !(rg_f[3 + r] >= 0.0f)) return ORC_EINVAL;
+            if (rg_f[r] > 0.0f && !rand) return ORC_EINVAL;
+        }
+    }
     if (policy < ORC_POLICY_ARGMIN || policy > ORC_POLICY_P2C) return ORC_EINVAL;
     if (policy == ORC_POLICY_SOFTMAX && !(tau > 0.0f)) return ORC_EINVAL;
     if (!rand && (policy == ORC_POLICY_SOFTMAX || policy == ORC_POLICY_RANDOM || policy == ORC_POLICY_P2C))
@@ -451,8 +515,9 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
     int64_t* step_first = (int64_t*)calloc((size_t)H, sizeof(int64_t));
     int64_t* step_count = (int64_t*)calloc((size_t)H, sizeof(int64_t));
     int64_t* u_ring = (int64_t*)calloc((size_t)(ctrl_window > 0 ? ctrl_window : 1), sizeof(int64_t));
+    int64_t* inflight_n = (int64_t*)calloc((size_t)W, sizeof(int64_t));
     if (!lru || !A || !o_row || !queue || !next_turn || !route_conv || !step_first ||
-        !step_count || !u_ring) { rc = ORC_ENOMEM; goto done; }
+        !step_count || !u_ring || !inflight_n) { rc = ORC_ENOMEM; goto done; }
     for (int32_t j = 0; j < W; ++j)
         if (lru_init(&lru[j], cache_blocks + max_P + 1) != ORC_OK) { rc = ORC_ENOMEM; goto done; }
 
@@ -466,12 +531,15 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
     int64_t t = 0;            /* routes done */
     int64_t u_sum = 0;        /* sum of the last ctrl_window load samples */
     int prev_active = 0;
+    double rg_ewma = 0.0;     /* regime controller: smoothed latency, regime, hysteresis counters */
+    int32_t rg_regime = 0, rg_up = 0, rg_down = 0;
 
     for (int64_t s = 0;; ++s) {
         const int64_t slot = s % H;
         if (s >= H) {                               /* release the routes of step s-H */
             for (int64_t r = step_first[slot]; r < step_first[slot] + step_count[slot]; ++r) {
                 A[route_worker[r]] -= route_blocks[r];
+                inflight_n[route_worker[r]] -= 1;
                 int32_t c = route_conv[r];
                 if (next_turn[c] < turn_off[c + 1]) { queue[(q_head + q_size) % q_cap] = c; ++q_size; }
             }
@@ -494,8 +562,16 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
             const uint64_t* h = chains + chain_off[c];
 
             float w_eff = w_ov;
+            int32_t pol = policy;
+            float tau_eff = tau;
             int active = 0;
-            if (controller && t >= ctrl_window &&
+            if (controller == 2) {
+                w_eff = rg_f[3 + rg_regime];
+                tau_eff = rg_f[rg_regime];
+                pol = tau_eff > 0.0f ? ORC_POLICY_SOFTMAX : ORC_POLICY_ARGMIN;
+                if (rg_regime > 0) totals[3] += 1;
+            }
+            if (controller == 1 && t >= ctrl_window &&
                 (int64_t)ctrl_den * u_sum > (int64_t)ctrl_num * ctrl_window * W * (int64_t)cap)
                 active = 1;
             if (active) {
@@ -512,8 +588,9 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
                 overlap[t * W + j] = o;
                 cost[t * W + j] = cj;
             }
-            const int32_t sigma = orc_select(policy, tau, W, cost + t * W, t, rand ? rand[2 * t] : 0u,
+            const int32_t sigma = orc_select(pol, tau_eff, W, cost + t * W, t, rand ? rand[2 * t] : 0u,
                                              rand ? rand[2 * t + 1] : 0u);
+            if (route_regime) route_regime[t] = controller == 2 ? rg_regime : 0;
 
             int err = 0;
             for (int32_t k2 = P - 1; k2 >= 0; --k2) lru_touch(&lru[sigma], h[k2], &err);
@@ -528,10 +605,14 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
                     evicted_keys[totals[1] + ev - 1] = key;
             }
             A[sigma] += P;
+            inflight_n[sigma] += 1;
+            if (controller == 2)
+                totals[4] += orc_regime_step(rg_d, rg_i, orc_latency(rg_d, rg_i, inflight_n[sigma]), t, &rg_ewma,
+                                             &rg_regime, &rg_up, &rg_down);
 
             int64_t u = 0;
             for (int32_t j = 0; j < W; ++j) u += A[j];
-            if (controller) {
+            if (controller == 1) {
                 int64_t pos = t % ctrl_window;
                 if (t >= ctrl_window) u_sum -= u_ring[pos];
                 u_ring[pos] = u;
@@ -566,7 +647,7 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
 done:
     if (lru)
         for (int32_t j = 0; j < W; ++j) lru_free(&lru[j]);
-    free(lru); free(A); free(o_row); free(queue); free(next_turn); free(route_conv);
+    free(lru); free(A); free(o_row); free(queue); free(next_turn); free(route_conv); free(inflight_n);
     free(step_first); free(step_count); free(u_ring);
     return rc;
 }

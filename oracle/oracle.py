@@ -65,6 +65,7 @@ def lib():
             L.orc_simulate_episode.argtypes = [
                 i32, i32, i32, i32, f32, f32, f32, i32, i32, f32, i32, i32, i32,
                 i32, f32, p,
+                p, p, p, p,
                 i32, p, p, p, p,
                 p, p, p, p, p, p, p, p, p, p,
                 p, p, p, i64, p]
@@ -72,6 +73,10 @@ def lib():
             L.orc_exp_neg.argtypes = [f32]
             L.orc_select.restype = i32
             L.orc_select.argtypes = [i32, f32, i32, p, i64, C.c_uint32, C.c_uint32]
+            L.orc_latency.restype = C.c_double
+            L.orc_latency.argtypes = [p, p, i64]
+            L.orc_regime_step.restype = C.c_int
+            L.orc_regime_step.argtypes = [p, p, C.c_double, i64, p, p, p, p]
             L.orc_poa_matrix.restype = C.c_int
             L.orc_poa_matrix.argtypes = [i32, i32, p, p, p, f32, f32, f32, i32, i32, f32, p, p]
             L.orc_poa_window.restype = C.c_int
@@ -190,8 +195,34 @@ def select(policy: int, tau: float, costs, t: int = 0, r0: int = 0, r1: int = 0)
     return int(lib().orc_select(int(policy), float(tau), int(c.shape[0]), _ptr(c), int(t), int(r0), int(r1)))
 
 
+def regime_arrays(regime=None):
+    """(fp64, int32, fp32) parameter arrays of the regime controller."""
+    from paper_2606_17081_amd.workload import REGIME_PARAMS
+    r = dict(REGIME_PARAMS if regime is None else regime)
+    rd = np.array([r["alpha"], r["theta1"], r["theta2"], r["eps"], r["a"], r["b"], r["d"]], np.float64)
+    ri = np.array([r["k"], r["beta"], r["n_sat"]], np.int32)
+    rf = np.array(list(r["tau"]) + list(r["w_ov"]), np.float32)
+    return rd, ri, rf
+
+
+def latency(n: int, regime=None) -> float:
+    rd, ri, _ = regime_arrays(regime)
+    return float(lib().orc_latency(_ptr(rd), _ptr(ri), int(n)))
+
+
+def regime_step(lat: float, sample: int, state, regime=None):
+    """One sample of the regime controller; state = [ewma, regime, up, down] is updated."""
+    rd, ri, _ = regime_arrays(regime)
+    e = np.array([state[0]], np.float64)
+    g = np.array(state[1:4], np.int32)
+    moved = lib().orc_regime_step(_ptr(rd), _ptr(ri), float(lat), int(sample), _ptr(e), _ptr(g[0:]),
+                                  C.c_void_p(g.ctypes.data + 4), C.c_void_p(g.ctypes.data + 8))
+    state[:] = [float(e[0]), int(g[0]), int(g[1]), int(g[2])]
+    return int(moved)
+
+
 def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, chains,
-                     dump: bool = False, evicted_cap: int = 0, rand=None) -> Dict[str, np.ndarray]:
+                     dump: bool = False, evicted_cap: int = 0, rand=None, regime=None) -> Dict[str, np.ndarray]:
     """One routing episode; arrays must be rebased (turn_off[0] == chain_off[0] == 0).
     rand: two uint32 words per route (the stochastic policies' draws); drawn by
     workload.route_rand when not given."""
@@ -207,11 +238,12 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         route_step=np.zeros(n, np.int32), route_blocks=np.zeros(n, np.int32),
         overlap=np.zeros((n, W), np.int32), cost=np.zeros((n, W), np.float32),
         evict_count=np.zeros(n, np.int32), evict_digest=np.zeros(n, np.uint64),
-        last_hash=np.zeros(n, np.uint64), totals=np.zeros(8, np.int64))
+        last_hash=np.zeros(n, np.uint64), totals=np.zeros(8, np.int64), route_regime=np.zeros(n, np.int32))
     policy = int(getattr(spec, "policy", 0))
     tau = float(getattr(spec, "tau", 0.0))
+    rd, ri, rf = regime_arrays(regime)
     if rand is None:
-        if policy in (1, 3, 4):         # softmax, random, power of two choices draw per route
+        if policy in (1, 3, 4) or (spec.controller == 2 and np.any(rf[:3] > 0)):   # draws per route
             from paper_2606_17081_amd.workload import route_rand
             rand = route_rand(spec, n)
         else:
@@ -228,6 +260,7 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         spec.w_ov, spec.w_act, spec.w_sat, spec.cap,
         spec.controller, spec.ctrl_w_ov, spec.ctrl_window, spec.ctrl_num, spec.ctrl_den,
         policy, tau, g(rand),
+        _ptr(rd), _ptr(ri), _ptr(rf), g(out["route_regime"]),
         n_conv, _ptr(turn_off), g(turn_blocks), _ptr(chain_off), g(chains),
         g(out["route_turn"]), g(out["route_worker"]), g(out["route_step"]),
         g(out["route_blocks"]), g(out["overlap"]), g(out["cost"]),

@@ -219,7 +219,7 @@ class EpisodeSpec:
     w_act: float = 0.5
     w_sat: float = 4.0
     cap: int = 512            # active blocks at which the overload term starts
-    controller: int = 0       # 1: switch to ctrl_w_ov when the windowed load is high
+    controller: int = 0       # 1: switch to ctrl_w_ov when the windowed load is high; 2: regime controller
     ctrl_w_ov: float = 0.25
     ctrl_window: int = 128
     ctrl_num: int = 9         # threshold num/den of mean load per unit capacity
@@ -230,6 +230,14 @@ class EpisodeSpec:
     @property
     def routes_per_step(self) -> int:
         return self.concurrency // self.hold_steps
+
+
+# Regime controller (controller = 2): the paper's EWMA weight, its 70B thresholds
+# (seconds) and its (temperature, overlap weight) per regime Below / Transition /
+# Saturated; the latency model is the PoA-hat matrix's; k and eps are not given
+# by the paper (fill-ins).
+REGIME_PARAMS = dict(alpha=0.3, theta1=0.3, theta2=2.0, eps=0.05, k=3, a=0.005, b=0.020, d=0.010, beta=2,
+                     n_sat=64, tau=(0.0, 0.7, 0.8), w_ov=(1.0, 1.0, 0.1))
 
 
 # Worker-selection policies of an episode (the routing library's RK_POLICY_* codes).

@@ -33,9 +33,11 @@ def overlap_set(chain, cached: set) -> int:
 
 
 def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blocks, chains_per_conv,
-            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10, select=None):
+            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10, select=None, regime=None):
     """Sequential routing episode with OrderedDict LRU caches; select(costs, t)
-    picks the worker of route t (default: least cost, lowest index)."""
+    picks the worker of route t (default: least cost, lowest index).  With
+    controller 2, regime = (params(r) -> (tau, w_ov), step(n, t) -> new
+    regime, select_tau(costs, t, tau)) drives the regime controller."""
     n_conv = len(turn_off) - 1
     caches = [OrderedDict() for _ in range(W)]   # key -> None, oldest first
     A = [0] * W
@@ -45,11 +47,14 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
     routes = []
     us = []
     prev_active = False
+    nflight = [0] * W
+    rg = 0
     s = 0
     while True:
         if s - H in steps:
             for (j, P, c) in steps.pop(s - H):
                 A[j] -= P
+                nflight[j] -= 1
                 if next_turn[c] < turn_off[c + 1]:
                     queue.append(c)
         inflight = sum(len(v) for k, v in steps.items() if s - H < k < s)
@@ -63,13 +68,19 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
             P = int(turn_blocks[turn])
             h = [int(x) for x in chains_per_conv[c][:P]]
             w_eff = f32(w_ov)
-            active = (controller and len(us) >= ctrl_window and
+            active = (controller == 1 and len(us) >= ctrl_window and
                       ctrl_den * sum(us[-ctrl_window:]) > ctrl_num * ctrl_window * W * cap)
             if active:
                 w_eff = min(f32(w_ov), f32(ctrl_w_ov))
+            route_regime = rg if controller == 2 else 0
+            if controller == 2:
+                rtau, rw = regime[0](rg)
+                w_eff = f32(rw)
             ovl = [overlap_set(h, caches[j].keys()) for j in range(W)]
             costs = [cost_f32(w_eff, w_act, w_sat, cap, P, ovl[j], A[j]) for j in range(W)]
-            if select is None:
+            if controller == 2 and rtau > 0:
+                sigma = int(regime[2](costs, len(routes), rtau))
+            elif select is None:
                 sigma = 0
                 for j in range(1, W):
                     if costs[j] < costs[sigma]:
@@ -87,8 +98,11 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
                 key, _ = cache.popitem(last=False)
                 evicted.append(key)
             A[sigma] += P
+            nflight[sigma] += 1
+            if controller == 2:
+                rg = int(regime[1](nflight[sigma], len(routes)))
             us.append(sum(A))
-            routes.append(dict(turn=turn, worker=sigma, step=s, P=P, overlap=ovl, cost=costs,
+            routes.append(dict(turn=turn, worker=sigma, step=s, P=P, overlap=ovl, cost=costs, regime=route_regime,
                                evicted=evicted, active=bool(active),
                                first_active=bool(active and not prev_active)))
             prev_active = bool(active)
