@@ -215,6 +215,19 @@ int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains, const int
  *     (a sample is taken after every route; at least ctrl_window samples are
  *     needed), a load-triggered switch of the overlap weight in the spirit of
  *     Section 6.3;
+ *   - with controller = 2 (the regime controller of Sections 6.2-6.3), the
+ *     route's temperature and overlap weight come from the current regime r
+ *     (regime.tau[r], regime.w_ov[r]; Tab. regime-params): tau = 0 routes by
+ *     argmin, tau > 0 by the softmax below, and the episode's policy, tau
+ *     and w_ov are not used.  After every route the chosen worker's latency
+ *     f(n) = a n + b + d / max(n_sat - n, 1)^beta (Eq. latency-superlinear,
+ *     n = its requests in flight including the new one) stands in for TTFT:
+ *     ewma = f for the first route, else alpha f + (1 - alpha) ewma
+ *     (Eq. saturation-signal); the regime (Eq. saturation-state) moves
+ *     Below -> Transition after k consecutive samples with ewma > theta1,
+ *     Transition -> Saturated after k with ewma >= theta2, and back down
+ *     after k with ewma < theta1 - eps (resp. theta2 - eps), one regime per
+ *     sample, counters restarting after a change; all in fp64;
  *   - the worker sigma is chosen by the episode's policy from the W costs of
  *     route t (its index in the episode) and the two random words r0, r1 of
  *     its output row (route_rand[2 * row], route_rand[2 * row + 1]):
@@ -246,7 +259,7 @@ typedef struct {
     int32_t n_conv;          /* conversations in the episode, >= 0                     */
     int32_t hold_steps;      /* H >= 1                                                 */
     int32_t routes_per_step; /* >= 1                                                   */
-    int32_t controller;      /* 0 off, 1 on                                            */
+    int32_t controller;      /* 0 off, 1 load switch, 2 regime controller (see below)  */
     int32_t ctrl_window;     /* >= 1 when the controller is on                         */
     int32_t ctrl_num;        /* >= 0                                                   */
     int32_t ctrl_den;        /* >= 1                                                   */
@@ -264,6 +277,19 @@ typedef struct {
 #define RK_POLICY_ROUND_ROBIN 2
 #define RK_POLICY_RANDOM      3
 #define RK_POLICY_P2C         4
+
+typedef struct {
+    double  alpha;           /* EWMA weight of the newest sample, (0, 1]               */
+    double  theta1, theta2;  /* regime thresholds (seconds), theta1 <= theta2           */
+    double  eps;             /* hysteresis margin (seconds), >= 0                       */
+    int32_t k;               /* consecutive samples for a regime change, >= 1           */
+    int32_t beta;            /* exponent of the saturation term, 1..8                   */
+    double  a, b, d;         /* latency model (seconds)                                 */
+    int32_t n_sat;           /* requests at which the saturation term peaks, >= 1       */
+    float   tau[3];          /* temperature per regime (Below, Transition, Saturated)   */
+    float   w_ov[3];         /* overlap weight per regime, >= 0                         */
+} rk_regime_params;          /* 96 bytes; invalid values set RK_DEV_BAD_PARAMS for the
+                                episodes with controller = 2                          */
 
 typedef struct {
     int32_t E;                       /* episodes (>= 0)                                 */
@@ -289,6 +315,7 @@ typedef struct {
     const uint32_t* route_rand;      /* 2 uniform 32-bit words per output row, read by the
                                         SOFTMAX, RANDOM and P2C policies; may be NULL when
                                         no episode uses them                             */
+    rk_regime_params regime;         /* for the episodes with controller = 2            */
 } rk_episode_batch;
 
 /* Outputs, one row per route in routing order, written at out_base + t of the
@@ -305,7 +332,11 @@ typedef struct {
     uint64_t* last_hash;      /* [rows]   h_{P-1} of the routed prompt (0 if P == 0)    */
     int64_t* totals;          /* [E*8]    per episode: sum(P - o_sigma), evictions,
                                  sum(P), controller routes, controller activations,
-                                 steps, sum(o_sigma), blocks cached at the end          */
+                                 steps, sum(o_sigma), blocks cached at the end; with
+                                 controller = 2 the 4th and 5th count routes outside
+                                 Below and regime moves up                           */
+    int32_t* route_regime;    /* [rows]   regime the route was made in (0 without the
+                                 regime controller)                                  */
 } rk_episode_outputs;
 
 /* Workspace bytes needed by rk_simulate_episodes for this batch shape. */

@@ -53,6 +53,7 @@ struct EpArgs {
     const int64_t* chain_off;
     const uint64_t* chains;
     const uint32_t* route_rand;
+    rk_regime_params regime;
     rk_episode_outputs out;
     unsigned char* ws;
     EpisodeLayout L;
@@ -475,6 +476,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     uint32_t* s_tail = s_head + W;
     int32_t* s_live = (int32_t*)(s_tail + W);
     int32_t* s_used = s_live + W;
+    int32_t* s_N = s_used + W;                              // requests in flight per worker
     // in-flight routes of the last H steps, by step slot
     int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // worker
     int32_t* s_stP = s_stw + a.max_inflight;               // prompt blocks
@@ -501,16 +503,30 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     const int32_t H = prm.hold_steps, rps = prm.routes_per_step, n_conv = prm.n_conv;
     const bool bad = H < 1 || rps < 1 || rps > a.max_rps || (int64_t)H * rps > a.max_inflight ||
                      n_conv < 0 || n_conv > a.max_conv || prm.cap_blocks < 1 ||
-                     (prm.controller && (prm.ctrl_window < 1 || prm.ctrl_window > a.max_ctrl_window ||
-                                         prm.ctrl_den < 1 || prm.ctrl_num < 0));
+                     (prm.controller == 1 && (prm.ctrl_window < 1 || prm.ctrl_window > a.max_ctrl_window ||
+                                              prm.ctrl_den < 1 || prm.ctrl_num < 0));
     if (bad) {
         if (tid == 0) atomicOr(a.status, RK_DEV_TOO_LARGE);
         return;
     }
     const int32_t policy = prm.policy;
     const float tau = prm.tau;
-    const bool draws = policy == RK_POLICY_SOFTMAX || policy == RK_POLICY_RANDOM || policy == RK_POLICY_P2C;
-    if (policy < RK_POLICY_ARGMIN || policy > RK_POLICY_P2C || (policy == RK_POLICY_SOFTMAX && !(tau > 0.0f)) ||
+    const bool regime_ctl = prm.controller == 2;
+    const rk_regime_params& rg = a.regime;
+    bool rg_ok = true, rg_draws = false;
+    if (regime_ctl) {
+        rg_ok = rg.alpha > 0.0 && rg.alpha <= 1.0 && rg.theta1 <= rg.theta2 && rg.eps >= 0.0 && rg.k >= 1 &&
+                rg.beta >= 1 && rg.beta <= 8 && rg.n_sat >= 1;
+        for (int r = 0; r < 3; ++r) {
+            rg_ok = rg_ok && rg.tau[r] >= 0.0f && rg.w_ov[r] >= 0.0f;
+            rg_draws = rg_draws || rg.tau[r] > 0.0f;
+        }
+    }
+    const bool draws = rg_draws || (!regime_ctl && (policy == RK_POLICY_SOFTMAX || policy == RK_POLICY_RANDOM ||
+                                                    policy == RK_POLICY_P2C));
+    if (prm.controller < 0 || prm.controller > 2 || !rg_ok ||
+        (!regime_ctl && (policy < RK_POLICY_ARGMIN || policy > RK_POLICY_P2C ||
+                         (policy == RK_POLICY_SOFTMAX && !(tau > 0.0f)))) ||
         (draws && !a.route_rand)) {
         if (tid == 0) atomicOr(a.status, RK_DEV_BAD_PARAMS);
         return;
@@ -535,6 +551,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     }
     if (tid < W) {
         s_A[tid] = 0;
+        s_N[tid] = 0;
         s_head[tid] = 0;
         s_tail[tid] = 0;
         s_live[tid] = 0;
@@ -779,6 +796,8 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     bool step_open = false, prev_active = false;
     int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t u_sum = 0, u_tot = 0;
+    double rg_ewma = 0.0;                          // regime controller: smoothed latency, regime,
+    int32_t rg_r = 0, rg_up = 0, rg_down = 0;      // hysteresis counters
 
     for (;;) {
         // ---- A. the batch: the next nb queued requests (queue order is routing order)
@@ -883,10 +902,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             if (wave == 0) {
                 event = EV_BATCH;
                 // lane j < W keeps worker j's load, log tail and block counts in registers
-                int32_t rA = 0, rlive = 0, rused = 0;
+                int32_t rA = 0, rlive = 0, rused = 0, rN = 0;
                 uint32_t rtail = 0;
                 if (lane < W) {
                     rA = s_A[lane];
+                    rN = s_N[lane];
                     rtail = s_tail[lane];
                     rlive = s_live[lane];
                     rused = s_used[lane];
@@ -896,7 +916,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         // release the routes of step s - H; queue their conversations' next turns
                         const int32_t slot = s % H, sb = slot * rps;
                         if (s >= H) {
-                            if (lane < W) s_A[lane] = rA;
+                            if (lane < W) {
+                                s_A[lane] = rA;
+                                s_N[lane] = rN;
+                            }
                             ep_wave_sync();
                             const int32_t nprev = s_stepn[slot];
                             const int32_t qtail = sh.qhead + sh.qsize;
@@ -911,6 +934,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                                     more = (cc & kMoreTurns) != 0;
                                     rel += s_stP[sb + r];
                                     atomicSub(&s_A[s_stw[sb + r]], s_stP[sb + r]);
+                                    atomicSub(&s_N[s_stw[sb + r]], 1);
                                 }
                                 const unsigned long long mb = __ballot(more);
                                 if (more) g_queue[(qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull))) % qcap] = c;
@@ -919,7 +943,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                             u_tot -= ep_wave_sum(rel);
                             ep_wave_sync();
                             if (lane == 0) sh.qsize += pushed;
-                            if (lane < W) rA = s_A[lane];
+                            if (lane < W) {
+                                rA = s_A[lane];
+                                rN = s_N[lane];
+                            }
                             ep_wave_sync();
                         }
                         int32_t inflight = 0;
@@ -946,7 +973,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     // one route: controller, cost of every worker, argmin
                     const int32_t slot = s % H, sb = slot * rps;
                     bool active = false;
-                    if (prm.controller && t >= prm.ctrl_window)
+                    if (prm.controller == 1 && t >= prm.ctrl_window)
                         active = (int64_t)prm.ctrl_den * u_sum >
                                  (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
                     float w = prm.w_ov;
@@ -956,6 +983,14 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         if (!prev_active) tot[4] += 1;
                     }
                     prev_active = active;
+                    int32_t pol = policy;
+                    float tau_r = tau;
+                    if (regime_ctl) {
+                        w = rg.w_ov[rg_r];
+                        tau_r = rg.tau[rg_r];
+                        pol = tau_r > 0.0f ? RK_POLICY_SOFTMAX : RK_POLICY_ARGMIN;
+                        if (rg_r > 0) tot[3] += 1;
+                    }
                     const int32_t P = r_P[b];
                     const int64_t row = prm.out_base + (int64_t)t;
                     uint32_t bits = 0xFFFFFFFFu;
@@ -969,13 +1004,13 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         bits = __float_as_uint(__fadd_rn(cj, 0.0f));
                     }
                     int32_t sg;
-                    if (policy == RK_POLICY_ARGMIN) {
+                    if (pol == RK_POLICY_ARGMIN) {
                         const uint32_t mn = ep_wave_min_u32(bits);
                         sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
-                    } else if (policy == RK_POLICY_SOFTMAX) {
+                    } else if (pol == RK_POLICY_SOFTMAX) {
                         // weights exp((c_min - c_j) / tau); running sums in worker order
                         const float cmin = __uint_as_float(ep_wave_min_u32(bits));
-                        const float ej = lane < W ? exp_neg_f32(__fdiv_rn(__fsub_rn(cmin, cj), tau)) : 0.0f;
+                        const float ej = lane < W ? exp_neg_f32(__fdiv_rn(__fsub_rn(cmin, cj), tau_r)) : 0.0f;
                         float total = 0.0f;
                         for (int32_t j = 0; j < W; ++j)
                             total = __fadd_rn(total, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j)));
@@ -991,12 +1026,12 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                             if (run > thr) sg = j;
                         }
                         if (sg < 0) sg = last;
-                    } else if (policy == RK_POLICY_ROUND_ROBIN) {
+                    } else if (pol == RK_POLICY_ROUND_ROBIN) {
                         sg = t % W;
                     } else {
                         const int32_t ca = (int32_t)(((uint64_t)r_rnd[2 * b] * (uint64_t)W) >> 32);
                         sg = ca;
-                        if (policy == RK_POLICY_P2C && W > 1) {
+                        if (pol == RK_POLICY_P2C && W > 1) {
                             int32_t cb2 = (int32_t)(((uint64_t)r_rnd[2 * b + 1] * (uint64_t)(W - 1)) >> 32);
                             if (cb2 >= ca) ++cb2;
                             const float fa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), ca));
@@ -1011,6 +1046,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     const int32_t rc = r_c[b];
                     if (lane == sg) {
                         rA += P;
+                        rN += 1;
                         rtail = base + (uint32_t)P;
                         if (!scan) {
                             rlive = live_after;
@@ -1032,6 +1068,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         if (a.out.route_step) a.out.route_step[row] = (int32_t)s;
                         if (a.out.route_blocks) a.out.route_blocks[row] = P;
                         if (a.out.last_hash) a.out.last_hash[row] = r_last[b];
+                        if (a.out.route_regime) a.out.route_regime[row] = regime_ctl ? rg_r : 0;
                         if (!flush) {
                             if (a.out.evict_count) a.out.evict_count[row] = 0;
                             if (a.out.evict_digest) a.out.evict_digest[row] = 0ull;
@@ -1041,7 +1078,44 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         }
                     }
                     u_tot += P;
-                    if (prm.controller) {
+                    if (regime_ctl) {
+                        // the chosen worker's latency with the new request (already counted in
+                        // lane sg's rN) stands in for TTFT (fp64)
+                        const int32_t n_sg = __builtin_amdgcn_readlane(rN, sg);
+                        double gap = (double)(rg.n_sat - n_sg);
+                        gap = gap < 1.0 ? 1.0 : gap;
+                        double pw = gap;
+                        for (int32_t i = 1; i < rg.beta; ++i) pw = __dmul_rn(pw, gap);
+                        const double lat = __dadd_rn(__dadd_rn(__dmul_rn(rg.a, (double)n_sg), rg.b), __ddiv_rn(rg.d, pw));
+                        rg_ewma = t == 0 ? lat
+                                         : __dadd_rn(__dmul_rn(rg.alpha, lat), __dmul_rn(__dsub_rn(1.0, rg.alpha), rg_ewma));
+                        if (rg_r == 0) {
+                            rg_up = rg_ewma > rg.theta1 ? rg_up + 1 : 0;
+                            if (rg_up >= rg.k) {
+                                rg_r = 1;
+                                rg_up = rg_down = 0;
+                                tot[4] += 1;
+                            }
+                        } else if (rg_r == 1) {
+                            rg_up = rg_ewma >= rg.theta2 ? rg_up + 1 : 0;
+                            rg_down = rg_ewma < __dsub_rn(rg.theta1, rg.eps) ? rg_down + 1 : 0;
+                            if (rg_up >= rg.k) {
+                                rg_r = 2;
+                                rg_up = rg_down = 0;
+                                tot[4] += 1;
+                            } else if (rg_down >= rg.k) {
+                                rg_r = 0;
+                                rg_up = rg_down = 0;
+                            }
+                        } else {
+                            rg_down = rg_ewma < __dsub_rn(rg.theta2, rg.eps) ? rg_down + 1 : 0;
+                            if (rg_down >= rg.k) {
+                                rg_r = 1;
+                                rg_up = rg_down = 0;
+                            }
+                        }
+                    }
+                    if (prm.controller == 1) {
                         const int32_t pos = t % prm.ctrl_window;
                         if (t >= prm.ctrl_window) u_sum -= s_u[pos];
                         ep_wave_sync();
@@ -1071,6 +1145,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 }
                 if (lane < W) {
                     s_A[lane] = rA;
+                    s_N[lane] = rN;
                     s_tail[lane] = rtail;
                     s_live[lane] = rlive;
                     s_used[lane] = rused;
@@ -1183,6 +1258,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.chain_off = b->chain_off;
     a.chains = b->chains;
     a.route_rand = b->route_rand;
+    a.regime = b->regime;
     a.out = *out;
     a.ws = (unsigned char*)workspace;
     a.L = L;
@@ -1191,7 +1267,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     // batch that fits in 60 KiB (two episodes can then share a CU)
     size_t o = 0;
     a.lds_w = 0;
-    o = align_up(o + (size_t)b->W * 5 * 4, 16);
+    o = align_up(o + (size_t)b->W * 6 * 4, 16);
     a.lds_inflight = (uint32_t)o;
     o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
     a.lds_u = (uint32_t)o;

@@ -65,9 +65,10 @@ class EpisodeRunner:
         self.n_rows = out_base
         self.params_host = prm
         # the stochastic policies' draws: two words per output row (inputs, seeded per episode)
+        self.regime = dict(workload.regime)
         self.route_rand = None
-        if any(sp.policy in (rk.RK_POLICY_SOFTMAX, rk.RK_POLICY_RANDOM, rk.RK_POLICY_P2C)
-               for sp in self.episodes):
+        if any(sp.policy in (rk.RK_POLICY_SOFTMAX, rk.RK_POLICY_RANDOM, rk.RK_POLICY_P2C) or
+               (sp.controller == 2 and max(self.regime["tau"]) > 0) for sp in self.episodes):
             rr = np.zeros(2 * max(out_base, 1), np.uint32)
             for sp, (b0, n_routes, _, _) in zip(self.episodes, self.rows):
                 rr[2 * b0: 2 * (b0 + n_routes)] = route_rand(sp, n_routes)
@@ -77,7 +78,7 @@ class EpisodeRunner:
         self.max_conv = max((flat.conv_count[sp.seed] for sp in self.episodes), default=0)
         self.max_rps = max((sp.routes_per_step for sp in self.episodes), default=1)
         self.max_inflight = max((sp.routes_per_step * sp.hold_steps for sp in self.episodes), default=1)
-        self.max_ctrl_window = max([sp.ctrl_window for sp in self.episodes if sp.controller] + [1])
+        self.max_ctrl_window = max([sp.ctrl_window for sp in self.episodes if sp.controller == 1] + [1])
         self.max_window = max((sp.concurrency for sp in self.episodes), default=1)
 
         R, W = max(self.n_rows, 1), self.W
@@ -92,6 +93,7 @@ class EpisodeRunner:
         self.evict_digest = z(R, torch.int64)     # uint64 bits
         self.last_hash = z(R, torch.int64)        # uint64 bits
         self.totals = z((max(E, 1), 8), torch.int64)
+        self.route_regime = z(R, torch.int32)
         ws = rk.simulate_workspace_size(E, W, self.cache_blocks, self.max_blocks, self.max_conv)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
 
@@ -111,11 +113,11 @@ class EpisodeRunner:
         self.batch = rk.EpisodeBatch(E, W, self.cache_blocks, self.max_blocks, self.max_conv,
                                      self.max_inflight, self.max_rps, self.max_ctrl_window, probe_mode, 0,
                                      P(self.params), P(self.turn_off), P(self.turn_blocks), P(self.chain_off),
-                                     P(self.chains), P(self.route_rand))
+                                     P(self.chains), P(self.route_rand), rk.regime_params(self.regime))
         self.outputs = rk.EpisodeOutputs(P(self.route_turn), P(self.route_worker), P(self.route_step),
                                          P(self.route_blocks), P(self.overlap), P(self.cost),
                                          P(self.evict_count), P(self.evict_digest), P(self.last_hash),
-                                         P(self.totals))
+                                         P(self.totals), P(self.route_regime))
 
     # ---- the three stages of one step
     def hash(self, stream=None):
@@ -150,6 +152,7 @@ class EpisodeRunner:
             evict_digest=cpu(self.evict_digest[r0:r0 + n]).view(np.uint64),
             last_hash=cpu(self.last_hash[r0:r0 + n]).view(np.uint64),
             totals=cpu(self.totals[e]),
+            route_regime=cpu(self.route_regime[r0:r0 + n]),
         )
         if self.cost is not None:
             out["cost"] = cpu(self.cost[r0:r0 + n]).reshape(n, W)

@@ -43,19 +43,31 @@ class PoaParams(C.Structure):
                 ("C_cap", C.c_int32), ("w_c", C.c_float), ("K_fixed", C.c_int32)]
 
 
+class RegimeParams(C.Structure):
+    _fields_ = [("alpha", C.c_double), ("theta1", C.c_double), ("theta2", C.c_double), ("eps", C.c_double),
+                ("k", C.c_int32), ("beta", C.c_int32), ("a", C.c_double), ("b", C.c_double), ("d", C.c_double),
+                ("n_sat", C.c_int32), ("tau", C.c_float * 3), ("w_ov", C.c_float * 3)]
+
+
+def regime_params(r: dict) -> RegimeParams:
+    return RegimeParams(r["alpha"], r["theta1"], r["theta2"], r["eps"], r["k"], r["beta"], r["a"], r["b"], r["d"],
+                        r["n_sat"], (C.c_float * 3)(*r["tau"]), (C.c_float * 3)(*r["w_ov"]))
+
+
 class EpisodeBatch(C.Structure):
     _fields_ = [("E", C.c_int32), ("W", C.c_int32), ("cache_blocks", C.c_int32),
                 ("max_blocks", C.c_int32), ("max_conv", C.c_int32), ("max_inflight", C.c_int32),
                 ("max_routes_per_step", C.c_int32), ("max_ctrl_window", C.c_int32),
                 ("probe_mode", C.c_int32), ("reserved", C.c_int32),
                 ("params", C.c_void_p), ("turn_off", C.c_void_p), ("turn_blocks", C.c_void_p),
-                ("chain_off", C.c_void_p), ("chains", C.c_void_p), ("route_rand", C.c_void_p)]
+                ("chain_off", C.c_void_p), ("chains", C.c_void_p), ("route_rand", C.c_void_p),
+                ("regime", RegimeParams)]
 
 
 class EpisodeOutputs(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("route_turn", "route_worker", "route_step", "route_blocks",
                                           "overlap", "cost", "evict_count", "evict_digest",
-                                          "last_hash", "totals")]
+                                          "last_hash", "totals", "route_regime")]
 
 
 # rk_episode_params, 64 bytes, as a numpy record

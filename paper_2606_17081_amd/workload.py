@@ -267,6 +267,7 @@ class Workload:
     traces: Dict[int, Trace]
     episodes: List[EpisodeSpec]
     poa: dict = field(default_factory=dict)
+    regime: dict = field(default_factory=lambda: dict(REGIME_PARAMS))   # controller = 2 episodes
 
 
 POA_PARAMS = dict(a=0.005, b=0.020, d=0.010, beta=2, C_cap=64, w_c=0.015)
