@@ -254,7 +254,7 @@ def policy_bench(torch, rk, wl, stream, steps):
     policies): 16 seeds x 5 concurrency levels x 5 policies in one launch;
     PoA-hat per policy and concurrency level."""
     from paper_2606_17081_amd.episodes import EpisodeRunner
-    log("generating the policy sweep (16 traces, 400 episodes)")
+    log("generating the policy sweep (16 traces, 480 episodes)")
     w = wl.policy_workload()
     r = EpisodeRunner(w, keep_cost=False)
     r.hash()
@@ -278,9 +278,22 @@ def policy_bench(torch, rk, wl, stream, steps):
             v = np.array([poa[e] for e, sp in enumerate(r.episodes) if sp.policy == p and sp.concurrency == C])
             by_c[str(C)] = [round(float(v.mean()), 6), round(float(v.std()), 6)]
         out[name] = by_c
+    by_c, share = {}, {}
+    reg = r.route_regime[: r.n_rows].cpu().numpy()
+    for C in wl.SWEEP70B_C:
+        es = [e for e, sp in enumerate(r.episodes) if sp.controller == 2 and sp.concurrency == C]
+        if es:
+            v = poa[es]
+            by_c[str(C)] = [round(float(v.mean()), 6), round(float(v.std()), 6)]
+            rows = np.concatenate([np.arange(r.rows[e][0], r.rows[e][0] + r.rows[e][1]) for e in es])
+            share[str(C)] = [round(float(np.mean(reg[rows] == k)), 4) for k in range(3)]
+    if by_c:
+        out["regime controller"] = by_c
+        out["regime controller: share of routes Below/Transition/Saturated"] = share
     E = len(r.episodes)
     log(f"policies: {E} episodes, simulate {ts.mean_ms():.3f} ms, PoA {tp.mean_ms():.3f} ms")
-    return {"workload": "1P/5D-shaped traces, W=6, 4096 requests, C in {32..512} x 16 seeds x 5 policies",
+    return {"workload": "1P/5D-shaped traces, W=6, 4096 requests, C in {32..512} x 16 seeds x "
+                        "(5 policies + the regime controller)",
             "episodes": E, "simulate_ms": round(ts.mean_ms(), 4), "poa_ms": round(tp.mean_ms(), 4),
             "episodes_per_s": E / (ts.mean_ms() * 1e-3), "poa_hat_by_policy_and_C": out}
 

@@ -300,11 +300,15 @@ POLICY_SWEEP = ((POLICY_ARGMIN, 0.0), (POLICY_SOFTMAX, 16.0), (POLICY_ROUND_ROBI
 
 
 def policy_workload(seeds: Sequence[int] = range(16), concurrency: Sequence[int] = SWEEP70B_C,
-                    policies: Sequence = POLICY_SWEEP, n_req: int = 4096) -> Workload:
-    """The 1P/5D-shaped sweep traces routed by each selection policy."""
+                    policies: Sequence = POLICY_SWEEP, n_req: int = 4096, regime: bool = True) -> Workload:
+    """The 1P/5D-shaped sweep traces routed by each selection policy, and (regime)
+    by the regime controller with the paper's parameters."""
     traces = {int(s): sweep70b_trace(int(s), n_req) for s in seeds}
     eps = [EpisodeSpec(seed=int(s), concurrency=int(C), cap=32768, policy=int(p), tau=float(tau))
            for p, tau in policies for C in concurrency for s in seeds]
+    if regime:
+        eps += [EpisodeSpec(seed=int(s), concurrency=int(C), cap=32768, controller=2)
+                for C in concurrency for s in seeds]
     return Workload("policies", W=6, cache_blocks=65536, traces=traces, episodes=eps)
 
 
