@@ -11,7 +11,11 @@
 // the W nodes finds it (no negative cycles, since the partial assignment is
 // optimal).  Edge minima are kept across rows and recomputed only for workers
 // whose rows changed on the last path.  One wavefront solves one window; the
-// window's matrix lives in LDS when it fits, else in the workspace.
+// window's matrix lives in LDS when it fits, else in the workspace.  Lane y
+// keeps worker y's distance, predecessor and row count in registers, values
+// move between lanes by readlane and DPP, and the path is walked by the whole
+// wavefront in lockstep.  Windows are dispatched longest first (a bucket sort
+// by size class), since the longest ones set the length of the launch.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -22,6 +26,7 @@ constexpr int PT = 64;   // threads per window
 
 struct PoaArgs {
     int32_t n_windows, max_window, W, kmax;
+    const int32_t* order;  // dispatch order of the windows, or NULL for 0..n_windows-1
     int64_t n_rows;
     const int64_t* win_off;
     const int32_t* route_worker;
@@ -37,29 +42,95 @@ struct PoaArgs {
 
 __device__ __forceinline__ double dinf() { return __longlong_as_double(0x7ff0000000000000ll); }
 
-template <bool LDSMAT>
+// the double held by lane src (src uniform across the wavefront)
+__device__ __forceinline__ double lane_f64(double v, int32_t src)
+{
+    const long long b = __double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, src);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), src);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+__device__ __forceinline__ void pick(double& v, int32_t& j, double ov, int32_t oj)
+{
+    if (ov < v || (ov == v && oj < j)) {
+        v = ov;
+        j = oj;
+    }
+}
+
+template <int CTRL>
+__device__ __forceinline__ void argmin_dpp_step(double& v, int32_t& j)
+{
+    const long long b = __double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)b, (int)(uint32_t)b, CTRL, 0xF, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(b >> 32), (int)(uint32_t)(b >> 32),
+                                                              CTRL, 0xF, 0xF, false);
+    const int32_t oj = __builtin_amdgcn_update_dpp(j, j, CTRL, 0xF, 0xF, false);
+    pick(v, j, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)), oj);
+}
+
+// Least (value, index) pair over the 64 lanes, by value and then by index;
+// every lane receives it.  Swaps within quads, then the mirrored half row and
+// row, leave each row of 16 lanes holding its minimum; the four rows are then
+// combined in a fixed order.
+__device__ __forceinline__ void wave_argmin_f64(double& v, int32_t& j)
+{
+    argmin_dpp_step<0xB1>(v, j);    // quad_perm [1,0,3,2]
+    argmin_dpp_step<0x4E>(v, j);    // quad_perm [2,3,0,1]
+    argmin_dpp_step<0x141>(v, j);   // row_half_mirror
+    argmin_dpp_step<0x140>(v, j);   // row_mirror
+    double bv = lane_f64(v, 0);
+    int32_t bj = __builtin_amdgcn_readlane(j, 0);
+    for (int32_t r = 16; r < 64; r += 16) pick(bv, bj, lane_f64(v, r), __builtin_amdgcn_readlane(j, r));
+    v = bv;
+    j = bj;
+}
+
+// Dispatch order: windows by descending size class (bit length of m), so the
+// longest windows start first.  One workgroup; the order within a class is
+// whatever the atomics give (it only affects scheduling).
+__global__ __launch_bounds__(1024) void poa_order_kernel(int32_t n_windows, const int64_t* __restrict__ win_off,
+                                                          int32_t* __restrict__ order)
+{
+    __shared__ int32_t cnt[16], base[16];
+    const int tid = threadIdx.x;
+    if (tid < 16) cnt[tid] = 0;
+    __syncthreads();
+    auto cls = [&](int32_t w) {
+        const int64_t m = win_off[w + 1] - win_off[w];
+        return m <= 0 ? 0 : (m >= 4096 ? 13 : 64 - __clzll((unsigned long long)m));
+    };
+    for (int32_t w = tid; w < n_windows; w += blockDim.x) atomicAdd(&cnt[cls(w)], 1);
+    __syncthreads();
+    if (tid == 0) {
+        int32_t o = 0;
+        for (int32_t c = 15; c >= 0; --c) {
+            base[c] = o;
+            o += cnt[c];
+        }
+    }
+    __syncthreads();
+    for (int32_t w = tid; w < n_windows; w += blockDim.x) order[atomicAdd(&base[cls(w)], 1)] = w;
+}
+
+template <bool LDSMAT, int WMAX>
 __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ int32_t sh_bad;
-    __shared__ int32_t sh_hops;
     const int tid = threadIdx.x;
     const int32_t W = a.W;
     int32_t* s_n = (int32_t*)(smem + a.lds_int);   // [W] window counts of the greedy assignment
-    int32_t* s_cnt = s_n + W;                        // [W] rows per worker in the partial OPT
-    int32_t* s_pred = s_cnt + W;                     // [W]
-    int32_t* s_np = s_pred + W;                      // [W]
-    float* s_base = (float*)(s_np + W);              // [W]
+    float* s_base = (float*)(s_n + W);               // [W]
     int32_t* s_mem = (int32_t*)(s_base + W);         // [W * kmax] rows held by each worker
     int32_t* s_assign = s_mem + W * a.kmax;          // [max_window]
     int32_t* s_pos = s_assign + a.max_window;        // [max_window] index of a row in its worker's list
     int32_t* s_er = s_pos + a.max_window;            // [W * W] row realising each edge weight
-    int32_t* s_hx = s_er + W * W;                    // [W + 2] path moves: losing worker
-    int32_t* s_hy = s_hx + W + 2;                    // [W + 2]                gaining worker
-    int32_t* s_hr = s_hy + W + 2;                    // [W + 2]                row
     double* s_e = (double*)(smem + a.lds_dbl);       // [W * W] edge weights a -> b
 
-    for (int32_t w = blockIdx.x; w < a.n_windows; w += gridDim.x) {
+    for (int32_t wi = blockIdx.x; wi < a.n_windows; wi += gridDim.x) {
+        const int32_t w = a.order ? a.order[wi] : wi;
         const int64_t r0 = a.win_off[w], r1 = a.win_off[w + 1];
         const int64_t m64 = r1 - r0;
         if (r0 < 0 || m64 < 0 || r1 > a.n_rows || m64 > a.max_window) {
@@ -90,10 +161,7 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
         }
         float* cm = LDSMAT ? (float*)(smem + a.lds_mat) : a.cm + r0 * W;
         // ---- frozen matrix
-        for (int32_t j = tid; j < W; j += PT) {
-            s_n[j] = 0;
-            s_cnt[j] = 0;
-        }
+        for (int32_t j = tid; j < W; j += PT) s_n[j] = 0;
         for (int32_t pq = tid; pq < W * W; pq += PT) s_e[pq] = dinf();
         if (tid == 0) sh_bad = 0;
         __syncthreads();
@@ -137,19 +205,25 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
         // ---- successive shortest paths (lane y < W stands for worker y)
         for (int32_t pq = tid; pq < W * W; pq += PT) s_er[pq] = -1;
         __syncthreads();
+        const bool wl = tid < W;
+        int32_t cnt = 0;   // lane y: rows on worker y in the partial optimum
+        bool placed_all = true;
         for (int32_t i = 0; i < m; ++i) {
-            // Bellman-Ford over the workers, wavefront-synchronous: lane y keeps
-            // dist[y] and pred[y] in registers and reads the others by shuffles
-            double dist = tid < W ? (double)cm[(int64_t)i * W + tid] : dinf();
+            // Bellman-Ford over the workers (Jacobi rounds): lane y keeps dist[y]
+            // and pred[y]; lane y's column of edge weights sits in registers
+            double ecol[WMAX];
+#pragma unroll
+            for (int32_t x = 0; x < WMAX; ++x) ecol[x] = (x < W && wl) ? s_e[x * W + tid] : dinf();
+            double dist = wl ? (double)cm[(int64_t)i * W + tid] : dinf();
             int32_t pred = -1;
             for (int32_t round = 0;; ++round) {
                 double nd = dist;
                 int32_t pb = pred;
-                for (int32_t x = 0; x < W; ++x) {
-                    const double dx = __shfl(dist, x, 64);
-                    if (tid < W) {
-                        const double v = dx + s_e[x * W + tid];
-                        if (v < nd) {
+#pragma unroll
+                for (int32_t x = 0; x < WMAX; ++x) {
+                    if (x < W) {
+                        const double v = lane_f64(dist, x) + ecol[x];
+                        if (wl && v < nd) {
                             nd = v;
                             pb = x;
                         }
@@ -165,108 +239,103 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                 }
             }
             // target: least distance among workers with spare capacity (lowest index on ties)
-            int32_t t = -1;
-            {
-                double bd = tid < W && s_cnt[tid] < K ? dist : dinf();
-                int32_t bj = tid < W && s_cnt[tid] < K ? tid : 0x7fffffff;
-                for (int off = 32; off > 0; off >>= 1) {
-                    const double od = __shfl_xor(bd, off, 64);
-                    const int32_t oj = __shfl_xor(bj, off, 64);
-                    if (od < bd || (od == bd && oj < bj)) {
-                        bd = od;
-                        bj = oj;
-                    }
-                }
-                t = bj;
+            double bd = wl && cnt < K ? dist : dinf();
+            int32_t t = wl && cnt < K ? tid : 0x7fffffff;
+            wave_argmin_f64(bd, t);
+            if (t < 0 || t >= W) {   // no worker with spare capacity: impossible when K * W >= m
+                if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
+                placed_all = false;
+                break;
             }
-            if (tid < W) s_pred[tid] = pred;
-            __syncthreads();
-            if (tid == 0) {
-                // walk the path back from the target, moving one row per edge
-                int32_t y = t, hops = 0;
-                while (s_pred[y] >= 0 && hops <= W) {
-                    const int32_t x = s_pred[y];
-                    const int32_t r = s_er[x * W + y];
-                    int32_t kk = r >= 0 ? s_pos[r] : -1;
-                    if (kk < 0 || kk >= s_cnt[x] || s_mem[x * a.kmax + kk] != r || s_cnt[y] >= a.kmax) {
-                        atomicOr(a.status, RK_DEV_NO_CONVERGE);
-                        break;
-                    }
-                    const int32_t last = s_mem[x * a.kmax + s_cnt[x] - 1];
+            // walk the path back from the target, moving one row per edge; lane h
+            // records move h (losing worker, gaining worker, row)
+            int32_t hx = -1, hy = -1, hr = -1;
+            int32_t y = t, hops = 0;
+            for (;;) {
+                const int32_t x = __builtin_amdgcn_readlane(pred, y);
+                if (x < 0) break;
+                const int32_t cx = __builtin_amdgcn_readlane(cnt, x), cy = __builtin_amdgcn_readlane(cnt, y);
+                const int32_t r = s_er[x * W + y];
+                const int32_t kk = r >= 0 ? s_pos[r] : -1;
+                if (hops >= W - 1 || kk < 0 || kk >= cx || s_mem[x * a.kmax + kk] != r || cy >= a.kmax) {
+                    if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
+                    break;
+                }
+                const int32_t last = s_mem[x * a.kmax + cx - 1];
+                if (tid == 0) {
                     s_mem[x * a.kmax + kk] = last;
                     s_pos[last] = kk;
-                    s_cnt[x] -= 1;
-                    s_mem[y * a.kmax + s_cnt[y]] = r;
-                    s_pos[r] = s_cnt[y];
-                    s_cnt[y] += 1;
+                    s_mem[y * a.kmax + cy] = r;
+                    s_pos[r] = cy;
                     s_assign[r] = y;
-                    s_hx[hops] = x;        // x lost r ...
-                    s_hy[hops] = y;        // ... and y gained it
-                    s_hr[hops] = r;
-                    y = x;
-                    ++hops;
                 }
-                if (s_cnt[y] < a.kmax) {
-                    s_mem[y * a.kmax + s_cnt[y]] = i;
-                    s_pos[i] = s_cnt[y];
-                    s_cnt[y] += 1;
-                } else {
+                cnt += (tid == y) - (tid == x);
+                if (tid == hops) {
+                    hx = x;        // x lost r ...
+                    hy = y;        // ... and y gained it
+                    hr = r;
+                }
+                y = x;
+                ++hops;
+            }
+            {
+                const int32_t cy = __builtin_amdgcn_readlane(cnt, y);
+                if (cy < a.kmax) {
+                    if (tid == 0) {
+                        s_mem[y * a.kmax + cy] = i;
+                        s_pos[i] = cy;
+                    }
+                    cnt += tid == y;
+                } else if (tid == 0) {
                     atomicOr(a.status, RK_DEV_NO_CONVERGE);
                 }
-                s_assign[i] = y;
-                s_hx[hops] = -1;           // no loss
-                s_hy[hops] = y;            // the new row's worker gained row i
-                s_hr[hops] = i;
-                sh_hops = hops + 1;
+                if (tid == 0) s_assign[i] = y;
+                if (tid == hops) {
+                    hx = -1;       // no loss
+                    hy = y;        // the new row's worker gained row i
+                    hr = i;
+                }
+                ++hops;
             }
             __syncthreads();
             // ---- edge maintenance, e[x][z] = min over rows r on x of c[r][z] - c[r][x]:
             // an edge whose argmin row left x is recomputed over x's rows (all
-            // lanes scan, then a wavefront min); a gained row is folded in.
-            const int32_t nev = sh_hops;
-            for (int32_t h = 0; h < nev; ++h) {
-                const int32_t x = s_hx[h], r = s_hr[h];
+            // lanes scan, then a wavefront argmin); a gained row is folded in.
+            for (int32_t h = 0; h < hops; ++h) {
+                const int32_t x = __builtin_amdgcn_readlane(hx, h), r = __builtin_amdgcn_readlane(hr, h);
                 if (x < 0) continue;
-                for (int32_t z = 0; z < W; ++z) {
-                    if (z == x || s_er[x * W + z] != r) continue;
+                uint64_t lost = __ballot(wl && tid != x && s_er[x * W + tid] == r);
+                const int32_t cx = __builtin_amdgcn_readlane(cnt, x);
+                while (lost) {
+                    const int32_t z = __ffsll((unsigned long long)lost) - 1;
+                    lost &= lost - 1;
                     double best = dinf();
                     int32_t brow = 0x7fffffff;
-                    for (int32_t k = tid; k < s_cnt[x]; k += PT) {
+                    for (int32_t k = tid; k < cx; k += PT) {
                         const int32_t q = s_mem[x * a.kmax + k];
-                        const double v = (double)cm[(int64_t)q * W + z] - (double)cm[(int64_t)q * W + x];
-                        if (v < best || (v == best && q < brow)) {
-                            best = v;
-                            brow = q;
-                        }
+                        pick(best, brow, (double)cm[(int64_t)q * W + z] - (double)cm[(int64_t)q * W + x], q);
                     }
-                    for (int off = 32; off > 0; off >>= 1) {
-                        const double ob = __shfl_xor(best, off, 64);
-                        const int32_t orow = __shfl_xor(brow, off, 64);
-                        if (ob < best || (ob == best && orow < brow)) {
-                            best = ob;
-                            brow = orow;
-                        }
-                    }
+                    wave_argmin_f64(best, brow);
                     if (tid == 0) {
                         s_e[x * W + z] = best;
                         s_er[x * W + z] = brow == 0x7fffffff ? -1 : brow;
                     }
-                    __syncthreads();
                 }
             }
-            for (int32_t h = 0; h < nev; ++h) {
-                const int32_t y = s_hy[h], r = s_hr[h];
-                if (tid < W && tid != y) {
-                    const double v = (double)cm[(int64_t)r * W + tid] - (double)cm[(int64_t)r * W + y];
-                    if (v < s_e[y * W + tid]) {
-                        s_e[y * W + tid] = v;
-                        s_er[y * W + tid] = r;
+            for (int32_t h = 0; h < hops; ++h) {
+                const int32_t yg = __builtin_amdgcn_readlane(hy, h), r = __builtin_amdgcn_readlane(hr, h);
+                if (wl && tid != yg) {
+                    const double v = (double)cm[(int64_t)r * W + tid] - (double)cm[(int64_t)r * W + yg];
+                    if (v < s_e[yg * W + tid]) {
+                        s_e[yg * W + tid] = v;
+                        s_er[yg * W + tid] = r;
                     }
                 }
-                __syncthreads();
             }
+            __syncthreads();
         }
-        if (tid == 0 && a.coord) {
+        if (tid == 0 && a.coord && !placed_all) a.coord[w] = __longlong_as_double(0x7ff8000000000000ll);
+        if (tid == 0 && a.coord && placed_all) {
             double s = 0.0;
             for (int32_t i = 0; i < m; ++i) s += (double)cm[(int64_t)i * W + s_assign[i]];
             a.coord[w] = s;
@@ -297,7 +366,17 @@ extern "C" size_t rk_poa_workspace_size(int64_t n_rows, int32_t W)
 {
     if (n_rows < 0 || W < 1) return 0;
     return align_up((size_t)n_rows * (size_t)W * sizeof(float), 256) + 2 * 256 +
-           2 * align_up(((size_t)n_rows + 1) * sizeof(double), 256);
+           2 * align_up(((size_t)n_rows + 1) * sizeof(double), 256) +
+           align_up(((size_t)n_rows + 1) * sizeof(int32_t), 256);
+}
+
+template <bool LDSMAT>
+static void launch_windows(int32_t W, unsigned grid, size_t lds, hipStream_t s, const PoaArgs& a)
+{
+    if (W <= 8) hipLaunchKernelGGL((poa_window_kernel<LDSMAT, 8>), dim3(grid), dim3(PT), lds, s, a);
+    else if (W <= 16) hipLaunchKernelGGL((poa_window_kernel<LDSMAT, 16>), dim3(grid), dim3(PT), lds, s, a);
+    else if (W <= 32) hipLaunchKernelGGL((poa_window_kernel<LDSMAT, 32>), dim3(grid), dim3(PT), lds, s, a);
+    else hipLaunchKernelGGL((poa_window_kernel<LDSMAT, 64>), dim3(grid), dim3(PT), lds, s, a);
 }
 
 extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_t n_episodes,
@@ -326,6 +405,10 @@ extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_
     const size_t vec_bytes = align_up(((size_t)n_rows + 1) * sizeof(double), 256);
     double* selfish = selfish_out ? selfish_out : (double*)(ws + cm_bytes + 256);
     double* coord = coord_out ? coord_out : (double*)(ws + cm_bytes + 512 + vec_bytes);
+    // the dispatch order has room for n_rows + 1 windows; beyond that (many
+    // empty windows) the windows run in index order
+    int32_t* order = (n_windows > 1 && (size_t)n_windows <= (size_t)n_rows + 1)
+                         ? (int32_t*)(ws + cm_bytes + 512 + 2 * vec_bytes) : nullptr;
     if (n_episodes > 0 && (!selfish_out || !coord_out) && (size_t)n_windows > (size_t)n_rows + 1)
         return fail(RK_EINVAL, "rk_poa_estimate: pass selfish_out and coord_out when windows exceed rows");
     hipStream_t s = (hipStream_t)stream;
@@ -334,6 +417,7 @@ extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_
         PoaArgs a;
         a.n_windows = n_windows;
         a.max_window = max_window;
+        a.order = order;
         a.W = W;
         a.kmax = params.K_fixed > 0 ? (params.K_fixed < max_window ? params.K_fixed : max_window)
                                     : (max_window + W - 1) / W;
@@ -349,8 +433,7 @@ extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_
         a.status = st;
         size_t o = 0;
         a.lds_int = 0;
-        o = align_up(((size_t)W * 5 + (size_t)W * a.kmax + 2 * (size_t)max_window + (size_t)W * W +
-                      3 * ((size_t)W + 2)) * 4, 16);
+        o = align_up(((size_t)W * 2 + (size_t)W * a.kmax + 2 * (size_t)max_window + (size_t)W * W) * 4, 16);
         a.lds_dbl = (uint32_t)o;
         o = align_up(o + (size_t)W * W * 8, 16);
         const size_t limit = 60 * 1024;
@@ -360,9 +443,14 @@ extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_
         const bool lds_mat = o + mat <= limit;
         a.lds_mat = (uint32_t)o;
         if (lds_mat) o += mat;
+        if (order) {
+            hipLaunchKernelGGL(poa_order_kernel, dim3(1), dim3(1024), 0, s, n_windows, win_off, order);
+            int rc = hip_check(hipGetLastError(), "rk_poa_estimate order launch");
+            if (rc) return rc;
+        }
         unsigned grid = (unsigned)(n_windows < 65536 ? n_windows : 65536);
-        if (lds_mat) hipLaunchKernelGGL(poa_window_kernel<true>, dim3(grid), dim3(PT), o, s, a);
-        else hipLaunchKernelGGL(poa_window_kernel<false>, dim3(grid), dim3(PT), o, s, a);
+        if (lds_mat) launch_windows<true>(W, grid, o, s, a);
+        else launch_windows<false>(W, grid, o, s, a);
         int rc = hip_check(hipGetLastError(), "rk_poa_estimate window launch");
         if (rc) return rc;
     }
