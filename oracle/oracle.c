@@ -36,7 +36,11 @@
  *    request is routed given the loads and caches left by earlier ones.  The
  *    chosen worker's LRU cache touches the prompt's blocks from last to first
  *    (block 0 becomes most recent), inserts the missing ones and evicts least
- *    recently used blocks until it holds at most cache_blocks.
+ *    recently used blocks until it holds at most cache_blocks.  Per episode
+ *    the cache may instead follow the KV block manager's frequency policy
+ *    (Section 2.2): evict the least frequent block first, frequencies start
+ *    at 1, double on a hit and drop by 1 (not below 1) every decay_steps
+ *    routing steps.
  *  - Steps: a step routes up to C/H requests from the ready queue; a request
  *    stays active (its blocks count in A_j) for H steps, so C requests are in
  *    flight once the ramp is over (the semaphore-held concurrency of
@@ -155,6 +159,16 @@ float orc_route_cost(float w_ov, float w_act, float w_sat, int32_t cap,
 #define ORC_POLICY_ROUND_ROBIN 2
 #define ORC_POLICY_RANDOM 3
 #define ORC_POLICY_P2C 4
+
+/* Eviction policies of a worker's block cache: least recently used, or the
+ * KV block manager's frequency policy of Section 2.2 (frequency 1 on insert,
+ * doubled on a hit, minus 1 per time-decay step and never below 1; the least
+ * frequent block goes first, the least recently used among equals).  A
+ * time-decay step happens every decay_steps routing steps; frequencies stop
+ * doubling at ORC_FREQ_CAP. */
+#define ORC_EVICT_LRU 0
+#define ORC_EVICT_FREQ 1
+#define ORC_FREQ_CAP (1 << 20)
 
 /* exp(x) for x <= 0 in float arithmetic (Cody and Waite's argument
  * reduction): x = n ln2 + r with n = floor(x log2(e) + 1/2), ln2 split into a
@@ -301,6 +315,7 @@ int orc_score_batch(int32_t B, int32_t W, const uint64_t* chains, const int64_t*
 
 typedef struct {
     uint64_t key;
+    int64_t freq;         /* access frequency (frequency eviction only) */
     int32_t prev, next;   /* recency list */
     int32_t hnext;        /* bucket chain */
 } lru_node;
@@ -358,19 +373,24 @@ static void list_append(lru_t* c, int32_t i)
     c->newest = i;
 }
 
-/* Make key the most recently used entry; returns 1 if it was inserted. */
+/* Make key the most recently used entry; returns 1 if it was inserted.  An
+ * inserted entry starts at frequency 1 and a hit doubles the frequency, up to
+ * ORC_FREQ_CAP (Section 2.2, the KV block manager's frequency policy; the
+ * frequencies only matter under frequency eviction). */
 static int lru_touch(lru_t* c, uint64_t key, int* err)
 {
     int32_t i = lru_find(c, key);
     if (i >= 0) {
         list_unlink(c, i);
         list_append(c, i);
+        c->node[i].freq = 2 * c->node[i].freq < ORC_FREQ_CAP ? 2 * c->node[i].freq : ORC_FREQ_CAP;
         return 0;
     }
     if (c->free_head < 0) { *err = 1; return 0; }
     i = c->free_head;
     c->free_head = c->node[i].hnext;
     c->node[i].key = key;
+    c->node[i].freq = 1;
     c->node[i].hnext = c->bucket[key & c->mask];
     c->bucket[key & c->mask] = i;
     list_append(c, i);
@@ -378,10 +398,9 @@ static int lru_touch(lru_t* c, uint64_t key, int* err)
     return 1;
 }
 
-/* Remove the least recently used entry and return its key. */
-static uint64_t lru_evict_oldest(lru_t* c)
+/* Remove entry i and return its key. */
+static uint64_t lru_remove(lru_t* c, int32_t i)
 {
-    int32_t i = c->oldest;
     uint64_t key = c->node[i].key;
     list_unlink(c, i);
     int32_t* pp = &c->bucket[key & c->mask];
@@ -391,6 +410,36 @@ static uint64_t lru_evict_oldest(lru_t* c)
     c->free_head = i;
     c->size -= 1;
     return key;
+}
+
+/* Remove the least recently used entry and return its key. */
+static uint64_t lru_evict_oldest(lru_t* c)
+{
+    return lru_remove(c, c->oldest);
+}
+
+/* Frequency eviction: remove the entry of least frequency, the least recently
+ * used among equals, and return its key.  Frequencies never drop below 1, so
+ * the oldest entry at frequency 1, if any, is that entry; otherwise the
+ * minimum is found by a full pass. */
+static uint64_t lfu_evict(lru_t* c)
+{
+    for (int32_t i = c->oldest; i >= 0; i = c->node[i].next)
+        if (c->node[i].freq == 1) return lru_remove(c, i);
+    int64_t fmin = INT64_MAX;
+    for (int32_t i = c->oldest; i >= 0; i = c->node[i].next)
+        if (c->node[i].freq < fmin) fmin = c->node[i].freq;
+    int32_t i = c->oldest;
+    while (c->node[i].freq != fmin) i = c->node[i].next;
+    return lru_remove(c, i);
+}
+
+/* One time-decay step: every cached entry's frequency drops by 1, to no less
+ * than 1. */
+static void lfu_decay(lru_t* c)
+{
+    for (int32_t i = c->oldest; i >= 0; i = c->node[i].next)
+        if (c->node[i].freq > 1) c->node[i].freq -= 1;
 }
 
 static int32_t lru_overlap(const lru_t* c, const uint64_t* h, int32_t P)
@@ -469,6 +518,7 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
                          int32_t ctrl_num, int32_t ctrl_den,
                          int32_t policy, float tau, const uint32_t* rand,
                          const double* rg_d, const int32_t* rg_i, const float* rg_f, int32_t* route_regime,
+                         int32_t evict_policy, int32_t decay_steps,
                          int32_t n_conv, const int64_t* turn_off, const int32_t* turn_blocks,
                          const int64_t* chain_off, const uint64_t* chains,
                          int32_t* route_turn, int32_t* route_worker, int32_t* route_step,
@@ -493,6 +543,8 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
     }
     if (policy < ORC_POLICY_ARGMIN || policy > ORC_POLICY_P2C) return ORC_EINVAL;
     if (policy == ORC_POLICY_SOFTMAX && !(tau > 0.0f)) return ORC_EINVAL;
+    if (evict_policy != ORC_EVICT_LRU && evict_policy != ORC_EVICT_FREQ) return ORC_EINVAL;
+    if (evict_policy == ORC_EVICT_FREQ && decay_steps < 1) return ORC_EINVAL;
     if (!rand && (policy == ORC_POLICY_SOFTMAX || policy == ORC_POLICY_RANDOM || policy == ORC_POLICY_P2C))
         return ORC_EINVAL;
     const int64_t n_routes = turn_off[n_conv];
@@ -545,6 +597,8 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
             }
         }
         step_count[slot] = 0;
+        if (evict_policy == ORC_EVICT_FREQ && s > 0 && s % decay_steps == 0)
+            for (int32_t j = 0; j < W; ++j) lfu_decay(&lru[j]);   /* time-decay step */
         int64_t inflight = 0;
         for (int64_t k = 1; k < H && k <= s; ++k) inflight += step_count[(s - k) % H];
         if (q_size == 0 && inflight == 0) break;
@@ -598,7 +652,7 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
             int32_t ev = 0;
             uint64_t dig = 0;
             while (lru[sigma].size > cache_blocks) {
-                uint64_t key = lru_evict_oldest(&lru[sigma]);
+                uint64_t key = evict_policy == ORC_EVICT_FREQ ? lfu_evict(&lru[sigma]) : lru_evict_oldest(&lru[sigma]);
                 ev += 1;
                 dig += orc_splitmix64(key);
                 if (evicted_keys && totals[1] + ev - 1 < evicted_cap)

@@ -66,6 +66,7 @@ def lib():
                 i32, i32, i32, i32, f32, f32, f32, i32, i32, f32, i32, i32, i32,
                 i32, f32, p,
                 p, p, p, p,
+                i32, i32,
                 i32, p, p, p, p,
                 p, p, p, p, p, p, p, p, p, p,
                 p, p, p, i64, p]
@@ -261,6 +262,7 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         spec.controller, spec.ctrl_w_ov, spec.ctrl_window, spec.ctrl_num, spec.ctrl_den,
         policy, tau, g(rand),
         _ptr(rd), _ptr(ri), _ptr(rf), g(out["route_regime"]),
+        int(getattr(spec, "evict_policy", 0)), int(getattr(spec, "decay_steps", 0)),
         n_conv, _ptr(turn_off), g(turn_blocks), _ptr(chain_off), g(chains),
         g(out["route_turn"]), g(out["route_worker"]), g(out["route_step"]),
         g(out["route_blocks"]), g(out["overlap"]), g(out["cost"]),

@@ -226,10 +226,17 @@ class EpisodeSpec:
     ctrl_den: int = 10
     policy: int = 0           # POLICY_ARGMIN, POLICY_SOFTMAX, POLICY_ROUND_ROBIN, POLICY_RANDOM, POLICY_P2C
     tau: float = 0.0          # softmax temperature (> 0 with POLICY_SOFTMAX), in cost units
+    evict_policy: int = 0     # EVICT_LRU, or EVICT_FREQ (the KV block manager's frequency policy)
+    decay_steps: int = 0      # EVICT_FREQ: routing steps per time-decay step (>= 1)
 
     @property
     def routes_per_step(self) -> int:
         return self.concurrency // self.hold_steps
+
+
+# Eviction policies of the workers' block caches (the routing library's RK_EVICT_* codes).
+EVICT_LRU = 0    # least recently used block first
+EVICT_FREQ = 1   # least frequent block first (1 on insert, x2 per hit, -1 per decay step, floor 1)
 
 
 # Regime controller (controller = 2): the paper's EWMA weight, its 70B thresholds

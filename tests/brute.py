@@ -33,11 +33,15 @@ def overlap_set(chain, cached: set) -> int:
 
 
 def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blocks, chains_per_conv,
-            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10, select=None, regime=None):
+            controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10, select=None, regime=None,
+            freq=None):
     """Sequential routing episode with OrderedDict LRU caches; select(costs, t)
     picks the worker of route t (default: least cost, lowest index).  With
     controller 2, regime = (params(r) -> (tau, w_ov), step(n, t) -> new
-    regime, select_tau(costs, t, tau)) drives the regime controller."""
+    regime, select_tau(costs, t, tau)) drives the regime controller.  With
+    freq = (decay_steps, cap) the caches evict by frequency: a block enters at 1,
+    doubles per hit (at most cap), loses 1 per decay step (never below 1), and
+    the least frequent block, oldest among equals, is evicted first."""
     n_conv = len(turn_off) - 1
     caches = [OrderedDict() for _ in range(W)]   # key -> None, oldest first
     A = [0] * W
@@ -60,6 +64,10 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
         inflight = sum(len(v) for k, v in steps.items() if s - H < k < s)
         if not queue and inflight == 0:
             break
+        if freq is not None and s > 0 and s % freq[0] == 0:
+            for cch in caches:
+                for key in cch:
+                    cch[key] = max(cch[key] - 1, 1)
         take, queue = queue[:rps], queue[rps:]
         steps[s] = []
         for c in take:
@@ -91,11 +99,18 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
             for k in range(P - 1, -1, -1):
                 if h[k] in cache:
                     cache.move_to_end(h[k])
+                    if freq is not None:
+                        cache[h[k]] = min(2 * cache[h[k]], freq[1])
                 else:
-                    cache[h[k]] = None
+                    cache[h[k]] = 1
             evicted = []
             while len(cache) > cache_blocks:
-                key, _ = cache.popitem(last=False)
+                if freq is None:
+                    key, _ = cache.popitem(last=False)
+                else:
+                    fmin = min(cache.values())
+                    key = next(k for k, v in cache.items() if v == fmin)
+                    del cache[key]
                 evicted.append(key)
             A[sigma] += P
             nflight[sigma] += 1
