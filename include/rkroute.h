@@ -249,9 +249,17 @@ int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains, const int
  *     the last three are the static counterfactual policies of the
  *     discussion section, under the same cost;
  *   - the chosen worker sigma touches the prompt's blocks from last to first
- *     (block 0 ends most recent), inserting those it lacks, then evicts least
- *     recently used blocks until it holds at most cache_blocks; A_sigma += P.
- *     Caches start empty; blocks stay cached after a request is released.
+ *     (block 0 ends most recent), inserting those it lacks, then evicts blocks
+ *     until it holds at most cache_blocks; A_sigma += P.  Caches start empty;
+ *     blocks stay cached after a request is released.  Eviction order:
+ *       RK_EVICT_LRU   least recently used first;
+ *       RK_EVICT_FREQ  the KV block manager's frequency policy (Section 2.2):
+ *                      a block's frequency is 1 when inserted, doubles on a
+ *                      hit (at most RK_FREQ_CAP) and drops by 1, never below
+ *                      1, at every time-decay step (the start of each routing
+ *                      step s > 0 with s a multiple of decay_steps); the least
+ *                      frequent block goes first, the least recently used
+ *                      among equals.
  * The queue order, the touch order and the tie rule make every result unique.
  */
 typedef struct {
@@ -269,8 +277,15 @@ typedef struct {
     int64_t out_base;        /* first output row of this episode                       */
     int32_t policy;          /* RK_POLICY_*                                            */
     float   tau;             /* softmax temperature, > 0 with RK_POLICY_SOFTMAX        */
-} rk_episode_params;         /* 72 bytes; invalid policy fields set RK_DEV_BAD_PARAMS and
-                                leave the episode's outputs unwritten                 */
+    int32_t evict_policy;    /* RK_EVICT_*                                             */
+    int32_t decay_steps;     /* routing steps per time-decay step, >= 1 with RK_EVICT_FREQ */
+} rk_episode_params;         /* 80 bytes; invalid policy or eviction fields set
+                                RK_DEV_BAD_PARAMS and leave the episode's outputs
+                                unwritten                                             */
+
+#define RK_EVICT_LRU          0
+#define RK_EVICT_FREQ         1
+#define RK_FREQ_CAP           (1 << 20)
 
 #define RK_POLICY_ARGMIN      0
 #define RK_POLICY_SOFTMAX     1

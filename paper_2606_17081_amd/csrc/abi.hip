@@ -57,6 +57,7 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     L.off_slots = o;   o = align_up(o + (size_t)W * L.slots * sizeof(Slot), 256);
     L.off_log = o;     o = align_up(o + (size_t)W * L.ring * sizeof(uint32_t), 256);
     L.off_scratch = o; o = align_up(o + live_max * sizeof(uint64_t), 256);
+    L.off_scratch_f = o; o = align_up(o + live_max * sizeof(uint32_t), 256);
     L.off_queue = o;   o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);
     L.off_next = o;    o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);
     L.per_episode = o;

@@ -30,8 +30,21 @@
 //      the decided routes, a few routes per claim.
 // A route that must evict (and every route in scan mode, where caches need
 // not be prefix-closed) stops phase B: once every decided route's writes are
-// in, the least recently used blocks are evicted and the pending requests
-// searched again on that worker.
+// in, blocks are evicted and the pending requests searched again on that
+// worker.
+//
+// Frequency eviction keeps, per slot, the key K = f + e of a block whose
+// frequency was f after its last update in decay epoch e (epoch = routing
+// step / decay_steps); in epoch E its frequency is max(K - E, 1), the eager
+// decay applied lazily.  Within one epoch a hit doubles the frequency (capped)
+// and an insert leaves it at 1, operations that commute, so the writers apply
+// them with atomics in any order; phase B stops at every epoch change until
+// the earlier epoch's writes are in.  A parent block is at least as frequent
+// as its child and touched later, so caches stay prefix-closed, and the
+// victims -- the least frequent blocks, oldest first -- are the oldest blocks
+// at frequency 1: the route's own new blocks are such blocks, so there are
+// always enough.  Eviction walks the log from its head and skips the more
+// frequent records, which keep the head from moving past them.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -43,7 +56,7 @@ constexpr int NW = NT / 64;
 constexpr int kMaxBatch = 64;       // routes per batch (at most one wavefront of lanes)
 constexpr int32_t kMoreTurns = 0x40000000;   // flag on an in-flight conversation index: it has a next turn
 
-enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2 };
+enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2, EV_EPOCH = 3 };
 
 struct EpArgs {
     int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB;
@@ -66,7 +79,7 @@ constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 struct EpShared {
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone;
     int32_t woff[NW][KR + 1];
-    uint32_t new_head;
+    uint32_t new_head, first_kept;
     int64_t ev_row, ev_total;
     unsigned long long digest, rb_mask;
     int32_t wtot[NW];
@@ -98,6 +111,34 @@ __device__ __forceinline__ void load_slot(const Slot* p, uint64_t& key, uint32_t
     const uint4 v = *reinterpret_cast<const uint4*>(p);
     key = (uint64_t)v.x | ((uint64_t)v.y << 32);
     stamp = v.z;
+}
+
+__device__ __forceinline__ void load_slot(const Slot* p, uint64_t& key, uint32_t& stamp, uint32_t& fkey)
+{
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    key = (uint64_t)v.x | ((uint64_t)v.y << 32);
+    stamp = v.z;
+    fkey = v.w;
+}
+
+// Frequency update of a touched block in decay epoch ep: an insert leaves the
+// frequency at 1 (K at least ep + 1), a hit doubles max(K - ep, 1) up to
+// RK_FREQ_CAP.  Within one epoch these commute, so concurrent touches of a
+// block by several routes give the sequential result in any order.
+__device__ __forceinline__ void freq_touch(uint32_t* fk, bool inserted, uint32_t ep)
+{
+    if (inserted) {
+        __hip_atomic_fetch_max(fk, ep + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        return;
+    }
+    uint32_t old = __hip_atomic_load(fk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    for (;;) {
+        const uint32_t f = old > ep + 1u ? old - ep : 1u;
+        const uint32_t nf = f >= (uint32_t)RK_FREQ_CAP / 2u ? (uint32_t)RK_FREQ_CAP : 2u * f;
+        if (__hip_atomic_compare_exchange_strong(fk, &old, nf + ep, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP))
+            return;
+    }
 }
 
 constexpr int kWin = 4;    // slots read by one lookup (a run of this length is rare at load <= 0.5)
@@ -429,7 +470,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
-    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rrnd, lcp, bytes;
+    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rrnd, lcp, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
@@ -454,6 +495,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
     b.rsig = take(nb * 4, 4);
     b.rotab = take(nb * 4, 4);
     b.rstamp = take(nb * 4, 4);
+    b.rep = take(nb * 4, 4);
     b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
     b.bytes = (o + 15) / 16 * 16;
@@ -497,6 +539,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     int32_t* r_sig = (int32_t*)(bb + BL.rsig);             // chosen worker
     int32_t* r_otab = (int32_t*)(bb + BL.rotab);           // blocks known cached in sigma's table
     uint32_t* r_stamp = (uint32_t*)(bb + BL.rstamp);       // stamp of the last block
+    uint32_t* r_ep = (uint32_t*)(bb + BL.rep);             // decay epoch (frequency eviction)
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
 
@@ -524,7 +567,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     }
     const bool draws = rg_draws || (!regime_ctl && (policy == RK_POLICY_SOFTMAX || policy == RK_POLICY_RANDOM ||
                                                     policy == RK_POLICY_P2C));
+    const bool freq = prm.evict_policy == RK_EVICT_FREQ;
+    const int32_t dsteps = prm.decay_steps;
     if (prm.controller < 0 || prm.controller > 2 || !rg_ok ||
+        (prm.evict_policy != RK_EVICT_LRU && !freq) || (freq && dsteps < 1) ||
         (!regime_ctl && (policy < RK_POLICY_ARGMIN || policy > RK_POLICY_P2C ||
                          (policy == RK_POLICY_SOFTMAX && !(tau > 0.0f)))) ||
         (draws && !a.route_rand)) {
@@ -537,6 +583,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     Slot* g_slots = (Slot*)(ws + a.L.off_slots);
     uint32_t* g_log = (uint32_t*)(ws + a.L.off_log);
     uint64_t* g_scratch = (uint64_t*)(ws + a.L.off_scratch);
+    uint32_t* g_scratch_f = (uint32_t*)(ws + a.L.off_scratch_f);
     int32_t* g_queue = (int32_t*)(ws + a.L.off_queue);
     int32_t* g_next = (int32_t*)(ws + a.L.off_next);
     const uint64_t S = a.L.slots, smask = S - 1, R = a.L.ring, rmask = R - 1;
@@ -591,17 +638,21 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             const uint32_t pos = base + (uint32_t)tid;
             bool live = false;
             uint64_t key = 0;
+            uint32_t fk = 0;
             if (pos < tail) {
                 const uint32_t sl = tl[pos & rmask];
                 if (sl < S) {
                     uint32_t st;
-                    load_slot(tk + sl, key, st);
+                    load_slot(tk + sl, key, st, fk);
                     live = st == pos;
                 }
             }
             int32_t total;
             const int32_t rank = block_scan(live, sh.wtot, total);
-            if (live && (uint64_t)(cnt + rank) < scratch_cap) g_scratch[cnt + rank] = key;
+            if (live && (uint64_t)(cnt + rank) < scratch_cap) {
+                g_scratch[cnt + rank] = key;
+                g_scratch_f[cnt + rank] = fk;
+            }
             cnt += total;
         }
         if ((uint64_t)cnt > scratch_cap) {
@@ -618,7 +669,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         for (int32_t q = tid; q < cnt; q += NT) {
             int ins;
             const uint64_t sl = insert_or_touch(tk, smask, g_scratch[q], ins, a.status);
-            if (sl != ~0ull) tk[sl].stamp = (uint32_t)q;
+            if (sl != ~0ull) {
+                tk[sl].stamp = (uint32_t)q;
+                tk[sl].fkey = g_scratch_f[q];
+            }
             tl[(uint32_t)q & rmask] = (uint32_t)sl;
         }
         __syncthreads();
@@ -674,8 +728,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     int ins;
                     const uint64_t sl = touch_hinted(tk, smask, h, k < r_otab[b], ins, a.status);
                     // routes of one worker that share a block touch it concurrently: the latest stamp wins
-                    if (sl != ~0ull)
+                    if (sl != ~0ull) {
                         __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                        if (freq) freq_touch(&tk[sl].fkey, ins != 0, r_ep[b]);
+                    }
                     tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
                     my_ins += ins;
                 }
@@ -696,17 +752,21 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         if (my_ins) atomicAdd(&sh.ins, my_ins);
     };
 
-    // ---- evict least recently used blocks of worker sg down to the capacity (all threads)
-    auto evict = [&](int32_t sg) {
+    // ---- evict blocks of worker sg down to the capacity (all threads): live log records in log
+    //      (recency) order, under frequency eviction only those at frequency 1 in epoch ep; the
+    //      head moves to the first record left live
+    auto evict = [&](int32_t sg, uint32_t ep) {
         Slot* tk = g_slots + (uint64_t)sg * S;
         uint32_t* tl = g_log + (uint64_t)sg * R;
+        uint32_t head = s_head[sg];
         while (sh.remaining > 0) {
-            const uint32_t head = s_head[sg], tail = s_tail[sg];
+            const uint32_t tail = s_tail[sg];
             const int32_t rem = sh.remaining;
             if (head >= tail) {
                 __syncthreads();
                 if (tid == 0) {
                     atomicOr(a.status, RK_DEV_TABLE_FULL);
+                    s_head[sg] = min(sh.first_kept, tail);
                     sh.remaining = 0;
                 }
                 __syncthreads();
@@ -714,37 +774,40 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             }
             const uint32_t pos = head + (uint32_t)tid;
             uint32_t sl = 0;
-            bool live = false;
+            bool live = false, cand = false;
             uint64_t key = 0;
             if (pos < tail) {
                 sl = tl[pos & rmask];
                 if (sl < S) {
-                    uint32_t st;
-                    load_slot(tk + sl, key, st);
+                    uint32_t st, fk;
+                    load_slot(tk + sl, key, st, fk);
                     live = st == pos;
+                    cand = live && (!freq || fk <= ep + 1u);
                 }
             }
             int32_t total;
-            const int32_t rank = block_scan(live, sh.wtot, total);
-            if (live && rank < rem) {
+            const int32_t rank = block_scan(cand, sh.wtot, total);
+            const bool gone = cand && rank < rem;
+            if (gone) {
                 tk[sl].stamp = kTomb;
                 atomicAdd(&sh.digest, (unsigned long long)mix64(key));
                 if (rank == rem - 1) sh.new_head = pos + 1;
             }
+            if (live && !gone) atomicMin(&sh.first_kept, pos);
             __syncthreads();
             if (tid == 0) {
                 if (total >= rem) {
-                    s_head[sg] = sh.new_head;
+                    s_head[sg] = min(sh.first_kept, sh.new_head);
                     sh.ev += rem;
                     s_live[sg] -= rem;
                     sh.remaining = 0;
                 } else {
-                    s_head[sg] = min(head + (uint32_t)NT, tail);
                     sh.ev += total;
                     s_live[sg] -= total;
                     sh.remaining = rem - total;
                 }
             }
+            head = min(head + (uint32_t)NT, tail);
             __syncthreads();
         }
     };
@@ -904,6 +967,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 // lane j < W keeps worker j's load, log tail and block counts in registers
                 int32_t rA = 0, rlive = 0, rused = 0, rN = 0;
                 uint32_t rtail = 0;
+                int32_t run_ep = -1;   // decay epoch of the routes decided since the last sync
                 if (lane < W) {
                     rA = s_A[lane];
                     rN = s_N[lane];
@@ -970,6 +1034,15 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     }
                     const int32_t b = t - t0;
                     if (b >= nb) break;
+                    if (freq) {
+                        // a new decay epoch waits until the earlier epoch's cache writes are in
+                        const int32_t ep = s / dsteps;
+                        if (run_ep >= 0 && ep != run_ep) {
+                            event = EV_EPOCH;
+                            break;
+                        }
+                        run_ep = ep;
+                    }
                     // one route: controller, cost of every worker, argmin
                     const int32_t slot = s % H, sb = slot * rps;
                     bool active = false;
@@ -1056,6 +1129,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     if (lane == 0) {
                         r_sig[b] = sg;
                         r_stamp[b] = base;
+                        r_ep[b] = freq ? (uint32_t)run_ep : 0u;
                         r_otab[b] = o_tab[b * W + sg];
                         s_stw[sb + r_in_step] = sg;
                         s_stP[sb + r_in_step] = P;
@@ -1160,6 +1234,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             }
             __syncthreads();
             event = sh.event;
+            if (event == EV_EPOCH) {
+                if (tid == 0) sh.stop = 0;
+                __syncthreads();
+                continue;
+            }
             if (event != EV_FLUSH) break;
             // the route's worker (every decided route's writes are in): evict, search the pending
             // requests again
@@ -1175,9 +1254,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 sh.remaining = max(0, s_live[sg] - a.cache);
                 sh.ev = 0;
                 sh.digest = 0ull;
+                sh.first_kept = 0xFFFFFFFFu;
             }
             __syncthreads();
-            evict(sg);
+            evict(sg, r_ep[b]);
             search(b + 1, nb, sg);
             if (tid == 0) {
                 if (a.out.evict_count) a.out.evict_count[sh.ev_row] = sh.ev;

@@ -122,20 +122,21 @@ inline uint64_t next_pow2(uint64_t x)
     return p;
 }
 
-// One cached block of an episode's worker table: the chained hash and the
-// log position of its latest touch (kTomb once evicted).  Both travel in one
-// 16-byte load.
+// One cached block of an episode's worker table: the chained hash, the log
+// position of its latest touch (kTomb once evicted) and, under frequency
+// eviction, the block's frequency key (frequency plus the decay epoch of its
+// last update).  They travel in one 16-byte load.
 struct __align__(16) Slot {
     uint64_t key;
     uint32_t stamp;
-    uint32_t pad;
+    uint32_t fkey;
 };
 
 // Episode workspace layout (bytes), shared by the size query and the launch.
 struct EpisodeLayout {
     uint64_t slots;        // table slots per worker (power of two)
     uint64_t ring;         // LRU log records per worker (power of two)
-    size_t off_slots, off_log, off_scratch, off_queue, off_next;
+    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next;
     size_t per_episode;
 };
 EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv);

@@ -56,7 +56,7 @@ class EpisodeRunner:
             n_routes = int(flat.turn_off[cb + nc]) - tb
             prm[e] = (cb, nc, sp.hold_steps, sp.routes_per_step, sp.controller, sp.ctrl_window,
                       sp.ctrl_num, sp.ctrl_den, sp.cap, sp.w_ov, sp.w_act, sp.w_sat, sp.ctrl_w_ov, out_base,
-                      sp.policy, sp.tau)
+                      sp.policy, sp.tau, sp.evict_policy, sp.decay_steps)
             self.rows.append((out_base, n_routes, cb, tb))
             for k in range(0, n_routes, sp.concurrency):
                 win_off.append(out_base + min(k + sp.concurrency, n_routes))

@@ -20,6 +20,8 @@ LIB_PATH = os.path.join(HERE, "librkroute.so")
 RK_OK, RK_EINVAL, RK_ENOMEM, RK_EHIP, RK_ETABLEFULL, RK_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 RK_PROBE_PREFIX, RK_PROBE_SCAN = 0, 1
 RK_POLICY_ARGMIN, RK_POLICY_SOFTMAX, RK_POLICY_ROUND_ROBIN, RK_POLICY_RANDOM, RK_POLICY_P2C = range(5)
+RK_EVICT_LRU, RK_EVICT_FREQ = 0, 1
+RK_FREQ_CAP = 1 << 20
 DEV_BITS = {0x1: "bad offsets", 0x2: "short input", 0x4: "zero key", 0x8: "table full",
             0x10: "too large", 0x20: "no convergence", 0x40: "bad policy parameters"}
 
@@ -75,8 +77,9 @@ EPISODE_PARAMS_DTYPE = np.dtype([
     ("conv_begin", "<i8"), ("n_conv", "<i4"), ("hold_steps", "<i4"), ("routes_per_step", "<i4"),
     ("controller", "<i4"), ("ctrl_window", "<i4"), ("ctrl_num", "<i4"), ("ctrl_den", "<i4"),
     ("cap_blocks", "<i4"), ("w_ov", "<f4"), ("w_act", "<f4"), ("w_sat", "<f4"),
-    ("ctrl_w_ov", "<f4"), ("out_base", "<i8"), ("policy", "<i4"), ("tau", "<f4")])
-assert EPISODE_PARAMS_DTYPE.itemsize == 72
+    ("ctrl_w_ov", "<f4"), ("out_base", "<i8"), ("policy", "<i4"), ("tau", "<f4"),
+    ("evict_policy", "<i4"), ("decay_steps", "<i4")])
+assert EPISODE_PARAMS_DTYPE.itemsize == 80
 
 _lock = threading.Lock()
 _lib = None
