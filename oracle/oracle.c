@@ -40,7 +40,11 @@
  *    the cache may instead follow the KV block manager's frequency policy
  *    (Section 2.2): evict the least frequent block first, frequencies start
  *    at 1, double on a hit and drop by 1 (not below 1) every decay_steps
- *    routing steps.
+ *    routing steps.  With memory tiers (LRU only), the k1 most recently
+ *    used blocks of a worker form G1, the next k2 G2 and the rest G3
+ *    (Section 4.2): the order an exclusive hierarchy keeps when eviction
+ *    demotes a tier's least recent block and a hit promotes a block to G1.
+ *    The cost then charges the cached prefix per tier (Eq. kv-cost).
  *  - Steps: a step routes up to C/H requests from the ready queue; a request
  *    stays active (its blocks count in A_j) for H steps, so C requests are in
  *    flight once the ramp is over (the semaphore-held concurrency of
@@ -144,6 +148,26 @@ float orc_route_cost(float w_ov, float w_act, float w_sat, int32_t cap,
                      int32_t P, int32_t o, int64_t A)
 {
     float t1 = w_ov * (float)(P - o);
+    float t2 = w_act * (float)A;
+    float r = (float)(A + (int64_t)P) / (float)cap;
+    float x = fmaxf(r - 1.0f, 0.0f);
+    float t3 = w_sat * (x * x);
+    return (t1 + t2) + t3;
+}
+
+/* The same cost when the cached prefix spans memory tiers (Section 4.2,
+ * Eq. kv-cost): of the o cached blocks, o1 lead in G1 and o12 in G1 or G2; a
+ * block served from tier t counts tw[t] of a recomputed block, so the prefill
+ * term is (P - o) + tw0 o1 + tw1 (o12 - o1) + tw2 (o - o12), summed in that
+ * order. */
+float orc_route_cost_tiers(float w_ov, float w_act, float w_sat, int32_t cap, int32_t P, int32_t o,
+                           int32_t o1, int32_t o12, const float* tw, int64_t A)
+{
+    float pf = (float)(P - o);
+    pf = pf + tw[0] * (float)o1;
+    pf = pf + tw[1] * (float)(o12 - o1);
+    pf = pf + tw[2] * (float)(o - o12);
+    float t1 = w_ov * pf;
     float t2 = w_act * (float)A;
     float r = (float)(A + (int64_t)P) / (float)cap;
     float x = fmaxf(r - 1.0f, 0.0f);
@@ -316,6 +340,8 @@ int orc_score_batch(int32_t B, int32_t W, const uint64_t* chains, const int64_t*
 typedef struct {
     uint64_t key;
     int64_t freq;         /* access frequency (frequency eviction only) */
+    int64_t tmark;        /* route whose tier marking is in tier (memory tiers only) */
+    int32_t tier;         /* 1 = G1, 2 = G2 at route tmark */
     int32_t prev, next;   /* recency list */
     int32_t hnext;        /* bucket chain */
 } lru_node;
@@ -391,6 +417,7 @@ static int lru_touch(lru_t* c, uint64_t key, int* err)
     c->free_head = c->node[i].hnext;
     c->node[i].key = key;
     c->node[i].freq = 1;
+    c->node[i].tmark = -1;
     c->node[i].hnext = c->bucket[key & c->mask];
     c->bucket[key & c->mask] = i;
     list_append(c, i);
@@ -432,6 +459,29 @@ static uint64_t lfu_evict(lru_t* c)
     int32_t i = c->oldest;
     while (c->node[i].freq != fmin) i = c->node[i].next;
     return lru_remove(c, i);
+}
+
+/* Memory tiers as consecutive runs of the recency order: the k1 most recently
+ * used entries are in G1, the next k2 in G2, the rest in G3.  Marks them for
+ * route t. */
+static void lru_mark_tiers(lru_t* c, int64_t t, int32_t k1, int32_t k2)
+{
+    int32_t r = 0;
+    for (int32_t i = c->newest; i >= 0 && r < k1 + k2; i = c->node[i].prev, ++r) {
+        c->node[i].tmark = t;
+        c->node[i].tier = r < k1 ? 1 : 2;
+    }
+}
+
+/* Leading blocks of h held in tiers 1..max_tier as marked for route t. */
+static int32_t lru_tier_overlap(const lru_t* c, const uint64_t* h, int32_t P, int64_t t, int32_t max_tier)
+{
+    int32_t o = 0;
+    for (; o < P; ++o) {
+        int32_t i = lru_find(c, h[o]);
+        if (i < 0 || c->node[i].tmark != t || c->node[i].tier > max_tier) break;
+    }
+    return o;
 }
 
 /* One time-decay step: every cached entry's frequency drops by 1, to no less
@@ -519,6 +569,7 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
                          int32_t policy, float tau, const uint32_t* rand,
                          const double* rg_d, const int32_t* rg_i, const float* rg_f, int32_t* route_regime,
                          int32_t evict_policy, int32_t decay_steps,
+                         int32_t tier_g1, int32_t tier_g2, const float* tier_w, int32_t* tier_overlap,
                          int32_t n_conv, const int64_t* turn_off, const int32_t* turn_blocks,
                          const int64_t* chain_off, const uint64_t* chains,
                          int32_t* route_turn, int32_t* route_worker, int32_t* route_step,
@@ -545,6 +596,12 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
     if (policy == ORC_POLICY_SOFTMAX && !(tau > 0.0f)) return ORC_EINVAL;
     if (evict_policy != ORC_EVICT_LRU && evict_policy != ORC_EVICT_FREQ) return ORC_EINVAL;
     if (evict_policy == ORC_EVICT_FREQ && decay_steps < 1) return ORC_EINVAL;
+    const int tiers = tier_g1 > 0;
+    if (tier_g1 < 0 || tier_g2 < 0 || (int64_t)tier_g1 + tier_g2 > cache_blocks) return ORC_EINVAL;
+    if (tiers && (evict_policy != ORC_EVICT_LRU || !tier_w)) return ORC_EINVAL;
+    if (tiers)
+        for (int r = 0; r < 3; ++r)
+            if (!(tier_w[r] >= 0.0f)) return ORC_EINVAL;
     if (!rand && (policy == ORC_POLICY_SOFTMAX || policy == ORC_POLICY_RANDOM || policy == ORC_POLICY_P2C))
         return ORC_EINVAL;
     const int64_t n_routes = turn_off[n_conv];
@@ -637,7 +694,19 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
 
             for (int32_t j = 0; j < W; ++j) {
                 int32_t o = lru_overlap(&lru[j], h, P);
-                float cj = orc_route_cost(w_eff, w_act, w_sat, cap, P, o, A[j]);
+                float cj;
+                if (tiers) {
+                    lru_mark_tiers(&lru[j], t, tier_g1, tier_g2);
+                    int32_t o1 = lru_tier_overlap(&lru[j], h, P, t, 1);
+                    int32_t o12 = lru_tier_overlap(&lru[j], h, P, t, 2);
+                    if (tier_overlap) {
+                        tier_overlap[(t * W + j) * 2] = o1;
+                        tier_overlap[(t * W + j) * 2 + 1] = o12;
+                    }
+                    cj = orc_route_cost_tiers(w_eff, w_act, w_sat, cap, P, o, o1, o12, tier_w, A[j]);
+                } else {
+                    cj = orc_route_cost(w_eff, w_act, w_sat, cap, P, o, A[j]);
+                }
                 o_row[j] = o;
                 overlap[t * W + j] = o;
                 cost[t * W + j] = cj;

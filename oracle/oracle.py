@@ -67,6 +67,7 @@ def lib():
                 i32, f32, p,
                 p, p, p, p,
                 i32, i32,
+                i32, i32, p, p,
                 i32, p, p, p, p,
                 p, p, p, p, p, p, p, p, p, p,
                 p, p, p, i64, p]
@@ -239,7 +240,9 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         route_step=np.zeros(n, np.int32), route_blocks=np.zeros(n, np.int32),
         overlap=np.zeros((n, W), np.int32), cost=np.zeros((n, W), np.float32),
         evict_count=np.zeros(n, np.int32), evict_digest=np.zeros(n, np.uint64),
-        last_hash=np.zeros(n, np.uint64), totals=np.zeros(8, np.int64), route_regime=np.zeros(n, np.int32))
+        last_hash=np.zeros(n, np.uint64), totals=np.zeros(8, np.int64), route_regime=np.zeros(n, np.int32),
+        tier_overlap=np.zeros((n, W, 2), np.int32))
+    tw = np.ascontiguousarray(getattr(spec, "tier_w", (0.0, 0.25, 0.5)), dtype=np.float32)
     policy = int(getattr(spec, "policy", 0))
     tau = float(getattr(spec, "tau", 0.0))
     rd, ri, rf = regime_arrays(regime)
@@ -263,6 +266,7 @@ def simulate_episode(W, cache_blocks, spec, turn_off, turn_blocks, chain_off, ch
         policy, tau, g(rand),
         _ptr(rd), _ptr(ri), _ptr(rf), g(out["route_regime"]),
         int(getattr(spec, "evict_policy", 0)), int(getattr(spec, "decay_steps", 0)),
+        int(getattr(spec, "tier_g1", 0)), int(getattr(spec, "tier_g2", 0)), _ptr(tw), g(out["tier_overlap"]),
         n_conv, _ptr(turn_off), g(turn_blocks), _ptr(chain_off), g(chains),
         g(out["route_turn"]), g(out["route_worker"]), g(out["route_step"]),
         g(out["route_blocks"]), g(out["overlap"]), g(out["cost"]),

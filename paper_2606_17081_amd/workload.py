@@ -228,6 +228,9 @@ class EpisodeSpec:
     tau: float = 0.0          # softmax temperature (> 0 with POLICY_SOFTMAX), in cost units
     evict_policy: int = 0     # EVICT_LRU, or EVICT_FREQ (the KV block manager's frequency policy)
     decay_steps: int = 0      # EVICT_FREQ: routing steps per time-decay step (>= 1)
+    tier_g1: int = 0          # memory tiers (LRU only): blocks in G1 (0 = no tiers) ...
+    tier_g2: int = 0          # ... and in G2; G3 holds the rest of the cache
+    tier_w: tuple = (0.0, 0.25, 0.5)   # prefill weight of a block served from G1, G2, G3
 
     @property
     def routes_per_step(self) -> int:

@@ -25,6 +25,21 @@ def cost_f32(w_ov, w_act, w_sat, cap, P, o, A):
     return f32(f32(t1 + t2) + t3)
 
 
+def cost_tiers_f32(w_ov, w_act, w_sat, cap, P, o, o1, o12, tw, A):
+    """Router cost with the cached prefix split over memory tiers: o1 blocks in
+    G1, o12 - o1 in G2, o - o12 in G3, each weighted by tw in the prefill term."""
+    pf = f32(P - o)
+    pf = f32(pf + f32(tw[0]) * f32(o1))
+    pf = f32(pf + f32(tw[1]) * f32(o12 - o1))
+    pf = f32(pf + f32(tw[2]) * f32(o - o12))
+    t1 = f32(w_ov) * pf
+    t2 = f32(w_act) * f32(A)
+    r = f32(A + P) / f32(cap)
+    x = max(r - f32(1.0), f32(0.0))
+    t3 = f32(w_sat) * (x * x)
+    return f32(f32(t1 + t2) + t3)
+
+
 def overlap_set(chain, cached: set) -> int:
     o = 0
     while o < len(chain) and int(chain[o]) in cached:
@@ -34,14 +49,16 @@ def overlap_set(chain, cached: set) -> int:
 
 def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blocks, chains_per_conv,
             controller=0, ctrl_w_ov=0.25, ctrl_window=128, ctrl_num=9, ctrl_den=10, select=None, regime=None,
-            freq=None):
+            freq=None, tiers=None):
     """Sequential routing episode with OrderedDict LRU caches; select(costs, t)
     picks the worker of route t (default: least cost, lowest index).  With
     controller 2, regime = (params(r) -> (tau, w_ov), step(n, t) -> new
     regime, select_tau(costs, t, tau)) drives the regime controller.  With
     freq = (decay_steps, cap) the caches evict by frequency: a block enters at 1,
     doubles per hit (at most cap), loses 1 per decay step (never below 1), and
-    the least frequent block, oldest among equals, is evicted first."""
+    the least frequent block, oldest among equals, is evicted first.  With
+    tiers = (k1, k2, tw) a worker's k1 most recent blocks are G1 and the next k2
+    G2; routes record (o1, o12) per worker and pay the tiered cost."""
     n_conv = len(turn_off) - 1
     caches = [OrderedDict() for _ in range(W)]   # key -> None, oldest first
     A = [0] * W
@@ -85,7 +102,18 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
                 rtau, rw = regime[0](rg)
                 w_eff = f32(rw)
             ovl = [overlap_set(h, caches[j].keys()) for j in range(W)]
-            costs = [cost_f32(w_eff, w_act, w_sat, cap, P, ovl[j], A[j]) for j in range(W)]
+            if tiers is None:
+                costs = [cost_f32(w_eff, w_act, w_sat, cap, P, ovl[j], A[j]) for j in range(W)]
+                tov = None
+            else:
+                k1, k2, tw = tiers
+                tov = []
+                for j in range(W):
+                    order = list(caches[j].keys())[::-1]          # newest first
+                    g1, g12 = set(order[:k1]), set(order[:k1 + k2])
+                    tov.append((overlap_set(h, g1), overlap_set(h, g12)))
+                costs = [cost_tiers_f32(w_eff, w_act, w_sat, cap, P, ovl[j], tov[j][0], tov[j][1], tw, A[j])
+                         for j in range(W)]
             if controller == 2 and rtau > 0:
                 sigma = int(regime[2](costs, len(routes), rtau))
             elif select is None:
@@ -118,6 +146,7 @@ def episode(W, cache_blocks, H, rps, w_ov, w_act, w_sat, cap, turn_off, turn_blo
                 rg = int(regime[1](nflight[sigma], len(routes)))
             us.append(sum(A))
             routes.append(dict(turn=turn, worker=sigma, step=s, P=P, overlap=ovl, cost=costs, regime=route_regime,
+                               tier_overlap=tov,
                                evicted=evicted, active=bool(active),
                                first_active=bool(active and not prev_active)))
             prev_active = bool(active)
