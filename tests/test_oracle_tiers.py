@@ -14,9 +14,14 @@ def _tiered(spec, k1, k2, tw):
     return wl.EpisodeSpec(**{**spec.__dict__, "tier_g1": k1, "tier_g2": k2, "tier_w": tuple(tw)})
 
 
-def _twin(orc, rng, W, cache, spec, turn_off, turn_blocks, chains):
-    k1 = int(rng.integers(1, cache + 1))
-    k2 = int(rng.integers(0, cache - k1 + 1))
+def _tier_sizes(rng, cache, small=False):
+    k1 = int(rng.integers(1, max(1, cache // 3) + 1))     # small G1, so prefixes straddle tiers
+    k2 = int(rng.integers(1, max(1, cache // 4) + 1)) if small else int(rng.integers(0, cache - k1 + 1))
+    return k1, k2
+
+
+def _twin(orc, rng, W, cache, spec, turn_off, turn_blocks, chains, small=False):
+    k1, k2 = _tier_sizes(rng, cache, small)
     tw = [float(x) for x in rng.choice([0.0, 0.125, 0.3, 0.5, 1.0, 2.0], size=3)]
     spec = _tiered(spec, k1, k2, tw)
     flat, off = _flat_chains(chains)
@@ -108,3 +113,48 @@ def test_rejects_bad_parameters(orc):
         spec = wl.EpisodeSpec(**{**wl.EpisodeSpec(seed=0, concurrency=1, hold_steps=1).__dict__, **kw})
         with pytest.raises(ValueError):
             orc.simulate_episode(1, 4, spec, [0, 1], [1], off, flat)
+
+
+def _straddle_case(rng):
+    # conversations whose turns extend one chain, caches a few prompts deep: cached prefixes
+    # run through all three tiers
+    W, cache = int(rng.integers(1, 4)), int(rng.integers(24, 48))
+    n_conv = int(rng.integers(6, 16))
+    chains, turn_blocks, turn_off, nxt = [], [], [0], 1
+    shared = [list(range(1000 * (g + 1), 1000 * (g + 1) + 12)) for g in range(3)]
+    for _ in range(n_conv):
+        g = int(rng.integers(0, 3))
+        L = int(rng.integers(14, 30))
+        head = shared[g][: int(rng.integers(2, 12))]
+        ch = head + list(range(nxt, nxt + L - len(head)))
+        nxt += L
+        chains.append(ch)
+        tb = sorted(int(x) for x in rng.integers(len(head), L + 1, size=int(rng.integers(1, 4))))
+        turn_blocks.extend(tb)
+        turn_off.append(len(turn_blocks))
+    H, rps = int(rng.integers(1, 4)), int(rng.integers(1, 3))
+    spec = wl.EpisodeSpec(seed=0, concurrency=H * rps, hold_steps=H, w_ov=1.0, w_act=float(rng.choice([0.0, 0.5])),
+                          w_sat=0.0, cap=64)
+    return W, cache, spec, turn_off, turn_blocks, chains
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_matches_bruteforce_twin_straddling(orc, seed):
+    rng = np.random.default_rng(17000 + seed)
+    W, cache, spec, turn_off, turn_blocks, chains = _straddle_case(rng)
+    _twin(orc, rng, W, cache, spec, turn_off, turn_blocks, chains, small=True)
+
+
+def test_straddling_cases_cover_every_tier(orc):
+    # the straddling twin cases do put cached prefixes across G1, G2 and G3
+    n3 = 0
+    for seed in range(16):
+        rng = np.random.default_rng(17000 + seed)
+        W, cache, spec, turn_off, turn_blocks, chains = _straddle_case(rng)
+        k1, k2 = _tier_sizes(rng, cache, small=True)
+        tw = [float(x) for x in rng.choice([0.0, 0.125, 0.3, 0.5, 1.0, 2.0], size=3)]
+        flat, off = _flat_chains(chains)
+        out = orc.simulate_episode(W, cache, _tiered(spec, k1, k2, tw), turn_off, turn_blocks, off, flat)
+        t, o = out["tier_overlap"], out["overlap"]
+        n3 += int(((0 < t[..., 0]) & (t[..., 0] < t[..., 1]) & (t[..., 1] < o)).sum())
+    assert n3 >= 15
