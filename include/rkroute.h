@@ -260,6 +260,16 @@ int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains, const int
  *                      step s > 0 with s a multiple of decay_steps); the least
  *                      frequent block goes first, the least recently used
  *                      among equals.
+ *   - memory tiers (tier_g1 > 0, Section 4.2 and Eq. kv-cost): a worker's
+ *     tier_g1 most recently used blocks are in G1, the next tier_g2 in G2 and
+ *     the rest in G3 (the order of an exclusive hierarchy that demotes a
+ *     tier's least recent block and promotes a hit block to G1).  With o1 and
+ *     o12 the leading blocks of the prompt held in G1 and in G1 or G2, the
+ *     cost's prefill term becomes, in fp32 and this order,
+ *       ((((float)(P - o) + tier_w[0] * o1) + tier_w[1] * (o12 - o1))
+ *        + tier_w[2] * (o - o12));
+ *     every route then stops the batch (as in RK_PROBE_SCAN) so that later
+ *     requests see the new tier boundaries.
  * The queue order, the touch order and the tie rule make every result unique.
  */
 typedef struct {
@@ -279,7 +289,13 @@ typedef struct {
     float   tau;             /* softmax temperature, > 0 with RK_POLICY_SOFTMAX        */
     int32_t evict_policy;    /* RK_EVICT_*                                             */
     int32_t decay_steps;     /* routing steps per time-decay step, >= 1 with RK_EVICT_FREQ */
-} rk_episode_params;         /* 80 bytes; invalid policy or eviction fields set
+    int32_t tier_g1;         /* memory tiers: blocks in G1 (0 = no tiers), needs
+                                RK_EVICT_LRU and a batch with tiers != 0            */
+    int32_t tier_g2;         /* blocks in G2, >= 0, tier_g1 + tier_g2 <= cache_blocks;
+                                G3 holds the rest of the cache                      */
+    float   tier_w[3];       /* prefill weight of a cached block in G1, G2, G3, >= 0 */
+    int32_t tier_pad;        /* 0                                                    */
+} rk_episode_params;         /* 104 bytes; invalid policy, eviction or tier fields set
                                 RK_DEV_BAD_PARAMS and leave the episode's outputs
                                 unwritten                                             */
 
@@ -320,7 +336,8 @@ typedef struct {
                                         block is touched and evicted after its children):
                                         the first miss is found by a 64-way search;
                                         RK_PROBE_SCAN: scan from block 0 in 64-block steps */
-    int32_t reserved;                /* 0                                               */
+    int32_t tiers;                   /* nonzero when some episode has tier_g1 > 0: the
+                                        launch then keeps tier overlaps in LDS          */
     const rk_episode_params* params; /* [E], device                                     */
     const int64_t* turn_off;         /* turns of conversation c: turn_off[c] .. turn_off[c+1]-1 */
     const int32_t* turn_blocks;      /* prompt blocks P of each turn; a turn's prompt is the
@@ -352,6 +369,8 @@ typedef struct {
                                  Below and regime moves up                           */
     int32_t* route_regime;    /* [rows]   regime the route was made in (0 without the
                                  regime controller)                                  */
+    int32_t* tier_overlap;    /* [rows*W*2] (o1, o12) per worker with memory tiers (not
+                                 written without them)                               */
 } rk_episode_outputs;
 
 /* Workspace bytes needed by rk_simulate_episodes for this batch shape. */

@@ -45,6 +45,17 @@
 // at frequency 1: the route's own new blocks are such blocks, so there are
 // always enough.  Eviction walks the log from its head and skips the more
 // frequent records, which keep the head from moving past them.
+//
+// Memory tiers (LRU): G1 is the tier_g1 newest live records of a worker's log
+// and G1 u G2 the tier_g1 + tier_g2 newest, so each is the run of the log
+// from a boundary position to the tail, and a block is in G1 iff its stamp is
+// at least G1's boundary.  A route moves the boundaries of its worker: its P
+// touches add P records to each run and remove the hits whose old records lay
+// in it (the writers count those from the stamps atomicMax returns); the
+// boundary then walks forward over surplus live records.  Along a cached
+// prefix the stamps fall, so the tier overlaps o1 and o12 are found by binary
+// search on stamps.  Every route stops the batch so that later requests are
+// searched against the new boundaries.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -59,7 +70,7 @@ constexpr int32_t kMoreTurns = 0x40000000;   // flag on an in-flight conversatio
 enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2, EV_EPOCH = 3 };
 
 struct EpArgs {
-    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB;
+    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB, tiers;
     const rk_episode_params* params;
     const int64_t* turn_off;
     const int32_t* turn_blocks;
@@ -77,9 +88,9 @@ struct EpArgs {
 constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 
 struct EpShared {
-    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone;
+    int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
     int32_t woff[NW][KR + 1];
-    uint32_t new_head, first_kept;
+    uint32_t new_head, first_kept, adv;
     int64_t ev_row, ev_total;
     unsigned long long digest, rb_mask;
     int32_t wtot[NW];
@@ -166,6 +177,33 @@ __device__ __forceinline__ bool finish_lookup(const Slot* t, uint64_t smask, uin
         load_slot(t + s, kk, ss);
         if (kk == kEmpty) return false;
         if (kk == h && ss != kTomb) return true;
+        s = (s + 1) & smask;
+    }
+    return false;
+}
+
+// finish_lookup that also returns the live slot's stamp.
+__device__ __forceinline__ bool finish_lookup_stamp(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
+                                                    const uint64_t* k, const uint32_t* st, uint32_t& stamp)
+{
+#pragma unroll
+    for (int i = 0; i < kWin; ++i) {
+        if (k[i] == kEmpty) return false;
+        if (k[i] == h && st[i] != kTomb) {
+            stamp = st[i];
+            return true;
+        }
+    }
+    s = (s + kWin) & smask;
+    for (uint64_t n = kWin; n <= smask; ++n) {
+        uint64_t kk;
+        uint32_t ss;
+        load_slot(t + s, kk, ss);
+        if (kk == kEmpty) return false;
+        if (kk == h && ss != kTomb) {
+            stamp = ss;
+            return true;
+        }
         s = (s + 1) & smask;
     }
     return false;
@@ -468,12 +506,85 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
     }
 }
 
+// First position k < hi of each item's chain whose block is not held at a
+// stamp >= bound (not in the tier run that starts at log position bound), for
+// items i = threadIdx.x, + NT, ... < n; info names the chain, hi, the worker
+// table and the bound.  Binary search when the tier's blocks form a prefix of
+// the chain (prefix-closed caches: stamps fall along a cached prefix), else a
+// scan from block 0.
+template <class Info, class Put>
+__device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Info& info, const Put& put,
+                                              const Slot* slots, uint64_t S)
+{
+    const uint64_t smask = S - 1;
+    for (int32_t base = 0; base < n; base += NT * KI) {
+        int32_t lo[KI], hi[KI];
+        const uint64_t* ch[KI];
+        const Slot* tb[KI];
+        uint32_t bound[KI];
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            lo[u] = 0;
+            hi[u] = 0;
+            ch[u] = nullptr;
+            tb[u] = slots;
+            bound[u] = 0;
+            if (i < n) {
+                int32_t j;
+                info(i, ch[u], hi[u], j, bound[u]);
+                tb[u] = slots + (uint64_t)j * S;
+            }
+        }
+        for (;;) {
+            bool any = false;
+            int32_t mid[KI];
+            uint64_t hk[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                mid[u] = bsearch ? (lo[u] + hi[u]) >> 1 : lo[u];
+                hk[u] = 0ull;
+                if (lo[u] < hi[u]) {
+                    hk[u] = ch[u][mid[u]];
+                    any = true;
+                }
+            }
+            if (!any) break;
+            uint64_t kw[KI][kWin];
+            uint32_t sw[KI][kWin];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                if (lo[u] < hi[u]) {
+                    const uint64_t s0 = home_slot(hk[u], smask);
+#pragma unroll
+                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + ((s0 + x) & smask), kw[u][x], sw[u][x]);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                if (lo[u] < hi[u]) {
+                    uint32_t st = 0;
+                    const bool in = finish_lookup_stamp(tb[u], smask, hk[u], home_slot(hk[u], smask), kw[u], sw[u], st) &&
+                                    st >= bound[u];
+                    if (in) lo[u] = mid[u] + 1;
+                    else hi[u] = mid[u];
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            if (i < n) put(i, lo[u]);
+        }
+    }
+}
+
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
-    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rrnd, lcp, bytes;
+    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rrnd, lcp, t1, t12, bytes;
 };
 
-__host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
+__host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool tiers)
 {
     BatchLayout b;
     uint32_t o = 0;
@@ -498,6 +609,8 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W)
     b.rep = take(nb * 4, 4);
     b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
+    b.t1 = take(tiers ? nb * w * 2 : 0, 4);
+    b.t12 = take(tiers ? nb * w * 2 : 0, 4);
     b.bytes = (o + 15) / 16 * 16;
     return b;
 }
@@ -519,6 +632,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     int32_t* s_live = (int32_t*)(s_tail + W);
     int32_t* s_used = s_live + W;
     int32_t* s_N = s_used + W;                              // requests in flight per worker
+    uint32_t* s_b1 = (uint32_t*)(s_N + W);                  // memory tiers: G1's boundary in the log,
+    uint32_t* s_b2 = s_b1 + W;                              //   G1 u G2's boundary,
+    int32_t* s_n1 = (int32_t*)(s_b2 + W);                   //   live records from each boundary on
+    int32_t* s_n2 = s_n1 + W;
     // in-flight routes of the last H steps, by step slot
     int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // worker
     int32_t* s_stP = s_stw + a.max_inflight;               // prompt blocks
@@ -526,7 +643,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     int32_t* s_stepn = s_stc + a.max_inflight;             // routes per step slot
     int64_t* s_u = (int64_t*)(smem + a.lds_u);             // controller load samples
     // the batch
-    const BatchLayout BL = batch_layout(NB, W);
+    const BatchLayout BL = batch_layout(NB, W, a.tiers != 0);
     unsigned char* bb = smem + a.lds_batch;
     int64_t* r_cb = (int64_t*)(bb + BL.rcb);               // chain base
     uint64_t* r_last = (uint64_t*)(bb + BL.rlast);         // h_{P-1}
@@ -542,6 +659,8 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     uint32_t* r_ep = (uint32_t*)(bb + BL.rep);             // decay epoch (frequency eviction)
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
+    uint16_t* t1_tab = (uint16_t*)(bb + BL.t1);            // [b][j] leading blocks in G1 (tiers)
+    uint16_t* t12_tab = (uint16_t*)(bb + BL.t12);          // [b][j] leading blocks in G1 u G2 (tiers)
 
     const int32_t H = prm.hold_steps, rps = prm.routes_per_step, n_conv = prm.n_conv;
     const bool bad = H < 1 || rps < 1 || rps > a.max_rps || (int64_t)H * rps > a.max_inflight ||
@@ -569,7 +688,12 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                                                     policy == RK_POLICY_P2C));
     const bool freq = prm.evict_policy == RK_EVICT_FREQ;
     const int32_t dsteps = prm.decay_steps;
-    if (prm.controller < 0 || prm.controller > 2 || !rg_ok ||
+    const bool tiers = prm.tier_g1 > 0;
+    const int32_t K1 = prm.tier_g1, K12 = prm.tier_g1 + prm.tier_g2;
+    const bool tiers_ok = prm.tier_g1 >= 0 && prm.tier_g2 >= 0 && (int64_t)prm.tier_g1 + prm.tier_g2 <= a.cache &&
+                          (!tiers || (a.tiers != 0 && !freq && prm.tier_w[0] >= 0.0f && prm.tier_w[1] >= 0.0f &&
+                                      prm.tier_w[2] >= 0.0f));
+    if (prm.controller < 0 || prm.controller > 2 || !rg_ok || !tiers_ok ||
         (prm.evict_policy != RK_EVICT_LRU && !freq) || (freq && dsteps < 1) ||
         (!regime_ctl && (policy < RK_POLICY_ARGMIN || policy > RK_POLICY_P2C ||
                          (policy == RK_POLICY_SOFTMAX && !(tau > 0.0f)))) ||
@@ -599,6 +723,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     if (tid < W) {
         s_A[tid] = 0;
         s_N[tid] = 0;
+        s_b1[tid] = 0;
+        s_b2[tid] = 0;
+        s_n1[tid] = 0;
+        s_n2[tid] = 0;
         s_head[tid] = 0;
         s_tail[tid] = 0;
         s_live[tid] = 0;
@@ -622,6 +750,8 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         sh.qhead = 0;
         sh.qsize = qn;
         sh.ins = 0;
+        sh.h1 = 0;
+        sh.h2 = 0;
         sh.ev_total = 0;
         sh.tdone = 0;
     }
@@ -681,6 +811,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             s_tail[j] = (uint32_t)cnt;
             s_live[j] = cnt;
             s_used[j] = cnt;
+            // the live records keep their order: a tier's run is now the last n of them
+            s_n1[j] = min(s_n1[j], cnt);
+            s_n2[j] = min(s_n2[j], cnt);
+            s_b1[j] = (uint32_t)(cnt - s_n1[j]);
+            s_b2[j] = (uint32_t)(cnt - s_n2[j]);
         }
         __syncthreads();
     };
@@ -692,7 +827,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     //      synchronizes.
     auto writer = [&]() {
         int32_t* woff = sh.woff[wave];
-        int my_ins = 0;
+        int my_ins = 0, my_h1 = 0, my_h2 = 0;
         for (;;) {
             const int32_t c = __builtin_amdgcn_readfirstlane(
                 __hip_atomic_load(&sh.claimed, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
@@ -729,8 +864,13 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     const uint64_t sl = touch_hinted(tk, smask, h, k < r_otab[b], ins, a.status);
                     // routes of one worker that share a block touch it concurrently: the latest stamp wins
                     if (sl != ~0ull) {
-                        __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                        const uint32_t old = __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED,
+                                                                    __HIP_MEMORY_SCOPE_WORKGROUP);
                         if (freq) freq_touch(&tk[sl].fkey, ins != 0, r_ep[b]);
+                        if (tiers && !ins) {       // a hit whose old record lay in a tier's run
+                            my_h1 += old >= s_b1[sg];
+                            my_h2 += old >= s_b2[sg];
+                        }
                     }
                     tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
                     my_ins += ins;
@@ -750,6 +890,54 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             __builtin_amdgcn_s_sleep(2);
         }
         if (my_ins) atomicAdd(&sh.ins, my_ins);
+        if (my_h1) atomicAdd(&sh.h1, my_h1);
+        if (my_h2) atomicAdd(&sh.h2, my_h2);
+    };
+
+    // ---- memory tiers: move worker j's boundary bk forward until the run from it holds at most K
+    //      live records (all threads)
+    auto advance = [&](uint32_t* bk, int32_t* nk, int32_t K, int32_t j) {
+        const Slot* tk = g_slots + (uint64_t)j * S;
+        const uint32_t* tl = g_log + (uint64_t)j * R;
+        uint32_t b = bk[j];
+        int32_t n = nk[j];
+        const uint32_t tail = s_tail[j];
+        while (n > K) {
+            if (b >= tail) {
+                if (tid == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
+                n = K;
+                break;
+            }
+            const uint32_t pos = b + (uint32_t)tid;
+            bool live = false;
+            if (pos < tail) {
+                const uint32_t sl = tl[pos & rmask];
+                if (sl < S) {
+                    uint64_t key;
+                    uint32_t st;
+                    load_slot(tk + sl, key, st);
+                    live = st == pos;
+                }
+            }
+            int32_t total;
+            const int32_t rank = block_scan(live, sh.wtot, total);
+            const int32_t need = n - K;
+            if (total >= need) {
+                if (live && rank == need - 1) sh.adv = pos + 1;
+                __syncthreads();
+                b = sh.adv;
+                n = K;
+            } else {
+                n -= total;
+                b = min(b + (uint32_t)NT, tail);
+            }
+        }
+        __syncthreads();
+        if (tid == 0) {
+            bk[j] = b;
+            nk[j] = n;
+        }
+        __syncthreads();
     };
 
     // ---- evict blocks of worker sg down to the capacity (all threads): live log records in log
@@ -854,6 +1042,43 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         __syncthreads();
     };
 
+    // tier overlaps of batch routes b in [b_lo, nb) on worker j (j < 0: every worker): o12 within
+    // the cached prefix o_tab, then o1 within o12
+    auto tier_search = [&](int32_t b_lo, int32_t nb, int32_t j) {
+        const int32_t per = j < 0 ? W : 1;
+        const int32_t n = (nb - b_lo) * per;
+        tier_searches(
+            n, !scan,
+            [&](int32_t i, const uint64_t*& ch, int32_t& hi, int32_t& jj, uint32_t& bound) {
+                const int32_t b = b_lo + i / per;
+                jj = j < 0 ? i % per : j;
+                ch = a.chains + r_cb[b];
+                hi = o_tab[b * W + jj];
+                bound = s_b2[jj];
+            },
+            [&](int32_t i, int32_t v) {
+                const int32_t b = b_lo + i / per;
+                t12_tab[b * W + (j < 0 ? i % per : j)] = (uint16_t)v;
+            },
+            g_slots, S);
+        __syncthreads();
+        tier_searches(
+            n, !scan,
+            [&](int32_t i, const uint64_t*& ch, int32_t& hi, int32_t& jj, uint32_t& bound) {
+                const int32_t b = b_lo + i / per;
+                jj = j < 0 ? i % per : j;
+                ch = a.chains + r_cb[b];
+                hi = t12_tab[b * W + jj];
+                bound = s_b1[jj];
+            },
+            [&](int32_t i, int32_t v) {
+                const int32_t b = b_lo + i / per;
+                t1_tab[b * W + (j < 0 ? i % per : j)] = (uint16_t)v;
+            },
+            g_slots, S);
+        __syncthreads();
+    };
+
     // state of the routing sequence, kept by wavefront 0
     int32_t t = 0, s = 0, r_in_step = 0, n_step = 0;
     bool step_open = false, prev_active = false;
@@ -932,6 +1157,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         nb = sh.nb;
         // every (request, worker) overlap against the caches as they stand
         search(0, nb, -1);
+        if (tiers) tier_search(0, nb, -1);
         // common prefix of every pair of the batch's chains (prefix mode)
         if (!scan) {
             const int32_t npair = nb * (nb - 1) / 2;
@@ -1071,7 +1297,17 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     float cj = 0.0f;
                     if (lane < W) {
                         oj = o_cur[b * W + lane];
-                        cj = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
+                        if (tiers) {
+                            const int32_t o1 = t1_tab[b * W + lane], o12 = t12_tab[b * W + lane];
+                            cj = route_cost_tiers(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, o1, o12,
+                                                  prm.tier_w, rA);
+                            if (a.out.tier_overlap) {
+                                a.out.tier_overlap[(row * W + lane) * 2] = o1;
+                                a.out.tier_overlap[(row * W + lane) * 2 + 1] = o12;
+                            }
+                        } else {
+                            cj = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
+                        }
                         if (a.out.overlap) a.out.overlap[row * W + lane] = oj;
                         if (a.out.cost) a.out.cost[row * W + lane] = cj;
                         bits = __float_as_uint(__fadd_rn(cj, 0.0f));
@@ -1115,7 +1351,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     const int32_t osg = __builtin_amdgcn_readlane(oj, sg);
                     const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + (scan ? 0 : P - osg);
                     const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
-                    const bool flush = scan || live_after > a.cache;
+                    const bool flush = scan || tiers || live_after > a.cache;
                     const int32_t rc = r_c[b];
                     if (lane == sg) {
                         rA += P;
@@ -1257,8 +1493,32 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 sh.first_kept = 0xFFFFFFFFu;
             }
             __syncthreads();
+            if (tiers) {
+                // the route's P records joined both tier runs; its hits left them where their old
+                // records lay inside
+                if (tid == 0) {
+                    s_n1[sg] += r_P[b] - sh.h1;
+                    s_n2[sg] += r_P[b] - sh.h2;
+                    sh.h1 = 0;
+                    sh.h2 = 0;
+                }
+                __syncthreads();
+                advance(s_b1, s_n1, K1, sg);
+                advance(s_b2, s_n2, K12, sg);
+            }
             evict(sg, r_ep[b]);
+            if (tiers) {
+                // evictions take the oldest records: a run keeps at most the live count
+                if (tid == 0) {
+                    s_n1[sg] = min(s_n1[sg], s_live[sg]);
+                    s_n2[sg] = min(s_n2[sg], s_live[sg]);
+                    s_b1[sg] = max(s_b1[sg], s_head[sg]);
+                    s_b2[sg] = max(s_b2[sg], s_head[sg]);
+                }
+                __syncthreads();
+            }
             search(b + 1, nb, sg);
+            if (tiers) tier_search(b + 1, nb, sg);
             if (tid == 0) {
                 if (a.out.evict_count) a.out.evict_count[sh.ev_row] = sh.ev;
                 if (a.out.evict_digest) a.out.evict_digest[sh.ev_row] = sh.digest;
@@ -1332,6 +1592,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.max_rps = b->max_routes_per_step;
     a.max_ctrl_window = b->max_ctrl_window;
     a.probe_mode = b->probe_mode;
+    a.tiers = b->tiers;
     a.params = b->params;
     a.turn_off = b->turn_off;
     a.turn_blocks = b->turn_blocks;
@@ -1347,7 +1608,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     // batch that fits in 60 KiB (two episodes can then share a CU)
     size_t o = 0;
     a.lds_w = 0;
-    o = align_up(o + (size_t)b->W * 6 * 4, 16);
+    o = align_up(o + (size_t)b->W * 10 * 4, 16);
     a.lds_inflight = (uint32_t)o;
     o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
     a.lds_u = (uint32_t)o;
@@ -1355,12 +1616,13 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.lds_batch = (uint32_t)o;
     const size_t limit = 60 * 1024;
     int32_t NB = kMaxBatch;
-    while (NB > 1 && o + batch_layout(NB, b->W).bytes > limit) NB /= 2;
-    if (o + batch_layout(NB, b->W).bytes > limit)
+    const bool tiers = b->tiers != 0;
+    while (NB > 1 && o + batch_layout(NB, b->W, tiers).bytes > limit) NB /= 2;
+    if (o + batch_layout(NB, b->W, tiers).bytes > limit)
         return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 60 KiB",
-                    o + (size_t)batch_layout(NB, b->W).bytes);
+                    o + (size_t)batch_layout(NB, b->W, tiers).bytes);
     a.NB = NB;
-    const size_t lds = o + batch_layout(NB, b->W).bytes;
+    const size_t lds = o + batch_layout(NB, b->W, tiers).bytes;
     hipStream_t s = (hipStream_t)stream;
     hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), lds, s, a);
     return hip_check(hipGetLastError(), "rk_simulate_episodes launch");

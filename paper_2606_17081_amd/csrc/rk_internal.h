@@ -57,6 +57,25 @@ __device__ __forceinline__ float route_cost(float w_ov, float w_act, float w_sat
     return __fadd_rn(__fadd_rn(t1, t2), t3);
 }
 
+// The cost when the cached prefix spans memory tiers (Section 4.2, Eq.
+// kv-cost): o1 leading blocks in G1, o12 in G1 or G2, the rest of the o cached
+// ones in G3; a block served from a tier counts tw of a recomputed block in the
+// prefill term, summed in tier order.
+__device__ __forceinline__ float route_cost_tiers(float w_ov, float w_act, float w_sat, int32_t cap, int32_t P,
+                                                  int32_t o, int32_t o1, int32_t o12, const float* tw, int32_t A)
+{
+    float pf = (float)(P - o);
+    pf = __fadd_rn(pf, __fmul_rn(tw[0], (float)o1));
+    pf = __fadd_rn(pf, __fmul_rn(tw[1], (float)(o12 - o1)));
+    pf = __fadd_rn(pf, __fmul_rn(tw[2], (float)(o - o12)));
+    float t1 = __fmul_rn(w_ov, pf);
+    float t2 = __fmul_rn(w_act, (float)A);
+    float r = __fdiv_rn((float)((int64_t)A + (int64_t)P), (float)cap);
+    float x = fmaxf(__fsub_rn(r, 1.0f), 0.0f);
+    float t3 = __fmul_rn(w_sat, __fmul_rn(x, x));
+    return __fadd_rn(__fadd_rn(t1, t2), t3);
+}
+
 // exp(x) for x <= 0 in float, Cody and Waite's method: x = n ln2 + r with
 // n = floor(x log2(e) + 1/2) and ln2 split into a part exact in float and a
 // correction, |r| <= ln2/2; exp(r) by its Taylor series to degree 7 (Horner);

@@ -56,7 +56,8 @@ class EpisodeRunner:
             n_routes = int(flat.turn_off[cb + nc]) - tb
             prm[e] = (cb, nc, sp.hold_steps, sp.routes_per_step, sp.controller, sp.ctrl_window,
                       sp.ctrl_num, sp.ctrl_den, sp.cap, sp.w_ov, sp.w_act, sp.w_sat, sp.ctrl_w_ov, out_base,
-                      sp.policy, sp.tau, sp.evict_policy, sp.decay_steps)
+                      sp.policy, sp.tau, sp.evict_policy, sp.decay_steps, sp.tier_g1, sp.tier_g2,
+                      tuple(float(x) for x in sp.tier_w), 0)
             self.rows.append((out_base, n_routes, cb, tb))
             for k in range(0, n_routes, sp.concurrency):
                 win_off.append(out_base + min(k + sp.concurrency, n_routes))
@@ -94,6 +95,8 @@ class EpisodeRunner:
         self.last_hash = z(R, torch.int64)        # uint64 bits
         self.totals = z((max(E, 1), 8), torch.int64)
         self.route_regime = z(R, torch.int32)
+        self.tiers = any(sp.tier_g1 > 0 for sp in self.episodes)
+        self.tier_overlap = z((R, W, 2), torch.int32) if self.tiers else None
         ws = rk.simulate_workspace_size(E, W, self.cache_blocks, self.max_blocks, self.max_conv)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
 
@@ -111,13 +114,14 @@ class EpisodeRunner:
 
         P = rk._ptr
         self.batch = rk.EpisodeBatch(E, W, self.cache_blocks, self.max_blocks, self.max_conv,
-                                     self.max_inflight, self.max_rps, self.max_ctrl_window, probe_mode, 0,
+                                     self.max_inflight, self.max_rps, self.max_ctrl_window, probe_mode,
+                                     int(self.tiers),
                                      P(self.params), P(self.turn_off), P(self.turn_blocks), P(self.chain_off),
                                      P(self.chains), P(self.route_rand), rk.regime_params(self.regime))
         self.outputs = rk.EpisodeOutputs(P(self.route_turn), P(self.route_worker), P(self.route_step),
                                          P(self.route_blocks), P(self.overlap), P(self.cost),
                                          P(self.evict_count), P(self.evict_digest), P(self.last_hash),
-                                         P(self.totals), P(self.route_regime))
+                                         P(self.totals), P(self.route_regime), P(self.tier_overlap))
 
     # ---- the three stages of one step
     def hash(self, stream=None):
@@ -156,6 +160,8 @@ class EpisodeRunner:
         )
         if self.cost is not None:
             out["cost"] = cpu(self.cost[r0:r0 + n]).reshape(n, W)
+        if self.tier_overlap is not None:
+            out["tier_overlap"] = cpu(self.tier_overlap[r0:r0 + n]).reshape(n, W, 2)
         w0, w1 = int(self.ep_win_off[e]), int(self.ep_win_off[e + 1])
         out["selfish"] = cpu(self.selfish[w0:w1])
         out["coordinated"] = cpu(self.coord[w0:w1])

@@ -60,7 +60,7 @@ class EpisodeBatch(C.Structure):
     _fields_ = [("E", C.c_int32), ("W", C.c_int32), ("cache_blocks", C.c_int32),
                 ("max_blocks", C.c_int32), ("max_conv", C.c_int32), ("max_inflight", C.c_int32),
                 ("max_routes_per_step", C.c_int32), ("max_ctrl_window", C.c_int32),
-                ("probe_mode", C.c_int32), ("reserved", C.c_int32),
+                ("probe_mode", C.c_int32), ("tiers", C.c_int32),
                 ("params", C.c_void_p), ("turn_off", C.c_void_p), ("turn_blocks", C.c_void_p),
                 ("chain_off", C.c_void_p), ("chains", C.c_void_p), ("route_rand", C.c_void_p),
                 ("regime", RegimeParams)]
@@ -69,17 +69,18 @@ class EpisodeBatch(C.Structure):
 class EpisodeOutputs(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("route_turn", "route_worker", "route_step", "route_blocks",
                                           "overlap", "cost", "evict_count", "evict_digest",
-                                          "last_hash", "totals", "route_regime")]
+                                          "last_hash", "totals", "route_regime", "tier_overlap")]
 
 
-# rk_episode_params, 64 bytes, as a numpy record
+# rk_episode_params, 104 bytes, as a numpy record
 EPISODE_PARAMS_DTYPE = np.dtype([
     ("conv_begin", "<i8"), ("n_conv", "<i4"), ("hold_steps", "<i4"), ("routes_per_step", "<i4"),
     ("controller", "<i4"), ("ctrl_window", "<i4"), ("ctrl_num", "<i4"), ("ctrl_den", "<i4"),
     ("cap_blocks", "<i4"), ("w_ov", "<f4"), ("w_act", "<f4"), ("w_sat", "<f4"),
     ("ctrl_w_ov", "<f4"), ("out_base", "<i8"), ("policy", "<i4"), ("tau", "<f4"),
-    ("evict_policy", "<i4"), ("decay_steps", "<i4")])
-assert EPISODE_PARAMS_DTYPE.itemsize == 80
+    ("evict_policy", "<i4"), ("decay_steps", "<i4"), ("tier_g1", "<i4"), ("tier_g2", "<i4"),
+    ("tier_w", "<f4", (3,)), ("tier_pad", "<i4")])
+assert EPISODE_PARAMS_DTYPE.itemsize == 104
 
 _lock = threading.Lock()
 _lib = None
