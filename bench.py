@@ -298,6 +298,57 @@ def policy_bench(torch, rk, wl, stream, steps):
             "episodes_per_s": E / (ts.mean_ms() * 1e-3), "poa_hat_by_policy_and_C": out}
 
 
+def cache_bench(torch, rk, wl, stream, steps, seeds=16):
+    """The long-context multi-turn traces (32 workers, 512 conversations,
+    16,384-block caches, C = 256) under LRU, frequency eviction (decay every 4
+    and 64 steps) and LRU with memory tiers (G1 = G2 = 4,096 blocks, G3 the
+    other 8,192; weights 0, 0.25, 0.5): PoA-hat, recomputed prefill blocks,
+    evictions and, with tiers, where the reused blocks came from."""
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    log(f"generating {seeds} multi-turn traces")
+    base = wl.multiturn_workload(seeds=range(seeds))
+    variants = [("lru", {}), ("frequency, decay every 4 steps", dict(evict_policy=wl.EVICT_FREQ, decay_steps=4)),
+                ("frequency, decay every 64 steps", dict(evict_policy=wl.EVICT_FREQ, decay_steps=64)),
+                ("lru, tiers G1/G2/G3 = 4096/4096/8192", dict(tier_g1=4096, tier_g2=4096))]
+    out = {}
+    for name, kw in variants:
+        eps = [wl.EpisodeSpec(**{**sp.__dict__, **kw}) for sp in base.episodes]
+        w = wl.Workload(base.name, W=base.W, cache_blocks=base.cache_blocks, traces=base.traces, episodes=eps)
+        r = EpisodeRunner(w, keep_cost=False)
+        r.hash()
+        r.simulate()
+        r.poa()
+        torch.cuda.synchronize()
+        ts = KernelTimer(torch, stream)
+        for _ in range(max(1, steps // 4)):
+            with ts:
+                r.simulate()
+        r.poa()
+        torch.cuda.synchronize()
+        assert rk.device_status(reset=True) == 0
+        E = len(eps)
+        tot = r.totals[:E].cpu().numpy()
+        poa = r.poa_hat[:E].cpu().numpy()
+        res = {"episodes": E, "simulate_ms": round(ts.mean_ms(), 3), "episodes_per_s": round(E / (ts.mean_ms() * 1e-3), 1),
+               "routes_per_s": float(r.n_rows / (ts.mean_ms() * 1e-3)),
+               "poa_hat": [round(float(poa.mean()), 6), round(float(poa.std()), 6)],
+               "recomputed_blocks_per_episode": round(float(tot[:, 0].mean()), 1),
+               "reused_blocks_per_episode": round(float(tot[:, 6].mean()), 1),
+               "evicted_blocks_per_episode": round(float(tot[:, 1].mean()), 1)}
+        if r.tier_overlap is not None:
+            n = r.n_rows
+            sig = r.route_worker[:n].long()
+            rows = torch.arange(n, device=sig.device)
+            t = r.tier_overlap[:n][rows, sig].long().cpu().numpy()
+            o = r.overlap[:n][rows, sig].long().cpu().numpy()
+            g1, g2, g3 = t[:, 0].sum(), (t[:, 1] - t[:, 0]).sum(), (o - t[:, 1]).sum()
+            res["reused_blocks_share_G1_G2_G3"] = [round(float(x / max(o.sum(), 1)), 4) for x in (g1, g2, g3)]
+        log(f"cache policies: {name}: {res}")
+        out[name] = res
+    return {"workload": f"long-context multi-turn traces, W=32, 512 conversations, 16384-block caches, C=256, "
+                        f"{seeds} seeds per variant", "variants": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -307,14 +358,15 @@ def main():
     ap.add_argument("--no-scoring", action="store_true")
     ap.add_argument("--cpu-seeds", type=int, default=64)
     ap.add_argument("--no-policies", action="store_true")
-    ap.add_argument("--only", choices=("all", "sweep", "scoring", "policies"), default="all",
+    ap.add_argument("--no-cache-policies", action="store_true")
+    ap.add_argument("--only", choices=("all", "sweep", "scoring", "policies", "cache"), default="all",
                     help="profiling passes: run only the sweep step or only the scoring kernel")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this size (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: the episode batch shards by episode with no exchange; "
-              "multi-GPU runs are not part of this build", file=sys.stderr)
+        print("bench.py measures one GPU only: episodes shard across GPUs with no exchange, "
+              "and runs on several GPUs are not provided", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -342,6 +394,10 @@ def main():
     if args.only == "policies":
         pol = policy_bench(torch, rk, wl, torch.cuda.current_stream(), args.steps)
         print(json.dumps({"policies": pol}), flush=True)
+        return
+    if args.only == "cache":
+        cp = cache_bench(torch, rk, wl, torch.cuda.current_stream(), args.steps)
+        print(json.dumps({"cache_policies": cp}), flush=True)
         return
     log("generating the sweep (64 traces of 4,096 requests)")
     w = wl.sweep70b_workload()
@@ -406,6 +462,11 @@ def main():
         torch.cuda.empty_cache()
         pol = policy_bench(torch, rk, wl, stream, args.steps)
 
+    cache_pol = None
+    if not args.no_cache_policies and args.only == "all":
+        torch.cuda.empty_cache()
+        cache_pol = cache_bench(torch, rk, wl, stream, args.steps)
+
     cpu = None
     if not args.no_cpu_baseline and args.only == "all":
         threads = max(1, min(16, os.cpu_count() or 1))
@@ -434,6 +495,7 @@ def main():
         "roofline": roofline,
         "score_batch": score,
         "policies": pol,
+        "cache_policies": cache_pol,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
