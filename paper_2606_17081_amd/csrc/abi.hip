@@ -98,21 +98,81 @@ __global__ __launch_bounds__(256) void block_fnv_kernel(int64_t n_seq, const int
     }
 }
 
-// Serial chaining of each sequence: one lane per sequence.
-__global__ __launch_bounds__(256) void chain_kernel(int64_t n_seq, const int64_t* __restrict__ tok_off,
-                                                    const int64_t* __restrict__ chain_off,
-                                                    uint64_t* __restrict__ chains)
+// Serial chaining of each sequence: one lane per sequence.  A wavefront runs
+// as long as its longest sequence, so each 1024-thread workgroup first ranks
+// its sequences by length (classes of 32 blocks, longest first) and hands
+// them to lanes in that order: the sequences of one wavefront then have
+// similar lengths.  The per-block values move through registers kChainChunk
+// at a time, and the next chunk's reads are issued before the current chunk
+// is chained, so a lane's memory latency overlaps its arithmetic.  Reads and
+// writes past a sequence's end are clamped to its last block (a write there
+// stores that block's final value), which keeps every memory instruction
+// unconditional.
+constexpr int kChainChunk = 16;
+constexpr int kChainWG = 1024;
+constexpr int kChainClasses = 32;
+
+__device__ __forceinline__ int64_t chain_length(int64_t s, const int64_t* __restrict__ tok_off,
+                                                const int64_t* __restrict__ chain_off, int64_t& c0)
 {
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= n_seq) return;
-    const int64_t c0 = chain_off[s], c1 = chain_off[s + 1];
-    const int64_t t0 = tok_off[s], t1 = tok_off[s + 1];
-    if (c1 < c0 || t1 < t0) return;
-    const int64_t n = min(c1 - c0, (t1 - t0) / 16);
+    c0 = chain_off[s];
+    const int64_t c1 = chain_off[s + 1], t0 = tok_off[s], t1 = tok_off[s + 1];
+    if (c1 < c0 || t1 < t0) return 0;
+    return min(c1 - c0, (t1 - t0) / 16);
+}
+
+__global__ __launch_bounds__(kChainWG) void chain_kernel(int64_t n_seq, const int64_t* __restrict__ tok_off,
+                                                         const int64_t* __restrict__ chain_off,
+                                                         uint64_t* __restrict__ chains)
+{
+    __shared__ int32_t cnt[kChainClasses], base[kChainClasses];
+    __shared__ int32_t order[kChainWG];
+    const int tid = threadIdx.x;
+    const int64_t s0 = (int64_t)blockIdx.x * kChainWG;
+    const int32_t m = (int32_t)min((int64_t)kChainWG, n_seq - s0);
+    if (tid < kChainClasses) cnt[tid] = 0;
+    __syncthreads();
+    int cls = 0;
+    if (tid < m) {
+        int64_t c0;
+        const int64_t n = chain_length(s0 + tid, tok_off, chain_off, c0);
+        cls = (int)min(n / 32, (int64_t)(kChainClasses - 1));
+        atomicAdd(&cnt[cls], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t o = 0;
+        for (int c = kChainClasses - 1; c >= 0; --c) {
+            base[c] = o;
+            o += cnt[c];
+        }
+    }
+    __syncthreads();
+    if (tid < m) order[atomicAdd(&base[cls], 1)] = tid;
+    __syncthreads();
+    if (tid >= m) return;
+    const int64_t s = s0 + order[tid];
+    int64_t c0;
+    const int64_t n = chain_length(s, tok_off, chain_off, c0);
+    if (n <= 0) return;
+    const int64_t last = c0 + n - 1;
+    uint64_t cur[kChainChunk], nxt[kChainChunk];
+#pragma unroll
+    for (int u = 0; u < kChainChunk; ++u) cur[u] = chains[min(c0 + u, last)];
     uint64_t h = 0;
-    for (int64_t k = 0; k < n; ++k) {
-        h = chain_next(h, chains[c0 + k]);
-        chains[c0 + k] = h;
+    for (int64_t k0 = 0; k0 < n; k0 += kChainChunk) {
+#pragma unroll
+        for (int u = 0; u < kChainChunk; ++u) nxt[u] = chains[min(c0 + k0 + kChainChunk + u, last)];
+#pragma unroll
+        for (int u = 0; u < kChainChunk; ++u) {
+            const uint64_t hn = chain_next(h, cur[u]);
+            h = k0 + u < n ? hn : h;
+            cur[u] = h;
+        }
+#pragma unroll
+        for (int u = 0; u < kChainChunk; ++u) chains[min(c0 + k0 + u, last)] = cur[u];
+#pragma unroll
+        for (int u = 0; u < kChainChunk; ++u) cur[u] = nxt[u];
     }
 }
 
@@ -205,8 +265,8 @@ int rk_hash_chains(int64_t n_seq, const int32_t* tokens, const int64_t* tok_off,
                        chain_off, chains, st);
     int rc = hip_check(hipGetLastError(), "rk_hash_chains fnv launch");
     if (rc) return rc;
-    const int64_t cblocks = (n_seq + 255) / 256;
-    hipLaunchKernelGGL(chain_kernel, dim3((unsigned)cblocks), dim3(256), 0, s, n_seq, tok_off, chain_off,
+    const int64_t cblocks = (n_seq + kChainWG - 1) / kChainWG;
+    hipLaunchKernelGGL(chain_kernel, dim3((unsigned)cblocks), dim3(kChainWG), 0, s, n_seq, tok_off, chain_off,
                        chains);
     return hip_check(hipGetLastError(), "rk_hash_chains chain launch");
 }
