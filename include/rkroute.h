@@ -338,6 +338,8 @@ typedef struct {
                                         RK_PROBE_SCAN: scan from block 0 in 64-block steps */
     int32_t tiers;                   /* nonzero when some episode has tier_g1 > 0: the
                                         launch then keeps tier overlaps in LDS          */
+    int32_t max_routes;              /* upper bound on any episode's routes (turns), >= 0 */
+    int32_t reserved;                /* 0                                               */
     const rk_episode_params* params; /* [E], device                                     */
     const int64_t* turn_off;         /* turns of conversation c: turn_off[c] .. turn_off[c+1]-1 */
     const int32_t* turn_blocks;      /* prompt blocks P of each turn; a turn's prompt is the
@@ -375,7 +377,7 @@ typedef struct {
 
 /* Workspace bytes needed by rk_simulate_episodes for this batch shape. */
 size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache_blocks,
-                                  int32_t max_blocks, int32_t max_conv);
+                                  int32_t max_blocks, int32_t max_conv, int32_t max_routes);
 
 /* Run E independent episodes, one workgroup each.  `batch` and `out` are HOST
  * structs holding device pointers; `workspace` is device memory of at least

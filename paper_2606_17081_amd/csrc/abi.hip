@@ -47,7 +47,8 @@ int32_t* status_word()
     return g_status_addr[dev];
 }
 
-EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv)
+EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv,
+                             int32_t max_routes)
 {
     EpisodeLayout L;
     uint64_t live_max = (uint64_t)cache_blocks + (uint64_t)max_blocks;
@@ -60,6 +61,8 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     L.off_scratch_f = o; o = align_up(o + live_max * sizeof(uint32_t), 256);
     L.off_queue = o;   o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);
     L.off_next = o;    o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);
+    L.off_hist = o;    o = align_up(o + ((size_t)max_routes + 1) * 2 * sizeof(int32_t), 256);
+    L.off_replay = o;  o = align_up(o + (size_t)kEpisodeThreads * 16, 256);
     L.per_episode = o;
     return L;
 }

@@ -33,6 +33,16 @@
 // in, blocks are evicted and the pending requests searched again on that
 // worker.
 //
+// Recency is kept lazily under LRU: until a worker first has to evict, its
+// stamps decide nothing, so the writers only insert the blocks it lacks (no
+// stamp or log writes, no touches of blocks it holds).  The routes' order and
+// worker are kept in a per-episode history; at the first eviction the
+// worker's recency is rebuilt from it -- every block gets the stamp of its
+// last touch, and the live records are laid down in the log in that order
+// (two passes over the worker's routes) -- and from then on the worker is
+// maintained eagerly.  Results are those of eager upkeep; episodes whose
+// caches never fill skip the recency work altogether.
+//
 // Frequency eviction keeps, per slot, the key K = f + e of a block whose
 // frequency was f after its last update in decay epoch e (epoch = routing
 // step / decay_steps); in epoch E its frequency is max(K - E, 1), the eager
@@ -62,7 +72,7 @@
 
 namespace rk {
 
-constexpr int NT = 256;
+constexpr int NT = kEpisodeThreads;
 constexpr int NW = NT / 64;
 constexpr int kMaxBatch = 64;       // routes per batch (at most one wavefront of lanes)
 constexpr int32_t kMoreTurns = 0x40000000;   // flag on an in-flight conversation index: it has a next turn
@@ -70,7 +80,8 @@ constexpr int32_t kMoreTurns = 0x40000000;   // flag on an in-flight conversatio
 enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2, EV_EPOCH = 3 };
 
 struct EpArgs {
-    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB, tiers;
+    int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB, tiers,
+        max_routes;
     const rk_episode_params* params;
     const int64_t* turn_off;
     const int32_t* turn_blocks;
@@ -115,6 +126,31 @@ __device__ __forceinline__ int32_t block_scan(bool flag, int32_t* wtot, int32_t&
     __syncthreads();
     total = tot;
     return off + rank;
+}
+
+// Exclusive prefix sum of v over the workgroup's threads (thread order) and the
+// total.  Every thread of the workgroup must call it.
+__device__ __forceinline__ int32_t block_excl_sum(int32_t v, int32_t* wtot, int32_t& total)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int32_t x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t o = __shfl_up(x, off, 64);
+        if (lane >= off) x += o;
+    }
+    if (lane == 63) wtot[w] = x;
+    __syncthreads();
+    int32_t off = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+        const int32_t t = wtot[k];
+        off += k < w ? t : 0;
+        tot += t;
+    }
+    __syncthreads();
+    total = tot;
+    return off + x - v;
 }
 
 __device__ __forceinline__ void load_slot(const Slot* p, uint64_t& key, uint32_t& stamp)
@@ -636,6 +672,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     uint32_t* s_b2 = s_b1 + W;                              //   G1 u G2's boundary,
     int32_t* s_n1 = (int32_t*)(s_b2 + W);                   //   live records from each boundary on
     int32_t* s_n2 = s_n1 + W;
+    int32_t* s_stamped = s_n2 + W;                          // recency kept (else insert-only until the first eviction)
     // in-flight routes of the last H steps, by step slot
     int32_t* s_stw = (int32_t*)(smem + a.lds_inflight);   // worker
     int32_t* s_stP = s_stw + a.max_inflight;               // prompt blocks
@@ -686,6 +723,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     }
     const bool draws = rg_draws || (!regime_ctl && (policy == RK_POLICY_SOFTMAX || policy == RK_POLICY_RANDOM ||
                                                     policy == RK_POLICY_P2C));
+    if (a.turn_off[prm.conv_begin + n_conv] - a.turn_off[prm.conv_begin] > (int64_t)a.max_routes) {
+        if (tid == 0) atomicOr(a.status, RK_DEV_TOO_LARGE);
+        return;
+    }
     const bool freq = prm.evict_policy == RK_EVICT_FREQ;
     const int32_t dsteps = prm.decay_steps;
     const bool tiers = prm.tier_g1 > 0;
@@ -710,6 +751,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     uint32_t* g_scratch_f = (uint32_t*)(ws + a.L.off_scratch_f);
     int32_t* g_queue = (int32_t*)(ws + a.L.off_queue);
     int32_t* g_next = (int32_t*)(ws + a.L.off_next);
+    int32_t* g_hist = (int32_t*)(ws + a.L.off_hist);       // per route: conversation, P | worker << 16
     const uint64_t S = a.L.slots, smask = S - 1, R = a.L.ring, rmask = R - 1;
     const uint64_t used_limit = S - S / 4;
     const uint64_t scratch_cap = (uint64_t)a.cache + (uint64_t)a.max_blocks;
@@ -727,6 +769,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         s_b2[tid] = 0;
         s_n1[tid] = 0;
         s_n2[tid] = 0;
+        s_stamped[tid] = freq || tiers;     // frequencies and tier runs need every touch
         s_head[tid] = 0;
         s_tail[tid] = 0;
         s_live[tid] = 0;
@@ -858,10 +901,20 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                     const int32_t P = r_P[b], sg = r_sig[b];
                     Slot* tk = g_slots + (uint64_t)sg * S;
                     uint32_t* tl = g_log + (uint64_t)sg * R;
+                    const bool known = k < r_otab[b];
+                    if (!s_stamped[sg]) {
+                        // recency not kept yet: only the blocks the worker may lack are inserted
+                        if (!known) {
+                            int ins;
+                            touch_hinted(tk, smask, a.chains[r_cb[b] + k], false, ins, a.status);
+                            my_ins += ins;
+                        }
+                        continue;
+                    }
                     const uint64_t h = a.chains[r_cb[b] + k];
                     const uint32_t stamp = r_stamp[b] + (uint32_t)(P - 1 - k);
                     int ins;
-                    const uint64_t sl = touch_hinted(tk, smask, h, k < r_otab[b], ins, a.status);
+                    const uint64_t sl = touch_hinted(tk, smask, h, known, ins, a.status);
                     // routes of one worker that share a block touch it concurrently: the latest stamp wins
                     if (sl != ~0ull) {
                         const uint32_t old = __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED,
@@ -936,6 +989,92 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         if (tid == 0) {
             bk[j] = b;
             nk[j] = n;
+        }
+        __syncthreads();
+    };
+
+    // ---- recency of worker j rebuilt from the episode's routes [0, t_end) (all threads): pass 1
+    //      gives every block the stamp of its last touch (routes in order, a route's blocks from last
+    //      to first, stamps counting up from 0), pass 2 keeps the touch that set each block's stamp
+    //      and lays the live records down in the log in that order, re-stamped 0, 1, ...
+    auto replay = [&](int32_t j, int32_t t_end) {
+        Slot* tk = g_slots + (uint64_t)j * S;
+        uint32_t* tl = g_log + (uint64_t)j * R;
+        int64_t* r_cbs = (int64_t*)(ws + a.L.off_replay);     // per chunk of routes, the worker's: chain
+        int32_t* r_off = (int32_t*)(r_cbs + NT);              // base, first touch index and P
+        int32_t* r_Ps = r_off + NT;
+        for (int pass = 0; pass < 2; ++pass) {
+            int64_t stamp0 = 0;      // original stamp of the chunk's first touch
+            int32_t live = 0;        // pass 2: live records laid down so far
+            for (int32_t base = 0; base < t_end; base += NT) {
+                const int32_t r = base + tid;
+                int32_t P = 0;
+                int64_t cb = 0;
+                if (r < t_end) {
+                    const int32_t pw = g_hist[2 * r + 1];
+                    if ((pw >> 16) == j) {
+                        P = pw & 0xFFFF;
+                        cb = a.chain_off[gc0 + g_hist[2 * r]];
+                    }
+                }
+                int32_t n_r, ptot;
+                const int32_t rank = block_scan(P > 0, sh.wtot, n_r);
+                const int32_t off = block_excl_sum(P, sh.wtot, ptot);
+                if (P > 0) {
+                    r_off[rank] = off;
+                    r_cbs[rank] = cb;
+                    r_Ps[rank] = P;
+                }
+                __syncthreads();
+                for (int32_t i0 = 0; i0 < ptot; i0 += NT) {
+                    const int32_t i = i0 + tid;
+                    uint64_t sl = ~0ull;
+                    uint32_t st = 0;
+                    bool last = false;
+                    if (i < ptot) {
+                        int32_t lo = 0, hi = n_r - 1;     // the route holding touch i
+                        while (lo < hi) {
+                            const int32_t mid = (lo + hi + 1) >> 1;
+                            if (r_off[mid] <= i) lo = mid;
+                            else hi = mid - 1;
+                        }
+                        const int32_t q = i - r_off[lo];            // touches go from the last block
+                        const int32_t k = r_Ps[lo] - 1 - q;         // to the first
+                        st = (uint32_t)(stamp0 + r_off[lo] + q);
+                        int ins;
+                        sl = touch_hinted(tk, smask, a.chains[r_cbs[lo] + k], true, ins, a.status);
+                        if (sl != ~0ull) {
+                            if (pass == 0)
+                                __hip_atomic_fetch_max(&tk[sl].stamp, st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                            else
+                                last = tk[sl].stamp == st;
+                        }
+                    }
+                    if (pass == 1) {
+                        // every thread has read its slot's stamp before any is rewritten
+                        int32_t nl;
+                        const int32_t lr = block_scan(last, sh.wtot, nl);
+                        if (last) {
+                            const uint32_t ns = (uint32_t)(live + lr);
+                            tk[sl].stamp = ns;
+                            tl[ns & rmask] = (uint32_t)sl;
+                        }
+                        live += nl;
+                    }
+                }
+                stamp0 += ptot;
+                __syncthreads();
+            }
+            __syncthreads();
+            if (pass == 1 && tid == 0) {
+                if (live != s_live[j]) atomicOr(a.status, RK_DEV_TABLE_FULL);
+                s_head[j] = 0;
+                s_tail[j] = (uint32_t)live;
+                s_stamped[j] = 1;
+            }
+            if (pass == 0 && stamp0 >= 0x40000000ll) {
+                if (tid == 0) atomicOr(a.status, RK_DEV_TOO_LARGE);
+            }
         }
         __syncthreads();
     };
@@ -1125,8 +1264,9 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             for (int32_t b = 0; b < nb; ++b) T += r_P[b];
             unsigned long long m = 0;
             for (int32_t j = 0; j < W; ++j)
-                if ((uint64_t)s_used[j] + (uint64_t)T > used_limit ||
-                    (uint64_t)(s_tail[j] - s_head[j]) + (uint64_t)T > R || (uint64_t)s_tail[j] + (uint64_t)T > 0x40000000u)
+                if (s_stamped[j] &&
+                    ((uint64_t)s_used[j] + (uint64_t)T > used_limit || (uint64_t)(s_tail[j] - s_head[j]) + (uint64_t)T > R ||
+                     (uint64_t)s_tail[j] + (uint64_t)T > 0x40000000u))
                     m |= 1ull << j;
             sh.rb_mask = m;
         }
@@ -1136,8 +1276,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             int64_t margin = INT64_MAX;
             for (int32_t j = 0; j < W; ++j) {
                 margin = min(margin, (int64_t)used_limit - (int64_t)s_used[j]);
-                margin = min(margin, (int64_t)R - (int64_t)(s_tail[j] - s_head[j]));
-                margin = min(margin, (int64_t)0x40000000 - (int64_t)s_tail[j]);
+                if (s_stamped[j]) {      // a worker without kept recency writes no log records
+                    margin = min(margin, (int64_t)R - (int64_t)(s_tail[j] - s_head[j]));
+                    margin = min(margin, (int64_t)0x40000000 - (int64_t)s_tail[j]);
+                }
             }
             int64_t acc = 0;
             int32_t n2 = 0;
@@ -1366,6 +1508,8 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         r_sig[b] = sg;
                         r_stamp[b] = base;
                         r_ep[b] = freq ? (uint32_t)run_ep : 0u;
+                        g_hist[2 * t] = rc & ~kMoreTurns;
+                        g_hist[2 * t + 1] = P | (sg << 16);
                         r_otab[b] = o_tab[b * W + sg];
                         s_stw[sb + r_in_step] = sg;
                         s_stP[sb + r_in_step] = P;
@@ -1506,6 +1650,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 advance(s_b1, s_n1, K1, sg);
                 advance(s_b2, s_n2, K12, sg);
             }
+            if (!s_stamped[sg] && sh.remaining > 0) replay(sg, sh.tdone);
             evict(sg, r_ep[b]);
             if (tiers) {
                 // evictions take the oldest records: a run keeps at most the live count
@@ -1545,10 +1690,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
 using namespace rk;
 
 extern "C" size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache_blocks, int32_t max_blocks,
-                                             int32_t max_conv)
+                                             int32_t max_conv, int32_t max_routes)
 {
-    if (E < 0 || W < 1 || cache_blocks < 1 || max_blocks < 1 || max_conv < 0) return 0;
-    const EpisodeLayout L = episode_layout(W, cache_blocks, max_blocks, max_conv);
+    if (E < 0 || W < 1 || cache_blocks < 1 || max_blocks < 1 || max_conv < 0 || max_routes < 0) return 0;
+    const EpisodeLayout L = episode_layout(W, cache_blocks, max_blocks, max_conv, max_routes);
     return L.per_episode * (size_t)E;
 }
 
@@ -1575,7 +1720,8 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     if (b->E == 0) return RK_OK;
     if (!b->params || !b->turn_off || !b->turn_blocks || !b->chain_off || !b->chains || !workspace)
         return fail(RK_EINVAL, "rk_simulate_episodes: NULL array");
-    const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv);
+    if (b->max_routes < 0) return fail(RK_EINVAL, "rk_simulate_episodes: max_routes < 0");
+    const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv, b->max_routes);
     const size_t need = L.per_episode * (size_t)b->E;
     if (ws_bytes < need)
         return fail(RK_ENOMEM, "rk_simulate_episodes: workspace %zu bytes < %zu needed", ws_bytes, need);
@@ -1593,6 +1739,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.max_ctrl_window = b->max_ctrl_window;
     a.probe_mode = b->probe_mode;
     a.tiers = b->tiers;
+    a.max_routes = b->max_routes;
     a.params = b->params;
     a.turn_off = b->turn_off;
     a.turn_blocks = b->turn_blocks;
@@ -1608,7 +1755,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     // batch that fits in 60 KiB (two episodes can then share a CU)
     size_t o = 0;
     a.lds_w = 0;
-    o = align_up(o + (size_t)b->W * 10 * 4, 16);
+    o = align_up(o + (size_t)b->W * 11 * 4, 16);
     a.lds_inflight = (uint32_t)o;
     o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
     a.lds_u = (uint32_t)o;

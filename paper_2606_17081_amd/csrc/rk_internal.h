@@ -151,13 +151,16 @@ struct __align__(16) Slot {
     uint32_t fkey;
 };
 
+constexpr int kEpisodeThreads = 256;   // threads of an episode's workgroup
+
 // Episode workspace layout (bytes), shared by the size query and the launch.
 struct EpisodeLayout {
     uint64_t slots;        // table slots per worker (power of two)
     uint64_t ring;         // LRU log records per worker (power of two)
-    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next;
+    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next, off_hist, off_replay;
     size_t per_episode;
 };
-EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv);
+EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv,
+                             int32_t max_routes);
 
 }  // namespace rk

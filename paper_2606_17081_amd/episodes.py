@@ -97,7 +97,8 @@ class EpisodeRunner:
         self.route_regime = z(R, torch.int32)
         self.tiers = any(sp.tier_g1 > 0 for sp in self.episodes)
         self.tier_overlap = z((R, W, 2), torch.int32) if self.tiers else None
-        ws = rk.simulate_workspace_size(E, W, self.cache_blocks, self.max_blocks, self.max_conv)
+        self.max_routes = max([n for (_, n, _, _) in self.rows] + [0])
+        ws = rk.simulate_workspace_size(E, W, self.cache_blocks, self.max_blocks, self.max_conv, self.max_routes)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
 
         self.win_off = up(np.array(win_off, np.int64), torch.int64)
@@ -115,7 +116,7 @@ class EpisodeRunner:
         P = rk._ptr
         self.batch = rk.EpisodeBatch(E, W, self.cache_blocks, self.max_blocks, self.max_conv,
                                      self.max_inflight, self.max_rps, self.max_ctrl_window, probe_mode,
-                                     int(self.tiers),
+                                     int(self.tiers), self.max_routes, 0,
                                      P(self.params), P(self.turn_off), P(self.turn_blocks), P(self.chain_off),
                                      P(self.chains), P(self.route_rand), rk.regime_params(self.regime))
         self.outputs = rk.EpisodeOutputs(P(self.route_turn), P(self.route_worker), P(self.route_step),

@@ -60,7 +60,8 @@ class EpisodeBatch(C.Structure):
     _fields_ = [("E", C.c_int32), ("W", C.c_int32), ("cache_blocks", C.c_int32),
                 ("max_blocks", C.c_int32), ("max_conv", C.c_int32), ("max_inflight", C.c_int32),
                 ("max_routes_per_step", C.c_int32), ("max_ctrl_window", C.c_int32),
-                ("probe_mode", C.c_int32), ("tiers", C.c_int32),
+                ("probe_mode", C.c_int32), ("tiers", C.c_int32), ("max_routes", C.c_int32),
+                ("reserved", C.c_int32),
                 ("params", C.c_void_p), ("turn_off", C.c_void_p), ("turn_blocks", C.c_void_p),
                 ("chain_off", C.c_void_p), ("chains", C.c_void_p), ("route_rand", C.c_void_p),
                 ("regime", RegimeParams)]
@@ -116,7 +117,7 @@ def lib():
             L.rk_route_score_index.restype = C.c_int
             L.rk_route_score_index.argtypes = [i32, i32, vp, vp, vp, i32, vp, CostParams, i32, vp, vp, vp, vp]
             L.rk_simulate_workspace_size.restype = sz
-            L.rk_simulate_workspace_size.argtypes = [i32, i32, i32, i32, i32]
+            L.rk_simulate_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32]
             L.rk_simulate_episodes.restype = C.c_int
             L.rk_simulate_episodes.argtypes = [C.POINTER(EpisodeBatch), C.POINTER(EpisodeOutputs), vp, sz, vp]
             L.rk_poa_workspace_size.restype = sz
@@ -301,8 +302,8 @@ def route_score_index(chains, chain_off, index, log2_slots: int, active_blocks, 
     return overlap, cost, argmin
 
 
-def simulate_workspace_size(E, W, cache_blocks, max_blocks, max_conv) -> int:
-    return int(lib().rk_simulate_workspace_size(E, W, cache_blocks, max_blocks, max_conv))
+def simulate_workspace_size(E, W, cache_blocks, max_blocks, max_conv, max_routes) -> int:
+    return int(lib().rk_simulate_workspace_size(E, W, cache_blocks, max_blocks, max_conv, max_routes))
 
 
 def simulate_episodes(batch: EpisodeBatch, outputs: EpisodeOutputs, workspace, stream=None):

@@ -59,18 +59,18 @@ def test_episode_and_poa_host_validation():
     if not rk.library_available():
         pytest.skip("librkroute.so not built")
     L = rk.lib()
-    b = rk.EpisodeBatch(1, 65, 16, 8, 4, 8, 2, 1, 0, 0, None, None, None, None, None)
+    b = rk.EpisodeBatch(1, 65, 16, 8, 4, 8, 2, 1, 0, 0, 4, 0, None, None, None, None, None)
     o = rk.EpisodeOutputs()
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), None, 0, None) == rk.RK_EUNSUPPORTED
-    b = rk.EpisodeBatch(1, 4, 16, 8, 4, 8, 2, 1, 3, 0, None, None, None, None, None)
+    b = rk.EpisodeBatch(1, 4, 16, 8, 4, 8, 2, 1, 3, 0, 4, 0, None, None, None, None, None)
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), None, 0, None) == rk.RK_EINVAL
-    b = rk.EpisodeBatch(0, 4, 16, 8, 4, 8, 2, 1, 0, 0, None, None, None, None, None)
+    b = rk.EpisodeBatch(0, 4, 16, 8, 4, 8, 2, 1, 0, 0, 4, 0, None, None, None, None, None)
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), None, 0, None) == rk.RK_OK
-    b = rk.EpisodeBatch(2, 4, 16, 8, 4, 8, 2, 1, 0, 0, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
+    b = rk.EpisodeBatch(2, 4, 16, 8, 4, 8, 2, 1, 0, 0, 4, 0, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
                         C.c_void_p(8), C.c_void_p(8))
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), 16, None) == rk.RK_ENOMEM
-    need = rk.simulate_workspace_size(2, 4, 16, 8, 4)
-    assert need > 0 and need == 2 * rk.simulate_workspace_size(1, 4, 16, 8, 4)
+    need = rk.simulate_workspace_size(2, 4, 16, 8, 4, 10)
+    assert need > 0 and need == 2 * rk.simulate_workspace_size(1, 4, 16, 8, 4, 10)
     pp = rk.PoaParams(0.005, 0.02, 0.01, 2, 64, 0.015, 0)
     assert L.rk_poa_estimate(1, None, 0, None, 8, 8, 65, None, None, None, pp, None, None, None, None, 0,
                              None) == rk.RK_EUNSUPPORTED
