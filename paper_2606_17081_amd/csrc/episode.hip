@@ -617,7 +617,8 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
 
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
-    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rrnd, lcp, t1, t12, bytes;
+    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
+        t1, t12, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool tiers)
@@ -643,6 +644,10 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     b.rotab = take(nb * 4, 4);
     b.rstamp = take(nb * 4, 4);
     b.rep = take(nb * 4, 4);
+    b.rstep = take(nb * 4, 4);
+    b.rreg = take(nb * 4, 4);
+    b.revc = take(nb * 4, 4);
+    b.revd = take(nb * 8, 8);
     b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
     b.t1 = take(tiers ? nb * w * 2 : 0, 4);
@@ -694,6 +699,10 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     int32_t* r_otab = (int32_t*)(bb + BL.rotab);           // blocks known cached in sigma's table
     uint32_t* r_stamp = (uint32_t*)(bb + BL.rstamp);       // stamp of the last block
     uint32_t* r_ep = (uint32_t*)(bb + BL.rep);             // decay epoch (frequency eviction)
+    int32_t* r_step = (int32_t*)(bb + BL.rstep);           // per-route outputs, written out at the end
+    int32_t* r_reg = (int32_t*)(bb + BL.rreg);             //   of the batch: step, regime, evictions
+    int32_t* r_evc = (int32_t*)(bb + BL.revc);             //   and their digest
+    uint64_t* r_evd = (uint64_t*)(bb + BL.revd);
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
     uint16_t* t1_tab = (uint16_t*)(bb + BL.t1);            // [b][j] leading blocks in G1 (tiers)
@@ -1229,6 +1238,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     for (;;) {
         // ---- A. the batch: the next nb queued requests (queue order is routing order)
         const int32_t qh0 = sh.qhead;
+        const int32_t tb0 = sh.tdone;        // routes decided before this batch
         int32_t nb = min(NB, sh.qsize);
         for (int32_t b = tid; b < nb; b += NT) {
             const int32_t c = g_queue[(qh0 + b) % qcap];
@@ -1450,7 +1460,6 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         } else {
                             cj = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
                         }
-                        if (a.out.overlap) a.out.overlap[row * W + lane] = oj;
                         if (a.out.cost) a.out.cost[row * W + lane] = cj;
                         bits = __float_as_uint(__fadd_rn(cj, 0.0f));
                     }
@@ -1517,16 +1526,11 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                         g_next[rc & ~kMoreTurns] = r_k[b] + 1;
                         sh.qhead = (sh.qhead + 1) % qcap;
                         sh.qsize -= 1;
-                        if (a.out.route_turn) a.out.route_turn[row] = r_turn[b];
-                        if (a.out.route_worker) a.out.route_worker[row] = sg;
-                        if (a.out.route_step) a.out.route_step[row] = (int32_t)s;
-                        if (a.out.route_blocks) a.out.route_blocks[row] = P;
-                        if (a.out.last_hash) a.out.last_hash[row] = r_last[b];
-                        if (a.out.route_regime) a.out.route_regime[row] = regime_ctl ? rg_r : 0;
-                        if (!flush) {
-                            if (a.out.evict_count) a.out.evict_count[row] = 0;
-                            if (a.out.evict_digest) a.out.evict_digest[row] = 0ull;
-                        } else {
+                        r_step[b] = (int32_t)s;
+                        r_reg[b] = regime_ctl ? rg_r : 0;
+                        r_evc[b] = 0;
+                        r_evd[b] = 0ull;
+                        if (flush) {
                             sh.ev_b = b;
                             sh.ev_row = row;
                         }
@@ -1665,13 +1669,31 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             search(b + 1, nb, sg);
             if (tiers) tier_search(b + 1, nb, sg);
             if (tid == 0) {
-                if (a.out.evict_count) a.out.evict_count[sh.ev_row] = sh.ev;
-                if (a.out.evict_digest) a.out.evict_digest[sh.ev_row] = sh.digest;
+                r_evc[sh.ev_b] = sh.ev;
+                r_evd[sh.ev_b] = sh.digest;
                 sh.ev_total += sh.ev;
             }
             __syncthreads();
         }
 
+        // the batch's per-route outputs, from LDS, by the whole workgroup
+        {
+            const int32_t nd = sh.tdone - tb0;
+            const int64_t row0 = prm.out_base + (int64_t)tb0;
+            for (int32_t b = tid; b < nd; b += NT) {
+                const int64_t row = row0 + b;
+                if (a.out.route_turn) a.out.route_turn[row] = r_turn[b];
+                if (a.out.route_worker) a.out.route_worker[row] = r_sig[b];
+                if (a.out.route_step) a.out.route_step[row] = r_step[b];
+                if (a.out.route_blocks) a.out.route_blocks[row] = r_P[b];
+                if (a.out.last_hash) a.out.last_hash[row] = r_last[b];
+                if (a.out.route_regime) a.out.route_regime[row] = r_reg[b];
+                if (a.out.evict_count) a.out.evict_count[row] = r_evc[b];
+                if (a.out.evict_digest) a.out.evict_digest[row] = r_evd[b];
+            }
+            if (a.out.overlap)
+                for (int32_t i = tid; i < nd * W; i += NT) a.out.overlap[row0 * W + i] = o_cur[i];
+        }
         if (tid == 0) sh.ins = 0;
         __syncthreads();
         if (event == EV_DONE) break;
