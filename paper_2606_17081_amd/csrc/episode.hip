@@ -100,7 +100,7 @@ constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 
 struct EpShared {
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
-    int32_t woff[NW][KR + 1];
+    int32_t woff[NW][KR + 1], wst[NW][KR];
     uint32_t new_head, first_kept, adv;
     int64_t ev_row, ev_total;
     unsigned long long digest, rb_mask;
@@ -617,7 +617,7 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
 
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
-    uint32_t rcb, rlast, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
+    uint32_t rcb, rlast, rfirst, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
         t1, t12, bytes;
 };
 
@@ -634,6 +634,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     const uint32_t nb = (uint32_t)NB, w = (uint32_t)W;
     b.rcb = take(nb * 8, 8);
     b.rlast = take(nb * 8, 8);
+    b.rfirst = take(nb * 8, 8);
     b.o_cur = take(nb * w * 4, 4);
     b.o_tab = take(nb * w * 4, 4);
     b.rc = take(nb * 4, 4);
@@ -656,7 +657,8 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     return b;
 }
 
-__global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
+// Two waves per SIMD: two episodes share a CU (the sweep has more episodes than CUs).
+__global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ EpShared sh;
@@ -689,6 +691,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
     unsigned char* bb = smem + a.lds_batch;
     int64_t* r_cb = (int64_t*)(bb + BL.rcb);               // chain base
     uint64_t* r_last = (uint64_t*)(bb + BL.rlast);         // h_{P-1}
+    uint64_t* r_first = (uint64_t*)(bb + BL.rfirst);       // h_0
     int32_t* o_cur = (int32_t*)(bb + BL.o_cur);            // [b][j] overlap as of now
     int32_t* o_tab = (int32_t*)(bb + BL.o_tab);            // [b][j] overlap found in the table
     int32_t* r_c = (int32_t*)(bb + BL.rc);                 // conversation (| kMoreTurns)
@@ -894,30 +897,38 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 }
                 if (!__builtin_amdgcn_readfirstlane(won)) continue;
-                // routes [c, hi): their blocks numbered consecutively
+                // routes [c, hi): the blocks each must write numbered consecutively -- all of
+                // them, or, on a worker whose recency is not kept yet, those past the prefix
+                // its table held (only those may be missing)
+                int32_t* wst = sh.wst[wave];
                 const int32_t nr = hi - c;
-                int32_t tot = 0;
-                const int32_t pr = lane < nr ? r_P[c + lane] : 0;
+                int32_t tot = 0, st0 = 0, pr = 0;
+                if (lane < nr) {
+                    const int32_t bl = c + lane;
+                    st0 = s_stamped[r_sig[bl]] ? 0 : r_otab[bl];
+                    pr = r_P[bl] - st0;
+                }
                 const int32_t off = ep_wave_excl_sum(pr, tot);
-                if (lane < nr) woff[lane] = off;
+                if (lane < nr) {
+                    woff[lane] = off;
+                    wst[lane] = st0;
+                }
                 if (lane == 0) woff[nr] = tot;
                 ep_wave_sync();
                 for (int32_t i = lane; i < tot; i += 64) {
                     int32_t r = 0;
                     while (r + 1 < nr && woff[r + 1] <= i) ++r;
                     const int32_t b = c + r;
-                    const int32_t k = i - woff[r];
+                    const int32_t k = wst[r] + (i - woff[r]);
                     const int32_t P = r_P[b], sg = r_sig[b];
                     Slot* tk = g_slots + (uint64_t)sg * S;
                     uint32_t* tl = g_log + (uint64_t)sg * R;
                     const bool known = k < r_otab[b];
                     if (!s_stamped[sg]) {
-                        // recency not kept yet: only the blocks the worker may lack are inserted
-                        if (!known) {
-                            int ins;
-                            touch_hinted(tk, smask, a.chains[r_cb[b] + k], false, ins, a.status);
-                            my_ins += ins;
-                        }
+                        // recency not kept yet: insert what the worker may lack
+                        int ins;
+                        touch_hinted(tk, smask, a.chains[r_cb[b] + k], false, ins, a.status);
+                        my_ins += ins;
                         continue;
                     }
                     const uint64_t h = a.chains[r_cb[b] + k];
@@ -1262,6 +1273,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
             r_P[b] = P;
             r_cb[b] = cb;
             r_last[b] = P > 0 ? a.chains[cb + P - 1] : 0ull;
+            r_first[b] = P > 0 ? a.chains[cb] : 0ull;
             const int64_t row = prm.out_base + (int64_t)sh.tdone + b;
             r_rnd[2 * b] = draws ? a.route_rand[2 * row] : 0u;
             r_rnd[2 * b + 1] = draws ? a.route_rand[2 * row + 1] : 0u;
@@ -1269,36 +1281,43 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
         __syncthreads();
         // workers without room for every block of the batch are compacted first; the batch is cut to
         // what the tightest worker can take (at least one request always fits after compaction)
-        if (tid == 0) {
-            int64_t T = 0;
-            for (int32_t b = 0; b < nb; ++b) T += r_P[b];
-            unsigned long long m = 0;
-            for (int32_t j = 0; j < W; ++j)
-                if (s_stamped[j] &&
-                    ((uint64_t)s_used[j] + (uint64_t)T > used_limit || (uint64_t)(s_tail[j] - s_head[j]) + (uint64_t)T > R ||
-                     (uint64_t)s_tail[j] + (uint64_t)T > 0x40000000u))
-                    m |= 1ull << j;
-            sh.rb_mask = m;
+        if (wave == 0) {
+            // wavefront 0: lane b holds request b's blocks, lane j tests worker j
+            int32_t Ttot;
+            ep_wave_excl_sum(lane < nb ? r_P[lane] : 0, Ttot);
+            const uint64_t T = (uint64_t)Ttot;
+            const bool full = lane < W && s_stamped[lane] &&
+                              ((uint64_t)s_used[lane] + T > used_limit ||
+                               (uint64_t)(s_tail[lane] - s_head[lane]) + T > R ||
+                               (uint64_t)s_tail[lane] + T > 0x40000000u);
+            const unsigned long long m = __ballot(full);
+            if (lane == 0) sh.rb_mask = m;
         }
         __syncthreads();
         for (unsigned long long m = sh.rb_mask; m; m &= m - 1ull) rebuild(__ffsll(m) - 1);
-        if (tid == 0) {
-            int64_t margin = INT64_MAX;
-            for (int32_t j = 0; j < W; ++j) {
-                margin = min(margin, (int64_t)used_limit - (int64_t)s_used[j]);
-                if (s_stamped[j]) {      // a worker without kept recency writes no log records
-                    margin = min(margin, (int64_t)R - (int64_t)(s_tail[j] - s_head[j]));
-                    margin = min(margin, (int64_t)0x40000000 - (int64_t)s_tail[j]);
+        if (wave == 0) {
+            // the tightest worker's room, then the longest run of requests that fits it
+            int64_t mj = INT64_MAX;
+            if (lane < W) {
+                mj = (int64_t)used_limit - (int64_t)s_used[lane];
+                if (s_stamped[lane]) {   // a worker without kept recency writes no log records
+                    mj = min(mj, (int64_t)R - (int64_t)(s_tail[lane] - s_head[lane]));
+                    mj = min(mj, (int64_t)0x40000000 - (int64_t)s_tail[lane]);
                 }
             }
-            int64_t acc = 0;
-            int32_t n2 = 0;
-            while (n2 < nb && acc + r_P[n2] <= margin) acc += r_P[n2++];
-            if (n2 == 0 && nb > 0) {
-                atomicOr(a.status, RK_DEV_TABLE_FULL);
-                n2 = 1;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) mj = min(mj, (int64_t)__shfl_xor(mj, off, 64));
+            int32_t Ttot;
+            const int32_t pb = lane < nb ? r_P[lane] : 0;
+            const int64_t incl = (int64_t)ep_wave_excl_sum(pb, Ttot) + pb;
+            int32_t n2 = __popcll(__ballot(lane < nb && incl <= mj));
+            if (lane == 0) {
+                if (n2 == 0 && nb > 0) {
+                    atomicOr(a.status, RK_DEV_TABLE_FULL);
+                    n2 = 1;
+                }
+                sh.nb = n2;
             }
-            sh.nb = n2;
         }
         if (tid == 0) {
             sh.decided = 0;
@@ -1322,7 +1341,7 @@ __global__ __launch_bounds__(NT) void episode_kernel(EpArgs a)
                 const uint64_t* ca = a.chains + r_cb[b];
                 const uint64_t* cc = a.chains + r_cb[b2];
                 int32_t lo = 0;
-                if (m > 0 && ca[0] == cc[0]) {
+                if (m > 0 && r_first[b] == r_first[b2]) {
                     int32_t hi = m;
                     lo = 1;
                     while (lo < hi) {
