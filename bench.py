@@ -76,12 +76,16 @@ def episode_algorithmic_bytes(runner) -> float:
     at its natural width (no cache-line rounding):
       per episode: clearing W tables of S slots (key 8 + stamp 4);
       per route:   per worker the keys a binary search for the first miss
-                   reads, ceil(log2(P + 1)) probes of 8 B; the chosen worker's
+                   reads, ceil(log2(P + 1)) probes of 8 B; 8 B of outputs per
+                   worker (overlap, cost) and 28 B per route; the first chain
+                   hash of the route compared with those of the other routes
+                   of its batch of 64 (8 B each);
+                   on a worker that evicts at some point of the episode, the
                    touch of P blocks (chain hash read 8, key read 8, stamp
                    write 4, log write 4) and insert of P - o keys (8 each);
-                   8 B of outputs per worker (overlap, cost) and 28 B per route;
-                   the first chain hash of the route compared with those of
-                   the other routes of its batch of 64 (8 B each);
+                   on a worker that never evicts, recency decides nothing, so
+                   only the P - o missing blocks: chain hash read 8, key
+                   write 8;
       per eviction: log read 4, stamp read 4 and write 4, key read 8."""
     W = runner.W
     n = runner.n_rows
@@ -93,8 +97,15 @@ def episode_algorithmic_bytes(runner) -> float:
     probes = np.ceil(np.log2(P + 1.0))
     live_max = runner.cache_blocks + runner.max_blocks      # table slots: next power of two >= 2 * live_max
     S = 1 << int(np.ceil(np.log2(2 * live_max)))
+    # routes on (episode, worker) pairs that evict at some point
+    evicting = np.zeros(n, bool)
+    for (r0, nr, _, _) in runner.rows:
+        sl = slice(r0, r0 + nr)
+        ws = np.unique(sig[sl][ev[sl] > 0])
+        evicting[sl] = np.isin(sig[sl], ws)
     b = len(runner.episodes) * W * S * 12.0
-    b += np.sum(8 * W * probes + 28 * P + 8 * (P - o_sig) + 8 * W + 28 + 8 * 63)
+    b += np.sum(8 * W * probes + 8 * W + 28 + 8 * 63)
+    b += np.sum(np.where(evicting, 28 * P + 8 * (P - o_sig), 16 * (P - o_sig)))
     b += np.sum(20 * ev)
     return float(b)
 
