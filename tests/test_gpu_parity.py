@@ -402,3 +402,22 @@ def test_snapshot_poa(gpu, orc):
                                  64, K=8, **pp)
         assert sel[w] == pytest.approx(s, rel=REL) and coo[w] == pytest.approx(c, rel=REL)
     assert float(hat[0]) == pytest.approx(sel.sum() / coo.sum(), rel=1e-12)
+
+
+def test_lazy_recency_late_first_eviction(gpu, orc):
+    """1P/5D-shaped traces with caches that fill only late in the episode (under LRU the kernel
+    keeps no recency until a worker first evicts, then rebuilds it from the whole history of
+    that worker's routes): every route, eviction count and digest against the oracle."""
+    base = wl.sweep70b_workload(seeds=range(2), concurrency=(32, 512))
+    late = 0
+    for cache in (12288, 24000, 40000):
+        w = wl.Workload("late-evict", W=base.W, cache_blocks=cache, traces=base.traces, episodes=base.episodes)
+        say("sweep-shaped episodes with", cache, "-block caches")
+        r = _run(gpu, w)
+        oc = {}
+        for e, sp in enumerate(base.episodes):
+            o = _oracle_episode(orc, w, sp, oc)
+            ev = np.nonzero(o["evict_count"])[0]
+            late += int(ev.size > 0 and ev[0] > len(o["evict_count"]) // 4)   # a long history before it
+            _compare_episode(r.episode_results(e), o, w.W, window=sp.concurrency, label=f"cache {cache} e{e}")
+    assert late >= 8
