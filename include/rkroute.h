@@ -55,7 +55,7 @@ typedef enum {
     RK_ENOMEM = -2,        /* workspace too small                             */
     RK_EHIP = -3,          /* a HIP runtime call or launch failed             */
     RK_ETABLEFULL = -4,    /* more keys than a table can hold                 */
-    RK_EUNSUPPORTED = -5   /* outside the sizes this build supports           */
+    RK_EUNSUPPORTED = -5   /* outside the sizes the library supports          */
 } rk_status;
 
 /* Device status bits (rk_device_status). */
