@@ -161,6 +161,21 @@ class KernelTimer:
         return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else 0.0
 
 
+def burst_ms(torch, stream, fn, n):
+    """Mean duration of n back-to-back launches of fn, from one pair of HIP
+    events on the launching stream around all of them (for launches of tens
+    of microseconds, where an event pair per launch would add its own
+    overhead to each)."""
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(n):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n
+
+
 def cpu_baseline(workload, seeds, threads):
     """The CPU oracle on a bounded sample: hash the sampled traces, run every
     episode of those seeds (all five concurrency levels) and its PoA-hat."""
@@ -208,12 +223,8 @@ def scoring_bench(torch, rk, wl, stream, steps):
     am = torch.empty(inst.B, dtype=torch.int32, device="cuda")
     for _ in range(3):
         rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co, argmin=am)
-    ts = KernelTimer(torch, stream)
-    for _ in range(max(steps, 10)):
-        with ts:
-            rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active, overlap=ov, cost=co,
-                                 argmin=am)
-    ms = ts.mean_ms()
+    ms = burst_ms(torch, stream, lambda: rk.route_score_batch(chains, chain_off, tables, inst.log2_slots, active,
+                                                              overlap=ov, cost=co, argmin=am), max(steps, 10))
     assert rk.device_status(reset=True) == 0
     salg = score_algorithmic_bytes(inst)
     ach = salg / (ms * 1e-3) / 1e9
@@ -230,11 +241,8 @@ def scoring_bench(torch, rk, wl, stream, steps):
             rk.index_build(keys, inst.key_off, lg, index=index)
     for _ in range(3):
         rk.route_score_index(chains, chain_off, index, lg, active, overlap=ov, cost=co, argmin=am)
-    ti = KernelTimer(torch, stream)
-    for _ in range(max(steps, 10)):
-        with ti:
-            rk.route_score_index(chains, chain_off, index, lg, active, overlap=ov, cost=co, argmin=am)
-    ms_i = ti.mean_ms()
+    ms_i = burst_ms(torch, stream, lambda: rk.route_score_index(chains, chain_off, index, lg, active, overlap=ov,
+                                                                cost=co, argmin=am), max(steps, 10))
     assert rk.device_status(reset=True) == 0
     ov_i = ov.cpu().numpy()
     assert np.array_equal(ov_i, ov_ref), "index and table scorers disagree"

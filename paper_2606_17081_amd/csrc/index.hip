@@ -19,7 +19,8 @@
 //   - SCAN mode (any sets): positions from block 0 in rounds of 64; a
 //     running AND of the masks gives each worker's first miss exactly, and
 //     the scan stops once no worker is left.
-// One wavefront scores one request; lane j owns worker j's overlap and cost.
+// One wavefront scores two consecutive requests; lane j owns worker j's
+// overlap and cost.
 #include <hip/hip_runtime.h>
 
 #include "rk_internal.h"
@@ -66,39 +67,6 @@ __device__ __forceinline__ uint64_t index_lookup(const IndexSlot* __restrict__ t
     return index_walk(t, smask, h, home_group(h, smask));
 }
 
-// Inclusive prefix AND of a 64-bit value across the wavefront's lanes.
-__device__ __forceinline__ uint64_t wave_prefix_and(uint64_t v)
-{
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint64_t o = __shfl_up(v, off, 64);
-        if (lane >= off) v &= o;
-    }
-    return v;
-}
-
-__device__ __forceinline__ uint64_t wave_or_u64(uint64_t v)
-{
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v |= __shfl_xor(v, off, 64);
-    return v;
-}
-
-// Exclusive prefix sum across the wavefront; total receives the full sum.
-__device__ __forceinline__ int32_t wave_excl_sum(int32_t v, int32_t& total)
-{
-    const int lane = threadIdx.x & 63;
-    int32_t x = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int32_t o = __shfl_up(x, off, 64);
-        if (lane >= off) x += o;
-    }
-    total = __shfl(x, 63, 64);
-    return x - v;
-}
-
 // First index in [lo, hi) whose mask lacks bit j, for masks in which bit j
 // never comes back once cleared; hi if none.
 __device__ __forceinline__ int32_t first_clear(const uint64_t* m, int32_t lo, int32_t hi, int32_t j)
@@ -124,156 +92,187 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-constexpr int IWAVES = 1;         // wavefronts per workgroup: a finished request frees its slot at once
+constexpr int kRPW = 2;           // requests per wavefront: their offsets and chains are loaded together
 constexpr int kRound1Min = 64;    // chains longer than this get the coarse first round
 constexpr int kStage = 256;       // leading chain blocks staged in LDS, read in one coalesced pass
 constexpr int kStageRegs = kStage / 64;
 
 struct IdxLds {
-    uint64_t ch[kStage];     // the request's first kStage chain hashes
-    uint64_t m[64];          // masks of the current round (prefix ANDs in rounds 1-2)
-    int32_t q[64];           // second-round sample positions
-    int32_t ioff[65];        // start of each sample interval's positions in the third round
+    uint64_t ch[kRPW][kStage];   // the first kStage chain hashes of each of the wavefront's requests
+    uint64_t m[64];              // masks of the current round (prefix ANDs in rounds 1-2)
+    int32_t ioff[65];            // start of each sample interval's positions in the third round
 };
 
+// Position of second-round sample k: every position when the round is exact,
+// else the power-of-two grid of step st2, clamped to U - 1.
+__device__ __forceinline__ int32_t round2_pos(int32_t k, bool exact, int64_t st2, int32_t U)
+{
+    return exact ? k : (int32_t)min((int64_t)(k + 1) * st2, (int64_t)U) - 1;
+}
+
+// One wavefront scores kRPW consecutive requests; lane j owns worker j.  The
+// requests' chain offsets come in one load and their leading chain blocks in
+// one coalesced pass into LDS, so only the first request waits for them.
 template <int MODE>
-__global__ __launch_bounds__(64 * IWAVES) void score_index_kernel(
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(8))) void score_index_kernel(
     int32_t B, int32_t W, const uint64_t* __restrict__ chains, const int64_t* __restrict__ chain_off,
     const IndexSlot* __restrict__ index, int32_t log2_slots, const int32_t* __restrict__ active, rk_cost_params p,
     int32_t* __restrict__ ov_out, float* __restrict__ cost_out, int32_t* __restrict__ am_out, int32_t* status)
 {
-    __shared__ IdxLds lds_all[IWAVES];
-    IdxLds& L = lds_all[threadIdx.x >> 6];
+    __shared__ IdxLds L;
     const int32_t lane = threadIdx.x & 63;
-    const int64_t nwaves = (int64_t)gridDim.x * IWAVES;
     const uint64_t smask = (1ull << log2_slots) - 1;
     const int32_t A = lane < W ? active[lane] : 0;
     const uint64_t all = W == 64 ? ~0ull : ((1ull << W) - 1ull);
+    const int64_t npairs = ((int64_t)B + kRPW - 1) / kRPW;
 
     // Workgroups are handed to the 8 XCDs round-robin; renumber them so each
     // XCD walks one contiguous range of requests (gridDim.x is a multiple of 8).
     const uint32_t nb8 = gridDim.x >> 3;
     const uint32_t lb = (blockIdx.x & 7u) * nb8 + (blockIdx.x >> 3);
-    for (int64_t i = (int64_t)lb * IWAVES + (threadIdx.x >> 6); i < B; i += nwaves) {
-        const int64_t c0 = chain_off[i], c1 = chain_off[i + 1];
-        int32_t P = 0;
-        if (c1 < c0 || c1 - c0 > 0x7fffffff) {
-            if (lane == 0) atomicOr(status, RK_DEV_BAD_OFFSETS);
-        } else {
-            P = (int32_t)(c1 - c0);
+    for (int64_t g = lb; g < npairs; g += gridDim.x) {
+        const int64_t i0 = g * kRPW;
+        const int32_t nr = (int32_t)min((int64_t)kRPW, (int64_t)B - i0);
+        const int64_t offv = lane <= nr ? chain_off[i0 + lane] : 0;
+        int64_t c[kRPW + 1];
+#pragma unroll
+        for (int r = 0; r <= kRPW; ++r) c[r] = (int64_t)readlane64((uint64_t)offv, r);
+        int32_t Pr[kRPW];
+#pragma unroll
+        for (int r = 0; r < kRPW; ++r) {
+            Pr[r] = 0;
+            if (r < nr) {
+                if (c[r + 1] < c[r] || c[r + 1] - c[r] > 0x7fffffff) {
+                    if (lane == 0) atomicOr(status, RK_DEV_BAD_OFFSETS);
+                } else {
+                    Pr[r] = (int32_t)(c[r + 1] - c[r]);
+                }
+            }
         }
-        const uint64_t* __restrict__ hg = chains + c0;
-        wave_sync();   // the previous request's reads of L.ch are done
+        wave_sync();   // the previous requests' reads of L.ch are done
         {
-            const int32_t n = min(P, kStage);
-            uint64_t v[kStageRegs];
+            uint64_t v[kRPW][kStageRegs];
 #pragma unroll
-            for (int k = 0; k < kStageRegs; ++k) v[k] = lane + 64 * k < n ? hg[lane + 64 * k] : 0ull;
+            for (int r = 0; r < kRPW; ++r) {
+                const int32_t n = min(Pr[r], kStage);
+                const uint64_t* __restrict__ hg = chains + c[r];
 #pragma unroll
-            for (int k = 0; k < kStageRegs; ++k) L.ch[lane + 64 * k] = v[k];
+                for (int k = 0; k < kStageRegs; ++k) v[r][k] = lane + 64 * k < n ? hg[lane + 64 * k] : 0ull;
+            }
+#pragma unroll
+            for (int r = 0; r < kRPW; ++r)
+#pragma unroll
+                for (int k = 0; k < kStageRegs; ++k) L.ch[r][lane + 64 * k] = v[r][k];
         }
         wave_sync();
-        auto h = [&](int32_t x) -> uint64_t { return x < kStage ? L.ch[x] : hg[x]; };
-        int32_t o = 0;   // lane j: overlap on worker j
 
-        if (MODE == RK_PROBE_SCAN) {
-            uint64_t carry = all;
-            bool done = false;
-            for (int32_t base = 0; base < P && carry != 0ull; base += 64) {
-                const int32_t n = min(64, P - base);
-                const uint64_t m = lane < n ? index_lookup(index, smask, h(base + lane)) : 0ull;
-                const uint64_t pa = wave_prefix_and(m) & carry;
-                L.m[lane] = pa;
-                wave_sync();
-                if (lane < W && !done) {
-                    const int32_t f = first_clear(L.m, 0, n, lane);
-                    o += f;
-                    done = f < n;
-                }
-                carry = __shfl(pa, n - 1, 64);
-                wave_sync();
-            }
-        } else {
-            // ---- round 1: every worker's first miss lies in [0, U).  Sample
-            // positions sit on a power-of-two grid (clamped to the chain's end)
-            // so requests of one prefix group probe the same index slots.
-            int32_t U = P;
-            if (P > kRound1Min) {
-                const int64_t st1 = (int64_t)next_pow2_dev((uint32_t)P) >> 4;
-                const int32_t q1 = (int32_t)min((int64_t)(lane + 1) * st1, (int64_t)P) - 1;
-                const uint64_t m = lane < 16 ? index_lookup(index, smask, h(q1)) : all;
-                const uint64_t pa = wave_prefix_and(m & all);
-                const uint64_t z = __ballot(lane < 16 && pa == 0ull);
-                if (z) U = __shfl(q1, __ffsll((unsigned long long)z) - 1, 64) + 1;
-            }
-            // ---- round 2: every position of [0, U) when U <= 64, else 64 samples
-            // on the power-of-two grid of step next_pow2(U) / 64, clamped to U - 1
-            const bool exact = U <= 64;
-            const int32_t nq = exact ? U : 64;
-            const int64_t st2 = (int64_t)next_pow2_dev((uint32_t)U) >> 6;
-            const int32_t q = exact ? lane : (int32_t)min((int64_t)(lane + 1) * st2, (int64_t)U) - 1;
-            const uint64_t m = lane < nq ? index_lookup(index, smask, h(q)) : 0ull;
-            L.m[lane] = wave_prefix_and(m & all);
-            L.q[lane] = q;
-            wave_sync();
-            const int32_t t = lane < W ? first_clear(L.m, 0, nq, lane) : nq;
-            if (exact) {
-                o = t;   // t == U only when U == P: every position is cached
-            } else {
-                // ---- round 3: worker j's first miss is in (q[t-1], q[t]]; probe the inside
-                const uint64_t need = wave_or_u64(lane < W && t < 64 ? 1ull << t : 0ull);
-                const int32_t qprev = lane == 0 ? -1 : L.q[lane - 1];
-                const int32_t width = ((need >> lane) & 1ull) ? max(q - qprev - 1, 0) : 0;
-                int32_t total;
-                const int32_t off = wave_excl_sum(width, total);
-                L.ioff[lane] = off;
-                if (lane == 63) L.ioff[64] = total;
-                wave_sync();
-                const bool mine = lane < W && t < 64;
-                o = mine ? L.q[t] : P;
-                const int32_t a0 = mine ? L.ioff[t] : 0, a1 = mine ? L.ioff[t + 1] : 0;
-                const int32_t pbase = mine ? (t == 0 ? 0 : L.q[t - 1] + 1) : 0;
-                bool found = !mine;
-                for (int32_t b3 = 0; b3 < total; b3 += 64) {
-                    const int32_t idx = b3 + lane;
-                    uint64_t mm = 0ull;
-                    if (idx < total) {
-                        int32_t lo = 0, hi = 63;   // largest k with ioff[k] <= idx
-                        while (lo < hi) {
-                            const int32_t mid = (lo + hi + 1) >> 1;
-                            if (L.ioff[mid] <= idx) lo = mid;
-                            else hi = mid - 1;
-                        }
-                        const int32_t pos = (lo == 0 ? 0 : L.q[lo - 1] + 1) + (idx - L.ioff[lo]);
-                        mm = index_lookup(index, smask, h(pos));
-                    }
-                    wave_sync();   // the previous chunk's masks have been read
-                    L.m[lane] = mm;
+        for (int32_t r = 0; r < nr; ++r) {
+            const int64_t i = i0 + r;
+            const int32_t P = Pr[r];
+            const uint64_t* __restrict__ hg = chains + c[r];
+            const uint64_t* ch = L.ch[r];
+            auto h = [&](int32_t x) -> uint64_t { return x < kStage ? ch[x] : hg[x]; };
+            int32_t o = 0;   // lane j: overlap on worker j
+
+            if (MODE == RK_PROBE_SCAN) {
+                uint64_t carry = all;
+                bool done = false;
+                for (int32_t base = 0; base < P && carry != 0ull; base += 64) {
+                    const int32_t n = min(64, P - base);
+                    const uint64_t m = lane < n ? index_lookup(index, smask, h(base + lane)) : 0ull;
+                    const uint64_t pa = wave_scan_and_u64(m) & carry;
+                    L.m[lane] = pa;
                     wave_sync();
-                    if (!found) {
-                        const int32_t lo = max(a0, b3), hi = min(a1, b3 + 64);
-                        if (lo < hi) {
-                            const int32_t x = first_clear(L.m, lo - b3, hi - b3, lane) + b3;
-                            if (x < hi) {
-                                o = pbase + (x - a0);
-                                found = true;
+                    if (lane < W && !done) {
+                        const int32_t f = first_clear(L.m, 0, n, lane);
+                        o += f;
+                        done = f < n;
+                    }
+                    carry = readlane64(pa, n - 1);
+                    wave_sync();
+                }
+            } else {
+                // ---- round 1: every worker's first miss lies in [0, U).  Sample
+                // positions sit on a power-of-two grid (clamped to the chain's end)
+                // so requests of one prefix group probe the same index slots.
+                int32_t U = P;
+                if (P > kRound1Min) {
+                    const int64_t st1 = (int64_t)next_pow2_dev((uint32_t)P) >> 4;
+                    const int32_t q1 = (int32_t)min((int64_t)(lane + 1) * st1, (int64_t)P) - 1;
+                    const uint64_t m = lane < 16 ? index_lookup(index, smask, h(q1)) : all;
+                    const uint64_t pa = wave_scan_and_u64(m & all);
+                    const uint64_t z = __ballot(lane < 16 && pa == 0ull);
+                    if (z) U = __builtin_amdgcn_readlane(q1, __ffsll((unsigned long long)z) - 1) + 1;
+                }
+                // ---- round 2: every position of [0, U) when U <= 64, else 64 samples
+                // on the power-of-two grid of step next_pow2(U) / 64, clamped to U - 1
+                const bool exact = U <= 64;
+                const int32_t nq = exact ? U : 64;
+                const int64_t st2 = (int64_t)next_pow2_dev((uint32_t)U) >> 6;
+                const int32_t q = round2_pos(lane, exact, st2, U);
+                const uint64_t m = lane < nq ? index_lookup(index, smask, h(q)) : 0ull;
+                L.m[lane] = wave_scan_and_u64(m & all);
+                wave_sync();
+                const int32_t t = lane < W ? first_clear(L.m, 0, nq, lane) : nq;
+                if (exact) {
+                    o = t;   // t == U only when U == P: every position is cached
+                } else {
+                    // ---- round 3: worker j's first miss is in (q[t-1], q[t]]; probe the inside
+                    const uint64_t need = wave_or_u64(lane < W && t < 64 ? 1ull << t : 0ull);
+                    const int32_t qprev = lane == 0 ? -1 : round2_pos(lane - 1, false, st2, U);
+                    const int32_t width = ((need >> lane) & 1ull) ? max(q - qprev - 1, 0) : 0;
+                    int32_t total;
+                    const int32_t off = wave_excl_sum_dpp(width, total);
+                    L.ioff[lane] = off;
+                    if (lane == 63) L.ioff[64] = total;
+                    wave_sync();
+                    const bool mine = lane < W && t < 64;
+                    o = mine ? round2_pos(t, false, st2, U) : P;
+                    const int32_t a0 = mine ? L.ioff[t] : 0, a1 = mine ? L.ioff[t + 1] : 0;
+                    const int32_t pbase = mine ? (t == 0 ? 0 : round2_pos(t - 1, false, st2, U) + 1) : 0;
+                    bool found = !mine;
+                    for (int32_t b3 = 0; b3 < total; b3 += 64) {
+                        const int32_t idx = b3 + lane;
+                        uint64_t mm = 0ull;
+                        if (idx < total) {
+                            int32_t lo = 0, hi = 63;   // largest k with ioff[k] <= idx
+                            while (lo < hi) {
+                                const int32_t mid = (lo + hi + 1) >> 1;
+                                if (L.ioff[mid] <= idx) lo = mid;
+                                else hi = mid - 1;
+                            }
+                            const int32_t pos = (lo == 0 ? 0 : round2_pos(lo - 1, false, st2, U) + 1) +
+                                                (idx - L.ioff[lo]);
+                            mm = index_lookup(index, smask, h(pos));
+                        }
+                        wave_sync();   // the previous chunk's masks have been read
+                        L.m[lane] = mm;
+                        wave_sync();
+                        if (!found) {
+                            const int32_t lo = max(a0, b3), hi = min(a1, b3 + 64);
+                            if (lo < hi) {
+                                const int32_t x = first_clear(L.m, lo - b3, hi - b3, lane) + b3;
+                                if (x < hi) {
+                                    o = pbase + (x - a0);
+                                    found = true;
+                                }
                             }
                         }
                     }
                 }
+                wave_sync();   // L.m and L.ioff are free for the next request
             }
-            wave_sync();
-        }
 
-        uint64_t best = ~0ull;
-        if (lane < W) {
-            const float c = route_cost(p.w_ov, p.w_act, p.w_sat, p.cap_blocks, P, o, A);
-            if (ov_out) ov_out[i * W + lane] = o;
-            if (cost_out) cost_out[i * W + lane] = c;
-            best = argmin_key(c, lane);
+            uint64_t best = ~0ull;
+            if (lane < W) {
+                const float cst = route_cost(p.w_ov, p.w_act, p.w_sat, p.cap_blocks, P, o, A);
+                if (ov_out) ov_out[i * W + lane] = o;
+                if (cost_out) cost_out[i * W + lane] = cst;
+                best = argmin_key(cst, lane);
+            }
+            best = wave_min_u64(best);
+            if (lane == 0 && am_out) am_out[i] = (int32_t)(uint32_t)(best & 0xffffffffu);
         }
-        best = wave_min_u64(best);
-        if (lane == 0 && am_out) am_out[i] = (int32_t)(uint32_t)(best & 0xffffffffu);
     }
 }
 
@@ -367,16 +366,16 @@ extern "C" int rk_route_score_index(int32_t B, int32_t W, const uint64_t* chains
     int32_t* st = status_word();
     if (!st) return fail(RK_EHIP, "rk_route_score_index: no status word");
     hipStream_t s = (hipStream_t)stream;
-    int64_t blocks = ((int64_t)B + IWAVES - 1) / IWAVES;
+    int64_t blocks = ((int64_t)B + kRPW - 1) / kRPW;
     if (blocks > 1 << 20) blocks = 1 << 20;
     blocks = (blocks + 7) / 8 * 8;
     const IndexSlot* t = (const IndexSlot*)index;
     if (probe_mode == RK_PROBE_SCAN)
-        hipLaunchKernelGGL(score_index_kernel<RK_PROBE_SCAN>, dim3((unsigned)blocks), dim3(64 * IWAVES), 0, s, B, W,
+        hipLaunchKernelGGL(score_index_kernel<RK_PROBE_SCAN>, dim3((unsigned)blocks), dim3(64), 0, s, B, W,
                            chains, chain_off, t, log2_slots, active_blocks, params, overlap_out, cost_out, argmin_out,
                            st);
     else
-        hipLaunchKernelGGL(score_index_kernel<RK_PROBE_PREFIX>, dim3((unsigned)blocks), dim3(64 * IWAVES), 0, s, B,
+        hipLaunchKernelGGL(score_index_kernel<RK_PROBE_PREFIX>, dim3((unsigned)blocks), dim3(64), 0, s, B,
                            W, chains, chain_off, t, log2_slots, active_blocks, params, overlap_out, cost_out,
                            argmin_out, st);
     return hip_check(hipGetLastError(), "rk_route_score_index launch");

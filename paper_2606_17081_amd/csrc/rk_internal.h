@@ -105,14 +105,91 @@ __device__ __forceinline__ uint64_t argmin_key(float c, int32_t j)
     return ((uint64_t)__float_as_uint(__fadd_rn(c, 0.0f)) << 32) | (uint32_t)j;
 }
 
+// ------------------------------------------------- wavefront primitives (DPP)
+// Cross-lane steps as DPP operand modifiers of ordinary VALU instructions
+// (GFX9-family controls), so a scan or reduction over the 64 lanes costs a few
+// dependent VALU operations instead of round trips through the LDS crossbar.
+constexpr int kDppQuadSwap1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kDppQuadSwap2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowMirror = 0x140, kDppRowHalfMirror = 0x141;
+constexpr int kDppRowBcast15 = 0x142;     // lane 15 of each row to the whole next row
+constexpr int kDppRowBcast31 = 0x143;     // lane 31 to rows 2 and 3
+
+// v moved by the DPP control CTRL into the rows of ROWS; lanes without a
+// source, and rows outside ROWS, receive old.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ uint32_t dpp32(uint32_t old, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWS, 0xF, false);
+}
+
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ uint64_t dpp64(uint64_t old, uint64_t v)
+{
+    const uint32_t lo = dpp32<CTRL, ROWS>((uint32_t)old, (uint32_t)v);
+    const uint32_t hi = dpp32<CTRL, ROWS>((uint32_t)(old >> 32), (uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Lane l's value of v (l uniform across the wavefront).
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix AND over the lanes (lane order): shifts within each row of
+// 16 lanes, then each row's total carried into the rows after it.  All lanes
+// must be active.
+__device__ __forceinline__ uint64_t wave_scan_and_u64(uint64_t v)
+{
+    const uint64_t id = ~0ull;
+    v &= dpp64<kDppRowShr1>(id, v);
+    v &= dpp64<kDppRowShr2>(id, v);
+    v &= dpp64<kDppRowShr4>(id, v);
+    v &= dpp64<kDppRowShr8>(id, v);
+    v &= dpp64<kDppRowBcast15, 0xA>(id, v);
+    v &= dpp64<kDppRowBcast31, 0xC>(id, v);
+    return v;
+}
+
+// Exclusive prefix sum over the lanes; total receives the sum of all lanes.
+// All lanes must be active.
+__device__ __forceinline__ int32_t wave_excl_sum_dpp(int32_t v, int32_t& total)
+{
+    uint32_t x = (uint32_t)v;
+    x += dpp32<kDppRowShr1>(0u, x);
+    x += dpp32<kDppRowShr2>(0u, x);
+    x += dpp32<kDppRowShr4>(0u, x);
+    x += dpp32<kDppRowShr8>(0u, x);
+    x += dpp32<kDppRowBcast15, 0xA>(0u, x);
+    x += dpp32<kDppRowBcast31, 0xC>(0u, x);
+    total = __builtin_amdgcn_readlane((int)x, 63);
+    return (int32_t)x - v;
+}
+
+// Minimum / OR of v over the lanes, the same value in every lane: a butterfly
+// within each row of 16 (pair swap, quad swap, half-row mirror, row mirror),
+// then the four row results.  All lanes must be active.
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        uint64_t o = __shfl_xor(v, off, 64);
-        v = o < v ? o : v;
-    }
-    return v;
+    auto mn = [](uint64_t a, uint64_t b) { return b < a ? b : a; };
+    v = mn(v, dpp64<kDppQuadSwap1>(v, v));
+    v = mn(v, dpp64<kDppQuadSwap2>(v, v));
+    v = mn(v, dpp64<kDppRowHalfMirror>(v, v));
+    v = mn(v, dpp64<kDppRowMirror>(v, v));
+    return mn(mn(readlane64(v, 0), readlane64(v, 16)), mn(readlane64(v, 32), readlane64(v, 48)));
+}
+
+__device__ __forceinline__ uint64_t wave_or_u64(uint64_t v)
+{
+    v |= dpp64<kDppQuadSwap1>(v, v);
+    v |= dpp64<kDppQuadSwap2>(v, v);
+    v |= dpp64<kDppRowHalfMirror>(v, v);
+    v |= dpp64<kDppRowMirror>(v, v);
+    return (readlane64(v, 0) | readlane64(v, 16)) | (readlane64(v, 32) | readlane64(v, 48));
 }
 
 // ------------------------------------------------- read-only table probes

@@ -11,41 +11,61 @@
 
 namespace rk {
 
-// First miss by a scan from block 0 (any table).
-__device__ __forceinline__ int32_t overlap_scan(const uint64_t* __restrict__ h, int32_t P,
-                                                const uint64_t* __restrict__ t, uint64_t mask)
-{
-    int32_t o = 0;
-    while (o < P && table_has(t, mask, h[o])) ++o;
-    return o;
-}
+constexpr int kWinSlots = 4;      // slots one lookup loads together
+constexpr int kStageS = 512;      // leading chain hashes staged in LDS
 
-// First miss by binary search; exact when membership along the chain is
-// monotone (a block is cached only together with its parent).
-__device__ __forceinline__ int32_t overlap_bsearch(const uint64_t* __restrict__ h, int32_t P,
-                                                   const uint64_t* __restrict__ t, uint64_t mask)
+// Membership of key in a table probed linearly from key & mask: the slots of
+// a window starting at the home slot are loaded together, so one round trip
+// settles a lookup unless every slot of the window holds another key.
+__device__ __forceinline__ bool table_has_win(const uint64_t* __restrict__ t, uint64_t mask, uint64_t key)
 {
-    int32_t lo = 0, hi = P;
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (table_has(t, mask, h[mid])) lo = mid + 1;
-        else hi = mid;
+    uint64_t s = key & mask;
+    for (uint64_t n = 0; n <= mask; n += kWinSlots) {
+        uint64_t k[kWinSlots];
+#pragma unroll
+        for (int x = 0; x < kWinSlots; ++x) k[x] = t[(s + x) & mask];
+#pragma unroll
+        for (int x = 0; x < kWinSlots; ++x) {
+            if (k[x] == key) return true;
+            if (k[x] == kEmpty) return false;
+        }
+        s = (s + kWinSlots) & mask;
     }
-    return lo;
+    return false;
 }
 
-template <int MODE>
-__global__ __launch_bounds__(256) void score_kernel(int32_t B, int32_t W, const uint64_t* __restrict__ chains,
-                                                    const int64_t* __restrict__ chain_off,
-                                                    const uint64_t* __restrict__ tables, int32_t log2_slots,
-                                                    const int32_t* __restrict__ active, rk_cost_params p,
-                                                    int32_t* __restrict__ ov_out, float* __restrict__ cost_out,
-                                                    int32_t* __restrict__ am_out, int32_t* status)
+// LDS writes of one wavefront made visible to the other lanes of that wavefront.
+__device__ __forceinline__ void score_wave_sync()
 {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One wavefront per request; lane j owns worker j (and j + 64, ... when W > 64).
+// PREFIX mode: the first miss by binary lifting -- with lo blocks known
+// cached, test block lo + step - 1 for step = 2^k, ..., 2, 1 and advance lo by
+// step on a hit.  Exact when membership along the chain is monotone (a block
+// is cached only with its parent).  The positions tested depend only on the
+// outcomes, not on the chain's length, so requests of one prefix group that
+// stop at the same block test the same table slots and share cache lines.
+// SCAN mode: blocks from 0 until the first miss (any tables).
+template <int MODE>
+__global__ __launch_bounds__(64) void score_kernel(int32_t B, int32_t W, const uint64_t* __restrict__ chains,
+                                                   const int64_t* __restrict__ chain_off,
+                                                   const uint64_t* __restrict__ tables, int32_t log2_slots,
+                                                   const int32_t* __restrict__ active, rk_cost_params p,
+                                                   int32_t* __restrict__ ov_out, float* __restrict__ cost_out,
+                                                   int32_t* __restrict__ am_out, int32_t* status)
+{
+    __shared__ uint64_t s_ch[kStageS];
     const int lane = threadIdx.x & 63;
-    const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x >> 6);
     const uint64_t mask = (1ull << log2_slots) - 1;
-    for (int64_t i = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); i < B; i += nwaves) {
+    // Workgroups are handed to the 8 XCDs round-robin; renumber them so each
+    // XCD walks one contiguous range of requests (gridDim.x is a multiple of 8).
+    const uint32_t nb8 = gridDim.x >> 3;
+    const uint32_t lb = (blockIdx.x & 7u) * nb8 + (blockIdx.x >> 3);
+    for (int64_t i = lb; i < B; i += gridDim.x) {
         const int64_t c0 = chain_off[i], c1 = chain_off[i + 1];
         int32_t P = 0;
         if (c1 < c0 || c1 - c0 > 0x7fffffff) {
@@ -53,11 +73,31 @@ __global__ __launch_bounds__(256) void score_kernel(int32_t B, int32_t W, const 
         } else {
             P = (int32_t)(c1 - c0);
         }
-        const uint64_t* h = chains + c0;
+        const uint64_t* __restrict__ hg = chains + c0;
+        score_wave_sync();   // the previous request's reads of s_ch are done
+        {
+            const int32_t n = min(P, kStageS);
+            uint64_t v[kStageS / 64];
+#pragma unroll
+            for (int k = 0; k < kStageS / 64; ++k) v[k] = lane + 64 * k < n ? hg[lane + 64 * k] : 0ull;
+#pragma unroll
+            for (int k = 0; k < kStageS / 64; ++k) s_ch[lane + 64 * k] = v[k];
+        }
+        score_wave_sync();
+        auto h = [&](int32_t x) -> uint64_t { return x < kStageS ? s_ch[x] : hg[x]; };
+        const int32_t top = P > 0 ? (int32_t)(1u << (31 - __clz(P))) : 0;
         uint64_t best = ~0ull;
         for (int32_t j = lane; j < W; j += 64) {
-            const uint64_t* t = tables + ((uint64_t)j << log2_slots);
-            const int32_t o = MODE == RK_PROBE_SCAN ? overlap_scan(h, P, t, mask) : overlap_bsearch(h, P, t, mask);
+            const uint64_t* __restrict__ t = tables + ((uint64_t)j << log2_slots);
+            int32_t o = 0;
+            if (MODE == RK_PROBE_SCAN) {
+                while (o < P && table_has_win(t, mask, h(o))) ++o;
+            } else {
+                for (int32_t step = top; step > 0; step >>= 1) {
+                    const int32_t pos = o + step - 1;
+                    if (pos < P && table_has_win(t, mask, h(pos))) o += step;
+                }
+            }
             const float c = route_cost(p.w_ov, p.w_act, p.w_sat, p.cap_blocks, P, o, active[j]);
             if (ov_out) ov_out[i * W + j] = o;
             if (cost_out) cost_out[i * W + j] = c;
@@ -91,14 +131,15 @@ extern "C" int rk_route_score_batch(int32_t B, int32_t W, const uint64_t* chains
     int32_t* st = status_word();
     if (!st) return fail(RK_EHIP, "rk_route_score_batch: no status word");
     hipStream_t s = (hipStream_t)stream;
-    int64_t blocks = ((int64_t)B + 3) / 4;
+    int64_t blocks = B;
     if (blocks > 1 << 20) blocks = 1 << 20;
+    blocks = (blocks + 7) / 8 * 8;
     if (probe_mode == RK_PROBE_SCAN)
-        hipLaunchKernelGGL(score_kernel<RK_PROBE_SCAN>, dim3((unsigned)blocks), dim3(256), 0, s, B, W, chains,
+        hipLaunchKernelGGL(score_kernel<RK_PROBE_SCAN>, dim3((unsigned)blocks), dim3(64), 0, s, B, W, chains,
                            chain_off, tables, log2_slots, active_blocks, params, overlap_out, cost_out,
                            argmin_out, st);
     else
-        hipLaunchKernelGGL(score_kernel<RK_PROBE_PREFIX>, dim3((unsigned)blocks), dim3(256), 0, s, B, W, chains,
+        hipLaunchKernelGGL(score_kernel<RK_PROBE_PREFIX>, dim3((unsigned)blocks), dim3(64), 0, s, B, W, chains,
                            chain_off, tables, log2_slots, active_blocks, params, overlap_out, cost_out,
                            argmin_out, st);
     return hip_check(hipGetLastError(), "rk_route_score_batch launch");
