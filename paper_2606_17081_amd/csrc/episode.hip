@@ -188,61 +188,65 @@ __device__ __forceinline__ void freq_touch(uint32_t* fk, bool inserted, uint32_t
     }
 }
 
-constexpr int kWin = 4;    // slots read by one lookup (a run of this length is rare at load <= 0.5)
+constexpr int kWin = 4;    // slots of a group: one lookup reads one aligned group (64 bytes)
 
-// A key's probe walk starts at the first slot of its aligned group of kWin
-// slots (64 bytes), so a lookup's window is one aligned group.
+// A key's walk starts at the first slot of its aligned group of kWin slots and
+// goes group by group; within every group it visits the slots in its own
+// rotated order, from slot slot_pref(h) (hash bits independent of the group
+// index) on, so concurrent claims in one group rarely aim at the same slot.
+// An insert takes the first empty slot of that walk, and slots only fill
+// between compactions, so a lookup walking the same order meets the key
+// before any empty slot.  Callers load a group in the key's order: element r
+// of a loaded group is slot group_slot(h, r).
 __device__ __forceinline__ uint64_t home_slot(uint64_t h, uint64_t smask)
 {
     return h & smask & ~(uint64_t)(kWin - 1);
 }
 
-// Membership test finishing a walk whose first kWin slots (from s) are loaded.
-__device__ __forceinline__ bool finish_lookup(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
-                                              const uint64_t* k, const uint32_t* st)
+__device__ __forceinline__ uint32_t slot_pref(uint64_t h) { return (uint32_t)(h >> 62) & (uint32_t)(kWin - 1); }
+
+// Offset within its group of the r-th slot of h's order.
+__device__ __forceinline__ uint32_t group_slot(uint64_t h, int r)
 {
-#pragma unroll
-    for (int i = 0; i < kWin; ++i) {
-        if (k[i] == kEmpty) return false;
-        if (k[i] == h && st[i] != kTomb) return true;
-    }
-    s = (s + kWin) & smask;
-    for (uint64_t n = kWin; n <= smask; ++n) {
-        uint64_t kk;
-        uint32_t ss;
-        load_slot(t + s, kk, ss);
-        if (kk == kEmpty) return false;
-        if (kk == h && ss != kTomb) return true;
-        s = (s + 1) & smask;
-    }
-    return false;
+    return (slot_pref(h) + (uint32_t)r) & (uint32_t)(kWin - 1);
 }
 
-// finish_lookup that also returns the live slot's stamp.
+// Membership test finishing a walk whose first group (from s, in h's order) is
+// loaded; stamp receives the live slot's stamp.
 __device__ __forceinline__ bool finish_lookup_stamp(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
                                                     const uint64_t* k, const uint32_t* st, uint32_t& stamp)
 {
 #pragma unroll
-    for (int i = 0; i < kWin; ++i) {
-        if (k[i] == kEmpty) return false;
-        if (k[i] == h && st[i] != kTomb) {
-            stamp = st[i];
+    for (int r = 0; r < kWin; ++r) {
+        if (k[r] == kEmpty) return false;
+        if (k[r] == h && st[r] != kTomb) {
+            stamp = st[r];
             return true;
         }
     }
-    s = (s + kWin) & smask;
-    for (uint64_t n = kWin; n <= smask; ++n) {
-        uint64_t kk;
-        uint32_t ss;
-        load_slot(t + s, kk, ss);
-        if (kk == kEmpty) return false;
-        if (kk == h && ss != kTomb) {
-            stamp = ss;
-            return true;
+    // further groups one slot at a time (rare: a full first group)
+    for (uint64_t n = kWin; n <= smask; n += kWin) {
+        s = (s + kWin) & smask;
+#pragma unroll 1
+        for (int r = 0; r < kWin; ++r) {
+            uint64_t kk;
+            uint32_t ss;
+            load_slot(t + s + group_slot(h, r), kk, ss);
+            if (kk == kEmpty) return false;
+            if (kk == h && ss != kTomb) {
+                stamp = ss;
+                return true;
+            }
         }
-        s = (s + 1) & smask;
     }
     return false;
+}
+
+__device__ __forceinline__ bool finish_lookup(const Slot* t, uint64_t smask, uint64_t h, uint64_t s,
+                                              const uint64_t* k, const uint32_t* st)
+{
+    uint32_t stamp;
+    return finish_lookup_stamp(t, smask, h, s, k, st, stamp);
 }
 
 constexpr int32_t kFullProbe = 64;   // intervals this wide are probed position by position
@@ -307,7 +311,7 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t jfirst
                 hk[jj] = s_chain[q[jj]];
                 sh0[jj] = home_slot(hk[jj], smask);
 #pragma unroll
-                for (int i = 0; i < kWin; ++i) load_slot(t + ((sh0[jj] + i) & smask), kw[jj][i], sw[jj][i]);
+                for (int i = 0; i < kWin; ++i) load_slot(t + sh0[jj] + group_slot(hk[jj], i), kw[jj][i], sw[jj][i]);
             }
         }
 #pragma unroll
@@ -349,40 +353,47 @@ __device__ void wave_overlaps(const uint64_t* s_chain, int32_t P, int32_t jfirst
     }
 }
 
-// Find the live slot of h, or claim an empty slot for it.  Concurrent callers
-// insert distinct keys; a failed claim moves on along the probe sequence.
+// Find the live slot of h, or claim the first empty slot of its walk.
+// Concurrent callers may insert the same key: they walk the same order, so
+// the loser of a claim finds the key in that slot; a slot taken by another key
+// sends the walk to the next slot of the order.
 __device__ __forceinline__ uint64_t insert_or_touch(Slot* __restrict__ t, uint64_t smask, uint64_t h, int& inserted,
                                                    int32_t* status)
 {
     inserted = 0;
-    uint64_t s = home_slot(h, smask);
-    for (uint64_t n = 0; n <= smask; ++n) {
-        const uint64_t k = __hip_atomic_load(&t[s].key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        const uint32_t st = t[s].stamp;
-        if (k == h) {
-            if (st != kTomb) return s;
-        } else if (k == kEmpty) {
-            uint64_t prev = kEmpty;
-            if (__hip_atomic_compare_exchange_strong(&t[s].key, &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_WORKGROUP)) {
-                inserted = 1;
-                return s;
+    uint64_t g = home_slot(h, smask);
+    for (uint64_t n = 0; n <= smask; n += kWin) {
+#pragma unroll 1
+        for (int r = 0; r < kWin; ++r) {
+            const uint64_t sl = g + group_slot(h, r);
+            const uint64_t k = __hip_atomic_load(&t[sl].key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            const uint32_t st = t[sl].stamp;
+            if (k == h) {
+                if (st != kTomb) return sl;
+            } else if (k == kEmpty) {
+                uint64_t prev = kEmpty;
+                if (__hip_atomic_compare_exchange_strong(&t[sl].key, &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                    inserted = 1;
+                    return sl;
+                }
+                if (prev == h) return sl;    // a concurrent insert of h claimed it first
             }
-            if (prev == h) return s;
         }
-        s = (s + 1) & smask;
+        g = (g + kWin) & smask;
     }
     atomicOr(status, RK_DEV_TABLE_FULL);
     return ~0ull;
 }
 
 // Same result as insert_or_touch, in one memory round trip in the usual
-// case.  A block the overlap search found cached is looked up in a window of
-// kWin slots.  For a block past the overlap, the claim of its home slot is
-// issued together with the loads of the next kWin-1 slots: slots never return
-// to empty between compactions, so an empty home slot proves the key absent,
-// and an occupied one usually leaves a free slot in the window.  Anything else
-// falls back to the full walk.
+// case.  A block the overlap search found cached is looked up in its group.
+// For a block past the overlap, the claim of the first slot of its order is
+// issued together with the loads of the group's other slots: an empty first
+// slot proves the key absent (slots never return to empty between
+// compactions, and an insert of the key would have taken it), and an occupied
+// one usually leaves a free slot further along the group.  Anything else falls
+// back to the full walk.
 __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t smask, uint64_t h, bool cached_hint,
                                                  int& inserted, int32_t* status)
 {
@@ -392,29 +403,30 @@ __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t 
     uint32_t st[kWin];
     if (cached_hint) {
 #pragma unroll
-        for (int i = 0; i < kWin; ++i) load_slot(t + ((s + i) & smask), k[i], st[i]);
+        for (int r = 0; r < kWin; ++r) load_slot(t + s + group_slot(h, r), k[r], st[r]);
 #pragma unroll
-        for (int i = 0; i < kWin; ++i)
-            if (k[i] == h && st[i] != kTomb) return (s + i) & smask;
+        for (int r = 0; r < kWin; ++r)
+            if (k[r] == h && st[r] != kTomb) return s + group_slot(h, r);
     } else {
         uint64_t prev = kEmpty;
-        const bool won = __hip_atomic_compare_exchange_strong(&t[s].key, &prev, h, __ATOMIC_RELAXED,
+        const uint64_t s0 = s + group_slot(h, 0);
+        const bool won = __hip_atomic_compare_exchange_strong(&t[s0].key, &prev, h, __ATOMIC_RELAXED,
                                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 #pragma unroll
-        for (int i = 1; i < kWin; ++i) load_slot(t + ((s + i) & smask), k[i], st[i]);
+        for (int r = 1; r < kWin; ++r) load_slot(t + s + group_slot(h, r), k[r], st[r]);
         if (won) {
             inserted = 1;
-            return s;
+            return s0;
         }
-        if (prev != h) {           // home holds another key: look further in the window
+        if (prev != h) {           // the first slot holds another key: look further along the group
 #pragma unroll
-            for (int i = 1; i < kWin; ++i) {
-                const uint64_t si = (s + i) & smask;
-                if (k[i] == h) {
-                    if (st[i] != kTomb) return si;
+            for (int r = 1; r < kWin; ++r) {
+                const uint64_t si = s + group_slot(h, r);
+                if (k[r] == h) {
+                    if (st[r] != kTomb) return si;
                     continue;
                 }
-                if (k[i] != kEmpty) continue;
+                if (k[r] != kEmpty) continue;
                 uint64_t pi = kEmpty;
                 if (__hip_atomic_compare_exchange_strong(&t[si].key, &pi, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_WORKGROUP)) {
@@ -523,7 +535,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
                 if (lo[u] < hi[u]) {
                     const uint64_t s0 = home_slot(hk[u], smask);
 #pragma unroll
-                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + ((s0 + x) & smask), kw[u][x], sw[u][x]);
+                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + s0 + group_slot(hk[u], x), kw[u][x], sw[u][x]);
                 }
             }
 #pragma unroll
@@ -593,7 +605,7 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
                 if (lo[u] < hi[u]) {
                     const uint64_t s0 = home_slot(hk[u], smask);
 #pragma unroll
-                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + ((s0 + x) & smask), kw[u][x], sw[u][x]);
+                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + s0 + group_slot(hk[u], x), kw[u][x], sw[u][x]);
                 }
             }
 #pragma unroll
@@ -655,6 +667,24 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     b.t12 = take(tiers ? nb * w * 2 : 0, 4);
     b.bytes = (o + 15) / 16 * 16;
     return b;
+}
+
+// Empty worker tables for every episode of a launch, run before the episode
+// kernel: one grid over all of them moves the bytes at the chip's store rate,
+// where each episode clearing its own tables left the start of the episode
+// kernel bound by the uneven share of workgroups per CU.  Block x clears
+// chunk x % cpe (kClearChunk 16-byte slots) of episode x / cpe.
+constexpr uint32_t kClearChunk = 4096;
+
+__global__ __launch_bounds__(256) void episode_clear_kernel(unsigned char* __restrict__ ws, size_t per_episode,
+                                                          size_t off_slots, uint64_t n16, uint32_t cpe)
+{
+    const uint64_t e = blockIdx.x / cpe;
+    const uint64_t k0 = (uint64_t)(blockIdx.x % cpe) * kClearChunk;
+    const uint64_t k1 = min(k0 + kClearChunk, n16);
+    uint4* z = reinterpret_cast<uint4*>(ws + e * per_episode + off_slots);
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    for (uint64_t k = k0 + threadIdx.x; k < k1; k += 256) z[k] = zero;
 }
 
 // Two waves per SIMD: two episodes share a CU (the sweep has more episodes than CUs).
@@ -768,12 +798,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     const uint64_t used_limit = S - S / 4;
     const uint64_t scratch_cap = (uint64_t)a.cache + (uint64_t)a.max_blocks;
 
-    // ---- initial state: empty caches, idle workers, every first turn queued
-    {
-        uint4* z = reinterpret_cast<uint4*>(g_slots);
-        const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-        for (uint64_t i = tid; i < (uint64_t)W * S; i += NT) z[i] = zero;
-    }
+    // ---- initial state: empty caches (cleared by episode_clear_kernel before this launch), idle
+    //      workers, every first turn queued
     if (tid < W) {
         s_A[tid] = 0;
         s_N[tid] = 0;
@@ -905,7 +931,11 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 int32_t tot = 0, st0 = 0, pr = 0;
                 if (lane < nr) {
                     const int32_t bl = c + lane;
-                    st0 = s_stamped[r_sig[bl]] ? 0 : r_otab[bl];
+                    // a worker without kept recency gets the blocks past the route's overlap, which
+                    // counts the common prefixes with the batch's earlier routes on that worker:
+                    // those routes' writers insert them (and so on back to blocks in the table)
+                    const int32_t sgl = r_sig[bl];
+                    st0 = s_stamped[sgl] ? 0 : o_cur[bl * W + sgl];
                     pr = r_P[bl] - st0;
                 }
                 const int32_t off = ep_wave_excl_sum(pr, tot);
@@ -1812,6 +1842,15 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.NB = NB;
     const size_t lds = o + batch_layout(NB, b->W, tiers).bytes;
     hipStream_t s = (hipStream_t)stream;
+    const uint64_t n16 = (uint64_t)b->W * L.slots;          // 16-byte slots per episode
+    const uint64_t cpe = (n16 + kClearChunk - 1) / kClearChunk;
+    if (cpe * (uint64_t)b->E > 0x7fffffffull)
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %d episodes of %llu table slots exceed one clear launch",
+                    b->E, (unsigned long long)n16);
+    hipLaunchKernelGGL(episode_clear_kernel, dim3((unsigned)(cpe * (uint64_t)b->E)), dim3(256), 0, s,
+                       (unsigned char*)workspace, L.per_episode, L.off_slots, n16, (uint32_t)cpe);
+    int rc = hip_check(hipGetLastError(), "rk_simulate_episodes clear launch");
+    if (rc) return rc;
     hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), lds, s, a);
     return hip_check(hipGetLastError(), "rk_simulate_episodes launch");
 }
