@@ -77,7 +77,7 @@ constexpr int NW = NT / 64;
 constexpr int kMaxBatch = 64;       // routes per batch (at most one wavefront of lanes)
 constexpr int32_t kMoreTurns = 0x40000000;   // flag on an in-flight conversation index: it has a next turn
 
-enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2, EV_EPOCH = 3 };
+enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2, EV_EPOCH = 3, EV_ROOM = 4 };
 
 struct EpArgs {
     int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB, tiers,
@@ -461,27 +461,6 @@ static __device__ __forceinline__ uint32_t ep_wave_min_u32(uint32_t v)
     const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
     const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
     return min(min(r0, r1), min(r2, r3));
-}
-
-static __device__ __forceinline__ int32_t ep_wave_sum(int32_t v)
-{
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
-
-// Exclusive prefix sum across the wavefront; total receives the full sum.
-static __device__ __forceinline__ int32_t ep_wave_excl_sum(int32_t v, int32_t& total)
-{
-    const int lane = threadIdx.x & 63;
-    int32_t x = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int32_t o = __shfl_up(x, off, 64);
-        if (lane >= off) x += o;
-    }
-    total = __shfl(x, 63, 64);
-    return x - v;
 }
 
 constexpr int KI = 4;   // searches a thread keeps in flight together
@@ -938,7 +917,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     st0 = s_stamped[sgl] ? 0 : o_cur[bl * W + sgl];
                     pr = r_P[bl] - st0;
                 }
-                const int32_t off = ep_wave_excl_sum(pr, tot);
+                const int32_t off = wave_excl_sum_dpp(pr, tot);
                 if (lane < nr) {
                     woff[lane] = off;
                     wst[lane] = st0;
@@ -1270,6 +1249,10 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
 
     // state of the routing sequence, kept by wavefront 0
     int32_t t = 0, s = 0, r_in_step = 0, n_step = 0;
+    int32_t s_slot = 0;                            // s % H
+    int32_t c_pos = 0;                             // t % ctrl_window (load controller)
+    int32_t room_b = -1;                           // route last stopped for a compaction
+    const float inv_cap = (prm.cap_blocks & (prm.cap_blocks - 1)) == 0 ? 1.0f / (float)prm.cap_blocks : 0.0f;
     bool step_open = false, prev_active = false;
     int64_t tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t u_sum = 0, u_tot = 0;
@@ -1282,7 +1265,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         const int32_t tb0 = sh.tdone;        // routes decided before this batch
         int32_t nb = min(NB, sh.qsize);
         for (int32_t b = tid; b < nb; b += NT) {
-            const int32_t c = g_queue[(qh0 + b) % qcap];
+            const int32_t c = g_queue[qh0 + b >= qcap ? qh0 + b - qcap : qh0 + b];
             const int32_t k = g_next[c];
             const int64_t g = gc0 + c;
             const int64_t tb0 = a.turn_off[g], tb1 = a.turn_off[g + 1];
@@ -1309,46 +1292,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             r_rnd[2 * b + 1] = draws ? a.route_rand[2 * row + 1] : 0u;
         }
         __syncthreads();
-        // workers without room for every block of the batch are compacted first; the batch is cut to
-        // what the tightest worker can take (at least one request always fits after compaction)
-        if (wave == 0) {
-            // wavefront 0: lane b holds request b's blocks, lane j tests worker j
-            int32_t Ttot;
-            ep_wave_excl_sum(lane < nb ? r_P[lane] : 0, Ttot);
-            const uint64_t T = (uint64_t)Ttot;
-            const bool full = lane < W && s_stamped[lane] &&
-                              ((uint64_t)s_used[lane] + T > used_limit ||
-                               (uint64_t)(s_tail[lane] - s_head[lane]) + T > R ||
-                               (uint64_t)s_tail[lane] + T > 0x40000000u);
-            const unsigned long long m = __ballot(full);
-            if (lane == 0) sh.rb_mask = m;
-        }
-        __syncthreads();
-        for (unsigned long long m = sh.rb_mask; m; m &= m - 1ull) rebuild(__ffsll(m) - 1);
-        if (wave == 0) {
-            // the tightest worker's room, then the longest run of requests that fits it
-            int64_t mj = INT64_MAX;
-            if (lane < W) {
-                mj = (int64_t)used_limit - (int64_t)s_used[lane];
-                if (s_stamped[lane]) {   // a worker without kept recency writes no log records
-                    mj = min(mj, (int64_t)R - (int64_t)(s_tail[lane] - s_head[lane]));
-                    mj = min(mj, (int64_t)0x40000000 - (int64_t)s_tail[lane]);
-                }
-            }
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) mj = min(mj, (int64_t)__shfl_xor(mj, off, 64));
-            int32_t Ttot;
-            const int32_t pb = lane < nb ? r_P[lane] : 0;
-            const int64_t incl = (int64_t)ep_wave_excl_sum(pb, Ttot) + pb;
-            int32_t n2 = __popcll(__ballot(lane < nb && incl <= mj));
-            if (lane == 0) {
-                if (n2 == 0 && nb > 0) {
-                    atomicOr(a.status, RK_DEV_TABLE_FULL);
-                    n2 = 1;
-                }
-                sh.nb = n2;
-            }
-        }
+        // room in a worker's table and log is checked route by route when the route is decided
+        if (tid == 0) sh.nb = nb;
         if (tid == 0) {
             sh.decided = 0;
             sh.claimed = 0;
@@ -1395,6 +1340,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 int32_t rA = 0, rlive = 0, rused = 0, rN = 0;
                 uint32_t rtail = 0;
                 int32_t run_ep = -1;   // decay epoch of the routes decided since the last sync
+                int32_t q_head = sh.qhead, q_size = sh.qsize;   // the ready queue, kept in registers
                 if (lane < W) {
                     rA = s_A[lane];
                     rN = s_N[lane];
@@ -1402,10 +1348,12 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     rlive = s_live[lane];
                     rused = s_used[lane];
                 }
+                // workers that keep recency (write log records)
+                const unsigned long long stamped_mask = __ballot(lane < W && s_stamped[lane] != 0);
                 for (;;) {
                     if (!step_open) {
                         // release the routes of step s - H; queue their conversations' next turns
-                        const int32_t slot = s % H, sb = slot * rps;
+                        const int32_t slot = s_slot, sb = slot * rps;
                         if (s >= H) {
                             if (lane < W) {
                                 s_A[lane] = rA;
@@ -1413,7 +1361,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                             }
                             ep_wave_sync();
                             const int32_t nprev = s_stepn[slot];
-                            const int32_t qtail = sh.qhead + sh.qsize;
+                            const int32_t qtail = q_head + q_size;
                             int32_t pushed = 0, rel = 0;
                             for (int32_t base = 0; base < nprev; base += 64) {
                                 const int32_t r = base + lane;
@@ -1428,12 +1376,15 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                                     atomicSub(&s_N[s_stw[sb + r]], 1);
                                 }
                                 const unsigned long long mb = __ballot(more);
-                                if (more) g_queue[(qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull))) % qcap] = c;
+                                if (more) {
+                                    int32_t qi = qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull));
+                                    g_queue[qi >= qcap ? qi - qcap : qi] = c;
+                                }
                                 pushed += __popcll(mb);
                             }
-                            u_tot -= ep_wave_sum(rel);
+                            u_tot -= wave_sum_i32(rel);
                             ep_wave_sync();
-                            if (lane == 0) sh.qsize += pushed;
+                            q_size += pushed;
                             if (lane < W) {
                                 rA = s_A[lane];
                                 rN = s_N[lane];
@@ -1441,8 +1392,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                             ep_wave_sync();
                         }
                         int32_t inflight = 0;
-                        for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[(s - k) % H];
-                        const int32_t qs = sh.qsize;
+                        for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[s_slot >= k ? s_slot - k : s_slot - k + H];
+                        const int32_t qs = q_size;
                         if (qs == 0 && inflight == 0) {
                             event = EV_DONE;
                             break;
@@ -1456,12 +1407,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     }
                     if (r_in_step >= n_step) {
                         ++s;
+                        s_slot = s_slot + 1 == H ? 0 : s_slot + 1;
                         step_open = false;
                         continue;
                     }
                     const int32_t b = t - t0;
                     if (b >= nb) break;
-                    if (freq) {
+                    if (__builtin_expect(freq, 0)) {
                         // a new decay epoch waits until the earlier epoch's cache writes are in
                         const int32_t ep = s / dsteps;
                         if (run_ep >= 0 && ep != run_ep) {
@@ -1471,25 +1423,19 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         run_ep = ep;
                     }
                     // one route: controller, cost of every worker, argmin
-                    const int32_t slot = s % H, sb = slot * rps;
+                    const int32_t slot = s_slot, sb = slot * rps;
                     bool active = false;
-                    if (prm.controller == 1 && t >= prm.ctrl_window)
+                    if (__builtin_expect(prm.controller == 1 && t >= prm.ctrl_window, 0))
                         active = (int64_t)prm.ctrl_den * u_sum >
                                  (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
                     float w = prm.w_ov;
-                    if (active) {
-                        w = fminf(prm.w_ov, prm.ctrl_w_ov);
-                        tot[3] += 1;
-                        if (!prev_active) tot[4] += 1;
-                    }
-                    prev_active = active;
+                    if (active) w = fminf(prm.w_ov, prm.ctrl_w_ov);
                     int32_t pol = policy;
                     float tau_r = tau;
-                    if (regime_ctl) {
+                    if (__builtin_expect(regime_ctl, 0)) {
                         w = rg.w_ov[rg_r];
                         tau_r = rg.tau[rg_r];
                         pol = tau_r > 0.0f ? RK_POLICY_SOFTMAX : RK_POLICY_ARGMIN;
-                        if (rg_r > 0) tot[3] += 1;
                     }
                     const int32_t P = r_P[b];
                     const int64_t row = prm.out_base + (int64_t)t;
@@ -1498,7 +1444,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     float cj = 0.0f;
                     if (lane < W) {
                         oj = o_cur[b * W + lane];
-                        if (tiers) {
+                        if (__builtin_expect(tiers, 0)) {
                             const int32_t o1 = t1_tab[b * W + lane], o12 = t12_tab[b * W + lane];
                             cj = route_cost_tiers(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, o1, o12,
                                                   prm.tier_w, rA);
@@ -1507,13 +1453,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                                 a.out.tier_overlap[(row * W + lane) * 2 + 1] = o12;
                             }
                         } else {
-                            cj = route_cost(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, rA);
+                            cj = route_cost_ep(w, prm.w_act, prm.w_sat, prm.cap_blocks, inv_cap, P, oj, rA);
                         }
                         if (a.out.cost) a.out.cost[row * W + lane] = cj;
                         bits = __float_as_uint(__fadd_rn(cj, 0.0f));
                     }
                     int32_t sg;
-                    if (pol == RK_POLICY_ARGMIN) {
+                    if (__builtin_expect(pol == RK_POLICY_ARGMIN, 1)) {
                         const uint32_t mn = ep_wave_min_u32(bits);
                         sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
                     } else if (pol == RK_POLICY_SOFTMAX) {
@@ -1552,6 +1498,32 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + (scan ? 0 : P - osg);
                     const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
                     const bool flush = scan || tiers || live_after > a.cache;
+                    // a worker that keeps recency needs log records for the route's P touches and slots
+                    // for its new blocks: without room, stop before the route and compact that worker
+                    // (the cached sets and loads stay as they are, so the route is decided again alike)
+                    if (__builtin_expect((stamped_mask >> sg) & 1ull, 0)) {
+                        const uint32_t head = s_head[sg];
+                        const uint64_t add = scan ? (uint64_t)P : (uint64_t)(P - osg);
+                        if ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(rused, sg) + add > used_limit ||
+                            (uint64_t)(base - head) + (uint64_t)P > R || (uint64_t)base + (uint64_t)P > 0x40000000u) {
+                            if (room_b == t) {
+                                // still no room right after a compaction (the workspace layout always
+                                // leaves room for one route): report it and go on
+                                if (lane == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
+                            } else {
+                                room_b = t;
+                                if (lane == 0) sh.ev_b = sg;
+                                event = EV_ROOM;
+                                break;
+                            }
+                        }
+                    }
+                    if (active) {
+                        tot[3] += 1;
+                        if (!prev_active) tot[4] += 1;
+                    }
+                    prev_active = active;
+                    if (regime_ctl && rg_r > 0) tot[3] += 1;
                     const int32_t rc = r_c[b];
                     if (lane == sg) {
                         rA += P;
@@ -1573,8 +1545,6 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         s_stP[sb + r_in_step] = P;
                         s_stc[sb + r_in_step] = rc;
                         g_next[rc & ~kMoreTurns] = r_k[b] + 1;
-                        sh.qhead = (sh.qhead + 1) % qcap;
-                        sh.qsize -= 1;
                         r_step[b] = (int32_t)s;
                         r_reg[b] = regime_ctl ? rg_r : 0;
                         r_evc[b] = 0;
@@ -1585,7 +1555,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         }
                     }
                     u_tot += P;
-                    if (regime_ctl) {
+                    q_head = q_head + 1 == qcap ? 0 : q_head + 1;
+                    q_size -= 1;
+                    if (__builtin_expect(regime_ctl, 0)) {
                         // the chosen worker's latency with the new request (already counted in
                         // lane sg's rN) stands in for TTFT (fp64)
                         const int32_t n_sg = __builtin_amdgcn_readlane(rN, sg);
@@ -1622,8 +1594,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                             }
                         }
                     }
-                    if (prm.controller == 1) {
-                        const int32_t pos = t % prm.ctrl_window;
+                    if (__builtin_expect(prm.controller == 1, 0)) {
+                        const int32_t pos = c_pos;
+                        c_pos = c_pos + 1 == prm.ctrl_window ? 0 : c_pos + 1;
                         if (t >= prm.ctrl_window) u_sum -= s_u[pos];
                         ep_wave_sync();
                         if (lane == 0) s_u[pos] = u_tot;
@@ -1645,7 +1618,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     ep_wave_sync();
                     if (lane == 0)
                         __hip_atomic_store(&sh.decided, b + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-                    if (flush) {
+                    if (__builtin_expect(flush, 0)) {
                         event = EV_FLUSH;
                         break;
                     }
@@ -1658,6 +1631,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     s_used[lane] = rused;
                 }
                 if (lane == 0) {
+                    sh.qhead = q_head;
+                    sh.qsize = q_size;
                     sh.event = event;
                     sh.tdone = t;
                     __hip_atomic_store(&sh.stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -1667,6 +1642,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             }
             __syncthreads();
             event = sh.event;
+            if (event == EV_ROOM) {
+                // every decided route's writes are in: compact the route's worker, then decide on
+                rebuild(sh.ev_b);
+                if (tid == 0) sh.stop = 0;
+                __syncthreads();
+                continue;
+            }
             if (event == EV_EPOCH) {
                 if (tid == 0) sh.stop = 0;
                 __syncthreads();

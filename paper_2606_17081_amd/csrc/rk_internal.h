@@ -192,6 +192,35 @@ __device__ __forceinline__ uint64_t wave_or_u64(uint64_t v)
     return (readlane64(v, 0) | readlane64(v, 16)) | (readlane64(v, 32) | readlane64(v, 48));
 }
 
+// route_cost for the episodes, where A + P stays far below 2^31 (blocks in
+// flight), so the sum converts from 32 bits; a power-of-two cap divides by the
+// exact multiplication with its reciprocal inv_cap (the same correctly
+// rounded quotient), and inv_cap = 0 selects the division.
+__device__ __forceinline__ float route_cost_ep(float w_ov, float w_act, float w_sat, int32_t cap, float inv_cap,
+                                               int32_t P, int32_t o, int32_t A)
+{
+    float t1 = __fmul_rn(w_ov, (float)(P - o));
+    float t2 = __fmul_rn(w_act, (float)A);
+    const float L = (float)(A + P);
+    float r = inv_cap != 0.0f ? __fmul_rn(L, inv_cap) : __fdiv_rn(L, (float)cap);
+    float x = fmaxf(__fsub_rn(r, 1.0f), 0.0f);
+    float t3 = __fmul_rn(w_sat, __fmul_rn(x, x));
+    return __fadd_rn(__fadd_rn(t1, t2), t3);
+}
+
+// Sum of v over the lanes, the same value in every lane (DPP butterfly within
+// each row of 16, then the four row sums).  All lanes must be active.
+__device__ __forceinline__ int32_t wave_sum_i32(int32_t v)
+{
+    uint32_t x = (uint32_t)v;
+    x += dpp32<kDppQuadSwap1>(x, x);
+    x += dpp32<kDppQuadSwap2>(x, x);
+    x += dpp32<kDppRowHalfMirror>(x, x);
+    x += dpp32<kDppRowMirror>(x, x);
+    return (int32_t)(((uint32_t)__builtin_amdgcn_readlane((int)x, 0) + (uint32_t)__builtin_amdgcn_readlane((int)x, 16)) +
+                     ((uint32_t)__builtin_amdgcn_readlane((int)x, 32) + (uint32_t)__builtin_amdgcn_readlane((int)x, 48)));
+}
+
 // ------------------------------------------------- read-only table probes
 // Open addressing, home slot key & mask, linear probing; 0 is empty.
 __device__ __forceinline__ bool table_has(const uint64_t* __restrict__ t, uint64_t mask, uint64_t key)
