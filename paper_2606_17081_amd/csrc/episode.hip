@@ -1210,6 +1210,43 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         __syncthreads();
     };
 
+    // overlaps of batch routes b in [b_lo, nb) on worker j after j evicted (prefix mode): the
+    // caches stay prefix-closed, so an eviction can only cut a suffix off a route's cached prefix,
+    // and with every decided route's writes in, the table holds exactly o_cur[b][j] leading blocks
+    // before it.  One lookup of the last of them decides the usual case; otherwise a binary search
+    // within it finds the first block no longer live.
+    auto research = [&](int32_t b_lo, int32_t nb, int32_t j) {
+        const Slot* tj = g_slots + (uint64_t)j * S;
+        for (int32_t b = b_lo + tid; b < nb; b += NT) {
+            int32_t hi = o_cur[b * W + j];
+            if (hi > 0) {
+                const uint64_t* ch = a.chains + r_cb[b];
+                auto live = [&](int32_t k) {
+                    const uint64_t h = ch[k];
+                    const uint64_t s0 = home_slot(h, smask);
+                    uint64_t kw[kWin];
+                    uint32_t sw[kWin];
+#pragma unroll
+                    for (int x = 0; x < kWin; ++x) load_slot(tj + s0 + group_slot(h, x), kw[x], sw[x]);
+                    return finish_lookup(tj, smask, h, s0, kw, sw);
+                };
+                if (!live(hi - 1)) {
+                    int32_t lo = 0;
+                    --hi;
+                    while (lo < hi) {
+                        const int32_t mid = (lo + hi) >> 1;
+                        if (live(mid)) lo = mid + 1;
+                        else hi = mid;
+                    }
+                    hi = lo;
+                }
+            }
+            o_tab[b * W + j] = hi;
+            o_cur[b * W + j] = hi;
+        }
+        __syncthreads();
+    };
+
     // tier overlaps of batch routes b in [b_lo, nb) on worker j (j < 0: every worker): o12 within
     // the cached prefix o_tab, then o1 within o12
     auto tier_search = [&](int32_t b_lo, int32_t nb, int32_t j) {
@@ -1697,7 +1734,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 }
                 __syncthreads();
             }
-            search(b + 1, nb, sg);
+            if (!scan && !tiers) research(b + 1, nb, sg);
+            else search(b + 1, nb, sg);
             if (tiers) tier_search(b + 1, nb, sg);
             if (tid == 0) {
                 r_evc[sh.ev_b] = sh.ev;
