@@ -464,6 +464,7 @@ static __device__ __forceinline__ uint32_t ep_wave_min_u32(uint32_t v)
 }
 
 constexpr int KI = 4;   // searches a thread keeps in flight together
+constexpr int KP = 4;   // batch pairs a thread searches together for their common prefix
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n: item i
 // names a chain, its length and a worker table (info), and receives the
@@ -1341,28 +1342,63 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         // every (request, worker) overlap against the caches as they stand
         search(0, nb, -1);
         if (tiers) tier_search(0, nb, -1);
-        // common prefix of every pair of the batch's chains (prefix mode)
+        // common prefix of every pair of the batch's chains (prefix mode): a thread's pairs are
+        // searched KP at a time, each group in the depth of one binary search on equal hashes
         if (!scan) {
             const int32_t npair = nb * (nb - 1) / 2;
-            for (int32_t q = tid; q < npair; q += NT) {
-                int32_t b = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
-                while (b > 1 && b * (b - 1) / 2 > q) --b;
-                while ((b + 1) * b / 2 <= q) ++b;
-                const int32_t b2 = q - b * (b - 1) / 2;
-                const int32_t m = min(r_P[b], r_P[b2]);
-                const uint64_t* ca = a.chains + r_cb[b];
-                const uint64_t* cc = a.chains + r_cb[b2];
-                int32_t lo = 0;
-                if (m > 0 && r_first[b] == r_first[b2]) {
-                    int32_t hi = m;
-                    lo = 1;
-                    while (lo < hi) {
-                        const int32_t mid = (lo + hi) >> 1;
-                        if (ca[mid] == cc[mid]) lo = mid + 1;
-                        else hi = mid;
+            for (int32_t grp = 0; grp * KP * NT < npair; ++grp) {
+            int32_t lo[KP], hi[KP], pp[KP];   // pp: b | b2 << 8, or -1
+            int64_t ca[KP], cc[KP];
+#pragma unroll
+            for (int k = 0; k < KP; ++k) {
+                const int32_t q = tid + (grp * KP + k) * NT;
+                lo[k] = 0;
+                hi[k] = 0;
+                pp[k] = -1;
+                ca[k] = 0;
+                cc[k] = 0;
+                if (q < npair) {
+                    int32_t b = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
+                    while (b > 1 && b * (b - 1) / 2 > q) --b;
+                    while ((b + 1) * b / 2 <= q) ++b;
+                    const int32_t b2 = q - b * (b - 1) / 2;
+                    pp[k] = b | (b2 << 8);
+                    const int32_t m = min(r_P[b], r_P[b2]);
+                    if (m > 0 && r_first[b] == r_first[b2]) {
+                        lo[k] = 1;
+                        hi[k] = m;
+                        ca[k] = r_cb[b];
+                        cc[k] = r_cb[b2];
                     }
                 }
-                l_lcp[b * NB + b2] = (uint16_t)lo;
+            }
+            for (;;) {
+                bool any = false;
+                int32_t mid[KP];
+                uint64_t va[KP], vb[KP];
+#pragma unroll
+                for (int k = 0; k < KP; ++k) {
+                    mid[k] = (lo[k] + hi[k]) >> 1;
+                    va[k] = 0ull;
+                    vb[k] = 0ull;
+                    if (lo[k] < hi[k]) {
+                        va[k] = a.chains[ca[k] + mid[k]];
+                        vb[k] = a.chains[cc[k] + mid[k]];
+                        any = true;
+                    }
+                }
+                if (!any) break;
+#pragma unroll
+                for (int k = 0; k < KP; ++k) {
+                    if (lo[k] < hi[k]) {
+                        if (va[k] == vb[k]) lo[k] = mid[k] + 1;
+                        else hi[k] = mid[k];
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < KP; ++k)
+                if (pp[k] >= 0) l_lcp[(pp[k] & 0xff) * NB + (pp[k] >> 8)] = (uint16_t)lo[k];
             }
             __syncthreads();
         }
