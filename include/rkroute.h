@@ -334,12 +334,12 @@ typedef struct {
     int32_t probe_mode;              /* RK_PROBE_PREFIX: caches are prefix-closed along
                                         every chain, which holds for chained hashes (a
                                         block is touched and evicted after its children):
-                                        the first miss is found by a 64-way search;
+                                        the first miss is found by binary search;
                                         RK_PROBE_SCAN: scan from block 0 in 64-block steps */
     int32_t tiers;                   /* nonzero when some episode has tier_g1 > 0: the
                                         launch then keeps tier overlaps in LDS          */
     int32_t max_routes;              /* upper bound on any episode's routes (turns), >= 0 */
-    int32_t reserved;                /* 0                                               */
+    int32_t flags;                   /* RK_SIM_TABLES_CLEAR or 0                        */
     const rk_episode_params* params; /* [E], device                                     */
     const int64_t* turn_off;         /* turns of conversation c: turn_off[c] .. turn_off[c+1]-1 */
     const int32_t* turn_blocks;      /* prompt blocks P of each turn; a turn's prompt is the
@@ -379,13 +379,32 @@ typedef struct {
 size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache_blocks,
                                   int32_t max_blocks, int32_t max_conv, int32_t max_routes);
 
-/* Run E independent episodes, one workgroup each.  `batch` and `out` are HOST
- * structs holding device pointers; `workspace` is device memory of at least
- * rk_simulate_workspace_size(...) bytes (contents need not be initialised).
- * Calls that share a workspace must not overlap. */
+/* batch.flags: the workspace's cache tables are already empty for this batch,
+ * cleared by rk_simulate_clear_tables after the workspace's last use, so
+ * rk_simulate_episodes skips clearing them.  Without the flag it clears them
+ * first, on its own stream. */
+#define RK_SIM_TABLES_CLEAR 1
+
+/* Run E independent episodes, one workgroup each (Section 4.3: sequential
+ * greedy routing; Section 2.2: the router cost and the KV cache it reads).
+ * `batch` and `out` are HOST structs holding device pointers; `workspace` is
+ * device memory of at least rk_simulate_workspace_size(...) bytes (contents
+ * need not be initialised, except that with RK_SIM_TABLES_CLEAR the cache
+ * tables must have been cleared by rk_simulate_clear_tables).  Calls that
+ * share a workspace must not overlap.  Unknown flag bits: RK_EINVAL. */
 int rk_simulate_episodes(const rk_episode_batch* batch /* host */,
                          const rk_episode_outputs* out /* host */,
                          void* workspace, size_t ws_bytes, void* stream);
+
+/* Clear the cache tables of a workspace for `batch` (the same shape fields as
+ * the rk_simulate_episodes call that will use it; its pointers and params are
+ * not read), enqueued on `stream`, so that a later rk_simulate_episodes with
+ * RK_SIM_TABLES_CLEAR need not: a caller can clear on another stream while it
+ * hashes the next chains.  The caller orders the two calls (e.g. with an
+ * event) and keeps the workspace unused in between.  Validation as for
+ * rk_simulate_episodes' shape fields; ws_bytes too small: RK_ENOMEM. */
+int rk_simulate_clear_tables(const rk_episode_batch* batch /* host */, void* workspace, size_t ws_bytes,
+                             void* stream);
 
 /* ----------------------------------------------------------------- PoA-hat
  * For each window w of consecutive routes rows win_off[w] .. win_off[w+1]-1

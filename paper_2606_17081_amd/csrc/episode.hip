@@ -1824,30 +1824,65 @@ extern "C" size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache
     return L.per_episode * (size_t)E;
 }
 
+// Shape fields of a batch, shared by rk_simulate_episodes and rk_simulate_clear_tables.
+static int check_batch_shape(const char* who, const rk_episode_batch* b)
+{
+    if (b->E < 0) return fail(RK_EINVAL, "%s: E < 0", who);
+    if (b->W < 1 || b->W > 64) return fail(RK_EUNSUPPORTED, "%s: W outside 1..64", who);
+    if (b->cache_blocks < 1) return fail(RK_EINVAL, "%s: cache_blocks < 1", who);
+    if (b->max_blocks < 1 || b->max_blocks > 8192) return fail(RK_EUNSUPPORTED, "%s: max_blocks outside 1..8192", who);
+    if (b->max_conv < 0 || b->max_conv > (1 << 28)) return fail(RK_EINVAL, "%s: max_conv", who);
+    if (b->max_inflight < 1 || b->max_inflight > 8192)
+        return fail(RK_EUNSUPPORTED, "%s: max_inflight outside 1..8192", who);
+    if (b->max_routes_per_step < 1 || b->max_routes_per_step > b->max_inflight)
+        return fail(RK_EINVAL, "%s: max_routes_per_step outside 1..max_inflight", who);
+    if (b->max_ctrl_window < 1 || b->max_ctrl_window > 4096)
+        return fail(RK_EUNSUPPORTED, "%s: max_ctrl_window outside 1..4096", who);
+    if (b->probe_mode != RK_PROBE_PREFIX && b->probe_mode != RK_PROBE_SCAN)
+        return fail(RK_EINVAL, "%s: unknown probe_mode", who);
+    if ((int64_t)b->cache_blocks + b->max_blocks > (1ll << 29)) return fail(RK_EUNSUPPORTED, "%s: cache too large", who);
+    if (b->max_routes < 0) return fail(RK_EINVAL, "%s: max_routes < 0", who);
+    if (b->flags & ~RK_SIM_TABLES_CLEAR) return fail(RK_EINVAL, "%s: unknown flags %#x", who, (unsigned)b->flags);
+    return RK_OK;
+}
+
+// Enqueue episode_clear_kernel over every episode's tables.
+static int launch_table_clear(const char* who, const rk_episode_batch* b, const EpisodeLayout& L, void* workspace,
+                              hipStream_t s)
+{
+    const uint64_t n16 = (uint64_t)b->W * L.slots;          // 16-byte slots per episode
+    const uint64_t cpe = (n16 + kClearChunk - 1) / kClearChunk;
+    if (cpe * (uint64_t)b->E > 0x7fffffffull)
+        return fail(RK_EUNSUPPORTED, "%s: %d episodes of %llu table slots exceed one clear launch", who, b->E,
+                    (unsigned long long)n16);
+    hipLaunchKernelGGL(episode_clear_kernel, dim3((unsigned)(cpe * (uint64_t)b->E)), dim3(256), 0, s,
+                       (unsigned char*)workspace, L.per_episode, L.off_slots, n16, (uint32_t)cpe);
+    return hip_check(hipGetLastError(), who);
+}
+
+extern "C" int rk_simulate_clear_tables(const rk_episode_batch* b, void* workspace, size_t ws_bytes, void* stream)
+{
+    if (!b) return fail(RK_EINVAL, "rk_simulate_clear_tables: NULL batch");
+    int rc = check_batch_shape("rk_simulate_clear_tables", b);
+    if (rc) return rc;
+    if (b->E == 0) return RK_OK;
+    if (!workspace) return fail(RK_EINVAL, "rk_simulate_clear_tables: NULL workspace");
+    const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv, b->max_routes);
+    const size_t need = L.per_episode * (size_t)b->E;
+    if (ws_bytes < need)
+        return fail(RK_ENOMEM, "rk_simulate_clear_tables: workspace %zu bytes < %zu needed", ws_bytes, need);
+    return launch_table_clear("rk_simulate_clear_tables", b, L, workspace, (hipStream_t)stream);
+}
+
 extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_outputs* out, void* workspace,
                                     size_t ws_bytes, void* stream)
 {
     if (!b || !out) return fail(RK_EINVAL, "rk_simulate_episodes: NULL batch or outputs");
-    if (b->E < 0) return fail(RK_EINVAL, "rk_simulate_episodes: E < 0");
-    if (b->W < 1 || b->W > 64) return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: W outside 1..64");
-    if (b->cache_blocks < 1) return fail(RK_EINVAL, "rk_simulate_episodes: cache_blocks < 1");
-    if (b->max_blocks < 1 || b->max_blocks > 8192)
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: max_blocks outside 1..8192");
-    if (b->max_conv < 0 || b->max_conv > (1 << 28)) return fail(RK_EINVAL, "rk_simulate_episodes: max_conv");
-    if (b->max_inflight < 1 || b->max_inflight > 8192)
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: max_inflight outside 1..8192");
-    if (b->max_routes_per_step < 1 || b->max_routes_per_step > b->max_inflight)
-        return fail(RK_EINVAL, "rk_simulate_episodes: max_routes_per_step outside 1..max_inflight");
-    if (b->max_ctrl_window < 1 || b->max_ctrl_window > 4096)
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: max_ctrl_window outside 1..4096");
-    if (b->probe_mode != RK_PROBE_PREFIX && b->probe_mode != RK_PROBE_SCAN)
-        return fail(RK_EINVAL, "rk_simulate_episodes: unknown probe_mode");
-    if ((int64_t)b->cache_blocks + b->max_blocks > (1ll << 29))
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: cache too large");
+    int rc = check_batch_shape("rk_simulate_episodes", b);
+    if (rc) return rc;
     if (b->E == 0) return RK_OK;
     if (!b->params || !b->turn_off || !b->turn_blocks || !b->chain_off || !b->chains || !workspace)
         return fail(RK_EINVAL, "rk_simulate_episodes: NULL array");
-    if (b->max_routes < 0) return fail(RK_EINVAL, "rk_simulate_episodes: max_routes < 0");
     const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv, b->max_routes);
     const size_t need = L.per_episode * (size_t)b->E;
     if (ws_bytes < need)
@@ -1898,15 +1933,10 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.NB = NB;
     const size_t lds = o + batch_layout(NB, b->W, tiers).bytes;
     hipStream_t s = (hipStream_t)stream;
-    const uint64_t n16 = (uint64_t)b->W * L.slots;          // 16-byte slots per episode
-    const uint64_t cpe = (n16 + kClearChunk - 1) / kClearChunk;
-    if (cpe * (uint64_t)b->E > 0x7fffffffull)
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %d episodes of %llu table slots exceed one clear launch",
-                    b->E, (unsigned long long)n16);
-    hipLaunchKernelGGL(episode_clear_kernel, dim3((unsigned)(cpe * (uint64_t)b->E)), dim3(256), 0, s,
-                       (unsigned char*)workspace, L.per_episode, L.off_slots, n16, (uint32_t)cpe);
-    int rc = hip_check(hipGetLastError(), "rk_simulate_episodes clear launch");
-    if (rc) return rc;
+    if (!(b->flags & RK_SIM_TABLES_CLEAR)) {
+        rc = launch_table_clear("rk_simulate_episodes clear launch", b, L, workspace, s);
+        if (rc) return rc;
+    }
     hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), lds, s, a);
     return hip_check(hipGetLastError(), "rk_simulate_episodes launch");
 }

@@ -71,6 +71,20 @@ def test_episode_and_poa_host_validation():
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), 16, None) == rk.RK_ENOMEM
     need = rk.simulate_workspace_size(2, 4, 16, 8, 4, 10)
     assert need > 0 and need == 2 * rk.simulate_workspace_size(1, 4, 16, 8, 4, 10)
+    # flags: only RK_SIM_TABLES_CLEAR is known; the separate clear validates the same shape fields
+    b = rk.EpisodeBatch(2, 4, 16, 8, 4, 8, 2, 1, 0, 0, 4, 2, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
+                        C.c_void_p(8), C.c_void_p(8))
+    assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), need, None) == rk.RK_EINVAL
+    assert b"flags" in L.rk_last_error()
+    assert L.rk_simulate_clear_tables(None, C.c_void_p(8), need, None) == rk.RK_EINVAL
+    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), need, None) == rk.RK_EINVAL
+    b.flags = rk.RK_SIM_TABLES_CLEAR
+    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), 16, None) == rk.RK_ENOMEM
+    assert L.rk_simulate_clear_tables(C.byref(b), None, need, None) == rk.RK_EINVAL
+    b.W = 65
+    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), need, None) == rk.RK_EUNSUPPORTED
+    b.W, b.E = 4, 0
+    assert L.rk_simulate_clear_tables(C.byref(b), None, 0, None) == rk.RK_OK
     pp = rk.PoaParams(0.005, 0.02, 0.01, 2, 64, 0.015, 0)
     assert L.rk_poa_estimate(1, None, 0, None, 8, 8, 65, None, None, None, pp, None, None, None, None, 0,
                              None) == rk.RK_EUNSUPPORTED

@@ -421,3 +421,40 @@ def test_lazy_recency_late_first_eviction(gpu, orc):
             late += int(ev.size > 0 and ev[0] > len(o["evict_count"]) // 4)   # a long history before it
             _compare_episode(r.episode_results(e), o, w.W, window=sp.concurrency, label=f"cache {cache} e{e}")
     assert late >= 8
+
+
+def test_tables_cleared_on_another_stream(gpu, orc):
+    """rk_simulate_clear_tables on a second stream, ordered by an event, then
+    rk_simulate_episodes with RK_SIM_TABLES_CLEAR: the same routes, overlaps,
+    costs and evictions as the default path (which clears on its own stream),
+    over several launches on one workspace."""
+    torch, rk = gpu
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    w = wl.multiturn_workload(seeds=range(2), n_conv=96)
+    eps = [wl.EpisodeSpec(**{**sp.__dict__, "cap": 512}) for sp in w.episodes]
+    w2 = wl.Workload(w.name, W=w.W, cache_blocks=1024, traces=w.traces, episodes=eps)
+    r = EpisodeRunner(w2)
+    r.hash()
+    r.simulate()
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in (("w", r.route_worker), ("o", r.overlap), ("c", r.cost),
+                                      ("d", r.evict_digest), ("t", r.totals))}
+    assert int(ref["t"][:, 1].sum()) > 0, "the case must evict"
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    for _ in range(3):
+        for t in (r.route_worker, r.overlap, r.cost, r.evict_digest, r.totals):
+            t.zero_()
+        ev = torch.cuda.Event()
+        ev.record(main)              # the workspace's last use is done before the clear starts
+        side.wait_event(ev)
+        r.clear_tables(stream=side)
+        ev2 = torch.cuda.Event()
+        ev2.record(side)
+        main.wait_event(ev2)
+        r.simulate(tables_clear=True)
+        torch.cuda.synchronize()
+        _status_clean(rk)
+        for k, v in (("w", r.route_worker), ("o", r.overlap), ("c", r.cost), ("d", r.evict_digest),
+                     ("t", r.totals)):
+            assert torch.equal(v, ref[k]), k
