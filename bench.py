@@ -4,6 +4,11 @@ One step = one pass of the whole path over the 1P/5D-shaped sweep: block-hash
 chains of 64 traces of 4,096 requests, 320 routing episodes (W = 6 workers,
 C in {32, 64, 128, 256, 512} x 64 seeds), and the PoA-hat windows and ratios.
 Inputs (tokens, offsets, parameters) are resident in HBM before timing.
+Consecutive steps overlap on two streams (two sets of buffers take turns): a
+step's episodes run while the other stream finishes the previous step's
+PoA-hat and hashes and clears the tables for the next step; every step still
+does all of its work inside the timed region, and its results are checked
+against a sequential step.
 
 Also measured in the same run: the batched scoring kernel on 65,536 requests x
 64 workers with 2^20-slot tables, and the CPU oracle on a bounded sample of
@@ -424,55 +429,74 @@ def main():
         return
     log("generating the sweep (64 traces of 4,096 requests)")
     w = wl.sweep70b_workload()
-    runner = EpisodeRunner(w, keep_cost=True)
+    # Two runners (each with its own chains, outputs and workspace) take turns, so that consecutive
+    # steps can overlap: step k's episodes run on the main stream while the second stream computes
+    # step k-1's PoA-hat and hashes and clears the tables for step k+1.  Each step still does all of
+    # its work (hash, clear, episodes, PoA-hat) inside the timed region.
+    runners = [EpisodeRunner(w, keep_cost=True) for _ in range(2)]
+    runner = runners[0]
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
     log(f"{len(runner.episodes)} episodes, {runner.n_rows} routes, {runner.n_windows} PoA windows; warmup {args.warmup}")
-    for _ in range(args.warmup):
-        runner.step()
+    for _ in range(max(1, args.warmup)):      # at least one untimed sequential step: the reference
+        for r in runners:
+            r.step()
     torch.cuda.synchronize()
     assert rk.device_status(reset=True) == 0
+    # the sequential result every pipelined step must reproduce
+    E0, n0 = len(runner.episodes), runner.n_rows
+    ref_poa = runner.poa_hat[:E0].clone()
+    ref_route = runner.route_worker[:n0].clone()
 
-    # The tables' clear runs on a second stream: a step's episodes wait for their tables' clear,
-    # and the clear for the next step starts when a step's episodes are done, beside its PoA-hat
-    # and the next hashing (the first step's clear beside its hashing, inside the timed region).
     side = torch.cuda.Stream()
-    t_hash, t_sim, t_poa = KernelTimer(torch, stream), KernelTimer(torch, stream), KernelTimer(torch, stream)
-    t_clear = KernelTimer(torch, side)
+    t_sim = KernelTimer(torch, stream)
+    t_hash, t_clear, t_poa = KernelTimer(torch, side), KernelTimer(torch, side), KernelTimer(torch, side)
+    e_sim = [None] * args.steps
 
-    def clear_next():
-        done = torch.cuda.Event()
-        done.record(stream)            # the workspace's last use (the episodes) is done
-        side.wait_event(done)
+    def prepare(k):
+        """Hash and clear the tables for step k on the second stream, once the episodes of the
+        runner's previous step (k - 2) are done."""
+        r = runners[k % 2]
+        if k >= 2:
+            side.wait_event(e_sim[k - 2])
+        with t_hash:
+            r.hash(stream=side)
         with t_clear:
-            runner.clear_tables(stream=side)
+            r.clear_tables(stream=side)
         ready = torch.cuda.Event()
         ready.record(side)
         return ready
 
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ready = clear_next()
+    ready = prepare(0)
     for k in range(args.steps):
-        with t_hash:
-            runner.hash()
+        r = runners[k % 2]
         stream.wait_event(ready)
         with t_sim:
-            runner.simulate(tables_clear=True)
+            r.simulate(stream=stream, tables_clear=True)
+        done = torch.cuda.Event()
+        done.record(stream)
+        e_sim[k] = done
         if k + 1 < args.steps:
-            ready = clear_next()
+            ready = prepare(k + 1)
+        side.wait_event(done)
         with t_poa:
-            runner.poa()
+            r.poa(stream=side)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     assert rk.device_status(reset=True) == 0
+    for r in runners[: min(2, args.steps)]:
+        assert torch.equal(r.poa_hat[:E0], ref_poa), "pipelined steps differ from the sequential step (PoA-hat)"
+        assert torch.equal(r.route_worker[:n0], ref_route), "pipelined steps differ from the sequential step (routes)"
     ms_step = wall * 1e3 / args.steps
     E = len(runner.episodes)
     scorings = runner.n_rows * runner.W
     stage_ms = dict(hash=t_hash.mean_ms(), simulate=t_sim.mean_ms(), poa=t_poa.mean_ms())
     clear_ms = t_clear.mean_ms()
     clear_bytes = table_clear_bytes(runner)
-    log(f"step {ms_step:.3f} ms; stages {stage_ms}; table clear {clear_ms:.3f} ms on the second stream")
+    log(f"step {ms_step:.3f} ms; stages {stage_ms} (hash and PoA-hat on the second stream); "
+        f"table clear {clear_ms:.3f} ms on the second stream")
     poa_hat = runner.poa_hat[:E].cpu().numpy()
     per_C = {}
     for C in wl.SWEEP70B_C:
@@ -499,7 +523,7 @@ def main():
 
     score = None
     if not args.no_scoring and args.only == "all":
-        del runner
+        del runner, runners
         torch.cuda.empty_cache()
         score = scoring_bench(torch, rk, wl, stream, args.steps)
 
@@ -537,8 +561,12 @@ def main():
         "episodes_per_s": E / (ms_step * 1e-3),
         "routes_per_s": scorings / w.W / (ms_step * 1e-3),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "pipeline": "two runners take turns: step k's episodes on the main stream while the second stream "
+                    "runs step k-1's PoA-hat and hashes and clears step k+1's tables (stage times are "
+                    "measured under that overlap); every step's PoA-hat and routes are checked against a "
+                    "sequential step",
         "table_clear": {"kernel": "episode_clear_kernel", "avg_ms": round(clear_ms, 4),
-                        "stream": "second stream, beside the PoA-hat and the next hashing",
+                        "stream": "second stream, beside the next step's episodes",
                         "roofline": {"bound": "hbm", "achieved": round(clear_bytes / (clear_ms * 1e-3) / 1e9, 3),
                                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                      "frac": round(clear_bytes / (clear_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6),
