@@ -163,9 +163,8 @@ int rk_route_score_batch(int32_t B, int32_t W, const uint64_t* chains, const int
  * held as one open-addressing table of 2^log2_slots 16-byte slots
  *   struct { uint64_t key; uint64_t mask; }   (key 0 = empty slot)
  * where bit j of mask is set when worker j caches the block.  A key's home
- * slot is (key & (2^log2_slots - 4)), the first slot of an aligned 64-byte
- * group of four; collisions probe linearly upward with wrap-around, so a
- * lookup reads whole groups.  Worker count is limited to 64 by the mask.
+ * slot is (key & (2^log2_slots - 1)); collisions probe linearly upward one
+ * slot at a time with wrap-around.  Worker count is limited to 64 by the mask.
  *
  * rk_index_build -- clear the index and insert worker j's keys
  * keys[key_off[j] .. key_off[j+1]) for j < W (the same key sets as

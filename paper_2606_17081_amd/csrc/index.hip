@@ -39,32 +39,22 @@ __device__ __forceinline__ void load_slot(const IndexSlot* t, uint64_t s, uint64
     m = (uint64_t)v.z | ((uint64_t)v.w << 32);
 }
 
-constexpr uint64_t kGroup = 4;   // slots per 64-byte group: a key's probe walk starts at its group's first slot
-
-__device__ __forceinline__ uint64_t home_group(uint64_t h, uint64_t smask) { return h & smask & ~(kGroup - 1); }
-
-// Worker mask of block hash h (0 when no worker holds it), walking whole
-// aligned 64-byte groups from slot s (a group's first slot): the first group
-// resolves almost every lookup in one round trip.
-__device__ __forceinline__ uint64_t index_walk(const IndexSlot* __restrict__ t, uint64_t smask, uint64_t h, uint64_t s)
-{
-    for (uint64_t n = 0; n <= smask; n += kGroup) {
-        uint64_t k[kGroup], m[kGroup];
-#pragma unroll
-        for (uint64_t x = 0; x < kGroup; ++x) load_slot(t, s + x, k[x], m[x]);
-#pragma unroll
-        for (uint64_t x = 0; x < kGroup; ++x) {
-            if (k[x] == h) return m[x];
-            if (k[x] == kEmpty) return 0ull;
-        }
-        s = (s + kGroup) & smask;
-    }
-    return 0ull;
-}
-
+// Worker mask of block hash h (0 when no worker holds it): linear probing
+// one 16-byte slot per access from the home slot h & smask.  At the loads the
+// index is sized for, the home slot settles almost every lookup, and one slot
+// costs the smallest read the memory system serves; wider windows (an aligned
+// 32- or 64-byte group per access) moved more bytes per lookup and ran slower.
 __device__ __forceinline__ uint64_t index_lookup(const IndexSlot* __restrict__ t, uint64_t smask, uint64_t h)
 {
-    return index_walk(t, smask, h, home_group(h, smask));
+    uint64_t s = h & smask;
+    for (uint64_t n = 0; n <= smask; ++n) {
+        uint64_t k, m;
+        load_slot(t, s, k, m);
+        if (k == h) return m;
+        if (k == kEmpty) return 0ull;
+        s = (s + 1) & smask;
+    }
+    return 0ull;
 }
 
 // First index in [lo, hi) whose mask lacks bit j, for masks in which bit j
@@ -103,6 +93,35 @@ struct IdxLds {
     int32_t ioff[65];            // start of each sample interval's positions in the third round
 };
 
+constexpr int kFewBounds = 8;     // boundaries handled by a scalar loop; more take the LDS search
+constexpr int kDppWaveShr1 = 0x138;   // DPP: every lane takes lane - 1's value (lane 0 keeps old)
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
+{
+    auto mn = [](uint32_t a, uint32_t b) { return b < a ? b : a; };
+    v = mn(v, dpp32<kDppQuadSwap1>(v, v));
+    v = mn(v, dpp32<kDppQuadSwap2>(v, v));
+    v = mn(v, dpp32<kDppRowHalfMirror>(v, v));
+    v = mn(v, dpp32<kDppRowMirror>(v, v));
+    const auto rl = [&](int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); };
+    return mn(mn(rl(0), rl(16)), mn(rl(32), rl(48)));
+}
+
+// The router cost (Section 2.2, Eq. router-cost) in the operation order of
+// route_cost; when cap is a power of two, (A + P) / cap is the exact product
+// with 1 / cap.
+__device__ __forceinline__ float index_route_cost(const rk_cost_params& p, float inv_cap, int32_t P, int32_t o,
+                                                  int32_t A)
+{
+    const float t1 = __fmul_rn(p.w_ov, (float)(P - o));
+    const float t2 = __fmul_rn(p.w_act, (float)A);
+    const float L = (float)((int64_t)A + (int64_t)P);
+    const float r = inv_cap != 0.0f ? __fmul_rn(L, inv_cap) : __fdiv_rn(L, (float)p.cap_blocks);
+    const float x = fmaxf(__fsub_rn(r, 1.0f), 0.0f);
+    const float t3 = __fmul_rn(p.w_sat, __fmul_rn(x, x));
+    return __fadd_rn(__fadd_rn(t1, t2), t3);
+}
+
 // Position of second-round sample k: every position when the round is exact,
 // else the power-of-two grid of step st2, clamped to U - 1.
 __device__ __forceinline__ int32_t round2_pos(int32_t k, bool exact, int64_t st2, int32_t U)
@@ -124,6 +143,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(8))) void sc
     const uint64_t smask = (1ull << log2_slots) - 1;
     const int32_t A = lane < W ? active[lane] : 0;
     const uint64_t all = W == 64 ? ~0ull : ((1ull << W) - 1ull);
+    const float inv_cap = (p.cap_blocks & (p.cap_blocks - 1)) == 0 ? 1.0f / (float)p.cap_blocks : 0.0f;
     const int64_t npairs = ((int64_t)B + kRPW - 1) / kRPW;
 
     // Workgroups are handed to the 8 XCDs round-robin; renumber them so each
@@ -195,83 +215,152 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(8))) void sc
                 // ---- round 1: every worker's first miss lies in [0, U).  Sample
                 // positions sit on a power-of-two grid (clamped to the chain's end)
                 // so requests of one prefix group probe the same index slots.
+                // Masks along a chain only lose bits, so the first sample with an
+                // empty mask bounds every worker.
                 int32_t U = P;
                 if (P > kRound1Min) {
                     const int64_t st1 = (int64_t)next_pow2_dev((uint32_t)P) >> 4;
                     const int32_t q1 = (int32_t)min((int64_t)(lane + 1) * st1, (int64_t)P) - 1;
-                    const uint64_t m = lane < 16 ? index_lookup(index, smask, h(q1)) : all;
-                    const uint64_t pa = wave_scan_and_u64(m & all);
-                    const uint64_t z = __ballot(lane < 16 && pa == 0ull);
+                    const uint64_t m1 = lane < 16 ? index_lookup(index, smask, h(q1)) & all : all;
+                    const uint64_t z = __ballot(m1 == 0ull);
                     if (z) U = __builtin_amdgcn_readlane(q1, __ffsll((unsigned long long)z) - 1) + 1;
                 }
                 // ---- round 2: every position of [0, U) when U <= 64, else 64 samples
-                // on the power-of-two grid of step next_pow2(U) / 64, clamped to U - 1
+                // on the power-of-two grid of step next_pow2(U) / 64, clamped to U - 1.
+                // Sample k is a boundary when its mask lacks bits its predecessor's
+                // had (all W bits before sample 0); worker j's first missing sample
+                // t is the boundary that drops bit j.  A request has few boundaries
+                // (one per distinct overlap), so a loop over them costs a few scalar
+                // steps; many boundaries fall back to a search per worker in LDS.
                 const bool exact = U <= 64;
                 const int32_t nq = exact ? U : 64;
                 const int64_t st2 = (int64_t)next_pow2_dev((uint32_t)U) >> 6;
                 const int32_t q = round2_pos(lane, exact, st2, U);
-                const uint64_t m = lane < nq ? index_lookup(index, smask, h(q)) : 0ull;
-                L.m[lane] = wave_scan_and_u64(m & all);
-                wave_sync();
-                const int32_t t = lane < W ? first_clear(L.m, 0, nq, lane) : nq;
+                const uint64_t m = lane < nq ? index_lookup(index, smask, h(q)) & all : 0ull;
+                const uint64_t mp = dpp64<kDppWaveShr1>(all, m);   // sample lane - 1's mask
+                const uint64_t bnd = __ballot(lane < nq && mp != m);
+                const bool few = __popcll(bnd) <= kFewBounds;
+                int32_t t = nq;
+                if (few) {
+                    for (uint64_t b = bnd; b; b &= b - 1) {
+                        const int k = __ffsll((unsigned long long)b) - 1;
+                        if ((((readlane64(mp, k) & ~readlane64(m, k)) >> lane) & 1ull)) t = k;
+                    }
+                } else {
+                    L.m[lane] = m;
+                    wave_sync();
+                    if (lane < W) t = first_clear(L.m, 0, nq, lane);
+                    wave_sync();
+                }
                 if (exact) {
                     o = t;   // t == U only when U == P: every position is cached
                 } else {
-                    // ---- round 3: worker j's first miss is in (q[t-1], q[t]]; probe the inside
-                    const uint64_t need = wave_or_u64(lane < W && t < 64 ? 1ull << t : 0ull);
-                    const int32_t qprev = lane == 0 ? -1 : round2_pos(lane - 1, false, st2, U);
-                    const int32_t width = ((need >> lane) & 1ull) ? max(q - qprev - 1, 0) : 0;
-                    int32_t total;
-                    const int32_t off = wave_excl_sum_dpp(width, total);
-                    L.ioff[lane] = off;
-                    if (lane == 63) L.ioff[64] = total;
-                    wave_sync();
+                    // ---- round 3: worker j's first miss is in (q[t-1], q[t]]; probe the
+                    // inside of the boundary intervals, laid out one after another.
+                    const int32_t qprev = (int32_t)dpp32<kDppWaveShr1>(0xffffffffu, (uint32_t)q);
                     const bool mine = lane < W && t < 64;
                     o = mine ? round2_pos(t, false, st2, U) : P;
-                    const int32_t a0 = mine ? L.ioff[t] : 0, a1 = mine ? L.ioff[t + 1] : 0;
-                    const int32_t pbase = mine ? (t == 0 ? 0 : round2_pos(t - 1, false, st2, U) + 1) : 0;
-                    bool found = !mine;
-                    for (int32_t b3 = 0; b3 < total; b3 += 64) {
-                        const int32_t idx = b3 + lane;
-                        uint64_t mm = 0ull;
-                        if (idx < total) {
-                            int32_t lo = 0, hi = 63;   // largest k with ioff[k] <= idx
-                            while (lo < hi) {
-                                const int32_t mid = (lo + hi + 1) >> 1;
-                                if (L.ioff[mid] <= idx) lo = mid;
-                                else hi = mid - 1;
+                    int32_t pos = -1, a0 = 0, a1 = 0, pb = 0, nb3 = 0;
+                    uint64_t pstart = 0ull;   // the mask before the lane's position when it opens an interval
+                    bool opens = false;
+                    if (few) {
+                        for (uint64_t b = bnd; b; b &= b - 1) {
+                            const int k = __ffsll((unsigned long long)b) - 1;
+                            const int32_t qk = __builtin_amdgcn_readlane(q, k), qpk = __builtin_amdgcn_readlane(qprev, k);
+                            const int32_t w = max(qk - qpk - 1, 0);
+                            if (lane >= nb3 && lane < nb3 + w) pos = qpk + 1 + (lane - nb3);
+                            if (w > 0 && lane == nb3) {
+                                opens = true;
+                                pstart = readlane64(mp, k);
                             }
-                            const int32_t pos = (lo == 0 ? 0 : round2_pos(lo - 1, false, st2, U) + 1) +
-                                                (idx - L.ioff[lo]);
-                            mm = index_lookup(index, smask, h(pos));
+                            if (t == k) {
+                                a0 = nb3;
+                                a1 = nb3 + w;
+                                pb = qpk + 1;
+                            }
+                            nb3 += w;
                         }
-                        wave_sync();   // the previous chunk's masks have been read
-                        L.m[lane] = mm;
+                    }
+                    if (few && nb3 <= 64) {
+                        const uint64_t mm = pos >= 0 ? index_lookup(index, smask, h(pos)) & all : 0ull;
+                        // the shift runs on every lane (a lane whose source lane sat out
+                        // would receive the fill value), then the lanes that open an
+                        // interval take the mask before it instead
+                        const uint64_t left = dpp64<kDppWaveShr1>(all, mm);
+                        const uint64_t pv = opens ? pstart : left;
+                        const uint64_t b3 = __ballot(pos >= 0 && pv != mm);
+                        if (__popcll(b3) <= kFewBounds) {
+                            for (uint64_t b = b3; b; b &= b - 1) {
+                                const int x = __ffsll((unsigned long long)b) - 1;
+                                if ((((readlane64(pv, x) & ~readlane64(mm, x)) >> lane) & 1ull))
+                                    o = __builtin_amdgcn_readlane(pos, x);
+                            }
+                        } else {
+                            L.m[lane] = mm;
+                            wave_sync();
+                            if (mine && a1 > a0) {
+                                const int32_t f = first_clear(L.m, a0, a1, lane);
+                                if (f < a1) o = pb + (f - a0);
+                            }
+                            wave_sync();
+                        }
+                    } else {
+                        // many boundaries or more than 64 positions: chunks of 64
+                        // positions, each lane finding its interval by binary search
+                        const int32_t width = ((bnd >> lane) & 1ull) ? max(q - qprev - 1, 0) : 0;
+                        int32_t total;
+                        const int32_t off = wave_excl_sum_dpp(width, total);
+                        L.ioff[lane] = off;
+                        if (lane == 63) L.ioff[64] = total;
                         wave_sync();
-                        if (!found) {
-                            const int32_t lo = max(a0, b3), hi = min(a1, b3 + 64);
-                            if (lo < hi) {
-                                const int32_t x = first_clear(L.m, lo - b3, hi - b3, lane) + b3;
-                                if (x < hi) {
-                                    o = pbase + (x - a0);
-                                    found = true;
+                        const int32_t c0 = mine ? L.ioff[t] : 0, c1 = mine ? L.ioff[t + 1] : 0;
+                        const int32_t pbase = mine ? (t == 0 ? 0 : round2_pos(t - 1, false, st2, U) + 1) : 0;
+                        bool found = !mine;
+                        for (int32_t b3 = 0; b3 < total; b3 += 64) {
+                            const int32_t idx = b3 + lane;
+                            uint64_t mm = 0ull;
+                            if (idx < total) {
+                                int32_t lo = 0, hi = 63;   // largest k with ioff[k] <= idx
+                                while (lo < hi) {
+                                    const int32_t mid = (lo + hi + 1) >> 1;
+                                    if (L.ioff[mid] <= idx) lo = mid;
+                                    else hi = mid - 1;
+                                }
+                                const int32_t p3 = (lo == 0 ? 0 : round2_pos(lo - 1, false, st2, U) + 1) +
+                                                   (idx - L.ioff[lo]);
+                                mm = index_lookup(index, smask, h(p3)) & all;
+                            }
+                            wave_sync();   // the previous chunk's masks have been read
+                            L.m[lane] = mm;
+                            wave_sync();
+                            if (!found) {
+                                const int32_t lo = max(c0, b3), hi = min(c1, b3 + 64);
+                                if (lo < hi) {
+                                    const int32_t x = first_clear(L.m, lo - b3, hi - b3, lane) + b3;
+                                    if (x < hi) {
+                                        o = pbase + (x - c0);
+                                        found = true;
+                                    }
                                 }
                             }
                         }
+                        wave_sync();   // L.m and L.ioff are free for the next request
                     }
                 }
-                wave_sync();   // L.m and L.ioff are free for the next request
             }
 
-            uint64_t best = ~0ull;
+            // cost per worker; argmin = the lowest worker among those of minimal
+            // cost (non-negative floats order as their bit patterns)
+            uint32_t cb = 0xffffffffu;
             if (lane < W) {
-                const float cst = route_cost(p.w_ov, p.w_act, p.w_sat, p.cap_blocks, P, o, A);
+                const float cst = index_route_cost(p, inv_cap, P, o, A);
                 if (ov_out) ov_out[i * W + lane] = o;
                 if (cost_out) cost_out[i * W + lane] = cst;
-                best = argmin_key(cst, lane);
+                cb = __float_as_uint(__fadd_rn(cst, 0.0f));
             }
-            best = wave_min_u64(best);
-            if (lane == 0 && am_out) am_out[i] = (int32_t)(uint32_t)(best & 0xffffffffu);
+            const uint32_t cmin = wave_min_u32(cb);
+            const uint64_t win = __ballot(lane < W && cb == cmin);
+            if (lane == 0 && am_out) am_out[i] = __ffsll((unsigned long long)win) - 1;
         }
     }
 }
@@ -292,7 +381,7 @@ __global__ __launch_bounds__(256) void index_insert_kernel(const uint64_t* __res
             atomicOr(status, RK_DEV_ZERO_KEY);
             continue;
         }
-        uint64_t s = home_group(key, smask);
+        uint64_t s = key & smask;
         bool done = false;
         for (uint64_t probe = 0; probe <= smask; ++probe) {
             const unsigned long long prev = atomicCAS((unsigned long long*)&t[s].key, (unsigned long long)kEmpty,
