@@ -100,6 +100,63 @@ def test_index_staircase_many_intervals(gpu, orc):
     _status_clean(rk)
 
 
+def prefix_depth_instance(depths, lengths, n=4096, seed=0):
+    """Worker j caches the first depths[j] blocks of one base chain; request i
+    is its first lengths[i] blocks.  The depths place the workers' first misses
+    where a test wants them."""
+    rng = np.random.default_rng(seed)
+    base = rng.integers(1, 2 ** 63, size=n, dtype=np.int64).astype(np.uint64) | np.uint64(1)
+    depths = np.asarray(depths, np.int64)
+    keys = np.concatenate([base[:d] for d in depths]) if depths.sum() else np.zeros(0, np.uint64)
+    key_off = np.zeros(depths.size + 1, np.int64)
+    np.cumsum(depths, out=key_off[1:])
+    L = np.asarray(lengths, np.int64)
+    chain_off = np.zeros(L.size + 1, np.int64)
+    np.cumsum(L, out=chain_off[1:])
+    chains = np.concatenate([base[:l] for l in L])
+    return wl.ScoringInstance(W=depths.size, B=L.size, keys=keys, key_off=key_off, chains=chains,
+                              chain_off=chain_off, active=rng.integers(0, 9000, depths.size).astype(np.int32),
+                              log2_slots=20)
+
+
+PATH_LENGTHS = [1, 2, 17, 63, 64, 65, 100, 255, 256, 257, 511, 512, 700, 833, 1000, 1024, 1500, 2048, 3000,
+                4000, 4096]
+
+
+def path_depths(case, rng, W=64):
+    """Depth sets for the prefix search's paths: few boundaries everywhere;
+    few sample boundaries but many first misses inside the intervals between
+    them; many sample boundaries; few boundaries but more than 64 positions
+    between samples; many boundaries among the first 64 blocks."""
+    if case == "few":
+        return rng.choice([0, 37, 300, 301, 833, 4096], size=W)
+    if case == "clustered":
+        return np.array([16 * a + int(rng.integers(0, 15)) for a in rng.choice([5, 20, 33, 50], size=W)])
+    if case == "spread":
+        return rng.permutation(np.arange(0, 4096, 64))[:W]
+    if case == "wide":
+        return rng.choice([1500, 2900, 4096], size=W)
+    if case == "dense":
+        return rng.integers(0, 64, size=W)
+    raise ValueError(case)
+
+
+@pytest.mark.parametrize("case", ["few", "clustered", "spread", "wide", "dense"])
+def test_index_prefix_search_paths(gpu, orc, case):
+    """Each path of the prefix search (scalar loops over few boundaries, the
+    per-worker LDS searches when a round has many, the chunked third round when
+    the sample intervals hold more than 64 positions) against the oracle, on
+    requests that end before, at and past every worker's depth."""
+    torch, rk = gpu
+    rng = np.random.default_rng({"few": 1, "clustered": 2, "spread": 3, "wide": 4, "dense": 5}[case])
+    inst = prefix_depth_instance(path_depths(case, rng), PATH_LENGTHS, seed=5)
+    ref = orc.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                          inst.w_ov, inst.w_act, inst.w_sat, inst.cap)
+    say("prefix search paths", case)
+    _check(_score_index(rk, torch, inst, rk.RK_PROBE_PREFIX), ref)
+    _status_clean(rk)
+
+
 def test_index_scan_mode_arbitrary_sets(gpu, orc):
     """Keys from a tiny alphabet: worker sets are not prefix-closed along chains."""
     torch, rk = gpu
