@@ -98,6 +98,11 @@ struct EpArgs {
 
 constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 
+template <bool V>
+struct LeanTag {
+    static constexpr bool value = V;
+};
+
 struct EpShared {
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
     int32_t woff[NW][KR + 1], wst[NW][KR];
@@ -765,6 +770,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         return;
     }
     const int64_t gc0 = prm.conv_begin;
+    const bool lean = !scan && policy == RK_POLICY_ARGMIN && prm.controller == 0 && !freq && !tiers;
 
     unsigned char* ws = a.ws + (size_t)e * a.L.per_episode;
     Slot* g_slots = (Slot*)(ws + a.L.off_slots);
@@ -1406,310 +1412,322 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         // ---- B. routing decisions in order (wavefront 0); stops for a flush, a new batch or the end
         const int32_t t0 = t;
         int32_t event = EV_BATCH;
-        for (;;) {
-            if (wave == 0) {
-                event = EV_BATCH;
-                // lane j < W keeps worker j's load, log tail and block counts in registers
-                int32_t rA = 0, rlive = 0, rused = 0, rN = 0;
-                uint32_t rtail = 0;
-                int32_t run_ep = -1;   // decay epoch of the routes decided since the last sync
-                int32_t q_head = sh.qhead, q_size = sh.qsize;   // the ready queue, kept in registers
-                if (lane < W) {
-                    rA = s_A[lane];
-                    rN = s_N[lane];
-                    rtail = s_tail[lane];
-                    rlive = s_live[lane];
-                    rused = s_used[lane];
-                }
-                // workers that keep recency (write log records)
-                const unsigned long long stamped_mask = __ballot(lane < W && s_stamped[lane] != 0);
-                for (;;) {
-                    if (!step_open) {
-                        // release the routes of step s - H; queue their conversations' next turns
-                        const int32_t slot = s_slot, sb = slot * rps;
-                        if (s >= H) {
-                            if (lane < W) {
-                                s_A[lane] = rA;
-                                s_N[lane] = rN;
-                            }
-                            ep_wave_sync();
-                            const int32_t nprev = s_stepn[slot];
-                            const int32_t qtail = q_head + q_size;
-                            int32_t pushed = 0, rel = 0;
-                            for (int32_t base = 0; base < nprev; base += 64) {
-                                const int32_t r = base + lane;
-                                bool more = false;
-                                int32_t c = 0;
-                                if (r < nprev) {
-                                    const int32_t cc = s_stc[sb + r];
-                                    c = cc & ~kMoreTurns;
-                                    more = (cc & kMoreTurns) != 0;
-                                    rel += s_stP[sb + r];
-                                    atomicSub(&s_A[s_stw[sb + r]], s_stP[sb + r]);
-                                    atomicSub(&s_N[s_stw[sb + r]], 1);
-                                }
-                                const unsigned long long mb = __ballot(more);
-                                if (more) {
-                                    int32_t qi = qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull));
-                                    g_queue[qi >= qcap ? qi - qcap : qi] = c;
-                                }
-                                pushed += __popcll(mb);
-                            }
-                            u_tot -= wave_sum_i32(rel);
-                            ep_wave_sync();
-                            q_size += pushed;
-                            if (lane < W) {
-                                rA = s_A[lane];
-                                rN = s_N[lane];
-                            }
-                            ep_wave_sync();
-                        }
-                        int32_t inflight = 0;
-                        for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[s_slot >= k ? s_slot - k : s_slot - k + H];
-                        const int32_t qs = q_size;
-                        if (qs == 0 && inflight == 0) {
-                            event = EV_DONE;
-                            break;
-                        }
-                        n_step = min(rps, qs);
-                        if (lane == 0) s_stepn[slot] = n_step;
-                        if (n_step > 0) tot[5] = s + 1;
-                        r_in_step = 0;
-                        step_open = true;
-                        ep_wave_sync();
-                    }
-                    if (r_in_step >= n_step) {
-                        ++s;
-                        s_slot = s_slot + 1 == H ? 0 : s_slot + 1;
-                        step_open = false;
-                        continue;
-                    }
-                    const int32_t b = t - t0;
-                    if (b >= nb) break;
-                    if (__builtin_expect(freq, 0)) {
-                        // a new decay epoch waits until the earlier epoch's cache writes are in
-                        const int32_t ep = s / dsteps;
-                        if (run_ep >= 0 && ep != run_ep) {
-                            event = EV_EPOCH;
-                            break;
-                        }
-                        run_ep = ep;
-                    }
-                    // one route: controller, cost of every worker, argmin
+        // ---- B. the decisions of wavefront 0 (below).  LN: the episode runs in prefix
+        // mode, routed by argmin under LRU, without memory tiers or a controller; that
+        // copy of the decision loop is compiled with those features switched off,
+        // which shortens the serial decision chain.
+        auto decide = [&](auto lean_tag) {
+            constexpr bool LN = decltype(lean_tag)::value;
+            const bool freq_d = !LN && freq, tiers_d = !LN && tiers, regime_d = !LN && regime_ctl, scan_d = !LN && scan;
+            const bool ctrl1_d = !LN && prm.controller == 1;
+            const int32_t policy_d = LN ? RK_POLICY_ARGMIN : policy;
+            event = EV_BATCH;
+            // lane j < W keeps worker j's load, log tail and block counts in registers
+            int32_t rA = 0, rlive = 0, rused = 0, rN = 0;
+            uint32_t rtail = 0;
+            int32_t run_ep = -1;   // decay epoch of the routes decided since the last sync
+            int32_t q_head = sh.qhead, q_size = sh.qsize;   // the ready queue, kept in registers
+            if (lane < W) {
+                rA = s_A[lane];
+                rN = s_N[lane];
+                rtail = s_tail[lane];
+                rlive = s_live[lane];
+                rused = s_used[lane];
+            }
+            // workers that keep recency (write log records)
+            const unsigned long long stamped_mask = __ballot(lane < W && s_stamped[lane] != 0);
+            for (;;) {
+                if (!step_open) {
+                    // release the routes of step s - H; queue their conversations' next turns
                     const int32_t slot = s_slot, sb = slot * rps;
-                    bool active = false;
-                    if (__builtin_expect(prm.controller == 1 && t >= prm.ctrl_window, 0))
-                        active = (int64_t)prm.ctrl_den * u_sum >
-                                 (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
-                    float w = prm.w_ov;
-                    if (active) w = fminf(prm.w_ov, prm.ctrl_w_ov);
-                    int32_t pol = policy;
-                    float tau_r = tau;
-                    if (__builtin_expect(regime_ctl, 0)) {
-                        w = rg.w_ov[rg_r];
-                        tau_r = rg.tau[rg_r];
-                        pol = tau_r > 0.0f ? RK_POLICY_SOFTMAX : RK_POLICY_ARGMIN;
-                    }
-                    const int32_t P = r_P[b];
-                    const int64_t row = prm.out_base + (int64_t)t;
-                    uint32_t bits = 0xFFFFFFFFu;
-                    int32_t oj = 0;
-                    float cj = 0.0f;
-                    if (lane < W) {
-                        oj = o_cur[b * W + lane];
-                        if (__builtin_expect(tiers, 0)) {
-                            const int32_t o1 = t1_tab[b * W + lane], o12 = t12_tab[b * W + lane];
-                            cj = route_cost_tiers(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, o1, o12,
-                                                  prm.tier_w, rA);
-                            if (a.out.tier_overlap) {
-                                a.out.tier_overlap[(row * W + lane) * 2] = o1;
-                                a.out.tier_overlap[(row * W + lane) * 2 + 1] = o12;
-                            }
-                        } else {
-                            cj = route_cost_ep(w, prm.w_act, prm.w_sat, prm.cap_blocks, inv_cap, P, oj, rA);
+                    if (s >= H) {
+                        if (lane < W) {
+                            s_A[lane] = rA;
+                            s_N[lane] = rN;
                         }
-                        if (a.out.cost) a.out.cost[row * W + lane] = cj;
-                        bits = __float_as_uint(__fadd_rn(cj, 0.0f));
-                    }
-                    int32_t sg;
-                    if (__builtin_expect(pol == RK_POLICY_ARGMIN, 1)) {
-                        const uint32_t mn = ep_wave_min_u32(bits);
-                        sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
-                    } else if (pol == RK_POLICY_SOFTMAX) {
-                        // weights exp((c_min - c_j) / tau); running sums in worker order
-                        const float cmin = __uint_as_float(ep_wave_min_u32(bits));
-                        const float ej = lane < W ? exp_neg_f32(__fdiv_rn(__fsub_rn(cmin, cj), tau_r)) : 0.0f;
-                        float total = 0.0f;
-                        for (int32_t j = 0; j < W; ++j)
-                            total = __fadd_rn(total, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j)));
-                        const float u = __fmul_rn((float)(r_rnd[2 * b] >> 8), 5.9604644775390625e-8f);
-                        const float thr = __fmul_rn(u, total);
-                        float run = 0.0f;
-                        int32_t last = 0;
-                        sg = -1;
-                        for (int32_t j = 0; j < W && sg < 0; ++j) {
-                            const float e = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j));
-                            run = __fadd_rn(run, e);
-                            if (e > 0.0f) last = j;
-                            if (run > thr) sg = j;
-                        }
-                        if (sg < 0) sg = last;
-                    } else if (pol == RK_POLICY_ROUND_ROBIN) {
-                        sg = t % W;
-                    } else {
-                        const int32_t ca = (int32_t)(((uint64_t)r_rnd[2 * b] * (uint64_t)W) >> 32);
-                        sg = ca;
-                        if (pol == RK_POLICY_P2C && W > 1) {
-                            int32_t cb2 = (int32_t)(((uint64_t)r_rnd[2 * b + 1] * (uint64_t)(W - 1)) >> 32);
-                            if (cb2 >= ca) ++cb2;
-                            const float fa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), ca));
-                            const float fb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), cb2));
-                            if (fb < fa || (fb == fa && cb2 < ca)) sg = cb2;
-                        }
-                    }
-                    const int32_t osg = __builtin_amdgcn_readlane(oj, sg);
-                    const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + (scan ? 0 : P - osg);
-                    const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
-                    const bool flush = scan || tiers || live_after > a.cache;
-                    // a worker that keeps recency needs log records for the route's P touches and slots
-                    // for its new blocks: without room, stop before the route and compact that worker
-                    // (the cached sets and loads stay as they are, so the route is decided again alike)
-                    if (__builtin_expect((stamped_mask >> sg) & 1ull, 0)) {
-                        const uint32_t head = s_head[sg];
-                        const uint64_t add = scan ? (uint64_t)P : (uint64_t)(P - osg);
-                        if ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(rused, sg) + add > used_limit ||
-                            (uint64_t)(base - head) + (uint64_t)P > R || (uint64_t)base + (uint64_t)P > 0x40000000u) {
-                            if (room_b == t) {
-                                // still no room right after a compaction (the workspace layout always
-                                // leaves room for one route): report it and go on
-                                if (lane == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
-                            } else {
-                                room_b = t;
-                                if (lane == 0) sh.ev_b = sg;
-                                event = EV_ROOM;
-                                break;
-                            }
-                        }
-                    }
-                    if (active) {
-                        tot[3] += 1;
-                        if (!prev_active) tot[4] += 1;
-                    }
-                    prev_active = active;
-                    if (regime_ctl && rg_r > 0) tot[3] += 1;
-                    const int32_t rc = r_c[b];
-                    if (lane == sg) {
-                        rA += P;
-                        rN += 1;
-                        rtail = base + (uint32_t)P;
-                        if (!scan) {
-                            rlive = live_after;
-                            rused += P - osg;
-                        }
-                    }
-                    if (lane == 0) {
-                        r_sig[b] = sg;
-                        r_stamp[b] = base;
-                        r_ep[b] = freq ? (uint32_t)run_ep : 0u;
-                        g_hist[2 * t] = rc & ~kMoreTurns;
-                        g_hist[2 * t + 1] = P | (sg << 16);
-                        r_otab[b] = o_tab[b * W + sg];
-                        s_stw[sb + r_in_step] = sg;
-                        s_stP[sb + r_in_step] = P;
-                        s_stc[sb + r_in_step] = rc;
-                        g_next[rc & ~kMoreTurns] = r_k[b] + 1;
-                        r_step[b] = (int32_t)s;
-                        r_reg[b] = regime_ctl ? rg_r : 0;
-                        r_evc[b] = 0;
-                        r_evd[b] = 0ull;
-                        if (flush) {
-                            sh.ev_b = b;
-                            sh.ev_row = row;
-                        }
-                    }
-                    u_tot += P;
-                    q_head = q_head + 1 == qcap ? 0 : q_head + 1;
-                    q_size -= 1;
-                    if (__builtin_expect(regime_ctl, 0)) {
-                        // the chosen worker's latency with the new request (already counted in
-                        // lane sg's rN) stands in for TTFT (fp64)
-                        const int32_t n_sg = __builtin_amdgcn_readlane(rN, sg);
-                        double gap = (double)(rg.n_sat - n_sg);
-                        gap = gap < 1.0 ? 1.0 : gap;
-                        double pw = gap;
-                        for (int32_t i = 1; i < rg.beta; ++i) pw = __dmul_rn(pw, gap);
-                        const double lat = __dadd_rn(__dadd_rn(__dmul_rn(rg.a, (double)n_sg), rg.b), __ddiv_rn(rg.d, pw));
-                        rg_ewma = t == 0 ? lat
-                                         : __dadd_rn(__dmul_rn(rg.alpha, lat), __dmul_rn(__dsub_rn(1.0, rg.alpha), rg_ewma));
-                        if (rg_r == 0) {
-                            rg_up = rg_ewma > rg.theta1 ? rg_up + 1 : 0;
-                            if (rg_up >= rg.k) {
-                                rg_r = 1;
-                                rg_up = rg_down = 0;
-                                tot[4] += 1;
-                            }
-                        } else if (rg_r == 1) {
-                            rg_up = rg_ewma >= rg.theta2 ? rg_up + 1 : 0;
-                            rg_down = rg_ewma < __dsub_rn(rg.theta1, rg.eps) ? rg_down + 1 : 0;
-                            if (rg_up >= rg.k) {
-                                rg_r = 2;
-                                rg_up = rg_down = 0;
-                                tot[4] += 1;
-                            } else if (rg_down >= rg.k) {
-                                rg_r = 0;
-                                rg_up = rg_down = 0;
-                            }
-                        } else {
-                            rg_down = rg_ewma < __dsub_rn(rg.theta2, rg.eps) ? rg_down + 1 : 0;
-                            if (rg_down >= rg.k) {
-                                rg_r = 1;
-                                rg_up = rg_down = 0;
-                            }
-                        }
-                    }
-                    if (__builtin_expect(prm.controller == 1, 0)) {
-                        const int32_t pos = c_pos;
-                        c_pos = c_pos + 1 == prm.ctrl_window ? 0 : c_pos + 1;
-                        if (t >= prm.ctrl_window) u_sum -= s_u[pos];
                         ep_wave_sync();
-                        if (lane == 0) s_u[pos] = u_tot;
-                        u_sum += u_tot;
-                    }
-                    tot[0] += P - osg;
-                    tot[2] += P;
-                    tot[6] += osg;
-                    // later requests of the batch now find this chain on sg
-                    if (!scan) {
-                        const int32_t b2 = b + 1 + lane;
-                        if (b2 < nb) {
-                            const int32_t l = l_lcp[b2 * NB + b];
-                            if (l > o_cur[b2 * W + sg]) o_cur[b2 * W + sg] = l;
+                        const int32_t nprev = s_stepn[slot];
+                        const int32_t qtail = q_head + q_size;
+                        int32_t pushed = 0, rel = 0;
+                        for (int32_t base = 0; base < nprev; base += 64) {
+                            const int32_t r = base + lane;
+                            bool more = false;
+                            int32_t c = 0;
+                            if (r < nprev) {
+                                const int32_t cc = s_stc[sb + r];
+                                c = cc & ~kMoreTurns;
+                                more = (cc & kMoreTurns) != 0;
+                                rel += s_stP[sb + r];
+                                atomicSub(&s_A[s_stw[sb + r]], s_stP[sb + r]);
+                                atomicSub(&s_N[s_stw[sb + r]], 1);
+                            }
+                            const unsigned long long mb = __ballot(more);
+                            if (more) {
+                                int32_t qi = qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull));
+                                g_queue[qi >= qcap ? qi - qcap : qi] = c;
+                            }
+                            pushed += __popcll(mb);
                         }
+                        u_tot -= wave_sum_i32(rel);
+                        ep_wave_sync();
+                        q_size += pushed;
+                        if (lane < W) {
+                            rA = s_A[lane];
+                            rN = s_N[lane];
+                        }
+                        ep_wave_sync();
                     }
-                    ++t;
-                    ++r_in_step;
-                    ep_wave_sync();
-                    if (lane == 0)
-                        __hip_atomic_store(&sh.decided, b + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-                    if (__builtin_expect(flush, 0)) {
-                        event = EV_FLUSH;
+                    int32_t inflight = 0;
+                    for (int32_t k = 1; k < H && k <= s; ++k) inflight += s_stepn[s_slot >= k ? s_slot - k : s_slot - k + H];
+                    const int32_t qs = q_size;
+                    if (qs == 0 && inflight == 0) {
+                        event = EV_DONE;
                         break;
                     }
+                    n_step = min(rps, qs);
+                    if (lane == 0) s_stepn[slot] = n_step;
+                    if (n_step > 0) tot[5] = s + 1;
+                    r_in_step = 0;
+                    step_open = true;
+                    ep_wave_sync();
                 }
+                if (r_in_step >= n_step) {
+                    ++s;
+                    s_slot = s_slot + 1 == H ? 0 : s_slot + 1;
+                    step_open = false;
+                    continue;
+                }
+                const int32_t b = t - t0;
+                if (b >= nb) break;
+                if (__builtin_expect(freq_d, 0)) {
+                    // a new decay epoch waits until the earlier epoch's cache writes are in
+                    const int32_t ep = s / dsteps;
+                    if (run_ep >= 0 && ep != run_ep) {
+                        event = EV_EPOCH;
+                        break;
+                    }
+                    run_ep = ep;
+                }
+                // one route: controller, cost of every worker, argmin
+                const int32_t slot = s_slot, sb = slot * rps;
+                bool active = false;
+                if (__builtin_expect(ctrl1_d && t >= prm.ctrl_window, 0))
+                    active = (int64_t)prm.ctrl_den * u_sum >
+                             (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
+                float w = prm.w_ov;
+                if (active) w = fminf(prm.w_ov, prm.ctrl_w_ov);
+                int32_t pol = policy_d;
+                float tau_r = tau;
+                if (__builtin_expect(regime_d, 0)) {
+                    w = rg.w_ov[rg_r];
+                    tau_r = rg.tau[rg_r];
+                    pol = tau_r > 0.0f ? RK_POLICY_SOFTMAX : RK_POLICY_ARGMIN;
+                }
+                const int32_t P = r_P[b];
+                const int64_t row = prm.out_base + (int64_t)t;
+                uint32_t bits = 0xFFFFFFFFu;
+                int32_t oj = 0;
+                float cj = 0.0f;
                 if (lane < W) {
-                    s_A[lane] = rA;
-                    s_N[lane] = rN;
-                    s_tail[lane] = rtail;
-                    s_live[lane] = rlive;
-                    s_used[lane] = rused;
+                    oj = o_cur[b * W + lane];
+                    if (__builtin_expect(tiers_d, 0)) {
+                        const int32_t o1 = t1_tab[b * W + lane], o12 = t12_tab[b * W + lane];
+                        cj = route_cost_tiers(w, prm.w_act, prm.w_sat, prm.cap_blocks, P, oj, o1, o12,
+                                              prm.tier_w, rA);
+                        if (a.out.tier_overlap) {
+                            a.out.tier_overlap[(row * W + lane) * 2] = o1;
+                            a.out.tier_overlap[(row * W + lane) * 2 + 1] = o12;
+                        }
+                    } else {
+                        cj = route_cost_ep(w, prm.w_act, prm.w_sat, prm.cap_blocks, inv_cap, P, oj, rA);
+                    }
+                    if (a.out.cost) a.out.cost[row * W + lane] = cj;
+                    bits = __float_as_uint(__fadd_rn(cj, 0.0f));
+                }
+                int32_t sg;
+                if (__builtin_expect(pol == RK_POLICY_ARGMIN, 1)) {
+                    const uint32_t mn = ep_wave_min_u32(bits);
+                    sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
+                } else if (pol == RK_POLICY_SOFTMAX) {
+                    // weights exp((c_min - c_j) / tau); running sums in worker order
+                    const float cmin = __uint_as_float(ep_wave_min_u32(bits));
+                    const float ej = lane < W ? exp_neg_f32(__fdiv_rn(__fsub_rn(cmin, cj), tau_r)) : 0.0f;
+                    float total = 0.0f;
+                    for (int32_t j = 0; j < W; ++j)
+                        total = __fadd_rn(total, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j)));
+                    const float u = __fmul_rn((float)(r_rnd[2 * b] >> 8), 5.9604644775390625e-8f);
+                    const float thr = __fmul_rn(u, total);
+                    float run = 0.0f;
+                    int32_t last = 0;
+                    sg = -1;
+                    for (int32_t j = 0; j < W && sg < 0; ++j) {
+                        const float e = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ej), j));
+                        run = __fadd_rn(run, e);
+                        if (e > 0.0f) last = j;
+                        if (run > thr) sg = j;
+                    }
+                    if (sg < 0) sg = last;
+                } else if (pol == RK_POLICY_ROUND_ROBIN) {
+                    sg = t % W;
+                } else {
+                    const int32_t ca = (int32_t)(((uint64_t)r_rnd[2 * b] * (uint64_t)W) >> 32);
+                    sg = ca;
+                    if (pol == RK_POLICY_P2C && W > 1) {
+                        int32_t cb2 = (int32_t)(((uint64_t)r_rnd[2 * b + 1] * (uint64_t)(W - 1)) >> 32);
+                        if (cb2 >= ca) ++cb2;
+                        const float fa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), ca));
+                        const float fb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cj), cb2));
+                        if (fb < fa || (fb == fa && cb2 < ca)) sg = cb2;
+                    }
+                }
+                const int32_t osg = __builtin_amdgcn_readlane(oj, sg);
+                const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + (scan_d ? 0 : P - osg);
+                const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
+                const bool flush = scan_d || tiers_d || live_after > a.cache;
+                // a worker that keeps recency needs log records for the route's P touches and slots
+                // for its new blocks: without room, stop before the route and compact that worker
+                // (the cached sets and loads stay as they are, so the route is decided again alike)
+                if (__builtin_expect((stamped_mask >> sg) & 1ull, 0)) {
+                    const uint32_t head = s_head[sg];
+                    const uint64_t add = scan_d ? (uint64_t)P : (uint64_t)(P - osg);
+                    if ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(rused, sg) + add > used_limit ||
+                        (uint64_t)(base - head) + (uint64_t)P > R || (uint64_t)base + (uint64_t)P > 0x40000000u) {
+                        if (room_b == t) {
+                            // still no room right after a compaction (the workspace layout always
+                            // leaves room for one route): report it and go on
+                            if (lane == 0) atomicOr(a.status, RK_DEV_TABLE_FULL);
+                        } else {
+                            room_b = t;
+                            if (lane == 0) sh.ev_b = sg;
+                            event = EV_ROOM;
+                            break;
+                        }
+                    }
+                }
+                if (active) {
+                    tot[3] += 1;
+                    if (!prev_active) tot[4] += 1;
+                }
+                prev_active = active;
+                if (regime_d && rg_r > 0) tot[3] += 1;
+                const int32_t rc = r_c[b];
+                if (lane == sg) {
+                    rA += P;
+                    rN += 1;
+                    rtail = base + (uint32_t)P;
+                    if (!scan_d) {
+                        rlive = live_after;
+                        rused += P - osg;
+                    }
                 }
                 if (lane == 0) {
-                    sh.qhead = q_head;
-                    sh.qsize = q_size;
-                    sh.event = event;
-                    sh.tdone = t;
-                    __hip_atomic_store(&sh.stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    r_sig[b] = sg;
+                    r_stamp[b] = base;
+                    r_ep[b] = freq_d ? (uint32_t)run_ep : 0u;
+                    g_hist[2 * t] = rc & ~kMoreTurns;
+                    g_hist[2 * t + 1] = P | (sg << 16);
+                    r_otab[b] = o_tab[b * W + sg];
+                    s_stw[sb + r_in_step] = sg;
+                    s_stP[sb + r_in_step] = P;
+                    s_stc[sb + r_in_step] = rc;
+                    g_next[rc & ~kMoreTurns] = r_k[b] + 1;
+                    r_step[b] = (int32_t)s;
+                    r_reg[b] = regime_d ? rg_r : 0;
+                    r_evc[b] = 0;
+                    r_evd[b] = 0ull;
+                    if (flush) {
+                        sh.ev_b = b;
+                        sh.ev_row = row;
+                    }
                 }
+                u_tot += P;
+                q_head = q_head + 1 == qcap ? 0 : q_head + 1;
+                q_size -= 1;
+                if (__builtin_expect(regime_d, 0)) {
+                    // the chosen worker's latency with the new request (already counted in
+                    // lane sg's rN) stands in for TTFT (fp64)
+                    const int32_t n_sg = __builtin_amdgcn_readlane(rN, sg);
+                    double gap = (double)(rg.n_sat - n_sg);
+                    gap = gap < 1.0 ? 1.0 : gap;
+                    double pw = gap;
+                    for (int32_t i = 1; i < rg.beta; ++i) pw = __dmul_rn(pw, gap);
+                    const double lat = __dadd_rn(__dadd_rn(__dmul_rn(rg.a, (double)n_sg), rg.b), __ddiv_rn(rg.d, pw));
+                    rg_ewma = t == 0 ? lat
+                                     : __dadd_rn(__dmul_rn(rg.alpha, lat), __dmul_rn(__dsub_rn(1.0, rg.alpha), rg_ewma));
+                    if (rg_r == 0) {
+                        rg_up = rg_ewma > rg.theta1 ? rg_up + 1 : 0;
+                        if (rg_up >= rg.k) {
+                            rg_r = 1;
+                            rg_up = rg_down = 0;
+                            tot[4] += 1;
+                        }
+                    } else if (rg_r == 1) {
+                        rg_up = rg_ewma >= rg.theta2 ? rg_up + 1 : 0;
+                        rg_down = rg_ewma < __dsub_rn(rg.theta1, rg.eps) ? rg_down + 1 : 0;
+                        if (rg_up >= rg.k) {
+                            rg_r = 2;
+                            rg_up = rg_down = 0;
+                            tot[4] += 1;
+                        } else if (rg_down >= rg.k) {
+                            rg_r = 0;
+                            rg_up = rg_down = 0;
+                        }
+                    } else {
+                        rg_down = rg_ewma < __dsub_rn(rg.theta2, rg.eps) ? rg_down + 1 : 0;
+                        if (rg_down >= rg.k) {
+                            rg_r = 1;
+                            rg_up = rg_down = 0;
+                        }
+                    }
+                }
+                if (__builtin_expect(ctrl1_d, 0)) {
+                    const int32_t pos = c_pos;
+                    c_pos = c_pos + 1 == prm.ctrl_window ? 0 : c_pos + 1;
+                    if (t >= prm.ctrl_window) u_sum -= s_u[pos];
+                    ep_wave_sync();
+                    if (lane == 0) s_u[pos] = u_tot;
+                    u_sum += u_tot;
+                }
+                tot[0] += P - osg;
+                tot[2] += P;
+                tot[6] += osg;
+                // later requests of the batch now find this chain on sg
+                if (!scan_d) {
+                    const int32_t b2 = b + 1 + lane;
+                    if (b2 < nb) {
+                        const int32_t l = l_lcp[b2 * NB + b];
+                        if (l > o_cur[b2 * W + sg]) o_cur[b2 * W + sg] = l;
+                    }
+                }
+                ++t;
+                ++r_in_step;
+                ep_wave_sync();
+                if (lane == 0)
+                    __hip_atomic_store(&sh.decided, b + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                if (__builtin_expect(flush, 0)) {
+                    event = EV_FLUSH;
+                    break;
+                }
+            }
+            if (lane < W) {
+                s_A[lane] = rA;
+                s_N[lane] = rN;
+                s_tail[lane] = rtail;
+                s_live[lane] = rlive;
+                s_used[lane] = rused;
+            }
+            if (lane == 0) {
+                sh.qhead = q_head;
+                sh.qsize = q_size;
+                sh.event = event;
+                sh.tdone = t;
+                __hip_atomic_store(&sh.stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+        };
+        for (;;) {
+            if (wave == 0) {
+                if (lean) decide(LeanTag<true>{});
+                else decide(LeanTag<false>{});
             } else {
                 writer();
             }
