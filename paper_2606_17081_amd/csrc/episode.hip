@@ -931,6 +931,37 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 }
                 if (lane == 0) woff[nr] = tot;
                 ep_wave_sync();
+                // no claimed route's worker keeps recency yet: every block is an insert of a
+                // block the worker may lack; the next block's chain hash is fetched while this
+                // one is written
+                const bool lazy = __ballot(lane < nr && s_stamped[r_sig[c + lane]] != 0) == 0ull;
+                if (lazy) {
+                    auto locate = [&](int32_t i, int32_t& b, int32_t& k) {
+                        int32_t r = 0;
+                        while (r + 1 < nr && woff[r + 1] <= i) ++r;
+                        b = c + r;
+                        k = wst[r] + (i - woff[r]);
+                    };
+                    int32_t bn = 0, kn = 0;
+                    uint64_t hn = 0ull;
+                    if (lane < tot) {
+                        locate(lane, bn, kn);
+                        hn = a.chains[r_cb[bn] + kn];
+                    }
+                    for (int32_t i = lane; i < tot; i += 64) {
+                        const int32_t b = bn;
+                        const uint64_t h = hn;
+                        if (i + 64 < tot) {
+                            locate(i + 64, bn, kn);
+                            hn = a.chains[r_cb[bn] + kn];
+                        }
+                        int ins;
+                        touch_hinted(g_slots + (uint64_t)r_sig[b] * S, smask, h, false, ins, a.status);
+                        my_ins += ins;
+                    }
+                    ep_wave_sync();
+                    continue;
+                }
                 for (int32_t i = lane; i < tot; i += 64) {
                     int32_t r = 0;
                     while (r + 1 < nr && woff[r + 1] <= i) ++r;
