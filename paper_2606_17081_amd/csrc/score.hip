@@ -13,6 +13,7 @@ namespace rk {
 
 constexpr int kWinSlots = 4;      // slots one lookup loads together
 constexpr int kStageS = 512;      // leading chain hashes staged in LDS
+constexpr int kHintFan = 16;      // positions per round of the shared search on worker 0's table
 
 // Membership of key in a table probed linearly from key & mask: the slots of
 // a window starting at the home slot are loaded together, so one round trip
@@ -43,7 +44,13 @@ __device__ __forceinline__ void score_wave_sync()
 }
 
 // One wavefront per request; lane j owns worker j (and j + 64, ... when W > 64).
-// PREFIX mode: the first miss by binary lifting -- with lo blocks known
+// PREFIX mode with W <= 64: workers often hold a request's chain to the same
+// depth (a shared prefix cached everywhere), so the lanes first find worker 0's
+// overlap o0 together, in rounds of kHintFan probes of its table, and every
+// lane then checks o0 on its own table with two probes (block o0 - 1 cached,
+// block o0 missing); only a worker that fails the check searches further, by
+// binary lifting on the side of o0 that holds its first miss.
+// PREFIX mode otherwise: the first miss by binary lifting -- with lo blocks known
 // cached, test block lo + step - 1 for step = 2^k, ..., 2, 1 and advance lo by
 // step on a hit.  Exact when membership along the chain is monotone (a block
 // is cached only with its parent).  The positions tested depend only on the
@@ -87,6 +94,55 @@ __global__ __launch_bounds__(64) void score_kernel(int32_t B, int32_t W, const u
         auto h = [&](int32_t x) -> uint64_t { return x < kStageS ? s_ch[x] : hg[x]; };
         const int32_t top = P > 0 ? (int32_t)(1u << (31 - __clz(P))) : 0;
         uint64_t best = ~0ull;
+        if (MODE == RK_PROBE_PREFIX && W <= 64) {
+            // Phase A: the lanes search worker 0's table together.  [lo, hi) holds its
+            // first miss, with block lo - 1 cached (or lo == 0) and block hi missing (or
+            // hi == P); each round tests up to kHintFan positions spread over the interval.
+            int32_t lo = 0, hi = P;
+            while (hi > lo) {
+                const int32_t span = hi - lo;
+                const int32_t n = min(span, kHintFan);
+                // sample k (k < n) at the end of the k-th of n near-equal parts of [lo, hi)
+                const int32_t q = lo + (int32_t)(((int64_t)(lane + 1) * span) / n) - 1;
+                const bool hit = lane < n && table_has_win(tables, mask, h(q));
+                const uint64_t miss = __ballot(lane < n && !hit);
+                if (miss == 0ull) {
+                    lo = hi;
+                    break;
+                }
+                const int k = __ffsll((unsigned long long)miss) - 1;
+                const int32_t qk = __builtin_amdgcn_readlane(q, k);
+                const int32_t qp = k == 0 ? lo - 1 : __builtin_amdgcn_readlane(q, k - 1);
+                lo = qp + 1;
+                hi = qk;
+            }
+            const int32_t o0 = lo;   // worker 0's overlap
+            // Phase B: worker j's overlap is o0 when block o0 - 1 is in its table and
+            // block o0 is not; otherwise binary lifting on the side of o0 that holds it.
+            if (lane < W) {
+                const uint64_t* __restrict__ t = tables + ((uint64_t)lane << log2_slots);
+                const bool before = o0 == 0 || table_has_win(t, mask, h(o0 - 1));
+                const bool at = o0 < P && table_has_win(t, mask, h(o0));
+                int32_t o = o0;
+                if (!before || at) {
+                    // first miss in [b0, b1]: b0 blocks known cached, block b1 missing or b1 == P
+                    const int32_t b0 = before ? o0 + 1 : 0, b1 = before ? P : o0 - 1;
+                    o = b0;
+                    const int32_t len = b1 - b0;
+                    for (int32_t step = len > 0 ? (int32_t)(1u << (31 - __clz(len))) : 0; step > 0; step >>= 1) {
+                        const int32_t pos = o + step - 1;
+                        if (pos < b1 && table_has_win(t, mask, h(pos))) o += step;
+                    }
+                }
+                const float c = route_cost(p.w_ov, p.w_act, p.w_sat, p.cap_blocks, P, o, active[lane]);
+                if (ov_out) ov_out[i * W + lane] = o;
+                if (cost_out) cost_out[i * W + lane] = c;
+                best = argmin_key(c, lane);
+            }
+            best = wave_min_u64(best);
+            if (lane == 0 && am_out) am_out[i] = (int32_t)(uint32_t)(best & 0xffffffffu);
+            continue;
+        }
         for (int32_t j = lane; j < W; j += 64) {
             const uint64_t* __restrict__ t = tables + ((uint64_t)j << log2_slots);
             int32_t o = 0;

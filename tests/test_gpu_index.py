@@ -157,6 +157,37 @@ def test_index_prefix_search_paths(gpu, orc, case):
     _status_clean(rk)
 
 
+@pytest.mark.parametrize("case", ["few", "clustered", "spread", "wide", "dense", "w0-empty", "w0-full", "one"])
+def test_tables_shared_search_paths(gpu, orc, case):
+    """The per-worker-table scorer's shared search (worker 0's overlap found by
+    the whole wavefront, then checked on every table) when the check holds for
+    every worker, for some, for none, when worker 0 caches nothing or the whole
+    chain, and with a single worker."""
+    torch, rk = gpu
+    rng = np.random.default_rng(17)
+    if case == "w0-empty":
+        depths = np.concatenate([[0], rng.choice([300, 833, 4096], size=63)])
+    elif case == "w0-full":
+        depths = np.concatenate([[4096], np.zeros(63, np.int64)])
+    elif case == "one":
+        depths = np.array([833])
+    else:
+        depths = path_depths(case, np.random.default_rng({"few": 1, "clustered": 2, "spread": 3, "wide": 4,
+                                                           "dense": 5}[case]))
+    inst = prefix_depth_instance(depths, PATH_LENGTHS, seed=7)
+    ref = orc.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                          inst.w_ov, inst.w_act, inst.w_sat, inst.cap)
+    up = rk.to_device
+    say("table scorer shared search", case)
+    tables = rk.table_build(up(inst.keys), inst.key_off, 14)
+    for mode in (rk.RK_PROBE_PREFIX, rk.RK_PROBE_SCAN):
+        ov, co, am = rk.route_score_batch(up(inst.chains), up(inst.chain_off), tables, 14, up(inst.active),
+                                          inst.w_ov, inst.w_act, inst.w_sat, inst.cap, probe_mode=mode)
+        torch.cuda.synchronize()
+        _check((ov.cpu().numpy(), co.cpu().numpy(), am.cpu().numpy()), ref)
+    _status_clean(rk)
+
+
 def test_index_scan_mode_arbitrary_sets(gpu, orc):
     """Keys from a tiny alphabet: worker sets are not prefix-closed along chains."""
     torch, rk = gpu
