@@ -125,7 +125,9 @@ typedef struct {
 /* Overlap search modes for rk_route_score_batch. */
 #define RK_PROBE_PREFIX 0  /* tables are prefix-closed along every chain (a block is cached
                               only with its parent, as in a radix tree of blocks):
-                              the first miss is found by binary search              */
+                              membership along a chain is monotone and the first
+                              miss is found by searching positions out of order
+                              (results are unspecified for tables that are not)   */
 #define RK_PROBE_SCAN   1  /* any tables: first miss by a scan from block 0         */
 
 /*
