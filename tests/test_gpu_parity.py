@@ -458,3 +458,28 @@ def test_tables_cleared_on_another_stream(gpu, orc):
         for k, v in (("w", r.route_worker), ("o", r.overlap), ("c", r.cost), ("d", r.evict_digest),
                      ("t", r.totals)):
             assert torch.equal(v, ref[k]), k
+
+
+@pytest.mark.parametrize("name", ["sweep", "multiturn"])
+def test_lean_decision_loop_matches_full(gpu, name):
+    """Episodes routed by argmin under LRU without a controller run the lean
+    copy of the decision loop; the same episodes with the overlap-weight
+    controller switched on at a load it can never reach run the full copy and
+    must route identically (routes, overlaps, costs, evictions, totals)."""
+    from dataclasses import replace
+    torch, rk = gpu
+    base = (wl.sweep70b_workload(seeds=range(4), concurrency=(32, 512)) if name == "sweep"
+            else wl.multiturn_workload(seeds=range(2)))
+    full = wl.Workload(base.name, W=base.W, cache_blocks=base.cache_blocks, traces=base.traces,
+                       episodes=[replace(sp, controller=1, ctrl_num=1 << 30, ctrl_den=1) for sp in base.episodes])
+    outs = []
+    for w in (base, full):
+        say(name, "episodes", len(w.episodes), "controller", w.episodes[0].controller)
+        r = _run(gpu, w)
+        n = r.n_rows
+        outs.append([r.route_worker[:n].cpu().numpy(), r.overlap[:n].cpu().numpy(),
+                     r.cost[:n].cpu().numpy().view(np.uint32), r.evict_digest[:n].cpu().numpy(),
+                     r.totals.cpu().numpy()])
+        assert rk.device_status(reset=True) == 0
+    for k, (a, b) in enumerate(zip(*outs)):
+        assert np.array_equal(a, b), f"output {k} differs between the lean and the full decision loop"
