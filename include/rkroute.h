@@ -341,6 +341,14 @@ typedef struct {
                                         launch then keeps tier overlaps in LDS          */
     int32_t max_routes;              /* upper bound on any episode's routes (turns), >= 0 */
     int32_t flags;                   /* RK_SIM_TABLES_CLEAR or 0                        */
+    int32_t ws_slots;                /* episode workspaces the workspace holds: 0 (or >= E)
+                                        means one per episode; 1 <= ws_slots < E runs the
+                                        batch on ws_slots workgroups, each taking the next
+                                        episode in index order when it finishes one and
+                                        reusing its workspace (its cache tables cleared
+                                        by the workgroup before each episode), so that a
+                                        batch larger than device memory runs in one call  */
+    int32_t ws_pad;                  /* 0                                               */
     const rk_episode_params* params; /* [E], device                                     */
     const int64_t* turn_off;         /* turns of conversation c: turn_off[c] .. turn_off[c+1]-1 */
     const int32_t* turn_blocks;      /* prompt blocks P of each turn; a turn's prompt is the
@@ -376,30 +384,35 @@ typedef struct {
                                  written without them)                               */
 } rk_episode_outputs;
 
-/* Workspace bytes needed by rk_simulate_episodes for this batch shape. */
+/* Workspace bytes needed by rk_simulate_episodes for this batch shape, with E
+ * episode workspaces (pass min(E, ws_slots) when the batch sets ws_slots). */
 size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache_blocks,
                                   int32_t max_blocks, int32_t max_conv, int32_t max_routes);
 
 /* batch.flags: the workspace's cache tables are already empty for this batch,
  * cleared by rk_simulate_clear_tables after the workspace's last use, so
- * rk_simulate_episodes skips clearing them.  Without the flag it clears them
- * first, on its own stream. */
+ * rk_simulate_episodes skips clearing them (with ws_slots, for the first
+ * episode that runs in each workspace).  Without the flag it clears them
+ * first, on its own stream (with ws_slots, each workgroup clears its own
+ * before every episode). */
 #define RK_SIM_TABLES_CLEAR 1
 
 /* Run E independent episodes, one workgroup each (Section 4.3: sequential
  * greedy routing; Section 2.2: the router cost and the KV cache it reads).
  * `batch` and `out` are HOST structs holding device pointers; `workspace` is
- * device memory of at least rk_simulate_workspace_size(...) bytes (contents
- * need not be initialised, except that with RK_SIM_TABLES_CLEAR the cache
- * tables must have been cleared by rk_simulate_clear_tables).  Calls that
- * share a workspace must not overlap.  Unknown flag bits: RK_EINVAL. */
+ * device memory of at least rk_simulate_workspace_size(min(E, ws_slots or E),
+ * ...) bytes (contents need not be initialised, except that with
+ * RK_SIM_TABLES_CLEAR the cache tables must have been cleared by
+ * rk_simulate_clear_tables).  Results do not depend on ws_slots.  Calls that
+ * share a workspace must not overlap.  Unknown flag bits, ws_slots < 0 or
+ * ws_pad != 0: RK_EINVAL. */
 int rk_simulate_episodes(const rk_episode_batch* batch /* host */,
                          const rk_episode_outputs* out /* host */,
                          void* workspace, size_t ws_bytes, void* stream);
 
-/* Clear the cache tables of a workspace for `batch` (the same shape fields as
- * the rk_simulate_episodes call that will use it; its pointers and params are
- * not read), enqueued on `stream`, so that a later rk_simulate_episodes with
+/* Clear the cache tables of a workspace for `batch` (the same shape fields,
+ * ws_slots included, as the rk_simulate_episodes call that will use it; its
+ * pointers and params are not read), enqueued on `stream`, so that a later rk_simulate_episodes with
  * RK_SIM_TABLES_CLEAR need not: a caller can clear on another stream while it
  * hashes the next chains.  The caller orders the two calls (e.g. with an
  * event) and keeps the workspace unused in between.  Validation as for

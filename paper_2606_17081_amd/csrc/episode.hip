@@ -81,7 +81,7 @@ enum : int32_t { EV_BATCH = 0, EV_DONE = 1, EV_FLUSH = 2, EV_EPOCH = 3, EV_ROOM 
 
 struct EpArgs {
     int32_t E, W, cache, max_blocks, max_conv, max_inflight, max_rps, max_ctrl_window, probe_mode, NB, tiers,
-        max_routes;
+        max_routes, n_slots, flags;
     const rk_episode_params* params;
     const int64_t* turn_off;
     const int32_t* turn_blocks;
@@ -104,6 +104,7 @@ struct LeanTag {
 };
 
 struct EpShared {
+    int32_t next_e;
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
     int32_t woff[NW][KR + 1], wst[NW][KR];
     uint32_t new_head, first_kept, adv;
@@ -672,13 +673,49 @@ __global__ __launch_bounds__(256) void episode_clear_kernel(unsigned char* __res
     for (uint64_t k = k0 + threadIdx.x; k < k1; k += 256) z[k] = zero;
 }
 
+// The episode queue of a launch with fewer workspaces than episodes starts at 0.
+__global__ void episode_queue_init(int32_t* __restrict__ q)
+{
+    if (threadIdx.x == 0) *q = 0;
+}
+
 // Two waves per SIMD: two episodes share a CU (the sweep has more episodes than CUs).
+// With one workspace per episode, workgroup x runs episode x.  With fewer
+// workspaces (n_slots < E), workgroup x owns workspace x and takes episodes from
+// the launch's queue counter in index order until none is left, clearing its
+// tables before each one (a workspace's first episode skips that when the
+// caller cleared the tables).
+// The queued loop is a kernel of its own (Queued = true): a loop around the
+// episode keeps more values live across it, and the one-episode kernel keeps
+// its register allocation.
+template <bool Queued>
 __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ EpShared sh;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int e = blockIdx.x;
+    unsigned char* const ws = a.ws + (size_t)blockIdx.x * a.L.per_episode;
+    for (int32_t it = 0;; ++it) {
+    int32_t e = (int32_t)blockIdx.x;
+    if constexpr (Queued) {
+        if (tid == 0)
+            sh.next_e = __hip_atomic_fetch_add((int32_t*)(a.ws + a.L.off_ctl), 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        e = sh.next_e;
+        __syncthreads();
+        if (e >= a.E) break;
+        if (it > 0 || !(a.flags & RK_SIM_TABLES_CLEAR)) {
+            uint4* z = reinterpret_cast<uint4*>(ws + a.L.off_slots);
+            const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+            const uint64_t n16 = (uint64_t)a.W * a.L.slots;
+            for (uint64_t k = tid; k < n16; k += NT) z[k] = zero;
+            __syncthreads();
+        }
+    } else if (it > 0) {
+        break;
+    }
+    [&]() {
     const rk_episode_params prm = a.params[e];
     const int32_t W = a.W, NB = a.NB;
     const bool scan = a.probe_mode == RK_PROBE_SCAN;
@@ -772,7 +809,6 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     const int64_t gc0 = prm.conv_begin;
     const bool lean = !scan && policy == RK_POLICY_ARGMIN && prm.controller == 0 && !freq && !tiers;
 
-    unsigned char* ws = a.ws + (size_t)e * a.L.per_episode;
     Slot* g_slots = (Slot*)(ws + a.L.off_slots);
     uint32_t* g_log = (uint32_t*)(ws + a.L.off_log);
     uint64_t* g_scratch = (uint64_t*)(ws + a.L.off_scratch);
@@ -784,7 +820,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     const uint64_t used_limit = S - S / 4;
     const uint64_t scratch_cap = (uint64_t)a.cache + (uint64_t)a.max_blocks;
 
-    // ---- initial state: empty caches (cleared by episode_clear_kernel before this launch), idle
+    // ---- initial state: empty caches (cleared by episode_clear_kernel before this launch, or by the
+    //      workgroup before a queued episode), idle
     //      workers, every first turn queued
     if (tid < W) {
         s_A[tid] = 0;
@@ -1859,6 +1896,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         tot[7] = cachedsum;
         for (int k = 0; k < 8; ++k) a.out.totals[(int64_t)e * 8 + k] = tot[k];
     }
+    }();
+    __syncthreads();
+    }
 }
 
 }  // namespace rk
@@ -1892,19 +1932,27 @@ static int check_batch_shape(const char* who, const rk_episode_batch* b)
     if ((int64_t)b->cache_blocks + b->max_blocks > (1ll << 29)) return fail(RK_EUNSUPPORTED, "%s: cache too large", who);
     if (b->max_routes < 0) return fail(RK_EINVAL, "%s: max_routes < 0", who);
     if (b->flags & ~RK_SIM_TABLES_CLEAR) return fail(RK_EINVAL, "%s: unknown flags %#x", who, (unsigned)b->flags);
+    if (b->ws_slots < 0 || b->ws_pad != 0) return fail(RK_EINVAL, "%s: ws_slots < 0 or ws_pad != 0", who);
     return RK_OK;
 }
 
-// Enqueue episode_clear_kernel over every episode's tables.
+// Episode workspaces a batch uses: one per episode, or ws_slots when fewer.
+static int32_t batch_slots(const rk_episode_batch* b)
+{
+    return b->ws_slots > 0 && b->ws_slots < b->E ? b->ws_slots : b->E;
+}
+
+// Enqueue episode_clear_kernel over the tables of every workspace the batch uses.
 static int launch_table_clear(const char* who, const rk_episode_batch* b, const EpisodeLayout& L, void* workspace,
                               hipStream_t s)
 {
     const uint64_t n16 = (uint64_t)b->W * L.slots;          // 16-byte slots per episode
     const uint64_t cpe = (n16 + kClearChunk - 1) / kClearChunk;
-    if (cpe * (uint64_t)b->E > 0x7fffffffull)
-        return fail(RK_EUNSUPPORTED, "%s: %d episodes of %llu table slots exceed one clear launch", who, b->E,
-                    (unsigned long long)n16);
-    hipLaunchKernelGGL(episode_clear_kernel, dim3((unsigned)(cpe * (uint64_t)b->E)), dim3(256), 0, s,
+    const uint64_t nws = (uint64_t)batch_slots(b);
+    if (cpe * nws > 0x7fffffffull)
+        return fail(RK_EUNSUPPORTED, "%s: %llu workspaces of %llu table slots exceed one clear launch", who,
+                    (unsigned long long)nws, (unsigned long long)n16);
+    hipLaunchKernelGGL(episode_clear_kernel, dim3((unsigned)(cpe * nws)), dim3(256), 0, s,
                        (unsigned char*)workspace, L.per_episode, L.off_slots, n16, (uint32_t)cpe);
     return hip_check(hipGetLastError(), who);
 }
@@ -1917,7 +1965,7 @@ extern "C" int rk_simulate_clear_tables(const rk_episode_batch* b, void* workspa
     if (b->E == 0) return RK_OK;
     if (!workspace) return fail(RK_EINVAL, "rk_simulate_clear_tables: NULL workspace");
     const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv, b->max_routes);
-    const size_t need = L.per_episode * (size_t)b->E;
+    const size_t need = L.per_episode * (size_t)batch_slots(b);
     if (ws_bytes < need)
         return fail(RK_ENOMEM, "rk_simulate_clear_tables: workspace %zu bytes < %zu needed", ws_bytes, need);
     return launch_table_clear("rk_simulate_clear_tables", b, L, workspace, (hipStream_t)stream);
@@ -1933,7 +1981,8 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     if (!b->params || !b->turn_off || !b->turn_blocks || !b->chain_off || !b->chains || !workspace)
         return fail(RK_EINVAL, "rk_simulate_episodes: NULL array");
     const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv, b->max_routes);
-    const size_t need = L.per_episode * (size_t)b->E;
+    const int32_t n_slots = batch_slots(b);
+    const size_t need = L.per_episode * (size_t)n_slots;
     if (ws_bytes < need)
         return fail(RK_ENOMEM, "rk_simulate_episodes: workspace %zu bytes < %zu needed", ws_bytes, need);
     int32_t* st = status_word();
@@ -1951,6 +2000,8 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.probe_mode = b->probe_mode;
     a.tiers = b->tiers;
     a.max_routes = b->max_routes;
+    a.n_slots = n_slots;
+    a.flags = b->flags;
     a.params = b->params;
     a.turn_off = b->turn_off;
     a.turn_blocks = b->turn_blocks;
@@ -1982,10 +2033,17 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.NB = NB;
     const size_t lds = o + batch_layout(NB, b->W, tiers).bytes;
     hipStream_t s = (hipStream_t)stream;
-    if (!(b->flags & RK_SIM_TABLES_CLEAR)) {
+    if (n_slots < b->E) {
+        // queued episodes: each workgroup clears its own tables before an episode
+        hipLaunchKernelGGL(episode_queue_init, dim3(1), dim3(64), 0, s,
+                           (int32_t*)((unsigned char*)workspace + L.off_ctl));
+        rc = hip_check(hipGetLastError(), "rk_simulate_episodes queue init");
+        if (rc) return rc;
+    } else if (!(b->flags & RK_SIM_TABLES_CLEAR)) {
         rc = launch_table_clear("rk_simulate_episodes clear launch", b, L, workspace, s);
         if (rc) return rc;
     }
-    hipLaunchKernelGGL(episode_kernel, dim3((unsigned)b->E), dim3(NT), lds, s, a);
+    if (n_slots < b->E) hipLaunchKernelGGL(episode_kernel<true>, dim3((unsigned)n_slots), dim3(NT), lds, s, a);
+    else hipLaunchKernelGGL(episode_kernel<false>, dim3((unsigned)n_slots), dim3(NT), lds, s, a);
     return hip_check(hipGetLastError(), "rk_simulate_episodes launch");
 }

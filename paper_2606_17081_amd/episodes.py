@@ -20,7 +20,8 @@ from .workload import POA_PARAMS, EpisodeSpec, Workload, flatten_traces, route_r
 class EpisodeRunner:
     def __init__(self, workload: Workload, episodes: Optional[Sequence[EpisodeSpec]] = None,
                  probe_mode: int = rk.RK_PROBE_PREFIX, poa_params: Optional[dict] = None,
-                 keep_cost: bool = True, device=None, chains: Optional[np.ndarray] = None):
+                 keep_cost: bool = True, device=None, chains: Optional[np.ndarray] = None,
+                 ws_slots: int = 0):
         torch = rk._torch()
         self.torch = torch
         self.device = torch.device("cuda") if device is None else torch.device(device)
@@ -98,7 +99,11 @@ class EpisodeRunner:
         self.tiers = any(sp.tier_g1 > 0 for sp in self.episodes)
         self.tier_overlap = z((R, W, 2), torch.int32) if self.tiers else None
         self.max_routes = max([n for (_, n, _, _) in self.rows] + [0])
-        ws = rk.simulate_workspace_size(E, W, self.cache_blocks, self.max_blocks, self.max_conv, self.max_routes)
+        # ws_slots < E: that many episode workspaces, reused by the workgroups that take the
+        # episodes in turn (a batch larger than device memory runs in one launch)
+        self.ws_slots = int(ws_slots) if 0 < int(ws_slots) < E else 0
+        n_ws = self.ws_slots if self.ws_slots else E
+        ws = rk.simulate_workspace_size(n_ws, W, self.cache_blocks, self.max_blocks, self.max_conv, self.max_routes)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
 
         self.win_off = up(np.array(win_off, np.int64), torch.int64)
@@ -116,7 +121,7 @@ class EpisodeRunner:
         P = rk._ptr
         self.batch = rk.EpisodeBatch(E, W, self.cache_blocks, self.max_blocks, self.max_conv,
                                      self.max_inflight, self.max_rps, self.max_ctrl_window, probe_mode,
-                                     int(self.tiers), self.max_routes, 0,
+                                     int(self.tiers), self.max_routes, 0, self.ws_slots, 0,
                                      P(self.params), P(self.turn_off), P(self.turn_blocks), P(self.chain_off),
                                      P(self.chains), P(self.route_rand), rk.regime_params(self.regime))
         self.outputs = rk.EpisodeOutputs(P(self.route_turn), P(self.route_worker), P(self.route_step),

@@ -62,7 +62,7 @@ class EpisodeBatch(C.Structure):
                 ("max_blocks", C.c_int32), ("max_conv", C.c_int32), ("max_inflight", C.c_int32),
                 ("max_routes_per_step", C.c_int32), ("max_ctrl_window", C.c_int32),
                 ("probe_mode", C.c_int32), ("tiers", C.c_int32), ("max_routes", C.c_int32),
-                ("flags", C.c_int32),
+                ("flags", C.c_int32), ("ws_slots", C.c_int32), ("ws_pad", C.c_int32),
                 ("params", C.c_void_p), ("turn_off", C.c_void_p), ("turn_blocks", C.c_void_p),
                 ("chain_off", C.c_void_p), ("chains", C.c_void_p), ("route_rand", C.c_void_p),
                 ("regime", RegimeParams)]

@@ -483,3 +483,78 @@ def test_lean_decision_loop_matches_full(gpu, name):
         assert rk.device_status(reset=True) == 0
     for k, (a, b) in enumerate(zip(*outs)):
         assert np.array_equal(a, b), f"output {k} differs between the lean and the full decision loop"
+
+
+def test_queued_workspaces_match(gpu, orc):
+    """Fewer episode workspaces than episodes: 7 workgroups take 160 saturation
+    episodes in turn, each clearing its workspace's tables before every episode
+    (and, with RK_SIM_TABLES_CLEAR after rk_simulate_clear_tables, skipping the
+    clear of its first one).  Every output equals the launch with one workspace
+    per episode, and episodes run before and after a workspace changed hands
+    (the first 7 and the last ones of the queue) match the oracle."""
+    torch, rk = gpu
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    w = wl.saturation_workload(seeds=range(4))
+    say("saturation, one workspace per episode:", len(w.episodes), "episodes")
+    ref = _run(gpu, w)
+    n, E = ref.n_rows, len(w.episodes)
+    want = [t[:n].cpu().numpy() for t in (ref.route_worker, ref.overlap, ref.evict_count, ref.evict_digest,
+                                          ref.last_hash)]
+    want += [ref.cost[:n].cpu().numpy().view(np.uint32), ref.totals[:E].cpu().numpy(), ref.poa_hat[:E].cpu().numpy()]
+    r = EpisodeRunner(w, ws_slots=7)
+    assert r.workspace.numel() == rk.simulate_workspace_size(7, w.W, w.cache_blocks, r.max_blocks, r.max_conv,
+                                                             r.max_routes)
+    r.hash()
+    for rep in range(3):
+        say("7 workspaces, pass", rep)
+        for t in (r.route_worker, r.overlap, r.cost, r.evict_digest, r.totals, r.poa_hat):
+            t.zero_()
+        if rep == 2:
+            r.clear_tables()
+        r.simulate(tables_clear=rep == 2)
+        r.poa()
+        torch.cuda.synchronize()
+        _status_clean(rk)
+        got = [t[:n].cpu().numpy() for t in (r.route_worker, r.overlap, r.evict_count, r.evict_digest,
+                                             r.last_hash)]
+        got += [r.cost[:n].cpu().numpy().view(np.uint32), r.totals[:E].cpu().numpy(), r.poa_hat[:E].cpu().numpy()]
+        for k, (a, b) in enumerate(zip(want, got)):
+            assert np.array_equal(a, b), f"output {k} differs with 7 workspaces (pass {rep})"
+    cache = {}
+    for e in list(range(7)) + [E - 41, E - 1]:
+        sp = r.episodes[e]
+        say("oracle episode", e, "C", sp.concurrency, "w_ov", sp.w_ov)
+        o = _oracle_episode(orc, w, sp, cache)
+        _compare_episode(r.episode_results(e), o, w.W, window=sp.concurrency, label=f"queued e{e}")
+
+
+def test_saturation_full_launch_sampled(gpu, orc):
+    """All 10,240 saturation / controller episodes in one launch on 512 episode
+    workspaces (the benchmark's configuration); sampled episodes of every
+    concurrency level against the oracle, the first and the last of the queue
+    among them."""
+    torch, rk = gpu
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    say("generating 256 saturation traces")
+    w = wl.saturation_workload()
+    say("running", len(w.episodes), "episodes on 512 workspaces")
+    r = EpisodeRunner(w, ws_slots=512)
+    r.step()
+    torch.cuda.synchronize()
+    _status_clean(rk)
+    E = len(r.episodes)
+    idx = {(sp.seed, sp.concurrency, sp.w_ov): e for e, sp in enumerate(r.episodes)}
+    keys = [(0, 8, 0.0), (200, 8, 1.0), (255, 16, 2.0), (17, 32, 0.25), (99, 64, 0.5), (128, 128, 1.0),
+            (64, 256, 0.0), (3, 512, 2.0), (255, 1024, 2.0)]
+    cache = {}
+    for key in keys:
+        e = idx[key]
+        say("oracle episode", e, key)
+        o = _oracle_episode(orc, w, r.episodes[e], cache)
+        _compare_episode(r.episode_results(e), o, w.W, window=key[1], label=f"saturation {key}")
+    assert idx[(255, 1024, 2.0)] == E - 1
+    P = r.route_blocks[: r.n_rows].cpu().numpy()
+    ov = r.overlap[: r.n_rows].cpu().numpy()
+    assert np.all(ov >= 0) and np.all(ov <= P[:, None])
+    tot = r.totals[:E].cpu().numpy()
+    assert tot[:, 3].sum() > 0 and tot[:, 1].sum() > 0     # the controller fires, some episodes evict
