@@ -463,6 +463,25 @@ int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_t n_episode
                     double* selfish_out, double* coord_out, double* poa_hat_out,
                     void* workspace, size_t ws_bytes, void* stream);
 
+/* rk_poa_estimate without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, outputs and results as
+ * rk_poa_estimate minus workspace and ws_bytes: its scratch (the frozen
+ * matrices, the dispatch order and, when selfish_out or coord_out is NULL, the
+ * window sums) lives in a static device buffer of RK_POA_NOALLOC_BYTES that
+ * the library holds on each device it runs on until the process ends.  The
+ * call allocates nothing.  A shape whose rk_poa_workspace_size(n_rows, W)
+ * exceeds RK_POA_NOALLOC_BYTES returns RK_EUNSUPPORTED before any launch.
+ * Every call on one device shares that device's buffer and leaves its
+ * contents behind: calls that overlap on one GPU (e.g. on two streams) race,
+ * so the caller orders them. */
+#define RK_POA_NOALLOC_BYTES (64u << 20)
+int rk_poa_estimate_noalloc(int32_t n_windows, const int64_t* win_off, int32_t n_episodes,
+                            const int64_t* ep_win_off, int64_t n_rows, int32_t max_window, int32_t W,
+                            const int32_t* route_worker, const int32_t* overlap,
+                            const int32_t* route_blocks, rk_poa_params params,
+                            double* selfish_out, double* coord_out, double* poa_hat_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,6 +18,8 @@
 // by size class), since the longest ones set the length of the launch.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "rk_internal.h"
 
 namespace rk {
@@ -379,28 +381,40 @@ static void launch_windows(int32_t W, unsigned grid, size_t lds, hipStream_t s, 
     else hipLaunchKernelGGL((poa_window_kernel<LDSMAT, 64>), dim3(grid), dim3(PT), lds, s, a);
 }
 
-extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_t n_episodes,
-                               const int64_t* ep_win_off, int64_t n_rows, int32_t max_window, int32_t W,
-                               const int32_t* route_worker, const int32_t* overlap, const int32_t* route_blocks,
-                               rk_poa_params params, double* selfish_out, double* coord_out, double* poa_hat_out,
-                               void* workspace, size_t ws_bytes, void* stream)
+// Argument checks shared by rk_poa_estimate and rk_poa_estimate_noalloc;
+// RK_OK with *nothing set when there is no work.
+static int poa_check(const char* who, int32_t n_windows, const int64_t* win_off, int32_t n_episodes,
+                     const int64_t* ep_win_off, int64_t n_rows, int32_t max_window, int32_t W,
+                     const int32_t* route_worker, const int32_t* overlap, const int32_t* route_blocks,
+                     const rk_poa_params& params, const double* poa_hat_out, bool* nothing)
 {
-    if (n_windows < 0 || n_episodes < 0 || n_rows < 0) return fail(RK_EINVAL, "rk_poa_estimate: negative count");
-    if (W < 1 || W > 64) return fail(RK_EUNSUPPORTED, "rk_poa_estimate: W outside 1..64");
-    if (max_window < 1 || max_window > 4096) return fail(RK_EUNSUPPORTED, "rk_poa_estimate: max_window outside 1..4096");
-    if (params.beta < 1 || params.beta > 64) return fail(RK_EINVAL, "rk_poa_estimate: beta outside 1..64");
-    if (params.K_fixed < 0) return fail(RK_EINVAL, "rk_poa_estimate: K_fixed < 0");
-    if (n_windows == 0 && n_episodes == 0) return RK_OK;
+    *nothing = false;
+    if (n_windows < 0 || n_episodes < 0 || n_rows < 0) return fail(RK_EINVAL, "%s: negative count", who);
+    if (W < 1 || W > 64) return fail(RK_EUNSUPPORTED, "%s: W outside 1..64", who);
+    if (max_window < 1 || max_window > 4096) return fail(RK_EUNSUPPORTED, "%s: max_window outside 1..4096", who);
+    if (params.beta < 1 || params.beta > 64) return fail(RK_EINVAL, "%s: beta outside 1..64", who);
+    if (params.K_fixed < 0) return fail(RK_EINVAL, "%s: K_fixed < 0", who);
+    if (n_windows == 0 && n_episodes == 0) {
+        *nothing = true;
+        return RK_OK;
+    }
     if (n_episodes > 0 && (!ep_win_off || !poa_hat_out))
-        return fail(RK_EINVAL, "rk_poa_estimate: episodes need ep_win_off and poa_hat_out");
-    if (n_windows > 0 && (!win_off || !route_worker || !overlap || !route_blocks || !workspace))
-        return fail(RK_EINVAL, "rk_poa_estimate: NULL array");
-    const size_t need = rk_poa_workspace_size(n_rows, W);
-    if (ws_bytes < need) return fail(RK_ENOMEM, "rk_poa_estimate: workspace %zu bytes < %zu", ws_bytes, need);
+        return fail(RK_EINVAL, "%s: episodes need ep_win_off and poa_hat_out", who);
+    if (n_windows > 0 && (!win_off || !route_worker || !overlap || !route_blocks))
+        return fail(RK_EINVAL, "%s: NULL array", who);
+    return RK_OK;
+}
+
+// The launches of one estimate on a checked workspace of at least
+// rk_poa_workspace_size(n_rows, W) bytes.
+static int poa_launch(int32_t n_windows, const int64_t* win_off, int32_t n_episodes, const int64_t* ep_win_off,
+                      int64_t n_rows, int32_t max_window, int32_t W, const int32_t* route_worker,
+                      const int32_t* overlap, const int32_t* route_blocks, rk_poa_params params,
+                      double* selfish_out, double* coord_out, double* poa_hat_out, unsigned char* ws, void* stream)
+{
     int32_t* st = status_word();
     if (!st) return fail(RK_EHIP, "rk_poa_estimate: no status word");
 
-    unsigned char* ws = (unsigned char*)workspace;
     const size_t cm_bytes = align_up((size_t)n_rows * (size_t)W * sizeof(float), 256);
     const size_t vec_bytes = align_up(((size_t)n_rows + 1) * sizeof(double), 256);
     double* selfish = selfish_out ? selfish_out : (double*)(ws + cm_bytes + 256);
@@ -460,4 +474,79 @@ extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_
         return hip_check(hipGetLastError(), "rk_poa_estimate episode launch");
     }
     return RK_OK;
+}
+
+extern "C" int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_t n_episodes,
+                               const int64_t* ep_win_off, int64_t n_rows, int32_t max_window, int32_t W,
+                               const int32_t* route_worker, const int32_t* overlap, const int32_t* route_blocks,
+                               rk_poa_params params, double* selfish_out, double* coord_out, double* poa_hat_out,
+                               void* workspace, size_t ws_bytes, void* stream)
+{
+    bool nothing;
+    int rc = poa_check("rk_poa_estimate", n_windows, win_off, n_episodes, ep_win_off, n_rows, max_window, W,
+                       route_worker, overlap, route_blocks, params, poa_hat_out, &nothing);
+    if (rc || nothing) return rc;
+    if (n_windows > 0 && !workspace) return fail(RK_EINVAL, "rk_poa_estimate: NULL workspace");
+    const size_t need = rk_poa_workspace_size(n_rows, W);
+    if (ws_bytes < need) return fail(RK_ENOMEM, "rk_poa_estimate: workspace %zu bytes < %zu", ws_bytes, need);
+    return poa_launch(n_windows, win_off, n_episodes, ep_win_off, n_rows, max_window, W, route_worker, overlap,
+                      route_blocks, params, selfish_out, coord_out, poa_hat_out, (unsigned char*)workspace, stream);
+}
+
+// ---- the estimate without a caller workspace (for callers that cannot allocate)
+//
+// The workspace is a file-scope device array; each device holds its own copy
+// until the process ends.  Host code never passes the array's name to a kernel
+// (on the host it only stands for the symbol): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+
+static __device__ __align__(256) unsigned char scratch[RK_POA_NOALLOC_BYTES];
+
+static std::mutex g_scratch_mu;
+static unsigned char* g_scratch_addr[64];
+
+static unsigned char* scratch_address(int* err)
+{
+    int dev = 0;
+    *err = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        *err = 1;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        unsigned char* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) {
+            *err = 2;
+            return nullptr;
+        }
+        g_scratch_addr[dev] = ptr;
+    }
+    return g_scratch_addr[dev];
+}
+
+extern "C" int rk_poa_estimate_noalloc(int32_t n_windows, const int64_t* win_off, int32_t n_episodes,
+                                       const int64_t* ep_win_off, int64_t n_rows, int32_t max_window, int32_t W,
+                                       const int32_t* route_worker, const int32_t* overlap,
+                                       const int32_t* route_blocks, rk_poa_params params, double* selfish_out,
+                                       double* coord_out, double* poa_hat_out, void* stream)
+{
+    bool nothing;
+    int rc = poa_check("rk_poa_estimate_noalloc", n_windows, win_off, n_episodes, ep_win_off, n_rows, max_window,
+                       W, route_worker, overlap, route_blocks, params, poa_hat_out, &nothing);
+    if (rc || nothing) return rc;
+    const size_t need = rk_poa_workspace_size(n_rows, W);
+    if (need > (size_t)RK_POA_NOALLOC_BYTES)
+        return fail(RK_EUNSUPPORTED,
+                    "rk_poa_estimate_noalloc: %lld rows x %d workers need %zu bytes of workspace, more than the "
+                    "%zu of the static buffer (use rk_poa_estimate with a workspace)",
+                    (long long)n_rows, W, need, (size_t)RK_POA_NOALLOC_BYTES);
+    int err = 0;
+    unsigned char* ws = scratch_address(&err);
+    if (!ws)
+        return fail(RK_EHIP, "rk_poa_estimate_noalloc: %s", err == 1 ? "no current device"
+                                                                      : "hipGetSymbolAddress of the buffer failed");
+    return poa_launch(n_windows, win_off, n_episodes, ep_win_off, n_rows, max_window, W, route_worker, overlap,
+                      route_blocks, params, selfish_out, coord_out, poa_hat_out, ws, stream);
 }

@@ -29,7 +29,9 @@ DEV_BITS = {0x1: "bad offsets", 0x2: "short input", 0x4: "zero key", 0x8: "table
 EXPORTED = ("rk_status_string", "rk_last_error", "rk_device_status", "rk_hash_chains",
             "rk_table_build", "rk_route_score_batch", "rk_index_build", "rk_route_score_index",
             "rk_simulate_workspace_size",
-            "rk_simulate_episodes", "rk_simulate_clear_tables", "rk_poa_workspace_size", "rk_poa_estimate")
+            "rk_simulate_episodes", "rk_simulate_clear_tables", "rk_poa_workspace_size", "rk_poa_estimate",
+            "rk_poa_estimate_noalloc")
+RK_POA_NOALLOC_BYTES = 64 << 20
 
 
 class RkError(RuntimeError):
@@ -128,6 +130,9 @@ def lib():
             L.rk_poa_estimate.restype = C.c_int
             L.rk_poa_estimate.argtypes = [i32, vp, i32, vp, i64, i32, i32, vp, vp, vp, PoaParams,
                                           vp, vp, vp, vp, sz, vp]
+            L.rk_poa_estimate_noalloc.restype = C.c_int
+            L.rk_poa_estimate_noalloc.argtypes = [i32, vp, i32, vp, i64, i32, i32, vp, vp, vp, PoaParams,
+                                                  vp, vp, vp, vp]
             _lib = L
     return _lib
 
@@ -336,3 +341,15 @@ def poa_estimate(win_off, ep_win_off, n_rows: int, max_window: int, W: int, rout
                                  _ptr(selfish), _ptr(coord), _ptr(poa_hat), _ptr(workspace),
                                  workspace.numel() * workspace.element_size(), _stream(stream)),
            "rk_poa_estimate")
+
+
+def poa_estimate_noalloc(win_off, ep_win_off, n_rows: int, max_window: int, W: int, route_worker, overlap,
+                         route_blocks, params: PoaParams, selfish, coord, poa_hat, stream=None):
+    """poa_estimate on the library's static device buffer (rk_poa_estimate_noalloc):
+    no workspace argument, nothing allocated by the call."""
+    n_windows = win_off.numel() - 1
+    n_eps = 0 if ep_win_off is None else ep_win_off.numel() - 1
+    _check(lib().rk_poa_estimate_noalloc(n_windows, _ptr(win_off), n_eps, _ptr(ep_win_off), n_rows, max_window, W,
+                                         _ptr(route_worker), _ptr(overlap), _ptr(route_blocks), params,
+                                         _ptr(selfish), _ptr(coord), _ptr(poa_hat), _stream(stream)),
+           "rk_poa_estimate_noalloc")
