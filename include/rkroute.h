@@ -296,8 +296,9 @@ typedef struct {
                                 G3 holds the rest of the cache                      */
     float   tier_w[3];       /* prefill weight of a cached block in G1, G2, G3, >= 0 */
     int32_t tier_pad;        /* 0                                                    */
-} rk_episode_params;         /* 104 bytes; invalid policy, eviction or tier fields set
-                                RK_DEV_BAD_PARAMS and leave the episode's outputs
+} rk_episode_params;         /* 104 bytes; invalid policy, eviction or tier fields, or a
+                                negative or NaN weight (w_ov, w_act, w_sat, ctrl_w_ov),
+                                set RK_DEV_BAD_PARAMS and leave the episode's outputs
                                 unwritten                                             */
 
 #define RK_EVICT_LRU          0

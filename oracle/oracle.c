@@ -582,6 +582,8 @@ int orc_simulate_episode(int32_t W, int32_t cache_blocks, int32_t H, int32_t rou
     if (W < 1 || cache_blocks < 1 || H < 1 || routes_per_step < 1 || cap < 1 || n_conv < 0)
         return ORC_EINVAL;
     if (controller < 0 || controller > 2) return ORC_EINVAL;
+    /* the weights of the cost are non-negative (NaN rejected as well) */
+    if (!(w_ov >= 0.0f) || !(w_act >= 0.0f) || !(w_sat >= 0.0f) || !(ctrl_w_ov >= 0.0f)) return ORC_EINVAL;
     if (controller == 1 && (ctrl_window < 1 || ctrl_den < 1 || ctrl_num < 0)) return ORC_EINVAL;
     if (controller == 2) {
         if (!rg_d || !rg_i || !rg_f) return ORC_EINVAL;

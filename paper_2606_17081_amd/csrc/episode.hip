@@ -798,7 +798,10 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     const bool tiers_ok = prm.tier_g1 >= 0 && prm.tier_g2 >= 0 && (int64_t)prm.tier_g1 + prm.tier_g2 <= a.cache &&
                           (!tiers || (a.tiers != 0 && !freq && prm.tier_w[0] >= 0.0f && prm.tier_w[1] >= 0.0f &&
                                       prm.tier_w[2] >= 0.0f));
-    if (prm.controller < 0 || prm.controller > 2 || !rg_ok || !tiers_ok ||
+    // negative or NaN weights would break the argmin on cost bits (unsigned order is float order only
+    // for costs >= 0)
+    const bool weights_ok = prm.w_ov >= 0.0f && prm.w_act >= 0.0f && prm.w_sat >= 0.0f && prm.ctrl_w_ov >= 0.0f;
+    if (prm.controller < 0 || prm.controller > 2 || !rg_ok || !tiers_ok || !weights_ok ||
         (prm.evict_policy != RK_EVICT_LRU && !freq) || (freq && dsteps < 1) ||
         (!regime_ctl && (policy < RK_POLICY_ARGMIN || policy > RK_POLICY_P2C ||
                          (policy == RK_POLICY_SOFTMAX && !(tau > 0.0f)))) ||

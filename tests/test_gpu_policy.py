@@ -101,6 +101,14 @@ def test_bad_policy_parameters_flagged(gpu):
         torch.cuda.synchronize()
         bits = rk.device_status(reset=True)
         assert bits & 0x40, (p, tau, bits)
+    # negative or NaN weights (the argmin orders costs by their bits, which needs costs >= 0)
+    for field, value in (("w_ov", -1.0), ("w_act", -0.5), ("w_sat", float("nan")), ("ctrl_w_ov", -0.25)):
+        sp = wl.EpisodeSpec(seed=0, concurrency=8, cap=512, **{field: value})
+        r = EpisodeRunner(base, [sp])
+        r.simulate()
+        torch.cuda.synchronize()
+        assert rk.device_status(reset=True) & 0x40, field
+        assert int(r.totals[0, 2]) == 0, field          # outputs left unwritten
     # a policy that draws, launched without draws
     sp = wl.EpisodeSpec(seed=0, concurrency=8, cap=512, policy=wl.POLICY_RANDOM)
     r = EpisodeRunner(base, [sp])

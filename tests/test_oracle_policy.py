@@ -99,6 +99,14 @@ def test_bad_policies_rejected(orc):
         orc.simulate_trace(4, 256, wl.EpisodeSpec(seed=0, concurrency=8, policy=7), tr)
 
 
+@pytest.mark.parametrize("field,value", [("w_ov", -1.0), ("w_act", -0.5), ("w_sat", float("nan")),
+                                         ("ctrl_w_ov", -0.25)])
+def test_negative_or_nan_weights_rejected(orc, field, value):
+    tr = wl.tiny_trace(0)
+    with pytest.raises(ValueError):
+        orc.simulate_trace(4, 256, wl.EpisodeSpec(seed=0, concurrency=8, **{field: value}), tr)
+
+
 @pytest.mark.parametrize("policy,tau", [(SOFTMAX, 0.5), (SOFTMAX, 4.0), (RR, 0.0), (RANDOM, 0.0), (P2C, 0.0)])
 @pytest.mark.parametrize("seed", range(6))
 def test_episode_policies_match_twin(orc, policy, tau, seed):
