@@ -98,9 +98,12 @@ struct EpArgs {
 
 constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 
-template <bool V>
+// Which copy of the decision loop runs: 0 the full one, 1 the lean one (prefix
+// mode, argmin, LRU, no tiers, no controller), 2 the lean one with the load
+// controller.
+template <int V>
 struct LeanTag {
-    static constexpr bool value = V;
+    static constexpr int value = V;
 };
 
 struct EpShared {
@@ -811,6 +814,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     }
     const int64_t gc0 = prm.conv_begin;
     const bool lean = !scan && policy == RK_POLICY_ARGMIN && prm.controller == 0 && !freq && !tiers;
+    const bool lean_ctrl = !scan && policy == RK_POLICY_ARGMIN && prm.controller == 1 && !freq && !tiers;
 
     Slot* g_slots = (Slot*)(ws + a.L.off_slots);
     uint32_t* g_log = (uint32_t*)(ws + a.L.off_log);
@@ -1484,13 +1488,15 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         const int32_t t0 = t;
         int32_t event = EV_BATCH;
         // ---- B. the decisions of wavefront 0 (below).  LN: the episode runs in prefix
-        // mode, routed by argmin under LRU, without memory tiers or a controller; that
-        // copy of the decision loop is compiled with those features switched off,
-        // which shortens the serial decision chain.
+        // mode, routed by argmin under LRU, without memory tiers or the regime controller
+        // (LC: with the load controller, else without); those copies of the decision loop
+        // are compiled with the other features switched off, which shortens the serial
+        // decision chain.
         auto decide = [&](auto lean_tag) {
-            constexpr bool LN = decltype(lean_tag)::value;
+            constexpr bool LN = decltype(lean_tag)::value != 0;
+            constexpr bool LC = decltype(lean_tag)::value == 2;
             const bool freq_d = !LN && freq, tiers_d = !LN && tiers, regime_d = !LN && regime_ctl, scan_d = !LN && scan;
-            const bool ctrl1_d = !LN && prm.controller == 1;
+            const bool ctrl1_d = LC || (!LN && prm.controller == 1);
             const int32_t policy_d = LN ? RK_POLICY_ARGMIN : policy;
             event = EV_BATCH;
             // lane j < W keeps worker j's load, log tail and block counts in registers
@@ -1797,8 +1803,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         };
         for (;;) {
             if (wave == 0) {
-                if (lean) decide(LeanTag<true>{});
-                else decide(LeanTag<false>{});
+                if (lean) decide(LeanTag<1>{});
+                else if (lean_ctrl) decide(LeanTag<2>{});
+                else decide(LeanTag<0>{});
             } else {
                 writer();
             }
