@@ -396,7 +396,7 @@ def sweep_bench(torch, rk, wl, stream, steps, warmup):
 
     side = torch.cuda.Stream()
     t_sim = KernelTimer(torch, stream)
-    t_hash, t_clear, t_poa = KernelTimer(torch, side), KernelTimer(torch, side), KernelTimer(torch, side)
+    t_hash, t_poa = KernelTimer(torch, side), KernelTimer(torch, side)
     e_sim = [None] * steps
 
     def prepare(k):
@@ -405,8 +405,6 @@ def sweep_bench(torch, rk, wl, stream, steps, warmup):
             side.wait_event(e_sim[k - 2])
         with t_hash:
             r.hash(stream=side)
-        with t_clear:
-            r.clear_tables(stream=side)
         ready = torch.cuda.Event()
         ready.record(side)
         return ready
@@ -418,7 +416,7 @@ def sweep_bench(torch, rk, wl, stream, steps, warmup):
         r = runners[k % 2]
         stream.wait_event(ready)
         with t_sim:
-            r.simulate(stream=stream, tables_clear=True)
+            r.simulate(stream=stream)
         done = torch.cuda.Event()
         done.record(stream)
         e_sim[k] = done
@@ -435,11 +433,7 @@ def sweep_bench(torch, rk, wl, stream, steps, warmup):
         assert torch.equal(r.route_worker[:n0], ref_route), "pipelined steps differ from the sequential step (routes)"
     ms_step = wall * 1e3 / steps
     stage = dict(hash=t_hash.mean_ms(), simulate=t_sim.mean_ms(), poa=t_poa.mean_ms())
-    clear_ms = t_clear.mean_ms()
-    live_max = runner.cache_blocks + runner.max_blocks
-    S = 1 << int(np.ceil(np.log2(2 * live_max)))
-    clear_bytes = float(E0 * runner.W * S * 16)
-    log(f"sweep step {ms_step:.3f} ms; stages {stage}; table clear {clear_ms:.3f} ms on the second stream")
+    log(f"sweep step {ms_step:.3f} ms; stages {stage}")
     poa_hat = runner.poa_hat[:E0].cpu().numpy()
     per_C = {}
     for C in wl.SWEEP70B_C:
@@ -456,10 +450,7 @@ def sweep_bench(torch, rk, wl, stream, steps, warmup):
         "scorings_per_s": n0 * runner.W / (ms_step * 1e-3), "episodes_per_s": E0 / (ms_step * 1e-3),
         "stage_ms": {k: round(v, 4) for k, v in stage.items()},
         "pipeline": "two runners take turns: step k's episodes on the main stream while the second stream "
-                    "runs step k-1's PoA-hat and hashes and clears step k+1's tables",
-        "table_clear": {"kernel": "episode_clear_kernel", "avg_ms": round(clear_ms, 4),
-                        "algorithmic_bytes": clear_bytes,
-                        "frac": round(clear_bytes / (clear_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)},
+                    "runs step k-1's PoA-hat and hashes step k+1's traces",
         "roofline": roofline("episode_kernel", "sweep70b", sv["bytes"], stage["simulate"],
                              kernel_model_bytes=kb,
                              kernel_model_frac=round(kb / sim_s / 1e9 / HBM_PEAK_GBS, 6)),

@@ -341,14 +341,13 @@ typedef struct {
     int32_t tiers;                   /* nonzero when some episode has tier_g1 > 0: the
                                         launch then keeps tier overlaps in LDS          */
     int32_t max_routes;              /* upper bound on any episode's routes (turns), >= 0 */
-    int32_t flags;                   /* RK_SIM_TABLES_CLEAR or 0                        */
+    int32_t flags;                   /* 0 (no flags are defined)                        */
     int32_t ws_slots;                /* episode workspaces the workspace holds: 0 (or >= E)
                                         means one per episode; 1 <= ws_slots < E runs the
                                         batch on ws_slots workgroups, each taking the next
                                         episode in index order when it finishes one and
-                                        reusing its workspace (its cache tables cleared
-                                        by the workgroup before each episode), so that a
-                                        batch larger than device memory runs in one call  */
+                                        reusing its workspace, so that a batch larger than
+                                        device memory runs in one call                   */
     int32_t ws_pad;                  /* 0                                               */
     const rk_episode_params* params; /* [E], device                                     */
     const int64_t* turn_off;         /* turns of conversation c: turn_off[c] .. turn_off[c+1]-1 */
@@ -390,36 +389,23 @@ typedef struct {
 size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache_blocks,
                                   int32_t max_blocks, int32_t max_conv, int32_t max_routes);
 
-/* batch.flags: the workspace's cache tables are already empty for this batch,
- * cleared by rk_simulate_clear_tables after the workspace's last use, so
- * rk_simulate_episodes skips clearing them (with ws_slots, for the first
- * episode that runs in each workspace).  Without the flag it clears them
- * first, on its own stream (with ws_slots, each workgroup clears its own
- * before every episode). */
-#define RK_SIM_TABLES_CLEAR 1
-
 /* Run E independent episodes, one workgroup each (Section 4.3: sequential
  * greedy routing; Section 2.2: the router cost and the KV cache it reads).
  * `batch` and `out` are HOST structs holding device pointers; `workspace` is
  * device memory of at least rk_simulate_workspace_size(min(E, ws_slots or E),
- * ...) bytes (contents need not be initialised, except that with
- * RK_SIM_TABLES_CLEAR the cache tables must have been cleared by
- * rk_simulate_clear_tables).  Results do not depend on ws_slots.  Calls that
- * share a workspace must not overlap.  Unknown flag bits, ws_slots < 0 or
- * ws_pad != 0: RK_EINVAL. */
+ * ...) bytes whose contents need not be initialised: an episode clears the
+ * parts of its workspace it uses.  Results do not depend on ws_slots.  Calls
+ * that share a workspace must not overlap.  Nonzero flags, ws_slots < 0 or
+ * ws_pad != 0: RK_EINVAL.
+ * While a worker has not evicted yet (under LRU, in prefix mode), its cached
+ * set is kept as runs, one per route that added blocks (the route's blocks
+ * past its overlap, found again by a walk over the runs); at its first
+ * eviction, and from the start for frequency eviction, memory tiers and
+ * RK_PROBE_SCAN, it is kept block by block with its recency.  The results are
+ * the same either way. */
 int rk_simulate_episodes(const rk_episode_batch* batch /* host */,
                          const rk_episode_outputs* out /* host */,
                          void* workspace, size_t ws_bytes, void* stream);
-
-/* Clear the cache tables of a workspace for `batch` (the same shape fields,
- * ws_slots included, as the rk_simulate_episodes call that will use it; its
- * pointers and params are not read), enqueued on `stream`, so that a later rk_simulate_episodes with
- * RK_SIM_TABLES_CLEAR need not: a caller can clear on another stream while it
- * hashes the next chains.  The caller orders the two calls (e.g. with an
- * event) and keeps the workspace unused in between.  Validation as for
- * rk_simulate_episodes' shape fields; ws_bytes too small: RK_ENOMEM. */
-int rk_simulate_clear_tables(const rk_episode_batch* batch /* host */, void* workspace, size_t ws_bytes,
-                             void* stream);
 
 /* ----------------------------------------------------------------- PoA-hat
  * For each window w of consecutive routes rows win_off[w] .. win_off[w+1]-1

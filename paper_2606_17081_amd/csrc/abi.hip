@@ -54,6 +54,7 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     uint64_t live_max = (uint64_t)cache_blocks + (uint64_t)max_blocks;
     L.slots = next_pow2(2 * live_max);
     L.ring = next_pow2(2 * live_max);
+    L.runs = next_pow2(2 * (uint64_t)(max_routes > 2 ? max_routes : 2));   // at most one run per route
     size_t o = 0;
     L.off_slots = o;   o = align_up(o + (size_t)W * L.slots * sizeof(Slot), 256);
     L.off_log = o;     o = align_up(o + (size_t)W * L.ring * sizeof(uint32_t), 256);
@@ -64,6 +65,7 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     L.off_hist = o;    o = align_up(o + ((size_t)max_routes + 1) * 2 * sizeof(int32_t), 256);
     L.off_replay = o;  o = align_up(o + (size_t)kEpisodeThreads * 16, 256);
     L.off_ctl = o;     o = align_up(o + 256, 256);     // launch control (episode queue counter)
+    L.off_runs = o;    o = align_up(o + L.runs * sizeof(RunSlot), 256);
     L.per_episode = o;
     return L;
 }

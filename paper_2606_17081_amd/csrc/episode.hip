@@ -476,10 +476,11 @@ constexpr int KI = 4;   // searches a thread keeps in flight together
 constexpr int KP = 4;   // batch pairs a thread searches together for their common prefix
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n: item i
-// names a chain, its length and a worker table (info), and receives the
-// first chain position missing from the table (put).  Binary search per
-// thread, exact for tables prefix-closed along the chain; KI searches of a
-// thread issue their loads together.
+// names a chain, its length and a worker table (info, false for an item
+// this search does not handle), and receives the first chain position
+// missing from the table (put).  Binary search per thread, exact for tables
+// prefix-closed along the chain; KI searches of a thread issue their loads
+// together.
 template <class Info, class Put>
 __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, const Put& put, const Slot* slots,
                                                 uint64_t S)
@@ -489,6 +490,7 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
         int32_t lo[KI], hi[KI];
         const uint64_t* ch[KI];
         const Slot* tb[KI];
+        bool own[KI];
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
             const int32_t i = base + u * NT + (int32_t)threadIdx.x;
@@ -496,11 +498,14 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
             hi[u] = 0;
             ch[u] = nullptr;
             tb[u] = slots;
+            own[u] = false;
             if (i < n) {
                 int32_t P, j;
-                info(i, ch[u], P, j);
-                hi[u] = P;
-                tb[u] = slots + (uint64_t)j * S;
+                own[u] = info(i, ch[u], P, j);
+                if (own[u]) {
+                    hi[u] = P;
+                    tb[u] = slots + (uint64_t)j * S;
+                }
             }
         }
         for (;;) {
@@ -538,7 +543,203 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
             const int32_t i = base + u * NT + (int32_t)threadIdx.x;
-            if (i < n) put(i, lo[u]);
+            if (i < n && own[u]) put(i, lo[u]);
+        }
+    }
+}
+
+// ---- the run index of workers that keep no recency yet
+//
+// Until a worker first evicts (under LRU, in prefix mode), its cached set is
+// the union of the prefixes of the chains routed to it, i.e. a trie of blocks;
+// a route adds one path to that trie, the blocks [o, P) past the overlap o it
+// was decided with.  Such a path is a run, kept as one entry keyed by the hash
+// of its first block (the chained hash names the whole prefix, so a lookup by
+// the hash of block p of another chain finds the run exactly when that chain
+// reaches the run's first block).  A branch off the middle of a run is always
+// the first block of a later run, so the longest cached prefix of a chain is
+// found by walking: look up the run that starts at the current block, follow
+// it while the two chains agree (the first differing hash by binary search),
+// and look up again at the block where they part or where the run ends.  One
+// entry per route replaces an insert per new block.  All workers of an episode
+// share one table of 16-byte RunSlots, probed from run_home in aligned pairs.
+constexpr int kRunWin = 2;
+
+__device__ __forceinline__ uint64_t run_home(uint64_t h, int32_t j, uint64_t rsmask)
+{
+    return (h + (uint64_t)(j + 1) * 0x9E3779B97F4A7C15ull) & rsmask & ~(uint64_t)(kRunWin - 1);
+}
+
+// chain base index (below 2^40), worker (below 256) and end (below 2^16) of a run
+__device__ __forceinline__ uint64_t run_val(int64_t cb, int32_t j, int32_t end)
+{
+    return ((uint64_t)cb << 24) | ((uint64_t)(uint32_t)j << 16) | (uint64_t)(uint32_t)end;
+}
+
+__device__ __forceinline__ void load_run(const RunSlot* p, uint64_t& key, uint64_t& val)
+{
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    key = (uint64_t)v.x | ((uint64_t)v.y << 32);
+    val = (uint64_t)v.z | ((uint64_t)v.w << 32);
+}
+
+// Run of worker j starting with block hash h, whose first pair (from g) is
+// loaded in k, v; false when there is none.
+__device__ __forceinline__ bool run_finish(const RunSlot* rt, uint64_t rsmask, uint64_t h, int32_t j, uint64_t g,
+                                           const uint64_t* k, const uint64_t* v, uint64_t& val)
+{
+#pragma unroll
+    for (int r = 0; r < kRunWin; ++r) {
+        if (k[r] == kEmpty) return false;
+        if (k[r] == h && (int32_t)((v[r] >> 16) & 0xFFu) == j) {
+            val = v[r];
+            return true;
+        }
+    }
+    for (uint64_t n = kRunWin; n <= rsmask; n += kRunWin) {
+        g = (g + kRunWin) & rsmask;
+#pragma unroll 1
+        for (int r = 0; r < kRunWin; ++r) {
+            uint64_t kk, vv;
+            load_run(rt + g + r, kk, vv);
+            if (kk == kEmpty) return false;
+            if (kk == h && (int32_t)((vv >> 16) & 0xFFu) == j) {
+                val = vv;
+                return true;
+            }
+        }
+    }
+    return false;
+}
+
+// Add the run (h, val) of worker j.  Each (worker, first block) pair is added
+// at most once, so a slot already holding h belongs to another worker's run;
+// concurrent adds claim empty slots by compare-and-swap.
+__device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_t h, int32_t j, uint64_t val,
+                                           int32_t* status)
+{
+    uint64_t g = run_home(h, j, rsmask);
+    for (uint64_t n = 0; n <= rsmask; n += kRunWin) {
+#pragma unroll 1
+        for (int r = 0; r < kRunWin; ++r) {
+            uint64_t prev = kEmpty;
+            if (__hip_atomic_compare_exchange_strong(&rt[g + r].key, &prev, h, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                rt[g + r].val = val;
+                return;
+            }
+        }
+        g = (g + kRunWin) & rsmask;
+    }
+    atomicOr(status, RK_DEV_TABLE_FULL);
+}
+
+// Longest cached prefix for items i = threadIdx.x, + NT, ... < n on workers
+// without recency, by the run walk above; info and put as in prefix_searches.
+// KI walks of a thread issue their loads together; a walk step loads either
+// the item's hash at its current block, a run pair, or the two hashes a
+// binary-search step compares.
+template <class Info, class Put>
+__device__ __forceinline__ void run_searches(int32_t n, const Info& info, const Put& put, const RunSlot* rt,
+                                             uint64_t rsmask, const uint64_t* chains)
+{
+    enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3 };
+    for (int32_t base = 0; base < n; base += NT * KI) {
+        const uint64_t* ch[KI];
+        const uint64_t* rc[KI];
+        int32_t P[KI], jw[KI], o[KI], lo[KI], hi[KI], mode[KI];
+        uint64_t hq[KI], qhi[KI];
+        bool own[KI], qok[KI];
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            ch[u] = chains;
+            rc[u] = chains;
+            P[u] = 0;
+            jw[u] = 0;
+            o[u] = 0;
+            lo[u] = 0;
+            hi[u] = 0;
+            hq[u] = 0ull;
+            qhi[u] = 0ull;
+            qok[u] = false;
+            own[u] = i < n && info(i, ch[u], P[u], jw[u]);
+            mode[u] = own[u] && P[u] > 0 ? HASH : DONE;
+        }
+        for (;;) {
+            bool any = false;
+            uint64_t x0[KI], x1[KI], y0[KI], y1[KI];
+            int32_t mid[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                x0[u] = x1[u] = y0[u] = y1[u] = 0ull;
+                mid[u] = (lo[u] + hi[u]) >> 1;
+                if (mode[u] == HASH) {
+                    x0[u] = ch[u][o[u]];
+                    any = true;
+                } else if (mode[u] == LOOK) {
+                    const uint64_t g = run_home(hq[u], jw[u], rsmask);
+                    load_run(rt + g, x0[u], y0[u]);
+                    load_run(rt + g + 1, x1[u], y1[u]);
+                    any = true;
+                } else if (mode[u] == CMP) {
+                    x0[u] = ch[u][mid[u]];
+                    x1[u] = rc[u][mid[u]];
+                    any = true;
+                }
+            }
+            if (!any) break;
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                if (mode[u] == HASH) {
+                    hq[u] = x0[u];
+                    mode[u] = LOOK;
+                } else if (mode[u] == LOOK) {
+                    const uint64_t kk[kRunWin] = {x0[u], x1[u]}, vv[kRunWin] = {y0[u], y1[u]};
+                    uint64_t val = 0ull;
+                    if (!run_finish(rt, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
+                        mode[u] = DONE;
+                    } else {
+                        // the run holds blocks [o, end) of the chain at val >> 24
+                        rc[u] = chains + (int64_t)(val >> 24);
+                        const int32_t m = min(P[u], (int32_t)(val & 0xFFFFu));
+                        lo[u] = o[u] + 1;
+                        hi[u] = m;
+                        qok[u] = false;
+                        if (lo[u] >= hi[u]) {
+                            o[u] = m;
+                            mode[u] = o[u] < P[u] ? HASH : DONE;
+                        } else {
+                            mode[u] = CMP;
+                        }
+                    }
+                } else if (mode[u] == CMP) {
+                    // first block in [lo, hi) where the chains differ (hi: the run's end or P)
+                    if (x0[u] == x1[u]) {
+                        lo[u] = mid[u] + 1;
+                    } else {
+                        hi[u] = mid[u];
+                        qhi[u] = x0[u];
+                        qok[u] = true;
+                    }
+                    if (lo[u] >= hi[u]) {
+                        o[u] = lo[u];
+                        if (o[u] >= P[u]) {
+                            mode[u] = DONE;
+                        } else if (qok[u]) {
+                            hq[u] = qhi[u];      // the item's hash at hi, loaded by the step that set hi
+                            mode[u] = LOOK;
+                        } else {
+                            mode[u] = HASH;
+                        }
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            if (own[u]) put(i, o[u]);
         }
     }
 }
@@ -658,24 +859,6 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     return b;
 }
 
-// Empty worker tables for every episode of a launch, run before the episode
-// kernel: one grid over all of them moves the bytes at the chip's store rate,
-// where each episode clearing its own tables left the start of the episode
-// kernel bound by the uneven share of workgroups per CU.  Block x clears
-// chunk x % cpe (kClearChunk 16-byte slots) of episode x / cpe.
-constexpr uint32_t kClearChunk = 4096;
-
-__global__ __launch_bounds__(256) void episode_clear_kernel(unsigned char* __restrict__ ws, size_t per_episode,
-                                                          size_t off_slots, uint64_t n16, uint32_t cpe)
-{
-    const uint64_t e = blockIdx.x / cpe;
-    const uint64_t k0 = (uint64_t)(blockIdx.x % cpe) * kClearChunk;
-    const uint64_t k1 = min(k0 + kClearChunk, n16);
-    uint4* z = reinterpret_cast<uint4*>(ws + e * per_episode + off_slots);
-    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-    for (uint64_t k = k0 + threadIdx.x; k < k1; k += 256) z[k] = zero;
-}
-
 // The episode queue of a launch with fewer workspaces than episodes starts at 0.
 __global__ void episode_queue_init(int32_t* __restrict__ q)
 {
@@ -685,9 +868,9 @@ __global__ void episode_queue_init(int32_t* __restrict__ q)
 // Two waves per SIMD: two episodes share a CU (the sweep has more episodes than CUs).
 // With one workspace per episode, workgroup x runs episode x.  With fewer
 // workspaces (n_slots < E), workgroup x owns workspace x and takes episodes from
-// the launch's queue counter in index order until none is left, clearing its
-// tables before each one (a workspace's first episode skips that when the
-// caller cleared the tables).
+// the launch's queue counter in index order until none is left.  An episode
+// clears what it uses of its workspace itself, so no launch needs the
+// workspace cleared beforehand.
 // The queued loop is a kernel of its own (Queued = true): a loop around the
 // episode keeps more values live across it, and the one-episode kernel keeps
 // its register allocation.
@@ -708,13 +891,6 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         e = sh.next_e;
         __syncthreads();
         if (e >= a.E) break;
-        if (it > 0 || !(a.flags & RK_SIM_TABLES_CLEAR)) {
-            uint4* z = reinterpret_cast<uint4*>(ws + a.L.off_slots);
-            const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-            const uint64_t n16 = (uint64_t)a.W * a.L.slots;
-            for (uint64_t k = tid; k < n16; k += NT) z[k] = zero;
-            __syncthreads();
-        }
     } else if (it > 0) {
         break;
     }
@@ -823,13 +999,27 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     int32_t* g_queue = (int32_t*)(ws + a.L.off_queue);
     int32_t* g_next = (int32_t*)(ws + a.L.off_next);
     int32_t* g_hist = (int32_t*)(ws + a.L.off_hist);       // per route: conversation, P | worker << 16
-    const uint64_t S = a.L.slots, smask = S - 1, R = a.L.ring, rmask = R - 1;
+    RunSlot* g_runs = (RunSlot*)(ws + a.L.off_runs);       // run index of the workers without recency
+    const uint64_t S = a.L.slots, smask = S - 1, R = a.L.ring, rmask = R - 1, rsmask = a.L.runs - 1;
     const uint64_t used_limit = S - S / 4;
     const uint64_t scratch_cap = (uint64_t)a.cache + (uint64_t)a.max_blocks;
 
-    // ---- initial state: empty caches (cleared by episode_clear_kernel before this launch, or by the
-    //      workgroup before a queued episode), idle
-    //      workers, every first turn queued
+    // ---- initial state: empty caches, idle workers, every first turn queued.  The run index is
+    //      cleared here; a worker's block table when the worker starts keeping recency (here for
+    //      episodes that keep it from the start, at its first eviction for the others).
+    const bool eager = freq || tiers || scan;
+    auto clear_tables = [&](int32_t j_lo, int32_t j_hi) {
+        uint4* z = reinterpret_cast<uint4*>(g_slots + (uint64_t)j_lo * S);
+        const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+        const uint64_t n16 = (uint64_t)(j_hi - j_lo) * S;
+        for (uint64_t k = tid; k < n16; k += NT) z[k] = zero;
+    };
+    {
+        uint4* z = reinterpret_cast<uint4*>(g_runs);
+        const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+        for (uint64_t k = tid; k <= rsmask; k += NT) z[k] = zero;
+        if (eager) clear_tables(0, W);
+    }
     if (tid < W) {
         s_A[tid] = 0;
         s_N[tid] = 0;
@@ -837,7 +1027,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         s_b2[tid] = 0;
         s_n1[tid] = 0;
         s_n2[tid] = 0;
-        s_stamped[tid] = freq || tiers;     // frequencies and tier runs need every touch
+        s_stamped[tid] = eager;     // frequencies, tier runs and scans of any cached sets need every touch
         s_head[tid] = 0;
         s_tail[tid] = 0;
         s_live[tid] = 0;
@@ -953,59 +1143,33 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 }
                 if (!__builtin_amdgcn_readfirstlane(won)) continue;
-                // routes [c, hi): the blocks each must write numbered consecutively -- all of
-                // them, or, on a worker whose recency is not kept yet, those past the prefix
-                // its table held (only those may be missing)
+                // routes [c, hi).  A route on a worker that keeps no recency yet adds one run to
+                // the run index: the blocks past its decided overlap, which counts the common
+                // prefixes with the batch's earlier routes on that worker.  A route on a worker
+                // that keeps recency touches all of its blocks, numbered consecutively over the
+                // claimed routes.
                 int32_t* wst = sh.wst[wave];
                 const int32_t nr = hi - c;
-                int32_t tot = 0, st0 = 0, pr = 0;
+                int32_t tot = 0, pr = 0;
                 if (lane < nr) {
-                    const int32_t bl = c + lane;
-                    // a worker without kept recency gets the blocks past the route's overlap, which
-                    // counts the common prefixes with the batch's earlier routes on that worker:
-                    // those routes' writers insert them (and so on back to blocks in the table)
-                    const int32_t sgl = r_sig[bl];
-                    st0 = s_stamped[sgl] ? 0 : o_cur[bl * W + sgl];
-                    pr = r_P[bl] - st0;
+                    const int32_t bl = c + lane, sgl = r_sig[bl];
+                    if (s_stamped[sgl]) {
+                        pr = r_P[bl];
+                    } else {
+                        const int32_t st = o_cur[bl * W + sgl], Pl = r_P[bl];
+                        if (st < Pl)
+                            run_insert(g_runs, rsmask, a.chains[r_cb[bl] + st], sgl, run_val(r_cb[bl], sgl, Pl),
+                                       a.status);
+                    }
                 }
                 const int32_t off = wave_excl_sum_dpp(pr, tot);
+                if (tot == 0) continue;
                 if (lane < nr) {
                     woff[lane] = off;
-                    wst[lane] = st0;
+                    wst[lane] = 0;
                 }
                 if (lane == 0) woff[nr] = tot;
                 ep_wave_sync();
-                // no claimed route's worker keeps recency yet: every block is an insert of a
-                // block the worker may lack; the next block's chain hash is fetched while this
-                // one is written
-                const bool lazy = __ballot(lane < nr && s_stamped[r_sig[c + lane]] != 0) == 0ull;
-                if (lazy) {
-                    auto locate = [&](int32_t i, int32_t& b, int32_t& k) {
-                        int32_t r = 0;
-                        while (r + 1 < nr && woff[r + 1] <= i) ++r;
-                        b = c + r;
-                        k = wst[r] + (i - woff[r]);
-                    };
-                    int32_t bn = 0, kn = 0;
-                    uint64_t hn = 0ull;
-                    if (lane < tot) {
-                        locate(lane, bn, kn);
-                        hn = a.chains[r_cb[bn] + kn];
-                    }
-                    for (int32_t i = lane; i < tot; i += 64) {
-                        const int32_t b = bn;
-                        const uint64_t h = hn;
-                        if (i + 64 < tot) {
-                            locate(i + 64, bn, kn);
-                            hn = a.chains[r_cb[bn] + kn];
-                        }
-                        int ins;
-                        touch_hinted(g_slots + (uint64_t)r_sig[b] * S, smask, h, false, ins, a.status);
-                        my_ins += ins;
-                    }
-                    ep_wave_sync();
-                    continue;
-                }
                 for (int32_t i = lane; i < tot; i += 64) {
                     int32_t r = 0;
                     while (r + 1 < nr && woff[r + 1] <= i) ++r;
@@ -1015,13 +1179,6 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     Slot* tk = g_slots + (uint64_t)sg * S;
                     uint32_t* tl = g_log + (uint64_t)sg * R;
                     const bool known = k < r_otab[b];
-                    if (!s_stamped[sg]) {
-                        // recency not kept yet: insert what the worker may lack
-                        int ins;
-                        touch_hinted(tk, smask, a.chains[r_cb[b] + k], false, ins, a.status);
-                        my_ins += ins;
-                        continue;
-                    }
                     const uint64_t h = a.chains[r_cb[b] + k];
                     const uint32_t stamp = r_stamp[b] + (uint32_t)(P - 1 - k);
                     int ins;
@@ -1153,7 +1310,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         const int32_t k = r_Ps[lo] - 1 - q;         // to the first
                         st = (uint32_t)(stamp0 + r_off[lo] + q);
                         int ins;
-                        sl = touch_hinted(tk, smask, a.chains[r_cbs[lo] + k], true, ins, a.status);
+                        sl = touch_hinted(tk, smask, a.chains[r_cbs[lo] + k], pass == 1, ins, a.status);
                         if (sl != ~0ull) {
                             if (pass == 0)
                                 __hip_atomic_fetch_max(&tk[sl].stamp, st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -1255,21 +1412,38 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         if (!scan) {
             const int32_t per = j < 0 ? W : 1;
             const int32_t n = (nb - b_lo) * per;
-            prefix_searches(
-                n,
-                [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj) {
-                    const int32_t b = b_lo + i / per;
-                    jj = j < 0 ? i % per : j;
-                    ch = a.chains + r_cb[b];
-                    P = r_P[b];
-                },
-                [&](int32_t i, int32_t o) {
-                    const int32_t b = b_lo + i / per;
-                    const int32_t jj = j < 0 ? i % per : j;
-                    o_tab[b * W + jj] = o;
-                    o_cur[b * W + jj] = o;
-                },
-                g_slots, S);
+            auto put = [&](int32_t i, int32_t o) {
+                const int32_t b = b_lo + i / per;
+                const int32_t jj = j < 0 ? i % per : j;
+                o_tab[b * W + jj] = o;
+                o_cur[b * W + jj] = o;
+            };
+            // workers that keep recency: binary search in their block tables; the others: the
+            // run walk
+            const unsigned long long st = __ballot(lane < W && s_stamped[lane] != 0 && (j < 0 || lane == j));
+            const unsigned long long lz = __ballot(lane < W && s_stamped[lane] == 0 && (j < 0 || lane == j));
+            if (st)
+                prefix_searches(
+                    n,
+                    [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj) {
+                        const int32_t b = b_lo + i / per;
+                        jj = j < 0 ? i % per : j;
+                        ch = a.chains + r_cb[b];
+                        P = r_P[b];
+                        return s_stamped[jj] != 0;
+                    },
+                    put, g_slots, S);
+            if (lz)
+                run_searches(
+                    n,
+                    [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj) {
+                        const int32_t b = b_lo + i / per;
+                        jj = j < 0 ? i % per : j;
+                        ch = a.chains + r_cb[b];
+                        P = r_P[b];
+                        return s_stamped[jj] == 0;
+                    },
+                    put, g_runs, rsmask, a.chains);
         } else {
             for (int32_t b = b_lo + wave; b < nb; b += NW) {
                 const uint64_t* ch = a.chains + r_cb[b];
@@ -1394,6 +1568,10 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             if (P < 0 || (int64_t)P > ce - cb) {
                 atomicOr(a.status, RK_DEV_SHORT_INPUT);
                 P = P < 0 ? 0 : (int32_t)max((int64_t)0, ce - cb);
+            }
+            if (cb < 0 || cb >= (1ll << 40)) {     // a run keeps 40 bits of its chain's base
+                atomicOr(a.status, RK_DEV_BAD_OFFSETS);
+                P = 0;
             }
             if (P > a.max_blocks) {
                 atomicOr(a.status, RK_DEV_TOO_LARGE);
@@ -1854,7 +2032,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 advance(s_b1, s_n1, K1, sg);
                 advance(s_b2, s_n2, K12, sg);
             }
-            if (!s_stamped[sg] && sh.remaining > 0) replay(sg, sh.tdone);
+            if (!s_stamped[sg] && sh.remaining > 0) {
+                // the worker's first eviction: its blocks go into its (cleared) block table with
+                // the recency of its routes
+                clear_tables(sg, sg + 1);
+                __syncthreads();
+                replay(sg, sh.tdone);
+            }
             evict(sg, r_ep[b]);
             if (tiers) {
                 // evictions take the oldest records: a run keeps at most the live count
@@ -1923,7 +2107,7 @@ extern "C" size_t rk_simulate_workspace_size(int32_t E, int32_t W, int32_t cache
     return L.per_episode * (size_t)E;
 }
 
-// Shape fields of a batch, shared by rk_simulate_episodes and rk_simulate_clear_tables.
+// Shape fields of a batch.
 static int check_batch_shape(const char* who, const rk_episode_batch* b)
 {
     if (b->E < 0) return fail(RK_EINVAL, "%s: E < 0", who);
@@ -1941,7 +2125,7 @@ static int check_batch_shape(const char* who, const rk_episode_batch* b)
         return fail(RK_EINVAL, "%s: unknown probe_mode", who);
     if ((int64_t)b->cache_blocks + b->max_blocks > (1ll << 29)) return fail(RK_EUNSUPPORTED, "%s: cache too large", who);
     if (b->max_routes < 0) return fail(RK_EINVAL, "%s: max_routes < 0", who);
-    if (b->flags & ~RK_SIM_TABLES_CLEAR) return fail(RK_EINVAL, "%s: unknown flags %#x", who, (unsigned)b->flags);
+    if (b->flags != 0) return fail(RK_EINVAL, "%s: unknown flags %#x", who, (unsigned)b->flags);
     if (b->ws_slots < 0 || b->ws_pad != 0) return fail(RK_EINVAL, "%s: ws_slots < 0 or ws_pad != 0", who);
     return RK_OK;
 }
@@ -1950,35 +2134,6 @@ static int check_batch_shape(const char* who, const rk_episode_batch* b)
 static int32_t batch_slots(const rk_episode_batch* b)
 {
     return b->ws_slots > 0 && b->ws_slots < b->E ? b->ws_slots : b->E;
-}
-
-// Enqueue episode_clear_kernel over the tables of every workspace the batch uses.
-static int launch_table_clear(const char* who, const rk_episode_batch* b, const EpisodeLayout& L, void* workspace,
-                              hipStream_t s)
-{
-    const uint64_t n16 = (uint64_t)b->W * L.slots;          // 16-byte slots per episode
-    const uint64_t cpe = (n16 + kClearChunk - 1) / kClearChunk;
-    const uint64_t nws = (uint64_t)batch_slots(b);
-    if (cpe * nws > 0x7fffffffull)
-        return fail(RK_EUNSUPPORTED, "%s: %llu workspaces of %llu table slots exceed one clear launch", who,
-                    (unsigned long long)nws, (unsigned long long)n16);
-    hipLaunchKernelGGL(episode_clear_kernel, dim3((unsigned)(cpe * nws)), dim3(256), 0, s,
-                       (unsigned char*)workspace, L.per_episode, L.off_slots, n16, (uint32_t)cpe);
-    return hip_check(hipGetLastError(), who);
-}
-
-extern "C" int rk_simulate_clear_tables(const rk_episode_batch* b, void* workspace, size_t ws_bytes, void* stream)
-{
-    if (!b) return fail(RK_EINVAL, "rk_simulate_clear_tables: NULL batch");
-    int rc = check_batch_shape("rk_simulate_clear_tables", b);
-    if (rc) return rc;
-    if (b->E == 0) return RK_OK;
-    if (!workspace) return fail(RK_EINVAL, "rk_simulate_clear_tables: NULL workspace");
-    const EpisodeLayout L = episode_layout(b->W, b->cache_blocks, b->max_blocks, b->max_conv, b->max_routes);
-    const size_t need = L.per_episode * (size_t)batch_slots(b);
-    if (ws_bytes < need)
-        return fail(RK_ENOMEM, "rk_simulate_clear_tables: workspace %zu bytes < %zu needed", ws_bytes, need);
-    return launch_table_clear("rk_simulate_clear_tables", b, L, workspace, (hipStream_t)stream);
 }
 
 extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_outputs* out, void* workspace,
@@ -2044,13 +2199,9 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     const size_t lds = o + batch_layout(NB, b->W, tiers).bytes;
     hipStream_t s = (hipStream_t)stream;
     if (n_slots < b->E) {
-        // queued episodes: each workgroup clears its own tables before an episode
         hipLaunchKernelGGL(episode_queue_init, dim3(1), dim3(64), 0, s,
                            (int32_t*)((unsigned char*)workspace + L.off_ctl));
         rc = hip_check(hipGetLastError(), "rk_simulate_episodes queue init");
-        if (rc) return rc;
-    } else if (!(b->flags & RK_SIM_TABLES_CLEAR)) {
-        rc = launch_table_clear("rk_simulate_episodes clear launch", b, L, workspace, s);
         if (rc) return rc;
     }
     if (n_slots < b->E) hipLaunchKernelGGL(episode_kernel<true>, dim3((unsigned)n_slots), dim3(NT), lds, s, a);

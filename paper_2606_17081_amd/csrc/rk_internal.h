@@ -257,13 +257,24 @@ struct __align__(16) Slot {
     uint32_t fkey;
 };
 
+// A run of an episode's prefix index: a route added the blocks [o, end) of its
+// chain to a worker that held the blocks before o, keyed by the hash of block
+// o; val packs the chain's base index (bits 63..24), the worker (23..16) and
+// end (15..0).  Key 0 marks an empty slot.
+struct __align__(16) RunSlot {
+    uint64_t key;
+    uint64_t val;
+};
+
 constexpr int kEpisodeThreads = 256;   // threads of an episode's workgroup
 
 // Episode workspace layout (bytes), shared by the size query and the launch.
 struct EpisodeLayout {
     uint64_t slots;        // table slots per worker (power of two)
     uint64_t ring;         // LRU log records per worker (power of two)
-    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next, off_hist, off_replay, off_ctl;
+    uint64_t runs;         // run slots of the episode's prefix index (power of two)
+    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next, off_hist, off_replay, off_ctl,
+        off_runs;
     size_t per_episode;
 };
 EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv,

@@ -133,17 +133,8 @@ class EpisodeRunner:
     def hash(self, stream=None):
         rk.hash_chains(self.tokens, self.tok_off, self.chain_off, self.chains, stream=stream)
 
-    def clear_tables(self, stream=None):
-        """Clear the workspace's cache tables (may run on another stream, ahead of
-        a simulate(tables_clear=True) that the caller orders after it)."""
-        rk.simulate_clear_tables(self.batch, self.workspace, stream=stream)
-
-    def simulate(self, stream=None, tables_clear: bool = False):
-        self.batch.flags = rk.RK_SIM_TABLES_CLEAR if tables_clear else 0
-        try:
-            rk.simulate_episodes(self.batch, self.outputs, self.workspace, stream=stream)
-        finally:
-            self.batch.flags = 0
+    def simulate(self, stream=None):
+        rk.simulate_episodes(self.batch, self.outputs, self.workspace, stream=stream)
 
     def poa(self, stream=None):
         rk.poa_estimate(self.win_off, self.ep_win_off, self.n_rows, self.max_window, self.W,

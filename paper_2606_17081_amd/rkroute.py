@@ -21,7 +21,6 @@ RK_OK, RK_EINVAL, RK_ENOMEM, RK_EHIP, RK_ETABLEFULL, RK_EUNSUPPORTED = 0, -1, -2
 RK_PROBE_PREFIX, RK_PROBE_SCAN = 0, 1
 RK_POLICY_ARGMIN, RK_POLICY_SOFTMAX, RK_POLICY_ROUND_ROBIN, RK_POLICY_RANDOM, RK_POLICY_P2C = range(5)
 RK_EVICT_LRU, RK_EVICT_FREQ = 0, 1
-RK_SIM_TABLES_CLEAR = 1
 RK_FREQ_CAP = 1 << 20
 DEV_BITS = {0x1: "bad offsets", 0x2: "short input", 0x4: "zero key", 0x8: "table full",
             0x10: "too large", 0x20: "no convergence", 0x40: "bad policy parameters"}
@@ -29,7 +28,7 @@ DEV_BITS = {0x1: "bad offsets", 0x2: "short input", 0x4: "zero key", 0x8: "table
 EXPORTED = ("rk_status_string", "rk_last_error", "rk_device_status", "rk_hash_chains",
             "rk_table_build", "rk_route_score_batch", "rk_index_build", "rk_route_score_index",
             "rk_simulate_workspace_size",
-            "rk_simulate_episodes", "rk_simulate_clear_tables", "rk_poa_workspace_size", "rk_poa_estimate",
+            "rk_simulate_episodes", "rk_poa_workspace_size", "rk_poa_estimate",
             "rk_poa_estimate_noalloc")
 RK_POA_NOALLOC_BYTES = 64 << 20
 
@@ -123,8 +122,6 @@ def lib():
             L.rk_simulate_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32]
             L.rk_simulate_episodes.restype = C.c_int
             L.rk_simulate_episodes.argtypes = [C.POINTER(EpisodeBatch), C.POINTER(EpisodeOutputs), vp, sz, vp]
-            L.rk_simulate_clear_tables.restype = C.c_int
-            L.rk_simulate_clear_tables.argtypes = [C.POINTER(EpisodeBatch), vp, sz, vp]
             L.rk_poa_workspace_size.restype = sz
             L.rk_poa_workspace_size.argtypes = [i64, i32]
             L.rk_poa_estimate.restype = C.c_int
@@ -319,13 +316,6 @@ def simulate_episodes(batch: EpisodeBatch, outputs: EpisodeOutputs, workspace, s
     _check(lib().rk_simulate_episodes(C.byref(batch), C.byref(outputs), _ptr(workspace),
                                       workspace.numel() * workspace.element_size(), _stream(stream)),
            "rk_simulate_episodes")
-
-
-def simulate_clear_tables(batch: EpisodeBatch, workspace, stream=None):
-    """Launch rk_simulate_clear_tables: clear the workspace's cache tables for batch."""
-    _check(lib().rk_simulate_clear_tables(C.byref(batch), _ptr(workspace),
-                                          workspace.numel() * workspace.element_size(), _stream(stream)),
-           "rk_simulate_clear_tables")
 
 
 def poa_workspace_size(n_rows: int, W: int) -> int:

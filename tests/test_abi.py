@@ -71,31 +71,21 @@ def test_episode_and_poa_host_validation():
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), 16, None) == rk.RK_ENOMEM
     need = rk.simulate_workspace_size(2, 4, 16, 8, 4, 10)
     assert need > 0 and need == 2 * rk.simulate_workspace_size(1, 4, 16, 8, 4, 10)
-    # flags: only RK_SIM_TABLES_CLEAR is known; the separate clear validates the same shape fields
-    b = rk.EpisodeBatch(2, 4, 16, 8, 4, 8, 2, 1, 0, 0, 4, 2, 0, 0, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
+    # flags: none is defined
+    b = rk.EpisodeBatch(2, 4, 16, 8, 4, 8, 2, 1, 0, 0, 4, 1, 0, 0, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
                         C.c_void_p(8), C.c_void_p(8))
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), need, None) == rk.RK_EINVAL
     assert b"flags" in L.rk_last_error()
-    assert L.rk_simulate_clear_tables(None, C.c_void_p(8), need, None) == rk.RK_EINVAL
-    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), need, None) == rk.RK_EINVAL
-    b.flags = rk.RK_SIM_TABLES_CLEAR
-    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), 16, None) == rk.RK_ENOMEM
-    assert L.rk_simulate_clear_tables(C.byref(b), None, need, None) == rk.RK_EINVAL
-    b.W = 65
-    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), need, None) == rk.RK_EUNSUPPORTED
-    b.W, b.E = 4, 0
-    assert L.rk_simulate_clear_tables(C.byref(b), None, 0, None) == rk.RK_OK
     # workspace slots: fewer workspaces than episodes need less memory; negative counts or a
     # nonzero pad are rejected
-    b.E, b.flags = 2, 0
+    b.flags = 0
     one = rk.simulate_workspace_size(1, 4, 16, 8, 4, 4)
     b.ws_slots = -1
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), need, None) == rk.RK_EINVAL
     assert b"ws_slots" in L.rk_last_error()
     b.ws_slots, b.ws_pad = 1, 7
-    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), need, None) == rk.RK_EINVAL
+    assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), need, None) == rk.RK_EINVAL
     b.ws_pad = 0
-    assert L.rk_simulate_clear_tables(C.byref(b), C.c_void_p(8), one - 1, None) == rk.RK_ENOMEM
     assert L.rk_simulate_episodes(C.byref(b), C.byref(o), C.c_void_p(8), one - 1, None) == rk.RK_ENOMEM
     assert b"needed" in L.rk_last_error()
     pp = rk.PoaParams(0.005, 0.02, 0.01, 2, 64, 0.015, 0)

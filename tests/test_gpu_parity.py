@@ -423,41 +423,45 @@ def test_lazy_recency_late_first_eviction(gpu, orc):
     assert late >= 8
 
 
-def test_tables_cleared_on_another_stream(gpu, orc):
-    """rk_simulate_clear_tables on a second stream, ordered by an event, then
-    rk_simulate_episodes with RK_SIM_TABLES_CLEAR: the same routes, overlaps,
-    costs and evictions as the default path (which clears on its own stream),
-    over several launches on one workspace."""
+def test_workspace_contents_never_read(gpu, orc):
+    """An episode clears the parts of its workspace it uses (the run index at
+    its start; a worker's block table at its start under frequency eviction,
+    else at the worker's first eviction): launches on a workspace filled with
+    random bytes give the same routes, overlaps, costs, evictions and totals
+    as the first launch, for LRU episodes that evict and for frequency
+    eviction, in one launch."""
     torch, rk = gpu
     from paper_2606_17081_amd.episodes import EpisodeRunner
     w = wl.multiturn_workload(seeds=range(2), n_conv=96)
     eps = [wl.EpisodeSpec(**{**sp.__dict__, "cap": 512}) for sp in w.episodes]
+    eps += [wl.EpisodeSpec(**{**sp.__dict__, "cap": 512, "evict_policy": wl.EVICT_FREQ, "decay_steps": 3})
+            for sp in w.episodes]
     w2 = wl.Workload(w.name, W=w.W, cache_blocks=1024, traces=w.traces, episodes=eps)
     r = EpisodeRunner(w2)
     r.hash()
     r.simulate()
     torch.cuda.synchronize()
-    ref = {k: v.clone() for k, v in (("w", r.route_worker), ("o", r.overlap), ("c", r.cost),
-                                      ("d", r.evict_digest), ("t", r.totals))}
-    assert int(ref["t"][:, 1].sum()) > 0, "the case must evict"
-    side = torch.cuda.Stream()
-    main = torch.cuda.current_stream()
-    for _ in range(3):
-        for t in (r.route_worker, r.overlap, r.cost, r.evict_digest, r.totals):
+    _status_clean(rk)
+    outs = (r.route_worker, r.overlap, r.cost, r.evict_digest, r.totals)
+    ref = [t.clone() for t in outs]
+    assert int(ref[4][:, 1].sum()) > 0, "the case must evict"
+    gen = torch.Generator(device="cuda")
+    for rep in range(3):
+        gen.manual_seed(rep)
+        r.workspace.copy_(torch.randint(0, 256, r.workspace.shape, dtype=torch.uint8, device="cuda",
+                                        generator=gen))
+        for t in outs:
             t.zero_()
-        ev = torch.cuda.Event()
-        ev.record(main)              # the workspace's last use is done before the clear starts
-        side.wait_event(ev)
-        r.clear_tables(stream=side)
-        ev2 = torch.cuda.Event()
-        ev2.record(side)
-        main.wait_event(ev2)
-        r.simulate(tables_clear=True)
+        r.simulate()
         torch.cuda.synchronize()
         _status_clean(rk)
-        for k, v in (("w", r.route_worker), ("o", r.overlap), ("c", r.cost), ("d", r.evict_digest),
-                     ("t", r.totals)):
-            assert torch.equal(v, ref[k]), k
+        for k, (v, x) in enumerate(zip(outs, ref)):
+            assert torch.equal(v, x), f"output {k} differs after filling the workspace (pass {rep})"
+    for e in (0, 3):
+        sp = r.episodes[e]
+        say("oracle episode", e, "eviction policy", sp.evict_policy)
+        o = orc.simulate_trace(w2.W, w2.cache_blocks, sp, w2.traces[sp.seed])
+        _compare_episode(r.episode_results(e), o, w2.W, label=f"random workspace e{e}")
 
 
 @pytest.mark.parametrize("name", ["sweep", "multiturn"])
@@ -498,11 +502,11 @@ def test_lean_decision_loop_matches_full(gpu, name):
 
 def test_queued_workspaces_match(gpu, orc):
     """Fewer episode workspaces than episodes: 7 workgroups take 160 saturation
-    episodes in turn, each clearing its workspace's tables before every episode
-    (and, with RK_SIM_TABLES_CLEAR after rk_simulate_clear_tables, skipping the
-    clear of its first one).  Every output equals the launch with one workspace
-    per episode, and episodes run before and after a workspace changed hands
-    (the first 7 and the last ones of the queue) match the oracle."""
+    episodes in turn, each episode clearing what it uses of its workspace (the
+    last pass starts on a workspace filled with random bytes).  Every output
+    equals the launch with one workspace per episode, and episodes run before
+    and after a workspace changed hands (the first 7 and the last ones of the
+    queue) match the oracle."""
     torch, rk = gpu
     from paper_2606_17081_amd.episodes import EpisodeRunner
     w = wl.saturation_workload(seeds=range(4))
@@ -521,8 +525,8 @@ def test_queued_workspaces_match(gpu, orc):
         for t in (r.route_worker, r.overlap, r.cost, r.evict_digest, r.totals, r.poa_hat):
             t.zero_()
         if rep == 2:
-            r.clear_tables()
-        r.simulate(tables_clear=rep == 2)
+            r.workspace.copy_(torch.randint(0, 256, r.workspace.shape, dtype=torch.uint8, device="cuda"))
+        r.simulate()
         r.poa()
         torch.cuda.synchronize()
         _status_clean(rk)
