@@ -450,6 +450,133 @@ __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t 
 }
 
 
+constexpr int kRU = 4;   // touches a thread keeps in flight while a worker's recency is rebuilt
+
+// touch_hinted(t, smask, h[u], false, ...) for kRU keys (kEmpty: none) with the
+// claims and group loads of all of them issued before any result is used; the
+// slot of each key (~0 if none) goes to sl.
+__device__ __forceinline__ void touch_batch(Slot* __restrict__ t, uint64_t smask, const uint64_t* h, uint64_t* sl,
+                                            int32_t* status)
+{
+    uint64_t s0[kRU], prev[kRU], k[kRU][kWin];
+    uint32_t stv[kRU][kWin];
+    bool won[kRU];
+#pragma unroll
+    for (int u = 0; u < kRU; ++u) {
+        const uint64_t s = home_slot(h[u], smask);
+        s0[u] = s + group_slot(h[u], 0);
+        prev[u] = kEmpty;
+        won[u] = false;
+        if (h[u] != kEmpty)
+            won[u] = __hip_atomic_compare_exchange_strong(&t[s0[u]].key, &prev[u], h[u], __ATOMIC_RELAXED,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+#pragma unroll
+    for (int u = 0; u < kRU; ++u) {
+        const uint64_t s = home_slot(h[u], smask);
+#pragma unroll
+        for (int r = 1; r < kWin; ++r) {
+            k[u][r] = kEmpty;
+            stv[u][r] = 0;
+            if (h[u] != kEmpty) load_slot(t + s + group_slot(h[u], r), k[u][r], stv[u][r]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kRU; ++u) {
+        sl[u] = ~0ull;
+        if (h[u] == kEmpty) continue;
+        if (won[u] || prev[u] == h[u]) {
+            sl[u] = s0[u];
+            continue;
+        }
+        const uint64_t s = home_slot(h[u], smask);
+        bool done = false, retry = false;
+#pragma unroll
+        for (int r = 1; r < kWin && !done && !retry; ++r) {
+            const uint64_t si = s + group_slot(h[u], r);
+            if (k[u][r] == h[u]) {
+                if (stv[u][r] != kTomb) {
+                    sl[u] = si;
+                    done = true;
+                }
+                continue;
+            }
+            if (k[u][r] != kEmpty) continue;
+            uint64_t pi = kEmpty;
+            if (__hip_atomic_compare_exchange_strong(&t[si].key, &pi, h[u], __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                sl[u] = si;
+                done = true;
+            } else {
+                retry = true;      // lost a race for the slot: walk from the start
+            }
+        }
+        if (!done) {
+            int ins;
+            sl[u] = insert_or_touch(t, smask, h[u], ins, status);
+        }
+    }
+}
+
+// The live slot of each of kRU keys (kEmpty: none) and whether its stamp equals
+// st[u]; the groups of all of them are loaded before any result is used.
+__device__ __forceinline__ void find_batch(const Slot* __restrict__ t, uint64_t smask, const uint64_t* h, uint64_t* sl,
+                                           const uint32_t* st, bool* last)
+{
+    uint64_t k[kRU][kWin];
+    uint32_t stv[kRU][kWin];
+#pragma unroll
+    for (int u = 0; u < kRU; ++u) {
+        const uint64_t s = home_slot(h[u], smask);
+#pragma unroll
+        for (int r = 0; r < kWin; ++r) {
+            k[u][r] = kEmpty;
+            stv[u][r] = 0;
+            if (h[u] != kEmpty) load_slot(t + s + group_slot(h[u], r), k[u][r], stv[u][r]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kRU; ++u) {
+        sl[u] = ~0ull;
+        last[u] = false;
+        if (h[u] == kEmpty) continue;
+        const uint64_t s = home_slot(h[u], smask);
+        uint32_t stamp = 0;
+        bool found = false;
+#pragma unroll
+        for (int r = 0; r < kWin && !found; ++r) {
+            if (k[u][r] == kEmpty) break;
+            if (k[u][r] == h[u] && stv[u][r] != kTomb) {
+                sl[u] = s + group_slot(h[u], r);
+                stamp = stv[u][r];
+                found = true;
+            }
+        }
+        if (!found) {
+            // further groups (a full first group)
+            uint64_t g = s;
+            for (uint64_t n = kWin; n <= smask && !found; n += kWin) {
+                g = (g + kWin) & smask;
+                bool stop = false;
+#pragma unroll 1
+                for (int r = 0; r < kWin && !found && !stop; ++r) {
+                    uint64_t kk;
+                    uint32_t ss;
+                    load_slot(t + g + group_slot(h[u], r), kk, ss);
+                    if (kk == kEmpty) stop = true;
+                    else if (kk == h[u] && ss != kTomb) {
+                        sl[u] = g + group_slot(h[u], r);
+                        stamp = ss;
+                        found = true;
+                    }
+                }
+                if (stop) break;
+            }
+        }
+        last[u] = found && stamp == st[u];
+    }
+}
+
 static __device__ __forceinline__ void ep_wave_sync()
 {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -1294,40 +1421,54 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     r_Ps[rank] = P;
                 }
                 __syncthreads();
-                for (int32_t i0 = 0; i0 < ptot; i0 += NT) {
-                    const int32_t i = i0 + tid;
-                    uint64_t sl = ~0ull;
-                    uint32_t st = 0;
-                    bool last = false;
-                    if (i < ptot) {
-                        int32_t lo = 0, hi = n_r - 1;     // the route holding touch i
-                        while (lo < hi) {
-                            const int32_t mid = (lo + hi + 1) >> 1;
-                            if (r_off[mid] <= i) lo = mid;
-                            else hi = mid - 1;
-                        }
-                        const int32_t q = i - r_off[lo];            // touches go from the last block
-                        const int32_t k = r_Ps[lo] - 1 - q;         // to the first
-                        st = (uint32_t)(stamp0 + r_off[lo] + q);
-                        int ins;
-                        sl = touch_hinted(tk, smask, a.chains[r_cbs[lo] + k], pass == 1, ins, a.status);
-                        if (sl != ~0ull) {
-                            if (pass == 0)
-                                __hip_atomic_fetch_max(&tk[sl].stamp, st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                            else
-                                last = tk[sl].stamp == st;
+                // kRU touches per thread at a time, their memory operations issued together
+                for (int32_t i0 = 0; i0 < ptot; i0 += NT * kRU) {
+                    uint64_t h[kRU], sl[kRU];
+                    uint32_t st[kRU];
+                    bool last[kRU];
+#pragma unroll
+                    for (int u = 0; u < kRU; ++u) {
+                        const int32_t i = i0 + u * NT + tid;
+                        h[u] = kEmpty;
+                        st[u] = 0;
+                        sl[u] = ~0ull;
+                        last[u] = false;
+                        if (i < ptot) {
+                            int32_t lo = 0, hi = n_r - 1;     // the route holding touch i
+                            while (lo < hi) {
+                                const int32_t mid = (lo + hi + 1) >> 1;
+                                if (r_off[mid] <= i) lo = mid;
+                                else hi = mid - 1;
+                            }
+                            const int32_t q = i - r_off[lo];            // touches go from the last block
+                            const int32_t k = r_Ps[lo] - 1 - q;         // to the first
+                            st[u] = (uint32_t)(stamp0 + r_off[lo] + q);
+                            h[u] = a.chains[r_cbs[lo] + k];
                         }
                     }
-                    if (pass == 1) {
-                        // every thread has read its slot's stamp before any is rewritten
-                        int32_t nl;
-                        const int32_t lr = block_scan(last, sh.wtot, nl);
-                        if (last) {
-                            const uint32_t ns = (uint32_t)(live + lr);
-                            tk[sl].stamp = ns;
-                            tl[ns & rmask] = (uint32_t)sl;
+                    if (pass == 0) {
+                        // every block into the table (it starts empty), the latest touch's stamp kept
+                        touch_batch(tk, smask, h, sl, a.status);
+#pragma unroll
+                        for (int u = 0; u < kRU; ++u)
+                            if (sl[u] != ~0ull)
+                                __hip_atomic_fetch_max(&tk[sl[u]].stamp, st[u], __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+                    } else {
+                        find_batch(tk, smask, h, sl, st, last);
+                        // every thread has read its slots' stamps before any is rewritten; the
+                        // live records keep the order of their touches
+#pragma unroll
+                        for (int u = 0; u < kRU; ++u) {
+                            int32_t nl;
+                            const int32_t lr = block_scan(last[u], sh.wtot, nl);
+                            if (last[u]) {
+                                const uint32_t ns = (uint32_t)(live + lr);
+                                tk[sl[u]].stamp = ns;
+                                tl[ns & rmask] = (uint32_t)sl[u];
+                            }
+                            live += nl;
                         }
-                        live += nl;
                     }
                 }
                 stamp0 += ptot;
@@ -1345,6 +1486,143 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             }
         }
         __syncthreads();
+    };
+
+    // ---- recency of worker j rebuilt in one pass when the touches of its routes [0, t_end) fit the
+    //      log (all threads; false, with nothing written, when they do not).  The touches keep
+    //      their stamps (route after route, a route's blocks from last to first, counting up from
+    //      0), so every touch has its own log position: each touch that may be a block's latest
+    //      writes its record there and raises the block's stamp to its own, and a record is live
+    //      iff the block's stamp is its position, as in the eager upkeep.  The log positions of
+    //      all touches are cleared first.  Routes go newest first, so a touch that finds its
+    //      block already stamped by a later touch does nothing more.
+    auto materialize = [&](int32_t j, int32_t t_end) -> bool {
+        Slot* tk = g_slots + (uint64_t)j * S;
+        uint32_t* tl = g_log + (uint64_t)j * R;
+        int64_t* r_cbs = (int64_t*)(ws + a.L.off_replay);     // per chunk of routes, the worker's: chain
+        int32_t* r_off = (int32_t*)(r_cbs + NT);              // base, first touch index and P
+        int32_t* r_Ps = r_off + NT;
+        auto route_of = [&](int32_t r, int32_t& P, int64_t& cb) {
+            P = 0;
+            cb = 0;
+            if (r < t_end) {
+                const int32_t pw = g_hist[2 * r + 1];
+                if ((pw >> 16) == j) {
+                    P = pw & 0xFFFF;
+                    cb = a.chain_off[gc0 + g_hist[2 * r]];
+                }
+            }
+        };
+        int64_t T = 0;     // touches of the worker's routes
+        for (int32_t base = 0; base < t_end; base += NT) {
+            int32_t P;
+            int64_t cb;
+            route_of(base + tid, P, cb);
+            int32_t ptot;
+            block_excl_sum(P, sh.wtot, ptot);
+            T += ptot;
+        }
+        if (T > (int64_t)R) return false;
+        for (int64_t p = tid; p < T; p += NT) tl[p] = 0xFFFFFFFFu;
+        __syncthreads();
+        int64_t end = T;   // stamp after the last touch of the chunks done so far
+        const int32_t nchunk = (t_end + NT - 1) / NT;
+        for (int32_t c = nchunk - 1; c >= 0; --c) {
+            int32_t P;
+            int64_t cb;
+            route_of(c * NT + tid, P, cb);
+            int32_t n_r, ptot;
+            const int32_t rank = block_scan(P > 0, sh.wtot, n_r);
+            const int32_t off = block_excl_sum(P, sh.wtot, ptot);
+            if (P > 0) {
+                r_off[rank] = off;
+                r_cbs[rank] = cb;
+                r_Ps[rank] = P;
+            }
+            __syncthreads();
+            const int64_t stamp0 = end - ptot;
+            for (int32_t i0 = 0; i0 < ptot; i0 += NT * kRU) {
+                uint64_t h[kRU], k[kRU][kWin];
+                uint32_t st[kRU], stv[kRU][kWin];
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    const int32_t i = ptot - 1 - (i0 + u * NT + tid);    // the chunk's newest touches first
+                    h[u] = kEmpty;
+                    st[u] = 0;
+                    if (i >= 0) {
+                        int32_t lo = 0, hi = n_r - 1;     // the route holding touch i
+                        while (lo < hi) {
+                            const int32_t mid = (lo + hi + 1) >> 1;
+                            if (r_off[mid] <= i) lo = mid;
+                            else hi = mid - 1;
+                        }
+                        const int32_t q = i - r_off[lo];            // touches go from the last block
+                        const int32_t kb = r_Ps[lo] - 1 - q;        // to the first
+                        st[u] = (uint32_t)(stamp0 + r_off[lo] + q);
+                        h[u] = a.chains[r_cbs[lo] + kb];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    const uint64_t s0 = home_slot(h[u], smask);
+#pragma unroll
+                    for (int r = 0; r < kWin; ++r) {
+                        k[u][r] = kEmpty;
+                        stv[u][r] = 0;
+                        if (h[u] != kEmpty) load_slot(tk + s0 + group_slot(h[u], r), k[u][r], stv[u][r]);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    if (h[u] == kEmpty) continue;
+                    const uint64_t s0 = home_slot(h[u], smask);
+                    uint64_t sl = ~0ull;
+                    bool later = false;
+                    int empty = -1;
+#pragma unroll
+                    for (int r = 0; r < kWin; ++r) {
+                        if (sl == ~0ull && empty < 0) {
+                            if (k[u][r] == h[u]) {
+                                sl = s0 + group_slot(h[u], r);
+                                later = stv[u][r] > st[u];
+                            } else if (k[u][r] == kEmpty) {
+                                empty = r;
+                            }
+                        }
+                    }
+                    if (later) continue;      // a later touch of the block was stamped already
+                    if (sl == ~0ull) {
+                        bool done = false;
+                        if (empty >= 0) {
+                            const uint64_t si = s0 + group_slot(h[u], empty);
+                            uint64_t prev = kEmpty;
+                            if (__hip_atomic_compare_exchange_strong(&tk[si].key, &prev, h[u], __ATOMIC_RELAXED,
+                                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) ||
+                                prev == h[u]) {
+                                sl = si;
+                                done = true;
+                            }
+                        }
+                        if (!done) {
+                            int ins;
+                            sl = insert_or_touch(tk, smask, h[u], ins, a.status);
+                        }
+                    }
+                    if (sl == ~0ull) continue;
+                    __hip_atomic_fetch_max(&tk[sl].stamp, st[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    tl[st[u] & rmask] = (uint32_t)sl;
+                }
+            }
+            end = stamp0;
+            __syncthreads();
+        }
+        if (tid == 0) {
+            s_head[j] = 0;
+            s_tail[j] = (uint32_t)T;
+            s_stamped[j] = 1;
+        }
+        __syncthreads();
+        return true;
     };
 
     // ---- evict blocks of worker sg down to the capacity (all threads): live log records in log
@@ -2037,7 +2315,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 // the recency of its routes
                 clear_tables(sg, sg + 1);
                 __syncthreads();
-                replay(sg, sh.tdone);
+                if (!materialize(sg, sh.tdone)) replay(sg, sh.tdone);
             }
             evict(sg, r_ep[b]);
             if (tiers) {

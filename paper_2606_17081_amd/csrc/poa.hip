@@ -89,6 +89,20 @@ __device__ __forceinline__ void wave_argmin_f64(double& v, int32_t& j)
     j = bj;
 }
 
+// Sum of term(i) over the m rows of a window, the same value in every lane:
+// lane l adds rows l, l + 64, ... in order, then the 64 partial sums are added
+// in lane order (fp64; a fixed order, so every launch gives the same bits).
+template <class Term>
+__device__ __forceinline__ double window_sum(int32_t m, const Term& term)
+{
+    const int lane = threadIdx.x & 63;
+    double part = 0.0;
+    for (int32_t i = lane; i < m; i += PT) part += term(i);
+    double s = 0.0;
+    for (int32_t l = 0; l < PT && l < m; ++l) s += lane_f64(part, l);
+    return s;
+}
+
 // Dispatch order: windows by descending size class (bit length of m), so the
 // longest windows start first.  One workgroup; the order within a class is
 // whatever the atomics give (it only affects scheduling).
@@ -199,10 +213,9 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             }
             continue;
         }
-        if (tid == 0 && a.selfish) {
-            double s = 0.0;
-            for (int32_t i = 0; i < m; ++i) s += (double)cm[(int64_t)i * W + a.route_worker[r0 + i]];
-            a.selfish[w] = s;
+        if (a.selfish) {
+            const double s = window_sum(m, [&](int32_t i) { return (double)cm[(int64_t)i * W + a.route_worker[r0 + i]]; });
+            if (tid == 0) a.selfish[w] = s;
         }
         // ---- successive shortest paths (lane y < W stands for worker y)
         for (int32_t pq = tid; pq < W * W; pq += PT) s_er[pq] = -1;
@@ -337,10 +350,9 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             __syncthreads();
         }
         if (tid == 0 && a.coord && !placed_all) a.coord[w] = __longlong_as_double(0x7ff8000000000000ll);
-        if (tid == 0 && a.coord && placed_all) {
-            double s = 0.0;
-            for (int32_t i = 0; i < m; ++i) s += (double)cm[(int64_t)i * W + s_assign[i]];
-            a.coord[w] = s;
+        if (a.coord && placed_all) {
+            const double s = window_sum(m, [&](int32_t i) { return (double)cm[(int64_t)i * W + s_assign[i]]; });
+            if (tid == 0) a.coord[w] = s;
         }
         __syncthreads();
     }
