@@ -762,7 +762,8 @@ __device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_
 }
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n on workers
-// without recency, by the run walk above; info and put as in prefix_searches.
+// without recency, by the run walk above; info(i, ch, P, j, h0) as in
+// prefix_searches plus the item's hash at block 0, put as there.
 // KI walks of a thread issue their loads together; a walk step loads either
 // the item's hash at its current block, a run pair, or the two hashes a
 // binary-search step compares.
@@ -790,8 +791,8 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
             hq[u] = 0ull;
             qhi[u] = 0ull;
             qok[u] = false;
-            own[u] = i < n && info(i, ch[u], P[u], jw[u]);
-            mode[u] = own[u] && P[u] > 0 ? HASH : DONE;
+            own[u] = i < n && info(i, ch[u], P[u], jw[u], hq[u]);
+            mode[u] = own[u] && P[u] > 0 ? LOOK : DONE;
         }
         for (;;) {
             bool any = false;
@@ -1714,11 +1715,12 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             if (lz)
                 run_searches(
                     n,
-                    [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj) {
+                    [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj, uint64_t& h0) {
                         const int32_t b = b_lo + i / per;
                         jj = j < 0 ? i % per : j;
                         ch = a.chains + r_cb[b];
                         P = r_P[b];
+                        h0 = r_first[b];
                         return s_stamped[jj] == 0;
                     },
                     put, g_runs, rsmask, a.chains);
