@@ -309,38 +309,71 @@ def check_parity(runner, oracle_out: dict, label: str) -> dict:
 
 # ---------------------------------------------------------------- legs
 
-def saturation_bench(torch, rk, wl, stream, steps, warmup, slots):
-    """The headline: 10,240 saturation / controller episodes per step."""
+def saturation_bench(torch, rk, wl, stream, steps, warmup, slots, pipeline=True):
+    """The headline: 10,240 saturation / controller episodes per step.  With
+    pipeline, two runners take turns so that consecutive steps overlap: step
+    k's episodes run on the main stream while a second stream computes step
+    k-1's PoA-hat and hashes step k+1's traces; each step still does all of
+    its work inside the timed region."""
     from paper_2606_17081_amd.episodes import EpisodeRunner
     log("generating the saturation sweep (256 traces of 2,048 requests)")
     w = wl.saturation_workload()
-    r = EpisodeRunner(w, keep_cost=True, ws_slots=slots)
+    runners = [EpisodeRunner(w, keep_cost=True, ws_slots=slots) for _ in range(2 if pipeline else 1)]
+    r = runners[0]
     torch.cuda.synchronize()
     log(f"{len(r.episodes)} episodes, {r.n_rows} routes, {r.n_windows} PoA windows, {slots} episode workspaces "
-        f"({r.workspace.numel() / 1e9:.1f} GB); warmup {warmup}")
+        f"({r.workspace.numel() / 1e9:.1f} GB per runner, {len(runners)} runners); warmup {warmup}")
     for _ in range(max(1, warmup)):
-        r.step(stream=stream)
+        for x in runners:
+            x.step(stream=stream)
     torch.cuda.synchronize()
     assert rk.device_status(reset=True) == 0
-    ref_poa = r.poa_hat[: len(r.episodes)].clone()
-    t_hash, t_sim, t_poa = KernelTimer(torch, stream), KernelTimer(torch, stream), KernelTimer(torch, stream)
+    E, n = len(r.episodes), r.n_rows
+    ref_poa = r.poa_hat[:E].clone()
+    ref_route = r.route_worker[:n].clone()
+    side = torch.cuda.Stream() if pipeline else stream
+    t_sim = KernelTimer(torch, stream)
+    t_hash, t_poa = KernelTimer(torch, side), KernelTimer(torch, side)
+    e_sim = [None] * steps
+
+    def prepare(k):
+        x = runners[k % len(runners)]
+        if pipeline and k >= 2:
+            side.wait_event(e_sim[k - 2])
+        with t_hash:
+            x.hash(stream=side)
+        ready = torch.cuda.Event()
+        ready.record(side)
+        return ready
+
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
-        with t_hash:
-            r.hash(stream=stream)
+    ready = prepare(0)
+    for k in range(steps):
+        x = runners[k % len(runners)]
+        stream.wait_event(ready)
         with t_sim:
-            r.simulate(stream=stream)
+            x.simulate(stream=stream)
+        done = torch.cuda.Event()
+        done.record(stream)
+        e_sim[k] = done
+        if pipeline and k + 1 < steps:
+            ready = prepare(k + 1)
+        side.wait_event(done)
         with t_poa:
-            r.poa(stream=stream)
+            x.poa(stream=side)
+        if not pipeline and k + 1 < steps:
+            ready = prepare(k + 1)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     assert rk.device_status(reset=True) == 0
-    assert torch.equal(r.poa_hat[: len(r.episodes)], ref_poa), "timed steps differ from the warmup step"
+    for x in runners[: min(len(runners), steps)]:
+        assert torch.equal(x.poa_hat[:E], ref_poa), "timed steps differ from the warmup step (PoA-hat)"
+        assert torch.equal(x.route_worker[:n], ref_route), "timed steps differ from the warmup step (routes)"
+    del runners[1:]
     ms_step = wall * 1e3 / steps
     stage = dict(hash=t_hash.mean_ms(), simulate=t_sim.mean_ms(), poa=t_poa.mean_ms())
     log(f"saturation step {ms_step:.2f} ms; stages {stage}")
-    E, n = len(r.episodes), r.n_rows
     sv = episode_survey_bytes(r)
     kb = episode_kernel_bytes(r)
     sim_s = stage["simulate"] * 1e-3
@@ -362,6 +395,10 @@ def saturation_bench(torch, rk, wl, stream, steps, warmup, slots):
         "ms_per_step": round(ms_step, 4),
         "stage_ms": {k: round(v, 4) for k, v in stage.items()},
         "episode_workspaces": slots,
+        "pipeline": ("two runners take turns: step k's episodes on the main stream while the second stream runs "
+                     "step k-1's PoA-hat and hashes step k+1's traces (stage times measured under that overlap); "
+                     "the timed steps' PoA-hat and routes are checked against the warmup step")
+        if pipeline else "one stream: hash, episodes, PoA-hat",
         "roofline": roofline("episode_kernel", "saturation", sv["bytes"], stage["simulate"],
                              byte_model="survey: 8 B per logical probe sum(o + [o < P]), 24 B per prompt block, "
                                         "20 B per eviction, outputs",
@@ -671,6 +708,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--slots", type=int, default=512, help="episode workspaces of the headline launch")
+    ap.add_argument("--no-pipeline", action="store_true", help="headline steps one after another on one stream")
     ap.add_argument("--cpu-seeds", type=int, default=32, help="saturation seeds the oracle runs (all 40 episodes each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=("all", "saturation", "sweep", "scoring", "policies", "multiturn"),
@@ -717,7 +755,8 @@ def main():
     threads = oracle_threads()
     parity = {}
     # ---- headline: the saturation / controller sweep
-    r4, w4, sat = saturation_bench(torch, rk, wl, stream, args.steps, args.warmup, args.slots)
+    r4, w4, sat = saturation_bench(torch, rk, wl, stream, args.steps, args.warmup, args.slots,
+                                   pipeline=not args.no_pipeline)
     if only == "saturation":
         print(json.dumps({"saturation": sat}), flush=True)
         return

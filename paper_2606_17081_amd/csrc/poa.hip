@@ -139,10 +139,10 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
     const int32_t W = a.W;
     int32_t* s_n = (int32_t*)(smem + a.lds_int);   // [W] window counts of the greedy assignment
     float* s_base = (float*)(s_n + W);               // [W]
-    int32_t* s_mem = (int32_t*)(s_base + W);         // [W * kmax] rows held by each worker
-    int32_t* s_assign = s_mem + W * a.kmax;          // [max_window]
-    int32_t* s_pos = s_assign + a.max_window;        // [max_window] index of a row in its worker's list
-    int32_t* s_er = s_pos + a.max_window;            // [W * W] row realising each edge weight
+    // row indices and positions are below 4096: 16-bit, so that more windows fit a CU's LDS
+    int16_t* s_mem = (int16_t*)(s_base + W);         // [W * kmax] rows held by each worker
+    int16_t* s_pos = s_mem + W * a.kmax;             // [max_window] index of a row in its worker's list
+    int16_t* s_er = s_pos + a.max_window;            // [W * W] row realising each edge weight (-1: none)
     double* s_e = (double*)(smem + a.lds_dbl);       // [W * W] edge weights a -> b
 
     for (int32_t wi = blockIdx.x; wi < a.n_windows; wi += gridDim.x) {
@@ -278,11 +278,10 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                 }
                 const int32_t last = s_mem[x * a.kmax + cx - 1];
                 if (tid == 0) {
-                    s_mem[x * a.kmax + kk] = last;
-                    s_pos[last] = kk;
-                    s_mem[y * a.kmax + cy] = r;
-                    s_pos[r] = cy;
-                    s_assign[r] = y;
+                    s_mem[x * a.kmax + kk] = (int16_t)last;
+                    s_pos[last] = (int16_t)kk;
+                    s_mem[y * a.kmax + cy] = (int16_t)r;
+                    s_pos[r] = (int16_t)cy;
                 }
                 cnt += (tid == y) - (tid == x);
                 if (tid == hops) {
@@ -297,14 +296,13 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                 const int32_t cy = __builtin_amdgcn_readlane(cnt, y);
                 if (cy < a.kmax) {
                     if (tid == 0) {
-                        s_mem[y * a.kmax + cy] = i;
-                        s_pos[i] = cy;
+                        s_mem[y * a.kmax + cy] = (int16_t)i;
+                        s_pos[i] = (int16_t)cy;
                     }
                     cnt += tid == y;
                 } else if (tid == 0) {
                     atomicOr(a.status, RK_DEV_NO_CONVERGE);
                 }
-                if (tid == 0) s_assign[i] = y;
                 if (tid == hops) {
                     hx = -1;       // no loss
                     hy = y;        // the new row's worker gained row i
@@ -333,7 +331,7 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                     wave_argmin_f64(best, brow);
                     if (tid == 0) {
                         s_e[x * W + z] = best;
-                        s_er[x * W + z] = brow == 0x7fffffff ? -1 : brow;
+                        s_er[x * W + z] = (int16_t)(brow == 0x7fffffff ? -1 : brow);
                     }
                 }
             }
@@ -343,7 +341,7 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                     const double v = (double)cm[(int64_t)r * W + tid] - (double)cm[(int64_t)r * W + yg];
                     if (v < s_e[yg * W + tid]) {
                         s_e[yg * W + tid] = v;
-                        s_er[yg * W + tid] = r;
+                        s_er[yg * W + tid] = (int16_t)r;
                     }
                 }
             }
@@ -351,8 +349,13 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
         }
         if (tid == 0 && a.coord && !placed_all) a.coord[w] = __longlong_as_double(0x7ff8000000000000ll);
         if (a.coord && placed_all) {
-            const double s = window_sum(m, [&](int32_t i) { return (double)cm[(int64_t)i * W + s_assign[i]]; });
-            if (tid == 0) a.coord[w] = s;
+            // lane y adds the rows of worker y in list order, then the W sums in worker order
+            double part = 0.0;
+            if (wl)
+                for (int32_t k = 0; k < cnt; ++k) part += (double)cm[(int64_t)s_mem[tid * a.kmax + k] * W + tid];
+            double sum = 0.0;
+            for (int32_t y = 0; y < W; ++y) sum += lane_f64(part, y);
+            if (tid == 0) a.coord[w] = sum;
         }
         __syncthreads();
     }
@@ -459,7 +462,7 @@ static int poa_launch(int32_t n_windows, const int64_t* win_off, int32_t n_episo
         a.status = st;
         size_t o = 0;
         a.lds_int = 0;
-        o = align_up(((size_t)W * 2 + (size_t)W * a.kmax + 2 * (size_t)max_window + (size_t)W * W) * 4, 16);
+        o = align_up((size_t)W * 2 * 4 + ((size_t)W * a.kmax + (size_t)max_window + (size_t)W * W) * 2, 16);
         a.lds_dbl = (uint32_t)o;
         o = align_up(o + (size_t)W * W * 8, 16);
         const size_t limit = 60 * 1024;
