@@ -708,7 +708,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--slots", type=int, default=512, help="episode workspaces of the headline launch")
-    ap.add_argument("--no-pipeline", action="store_true", help="headline steps one after another on one stream")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="headline steps overlapped on two streams (PoA-hat and hashing beside the next episodes)")
+    ap.add_argument("--no-pipeline", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--cpu-seeds", type=int, default=32, help="saturation seeds the oracle runs (all 40 episodes each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=("all", "saturation", "sweep", "scoring", "policies", "multiturn"),
@@ -756,7 +758,7 @@ def main():
     parity = {}
     # ---- headline: the saturation / controller sweep
     r4, w4, sat = saturation_bench(torch, rk, wl, stream, args.steps, args.warmup, args.slots,
-                                   pipeline=not args.no_pipeline)
+                                   pipeline=args.pipeline and not args.no_pipeline)
     if only == "saturation":
         print(json.dumps({"saturation": sat}), flush=True)
         return
