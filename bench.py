@@ -13,7 +13,9 @@ element by element on the episodes the oracle ran:
   * the 1P/5D-shaped sweep (320 episodes, W = 6), consecutive steps
     overlapped on two streams, every episode checked against the oracle;
   * the batched scoring kernel on 65,536 requests x 64 workers with 2^20-slot
-    per-worker tables, and the global-index scorer on the same key sets;
+    per-worker tables (1,024 sampled requests against the oracle), and the
+    global-index scorer on the same key sets;
+  * the single tiny episode (W = 4, 64 requests), against the oracle;
   * the long-context multi-turn traces (128 episodes, W = 32) under LRU, and
     under frequency eviction and memory tiers on 16 of them;
   * the selection policies on the 1P/5D-shaped traces.
@@ -413,6 +415,31 @@ def saturation_bench(torch, rk, wl, stream, steps, warmup, slots, pipeline=True)
     return r, w, res
 
 
+def tiny_bench(torch, rk, wl, stream, steps, oracle=True):
+    """The single tiny episode (W = 4, 64 requests, C = 8): one step = hash +
+    episode + PoA-hat, timed over back-to-back steps; the oracle runs the same
+    episode and every output is compared."""
+    from paper_2606_17081_amd.episodes import EpisodeRunner
+    w = wl.tiny_workload()
+    r = EpisodeRunner(w, keep_cost=True)
+    for _ in range(3):
+        r.step(stream=stream)
+    n = max(steps, 20)
+    ms = burst_ms(torch, stream, lambda: r.step(stream=stream), n)
+    assert rk.device_status(reset=True) == 0
+    res = {"workload": "tiny: one episode, W=4 workers, 64 requests of 4..32 blocks, 8 prefix groups, cache 256, "
+                       "cap 512, C=8; hash + episode + PoA-hat",
+           "episodes": 1, "routes": r.n_rows, "ms_per_step": round(ms, 4),
+           "scorings_per_s": r.n_rows * w.W / (ms * 1e-3), "episodes_per_s": 1.0 / (ms * 1e-3),
+           "poa_hat": float(r.poa_hat[0].item())}
+    if oracle:
+        dt, routes, outs = run_oracle(w, list(enumerate(r.episodes)), 1)
+        res["oracle"] = {"seconds": round(dt, 6), "scorings_per_s": routes * w.W / dt, "threads": 1}
+        res["parity"] = check_parity(r, outs, "tiny")
+    log(f"tiny step {ms:.4f} ms")
+    return res
+
+
 def sweep_bench(torch, rk, wl, stream, steps, warmup):
     """The 1P/5D-shaped sweep (320 episodes): consecutive steps overlap on two
     streams (two runners take turns)."""
@@ -507,7 +534,7 @@ def index_log2_slots(n_keys: int) -> int:
     return b
 
 
-def scoring_bench(torch, rk, wl, stream, steps):
+def scoring_bench(torch, rk, wl, stream, steps, oracle=False):
     """The 65,536 x 64 snapshot scoring on the per-worker tables
     (rk_route_score_batch), and on the global block index
     (rk_route_score_index) built from the same key sets."""
@@ -531,6 +558,24 @@ def scoring_bench(torch, rk, wl, stream, steps):
     salg = score_algorithmic_bytes(inst)
     ach = salg / (ms * 1e-3) / 1e9
     log(f"scoring (tables): {ms:.4f} ms, {inst.B * inst.W / (ms * 1e-3):.4g} scorings/s, {ach:.1f} GB/s compulsory")
+    orc = None
+    if oracle:
+        # the oracle on a bounded sample of requests (its 64 key sets sorted first), compared element by element
+        from oracle import oracle as O
+        rows = np.unique(np.concatenate([[0, inst.B - 1], np.random.default_rng(1).integers(0, inst.B, 1022)]))
+        t0 = time.perf_counter()
+        r_ov, r_co, r_am = O.score_batch(inst.chains, inst.chain_off, inst.keys, inst.key_off, inst.active,
+                                         inst.w_ov, inst.w_act, inst.w_sat, inst.cap, rows=rows)
+        dt = time.perf_counter() - t0
+        co_ref, am_ref = co.cpu().numpy(), am.cpu().numpy()
+        bad = int((ov_ref[rows] != r_ov).any(axis=1).sum()
+                  + (co_ref[rows].view(np.uint32) != r_co.view(np.uint32)).any(axis=1).sum()
+                  + (am_ref[rows] != r_am).sum())
+        orc = {"sample": f"{rows.size} sampled requests x {inst.W} workers, including sorting the "
+                         f"{inst.W} key sets", "seconds": round(dt, 3),
+               "scorings_per_s": rows.size * inst.W / dt, "threads": 1}
+        parity = {"requests_checked": int(rows.size), "mismatches": bad}
+        log(f"scoring oracle {dt:.2f} s on {rows.size} requests; mismatches {bad}")
     del tables
     torch.cuda.empty_cache()
 
@@ -551,7 +596,7 @@ def scoring_bench(torch, rk, wl, stream, steps):
     build_ms = tb.mean_ms()
     log(f"scoring (index): {ms_i:.4f} ms; index build {build_ms:.3f} ms")
     wl_name = "scoring 65536 requests x 64 workers, 2^20-slot tables at load 0.5, chains of 16..512"
-    return {"workload": wl_name,
+    out = {"workload": wl_name,
             "scorings_per_s": inst.B * inst.W / (ms * 1e-3), "avg_ms": round(ms, 4),
             "roofline": roofline("score_kernel", "scoring", salg, ms,
                                  byte_model="survey compulsory: every table slot, chain hash and offset once, "
@@ -568,6 +613,10 @@ def scoring_bench(torch, rk, wl, stream, steps):
                       "roofline": roofline("score_index_kernel", "scoring", ialg, ms_i,
                                            byte_model="own: chains, offsets, outputs and one 16-byte index "
                                                       "slot per position of the union's first-miss scan")}}
+    if orc is not None:
+        out["oracle"] = orc
+        out["parity"] = parity
+    return out
 
 
 def policy_bench(torch, rk, wl, stream, steps):
@@ -713,7 +762,7 @@ def main():
     ap.add_argument("--no-pipeline", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--cpu-seeds", type=int, default=32, help="saturation seeds the oracle runs (all 40 episodes each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=("all", "saturation", "sweep", "scoring", "policies", "multiturn"),
+    ap.add_argument("--only", choices=("all", "saturation", "sweep", "scoring", "policies", "multiturn", "tiny"),
                     default="all", help="profiling passes: run one leg only, without the oracle")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this size (counter calibration)")
@@ -743,6 +792,9 @@ def main():
     only = args.only
     if only == "scoring":
         print(json.dumps({"score_batch": scoring_bench(torch, rk, wl, stream, args.steps)}), flush=True)
+        return
+    if only == "tiny":
+        print(json.dumps({"tiny": tiny_bench(torch, rk, wl, stream, args.steps, oracle=False)}), flush=True)
         return
     if only == "policies":
         print(json.dumps({"policies": policy_bench(torch, rk, wl, stream, args.steps)}), flush=True)
@@ -797,8 +849,14 @@ def main():
     del r2
     torch.cuda.empty_cache()
 
-    score = scoring_bench(torch, rk, wl, stream, args.steps)
+    score = scoring_bench(torch, rk, wl, stream, args.steps, oracle=not args.no_cpu_baseline)
+    if "parity" in score:
+        parity["scoring"] = score["parity"]
     torch.cuda.empty_cache()
+
+    tiny = tiny_bench(torch, rk, wl, stream, args.steps, oracle=not args.no_cpu_baseline)
+    if "parity" in tiny:
+        parity["tiny"] = tiny["parity"]
 
     r5, w5, multi = multiturn_bench(torch, rk, wl, stream, args.steps)
     if not args.no_cpu_baseline:
@@ -837,6 +895,7 @@ def main():
         "cpu_baseline": cpu,
         "parity": parity,
         "saturation": {k: v for k, v in sat.items() if k not in ("roofline", "probe_rate", "stage_ms")},
+        "tiny": tiny,
         "sweep70b": sweep,
         "score_batch": score,
         "multiturn": multi,

@@ -54,7 +54,10 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     uint64_t live_max = (uint64_t)cache_blocks + (uint64_t)max_blocks;
     L.slots = next_pow2(2 * live_max);
     L.ring = next_pow2(2 * live_max);
-    L.runs = next_pow2(2 * (uint64_t)(max_routes > 2 ? max_routes : 2));   // at most one run per route
+    // run index entries: a run's first block and its checkpoints, at most 2 per route plus one per
+    // 2^kCkptLog cached blocks of each worker, at load <= 1/2
+    L.runs = next_pow2(2 * (2 * (uint64_t)(max_routes > 2 ? max_routes : 2) +
+                            (uint64_t)W * ((live_max >> kCkptLog) + 1)));
     size_t o = 0;
     L.off_slots = o;   o = align_up(o + (size_t)W * L.slots * sizeof(Slot), 256);
     L.off_log = o;     o = align_up(o + (size_t)W * L.ring * sizeof(uint32_t), 256);

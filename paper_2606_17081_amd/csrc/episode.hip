@@ -680,17 +680,24 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
 // Until a worker first evicts (under LRU, in prefix mode), its cached set is
 // the union of the prefixes of the chains routed to it, i.e. a trie of blocks;
 // a route adds one path to that trie, the blocks [o, P) past the overlap o it
-// was decided with.  Such a path is a run, kept as one entry keyed by the hash
-// of its first block (the chained hash names the whole prefix, so a lookup by
-// the hash of block p of another chain finds the run exactly when that chain
-// reaches the run's first block).  A branch off the middle of a run is always
-// the first block of a later run, so the longest cached prefix of a chain is
-// found by walking: look up the run that starts at the current block, follow
-// it while the two chains agree (the first differing hash by binary search),
-// and look up again at the block where they part or where the run ends.  One
-// entry per route replaces an insert per new block.  All workers of an episode
-// share one table of 16-byte RunSlots, probed from run_home in aligned pairs.
+// was decided with.  Such a path is a run.  A run is entered in the index under
+// the hash of its first block and under the hash of every block of it at a
+// chain position that is a multiple of kCkpt (a checkpoint); each entry names
+// the run's chain and end.  The chained hash names the whole prefix, so an
+// entry keyed by the hash of block p of another chain is found exactly when
+// that chain reaches the entry's block, and since every cached block belongs
+// to exactly one run, block p at a checkpoint position is cached iff the
+// index holds it.  Caches are prefix-closed, so that membership is monotone
+// along a chain: a binary search over a chain's checkpoints finds the last
+// cached checkpoint c, and the first miss lies in (c, c + kCkpt].  There the
+// search follows c's run while the two chains agree (the first differing hash
+// by binary search) and looks up a run that starts where they part or where
+// the run ends; a branch off a run is always the first block of a later run.
+// A few entries per route replace an insert per new block.  All workers of an
+// episode share one table of 16-byte RunSlots, probed from run_home in
+// aligned pairs.
 constexpr int kRunWin = 2;
+constexpr int kCkpt = 1 << kCkptLog;
 
 __device__ __forceinline__ uint64_t run_home(uint64_t h, int32_t j, uint64_t rsmask)
 {
@@ -703,6 +710,18 @@ __device__ __forceinline__ uint64_t run_val(int64_t cb, int32_t j, int32_t end)
     return ((uint64_t)cb << 24) | ((uint64_t)(uint32_t)j << 16) | (uint64_t)(uint32_t)end;
 }
 
+// index entries of a run over blocks [st, P), st < P: its first block and the checkpoints past it
+__device__ __forceinline__ int32_t run_entries(int32_t st, int32_t P)
+{
+    return 1 + ((P - 1) >> kCkptLog) - (st >> kCkptLog);
+}
+
+// chain position of entry k of the run over [st, P)
+__device__ __forceinline__ int32_t run_entry_pos(int32_t st, int32_t k)
+{
+    return k == 0 ? st : (((st >> kCkptLog) + k) << kCkptLog);
+}
+
 __device__ __forceinline__ void load_run(const RunSlot* p, uint64_t& key, uint64_t& val)
 {
     const uint4 v = *reinterpret_cast<const uint4*>(p);
@@ -710,8 +729,8 @@ __device__ __forceinline__ void load_run(const RunSlot* p, uint64_t& key, uint64
     val = (uint64_t)v.z | ((uint64_t)v.w << 32);
 }
 
-// Run of worker j starting with block hash h, whose first pair (from g) is
-// loaded in k, v; false when there is none.
+// Entry of worker j keyed h, whose first pair (from g) is loaded in k, v;
+// false when there is none.
 __device__ __forceinline__ bool run_finish(const RunSlot* rt, uint64_t rsmask, uint64_t h, int32_t j, uint64_t g,
                                            const uint64_t* k, const uint64_t* v, uint64_t& val)
 {
@@ -739,9 +758,9 @@ __device__ __forceinline__ bool run_finish(const RunSlot* rt, uint64_t rsmask, u
     return false;
 }
 
-// Add the run (h, val) of worker j.  Each (worker, first block) pair is added
-// at most once, so a slot already holding h belongs to another worker's run;
-// concurrent adds claim empty slots by compare-and-swap.
+// Add the entry (h, val) of worker j.  Each block belongs to one run and is
+// entered at most once, so a slot already holding h belongs to another
+// worker's run; concurrent adds claim empty slots by compare-and-swap.
 __device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_t h, int32_t j, uint64_t val,
                                            int32_t* status)
 {
@@ -762,20 +781,22 @@ __device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_
 }
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n on workers
-// without recency, by the run walk above; info(i, ch, P, j, h0) as in
-// prefix_searches plus the item's hash at block 0, put as there.
-// KI walks of a thread issue their loads together; a walk step loads either
-// the item's hash at its current block, a run pair, or the two hashes a
-// binary-search step compares.
+// without recency; info(i, ch, P, j, h0) as in prefix_searches plus the
+// item's hash at block 0, put as there.  KI searches of a thread issue their
+// loads together.  A step of the checkpoint search (CKPT) loads a run pair and
+// the chain hashes at both checkpoints the next step may probe; a step of the
+// walk inside the last interval loads the item's hash at its current block
+// (HASH), a run pair (LOOK), or the two hashes a binary-search step compares
+// (CMP).  lim is the first position known to be missing (or P).
 template <class Info, class Put>
 __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const Put& put, const RunSlot* rt,
                                              uint64_t rsmask, const uint64_t* chains)
 {
-    enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3 };
+    enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3, CKPT = 4 };
     for (int32_t base = 0; base < n; base += NT * KI) {
         const uint64_t* ch[KI];
         const uint64_t* rc[KI];
-        int32_t P[KI], jw[KI], o[KI], lo[KI], hi[KI], mode[KI];
+        int32_t P[KI], jw[KI], o[KI], lo[KI], hi[KI], mode[KI], km[KI], lim[KI];
         uint64_t hq[KI], qhi[KI];
         bool own[KI], qok[KI];
 #pragma unroll
@@ -786,23 +807,37 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
             P[u] = 0;
             jw[u] = 0;
             o[u] = 0;
-            lo[u] = 0;
-            hi[u] = 0;
             hq[u] = 0ull;
             qhi[u] = 0ull;
             qok[u] = false;
             own[u] = i < n && info(i, ch[u], P[u], jw[u], hq[u]);
-            mode[u] = own[u] && P[u] > 0 ? LOOK : DONE;
+            // checkpoints [lo, hi) undecided (those below lo cached, from hi on missing); km is
+            // probed next, first checkpoint 0, whose hash is known.  While the checkpoint search
+            // runs, rc and o hold the chain and end of the run of the last cached checkpoint.
+            lo[u] = 0;
+            hi[u] = (P[u] + kCkpt - 1) >> kCkptLog;
+            km[u] = 0;
+            lim[u] = P[u];
+            mode[u] = own[u] && P[u] > 0 ? CKPT : DONE;
         }
         for (;;) {
             bool any = false;
-            uint64_t x0[KI], x1[KI], y0[KI], y1[KI];
+            uint64_t x0[KI], x1[KI], y0[KI], y1[KI], pm[KI];
             int32_t mid[KI];
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
-                x0[u] = x1[u] = y0[u] = y1[u] = 0ull;
+                x0[u] = x1[u] = y0[u] = y1[u] = pm[u] = 0ull;
                 mid[u] = (lo[u] + hi[u]) >> 1;
-                if (mode[u] == HASH) {
+                if (mode[u] == CKPT) {
+                    // with the run pair, the chain hashes of the next probe after a hit (into qhi)
+                    // and after a miss (pm)
+                    const uint64_t g = run_home(hq[u], jw[u], rsmask);
+                    load_run(rt + g, x0[u], y0[u]);
+                    load_run(rt + g + 1, x1[u], y1[u]);
+                    if (km[u] + 1 < hi[u]) qhi[u] = ch[u][((km[u] + 1 + hi[u]) >> 1) << kCkptLog];
+                    if (lo[u] < km[u]) pm[u] = ch[u][((lo[u] + km[u]) >> 1) << kCkptLog];
+                    any = true;
+                } else if (mode[u] == HASH) {
                     x0[u] = ch[u][o[u]];
                     any = true;
                 } else if (mode[u] == LOOK) {
@@ -819,7 +854,41 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
             if (!any) break;
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
-                if (mode[u] == HASH) {
+                if (mode[u] == CKPT) {
+                    const uint64_t kk[kRunWin] = {x0[u], x1[u]}, vv[kRunWin] = {y0[u], y1[u]};
+                    uint64_t val = 0ull;
+                    if (run_finish(rt, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
+                        rc[u] = chains + (int64_t)(val >> 24);
+                        o[u] = (int32_t)(val & 0xFFFFu);
+                        lo[u] = km[u] + 1;
+                        km[u] = (lo[u] + hi[u]) >> 1;
+                        hq[u] = qhi[u];
+                    } else {
+                        hi[u] = km[u];
+                        km[u] = (lo[u] + hi[u]) >> 1;
+                        hq[u] = pm[u];
+                    }
+                    if (lo[u] >= hi[u]) {
+                        if (lo[u] == 0) {
+                            mode[u] = DONE;          // block 0 missing: o stays 0
+                        } else {
+                            // the last cached checkpoint c is held by the run in rc, ending at o; the
+                            // first miss lies in (c, c + kCkpt], or at P
+                            const int32_t c = (lo[u] - 1) << kCkptLog;
+                            lim[u] = min(P[u], lo[u] << kCkptLog);
+                            const int32_t m = min(lim[u], o[u]);
+                            lo[u] = c + 1;
+                            hi[u] = m;
+                            qok[u] = false;
+                            if (lo[u] >= hi[u]) {
+                                o[u] = m;
+                                mode[u] = o[u] < lim[u] ? HASH : DONE;
+                            } else {
+                                mode[u] = CMP;
+                            }
+                        }
+                    }
+                } else if (mode[u] == HASH) {
                     hq[u] = x0[u];
                     mode[u] = LOOK;
                 } else if (mode[u] == LOOK) {
@@ -828,21 +897,21 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                     if (!run_finish(rt, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
                         mode[u] = DONE;
                     } else {
-                        // the run holds blocks [o, end) of the chain at val >> 24
+                        // the entry's run holds blocks [o, end) of the chain at val >> 24
                         rc[u] = chains + (int64_t)(val >> 24);
-                        const int32_t m = min(P[u], (int32_t)(val & 0xFFFFu));
+                        const int32_t m = min(lim[u], (int32_t)(val & 0xFFFFu));
                         lo[u] = o[u] + 1;
                         hi[u] = m;
                         qok[u] = false;
                         if (lo[u] >= hi[u]) {
                             o[u] = m;
-                            mode[u] = o[u] < P[u] ? HASH : DONE;
+                            mode[u] = o[u] < lim[u] ? HASH : DONE;
                         } else {
                             mode[u] = CMP;
                         }
                     }
                 } else if (mode[u] == CMP) {
-                    // first block in [lo, hi) where the chains differ (hi: the run's end or P)
+                    // first block in [lo, hi) where the chains differ (hi: the run's end or lim)
                     if (x0[u] == x1[u]) {
                         lo[u] = mid[u] + 1;
                     } else {
@@ -852,7 +921,7 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                     }
                     if (lo[u] >= hi[u]) {
                         o[u] = lo[u];
-                        if (o[u] >= P[u]) {
+                        if (o[u] >= lim[u]) {
                             mode[u] = DONE;
                         } else if (qok[u]) {
                             hq[u] = qhi[u];      // the item's hash at hi, loaded by the step that set hi
@@ -1278,23 +1347,21 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 // claimed routes.
                 int32_t* wst = sh.wst[wave];
                 const int32_t nr = hi - c;
-                int32_t tot = 0, pr = 0;
+                int32_t tot = 0, pr = 0, st = -1;
                 if (lane < nr) {
-                    const int32_t bl = c + lane, sgl = r_sig[bl];
+                    const int32_t bl = c + lane, sgl = r_sig[bl], Pl = r_P[bl];
                     if (s_stamped[sgl]) {
-                        pr = r_P[bl];
+                        pr = Pl;
                     } else {
-                        const int32_t st = o_cur[bl * W + sgl], Pl = r_P[bl];
-                        if (st < Pl)
-                            run_insert(g_runs, rsmask, a.chains[r_cb[bl] + st], sgl, run_val(r_cb[bl], sgl, Pl),
-                                       a.status);
+                        st = o_cur[bl * W + sgl];
+                        pr = st < Pl ? run_entries(st, Pl) : 0;
                     }
                 }
                 const int32_t off = wave_excl_sum_dpp(pr, tot);
                 if (tot == 0) continue;
                 if (lane < nr) {
                     woff[lane] = off;
-                    wst[lane] = 0;
+                    wst[lane] = st;         // a run's first block, or -1 for a route that touches every block
                 }
                 if (lane == 0) woff[nr] = tot;
                 ep_wave_sync();
@@ -1302,8 +1369,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     int32_t r = 0;
                     while (r + 1 < nr && woff[r + 1] <= i) ++r;
                     const int32_t b = c + r;
-                    const int32_t k = wst[r] + (i - woff[r]);
+                    const int32_t k = i - woff[r];
                     const int32_t P = r_P[b], sg = r_sig[b];
+                    if (wst[r] >= 0) {
+                        const int32_t pos = run_entry_pos(wst[r], k);
+                        run_insert(g_runs, rsmask, a.chains[r_cb[b] + pos], sg, run_val(r_cb[b], sg, P), a.status);
+                        continue;
+                    }
                     Slot* tk = g_slots + (uint64_t)sg * S;
                     uint32_t* tl = g_log + (uint64_t)sg * R;
                     const bool known = k < r_otab[b];

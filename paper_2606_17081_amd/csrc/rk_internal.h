@@ -257,14 +257,16 @@ struct __align__(16) Slot {
     uint32_t fkey;
 };
 
-// A run of an episode's prefix index: a route added the blocks [o, end) of its
-// chain to a worker that held the blocks before o, keyed by the hash of block
-// o; val packs the chain's base index (bits 63..24), the worker (23..16) and
-// end (15..0).  Key 0 marks an empty slot.
+// An entry of an episode's run index: a route added the blocks [o, end) of
+// its chain to a worker that held the blocks before o; the run is entered
+// under the hash of block o and of every block of it at a position that is a
+// multiple of 2^kCkptLog.  val packs the chain's base index (bits 63..24), the
+// worker (23..16) and end (15..0).  Key 0 marks an empty slot.
 struct __align__(16) RunSlot {
     uint64_t key;
     uint64_t val;
 };
+constexpr int kCkptLog = 4;
 
 constexpr int kEpisodeThreads = 256;   // threads of an episode's workgroup
 
