@@ -606,64 +606,81 @@ constexpr int KP = 4;   // batch pairs a thread searches together for their comm
 // names a chain, its length and a worker table (info, false for an item
 // this search does not handle), and receives the first chain position
 // missing from the table (put).  Binary search per thread, exact for tables
-// prefix-closed along the chain; KI searches of a thread issue their loads
-// together.
+// prefix-closed along the chain.  A step loads the probed block's group and
+// the chain hashes of both positions the next step may probe, so a step costs
+// one memory round trip; the KI searches of a thread issue the same loads
+// from addresses chosen by masks (a finished search reads the first group of
+// the slots and the first chain hash again), so that no branch separates
+// them and all are in flight together.
 template <class Info, class Put>
 __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, const Put& put, const Slot* slots,
-                                                uint64_t S)
+                                                uint64_t S, const uint64_t* chains)
 {
     const uint64_t smask = S - 1;
     for (int32_t base = 0; base < n; base += NT * KI) {
         int32_t lo[KI], hi[KI];
-        const uint64_t* ch[KI];
-        const Slot* tb[KI];
+        int64_t cb[KI];
+        uint64_t tbo[KI], hk[KI];
         bool own[KI];
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
             const int32_t i = base + u * NT + (int32_t)threadIdx.x;
             lo[u] = 0;
             hi[u] = 0;
-            ch[u] = nullptr;
-            tb[u] = slots;
+            cb[u] = 0;
+            tbo[u] = 0;
             own[u] = false;
             if (i < n) {
+                const uint64_t* ch = chains;
                 int32_t P, j;
-                own[u] = info(i, ch[u], P, j);
+                own[u] = info(i, ch, P, j);
                 if (own[u]) {
                     hi[u] = P;
-                    tb[u] = slots + (uint64_t)j * S;
+                    cb[u] = ch - chains;
+                    tbo[u] = (uint64_t)j * S;
                 }
             }
         }
+        bool act = false;
+#pragma unroll
+        for (int u = 0; u < KI; ++u) act |= lo[u] < hi[u];
+        // (the chains are not empty when some search of the thread is open)
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const int64_t m = -(int64_t)(lo[u] < hi[u]);
+            hk[u] = act ? chains[m & (cb[u] + ((lo[u] + hi[u]) >> 1))] : 0ull;
+        }
         for (;;) {
             bool any = false;
-            int32_t mid[KI];
-            uint64_t hk[KI];
 #pragma unroll
-            for (int u = 0; u < KI; ++u) {
-                mid[u] = (lo[u] + hi[u]) >> 1;
-                hk[u] = 0ull;
-                if (lo[u] < hi[u]) {
-                    hk[u] = ch[u][mid[u]];
-                    any = true;
-                }
-            }
+            for (int u = 0; u < KI; ++u) any |= lo[u] < hi[u];
             if (!any) break;
-            uint64_t kw[KI][kWin];
+            int32_t mid[KI];
+            uint64_t kw[KI][kWin], hc[KI], hd[KI];
             uint32_t sw[KI][kWin];
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
-                if (lo[u] < hi[u]) {
-                    const uint64_t s0 = home_slot(hk[u], smask);
+                mid[u] = (lo[u] + hi[u]) >> 1;
+                const int64_t m = -(int64_t)(lo[u] < hi[u]);
+                // the next probe after a hit (hc) and after a miss (hd); an empty range reads block 0
+                const int32_t mh = mid[u] + 1 < hi[u] ? (mid[u] + 1 + hi[u]) >> 1 : 0;
+                const int32_t mm = lo[u] < mid[u] ? (lo[u] + mid[u]) >> 1 : 0;
+                const Slot* g = slots + ((uint64_t)m & (tbo[u] + home_slot(hk[u], smask)));
 #pragma unroll
-                    for (int x = 0; x < kWin; ++x) load_slot(tb[u] + s0 + group_slot(hk[u], x), kw[u][x], sw[u][x]);
-                }
+                for (int x = 0; x < kWin; ++x) load_slot(g + group_slot(hk[u], x), kw[u][x], sw[u][x]);
+                hc[u] = chains[m & (cb[u] + mh)];
+                hd[u] = chains[m & (cb[u] + mm)];
             }
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
                 if (lo[u] < hi[u]) {
-                    if (finish_lookup(tb[u], smask, hk[u], home_slot(hk[u], smask), kw[u], sw[u])) lo[u] = mid[u] + 1;
-                    else hi[u] = mid[u];
+                    if (finish_lookup(slots + tbo[u], smask, hk[u], home_slot(hk[u], smask), kw[u], sw[u])) {
+                        lo[u] = mid[u] + 1;
+                        hk[u] = hc[u];
+                    } else {
+                        hi[u] = mid[u];
+                        hk[u] = hd[u];
+                    }
                 }
             }
         }
@@ -782,38 +799,42 @@ __device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n on workers
 // without recency; info(i, ch, P, j, h0) as in prefix_searches plus the
-// item's hash at block 0, put as there.  KI searches of a thread issue their
-// loads together.  A step of the checkpoint search (CKPT) loads a run pair and
-// the chain hashes at both checkpoints the next step may probe; a step of the
-// walk inside the last interval loads the item's hash at its current block
-// (HASH), a run pair (LOOK), or the two hashes a binary-search step compares
-// (CMP).  lim is the first position known to be missing (or P).
+// item's hash at block 0, put as there.  A step of the checkpoint search
+// (CKPT) loads a run pair and the chain hashes at both checkpoints the next
+// step may probe; a step of the walk inside the last interval loads the
+// item's hash at its current block (HASH), a run pair (LOOK), or the two
+// hashes a binary-search step compares (CMP).  lim is the first position known
+// to be missing (or P).  Every item of a thread issues the same four loads, a
+// run pair and two chain hashes, from addresses chosen by its mode (an item
+// that needs fewer reads the index's first pair or the first chain hash
+// again), so that no branch separates the KI items' loads and all of them are
+// in flight together.
 template <class Info, class Put>
 __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const Put& put, const RunSlot* rt,
                                              uint64_t rsmask, const uint64_t* chains)
 {
     enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3, CKPT = 4 };
     for (int32_t base = 0; base < n; base += NT * KI) {
-        const uint64_t* ch[KI];
-        const uint64_t* rc[KI];
+        int64_t cb[KI], rcb[KI];     // chain bases of the item and of the run it follows
         int32_t P[KI], jw[KI], o[KI], lo[KI], hi[KI], mode[KI], km[KI], lim[KI];
         uint64_t hq[KI], qhi[KI];
         bool own[KI], qok[KI];
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
             const int32_t i = base + u * NT + (int32_t)threadIdx.x;
-            ch[u] = chains;
-            rc[u] = chains;
+            const uint64_t* ch = chains;
             P[u] = 0;
             jw[u] = 0;
             o[u] = 0;
             hq[u] = 0ull;
             qhi[u] = 0ull;
             qok[u] = false;
-            own[u] = i < n && info(i, ch[u], P[u], jw[u], hq[u]);
+            own[u] = i < n && info(i, ch, P[u], jw[u], hq[u]);
+            cb[u] = ch - chains;
+            rcb[u] = 0;
             // checkpoints [lo, hi) undecided (those below lo cached, from hi on missing); km is
             // probed next, first checkpoint 0, whose hash is known.  While the checkpoint search
-            // runs, rc and o hold the chain and end of the run of the last cached checkpoint.
+            // runs, rcb and o hold the chain and end of the run of the last cached checkpoint.
             lo[u] = 0;
             hi[u] = (P[u] + kCkpt - 1) >> kCkptLog;
             km[u] = 0;
@@ -822,57 +843,51 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
         }
         for (;;) {
             bool any = false;
-            uint64_t x0[KI], x1[KI], y0[KI], y1[KI], pm[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) any |= mode[u] != DONE;
+            if (!any) break;
+            uint64_t x0[KI], x1[KI], y0[KI], y1[KI], hc[KI], hd[KI];
             int32_t mid[KI];
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
-                x0[u] = x1[u] = y0[u] = y1[u] = pm[u] = 0ull;
                 mid[u] = (lo[u] + hi[u]) >> 1;
-                if (mode[u] == CKPT) {
-                    // with the run pair, the chain hashes of the next probe after a hit (into qhi)
-                    // and after a miss (pm)
-                    const uint64_t g = run_home(hq[u], jw[u], rsmask);
-                    load_run(rt + g, x0[u], y0[u]);
-                    load_run(rt + g + 1, x1[u], y1[u]);
-                    if (km[u] + 1 < hi[u]) qhi[u] = ch[u][((km[u] + 1 + hi[u]) >> 1) << kCkptLog];
-                    if (lo[u] < km[u]) pm[u] = ch[u][((lo[u] + km[u]) >> 1) << kCkptLog];
-                    any = true;
-                } else if (mode[u] == HASH) {
-                    x0[u] = ch[u][o[u]];
-                    any = true;
-                } else if (mode[u] == LOOK) {
-                    const uint64_t g = run_home(hq[u], jw[u], rsmask);
-                    load_run(rt + g, x0[u], y0[u]);
-                    load_run(rt + g + 1, x1[u], y1[u]);
-                    any = true;
-                } else if (mode[u] == CMP) {
-                    x0[u] = ch[u][mid[u]];
-                    x1[u] = rc[u][mid[u]];
-                    any = true;
-                }
+                const int32_t md = mode[u];
+                // all-ones masks of the item's mode: addresses by masks, not branches
+                const int32_t mC = -(int32_t)(md == CKPT), mH = -(int32_t)(md == HASH), mM = -(int32_t)(md == CMP);
+                const int32_t mP = -(int32_t)(md == CKPT || md == LOOK);
+                // CKPT: the next probes after a hit (hc) and after a miss (hd)
+                const int32_t mh = km[u] + 1 < hi[u] ? (km[u] + 1 + hi[u]) >> 1 : 0;
+                const int32_t mm = lo[u] < km[u] ? (lo[u] + km[u]) >> 1 : 0;
+                const int32_t ic = (mC & (mh << kCkptLog)) | (mH & o[u]) | (mM & mid[u]);
+                const int32_t id = (mC & (mm << kCkptLog)) | (mM & mid[u]);
+                const int64_t bc = (int64_t)(mC | mH | mM) & cb[u];
+                const int64_t bd = ((int64_t)mC & cb[u]) | ((int64_t)mM & rcb[u]);
+                const uint64_t g = (uint64_t)(int64_t)mP & run_home(hq[u], jw[u], rsmask);
+                load_run(rt + g, x0[u], y0[u]);
+                load_run(rt + g + 1, x1[u], y1[u]);
+                hc[u] = chains[bc + ic];
+                hd[u] = chains[bd + id];
             }
-            if (!any) break;
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
                 if (mode[u] == CKPT) {
                     const uint64_t kk[kRunWin] = {x0[u], x1[u]}, vv[kRunWin] = {y0[u], y1[u]};
                     uint64_t val = 0ull;
                     if (run_finish(rt, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
-                        rc[u] = chains + (int64_t)(val >> 24);
+                        rcb[u] = (int64_t)(val >> 24);
                         o[u] = (int32_t)(val & 0xFFFFu);
                         lo[u] = km[u] + 1;
-                        km[u] = (lo[u] + hi[u]) >> 1;
-                        hq[u] = qhi[u];
+                        hq[u] = hc[u];
                     } else {
                         hi[u] = km[u];
-                        km[u] = (lo[u] + hi[u]) >> 1;
-                        hq[u] = pm[u];
+                        hq[u] = hd[u];
                     }
+                    km[u] = (lo[u] + hi[u]) >> 1;
                     if (lo[u] >= hi[u]) {
                         if (lo[u] == 0) {
                             mode[u] = DONE;          // block 0 missing: o stays 0
                         } else {
-                            // the last cached checkpoint c is held by the run in rc, ending at o; the
+                            // the last cached checkpoint c is held by the run at rcb, ending at o; the
                             // first miss lies in (c, c + kCkpt], or at P
                             const int32_t c = (lo[u] - 1) << kCkptLog;
                             lim[u] = min(P[u], lo[u] << kCkptLog);
@@ -889,7 +904,7 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                         }
                     }
                 } else if (mode[u] == HASH) {
-                    hq[u] = x0[u];
+                    hq[u] = hc[u];
                     mode[u] = LOOK;
                 } else if (mode[u] == LOOK) {
                     const uint64_t kk[kRunWin] = {x0[u], x1[u]}, vv[kRunWin] = {y0[u], y1[u]};
@@ -898,7 +913,7 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                         mode[u] = DONE;
                     } else {
                         // the entry's run holds blocks [o, end) of the chain at val >> 24
-                        rc[u] = chains + (int64_t)(val >> 24);
+                        rcb[u] = (int64_t)(val >> 24);
                         const int32_t m = min(lim[u], (int32_t)(val & 0xFFFFu));
                         lo[u] = o[u] + 1;
                         hi[u] = m;
@@ -912,11 +927,11 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                     }
                 } else if (mode[u] == CMP) {
                     // first block in [lo, hi) where the chains differ (hi: the run's end or lim)
-                    if (x0[u] == x1[u]) {
+                    if (hc[u] == hd[u]) {
                         lo[u] = mid[u] + 1;
                     } else {
                         hi[u] = mid[u];
-                        qhi[u] = x0[u];
+                        qhi[u] = hc[u];
                         qok[u] = true;
                     }
                     if (lo[u] >= hi[u]) {
@@ -1783,7 +1798,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         P = r_P[b];
                         return s_stamped[jj] != 0;
                     },
-                    put, g_slots, S);
+                    put, g_slots, S, a.chains);
             if (lz)
                 run_searches(
                     n,
@@ -1985,20 +2000,20 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             }
             for (;;) {
                 bool any = false;
+#pragma unroll
+                for (int k = 0; k < KP; ++k) any |= lo[k] < hi[k];
+                if (!any) break;
+                // addresses by masks (a closed search reads the first chain hash), so that the KP
+                // pairs' loads are in flight together
                 int32_t mid[KP];
                 uint64_t va[KP], vb[KP];
 #pragma unroll
                 for (int k = 0; k < KP; ++k) {
                     mid[k] = (lo[k] + hi[k]) >> 1;
-                    va[k] = 0ull;
-                    vb[k] = 0ull;
-                    if (lo[k] < hi[k]) {
-                        va[k] = a.chains[ca[k] + mid[k]];
-                        vb[k] = a.chains[cc[k] + mid[k]];
-                        any = true;
-                    }
+                    const int64_t m = -(int64_t)(lo[k] < hi[k]);
+                    va[k] = a.chains[m & (ca[k] + mid[k])];
+                    vb[k] = a.chains[m & (cc[k] + mid[k])];
                 }
-                if (!any) break;
 #pragma unroll
                 for (int k = 0; k < KP; ++k) {
                     if (lo[k] < hi[k]) {
