@@ -460,32 +460,26 @@ __device__ __forceinline__ void touch_batch(Slot* __restrict__ t, uint64_t smask
 {
     uint64_t s0[kRU], prev[kRU], k[kRU][kWin];
     uint32_t stv[kRU][kWin];
-    bool won[kRU];
+    // the claims return the slots' previous keys and the group loads use masked addresses (an
+    // empty key reads the first group), so nothing waits before all are issued
 #pragma unroll
     for (int u = 0; u < kRU; ++u) {
         const uint64_t s = home_slot(h[u], smask);
         s0[u] = s + group_slot(h[u], 0);
         prev[u] = kEmpty;
-        won[u] = false;
-        if (h[u] != kEmpty)
-            won[u] = __hip_atomic_compare_exchange_strong(&t[s0[u]].key, &prev[u], h[u], __ATOMIC_RELAXED,
-                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (h[u] != kEmpty) prev[u] = atomicCAS(reinterpret_cast<unsigned long long*>(&t[s0[u]].key), kEmpty, h[u]);
     }
 #pragma unroll
     for (int u = 0; u < kRU; ++u) {
-        const uint64_t s = home_slot(h[u], smask);
+        const Slot* g = t + ((uint64_t)(-(int64_t)(h[u] != kEmpty)) & home_slot(h[u], smask));
 #pragma unroll
-        for (int r = 1; r < kWin; ++r) {
-            k[u][r] = kEmpty;
-            stv[u][r] = 0;
-            if (h[u] != kEmpty) load_slot(t + s + group_slot(h[u], r), k[u][r], stv[u][r]);
-        }
+        for (int r = 1; r < kWin; ++r) load_slot(g + group_slot(h[u], r), k[u][r], stv[u][r]);
     }
 #pragma unroll
     for (int u = 0; u < kRU; ++u) {
         sl[u] = ~0ull;
         if (h[u] == kEmpty) continue;
-        if (won[u] || prev[u] == h[u]) {
+        if (prev[u] == kEmpty || prev[u] == h[u]) {
             sl[u] = s0[u];
             continue;
         }
@@ -1629,76 +1623,90 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             }
             __syncthreads();
             const int64_t stamp0 = end - ptot;
+            // kRU touches per thread, each step's memory operations issued for all of them before
+            // any result is used (addresses by masks: an empty touch reads chain hash 0 and the
+            // table's first group)
             for (int32_t i0 = 0; i0 < ptot; i0 += NT * kRU) {
                 uint64_t h[kRU], k[kRU][kWin];
                 uint32_t st[kRU], stv[kRU][kWin];
+                int64_t hoff[kRU];
+                bool v[kRU];
 #pragma unroll
                 for (int u = 0; u < kRU; ++u) {
                     const int32_t i = ptot - 1 - (i0 + u * NT + tid);    // the chunk's newest touches first
-                    h[u] = kEmpty;
-                    st[u] = 0;
-                    if (i >= 0) {
-                        int32_t lo = 0, hi = n_r - 1;     // the route holding touch i
-                        while (lo < hi) {
-                            const int32_t mid = (lo + hi + 1) >> 1;
-                            if (r_off[mid] <= i) lo = mid;
-                            else hi = mid - 1;
-                        }
-                        const int32_t q = i - r_off[lo];            // touches go from the last block
-                        const int32_t kb = r_Ps[lo] - 1 - q;        // to the first
-                        st[u] = (uint32_t)(stamp0 + r_off[lo] + q);
-                        h[u] = a.chains[r_cbs[lo] + kb];
+                    v[u] = i >= 0;
+                    const int32_t ii = v[u] ? i : 0;
+                    int32_t lo = 0, hi = n_r - 1;     // the route holding touch ii
+                    while (lo < hi) {
+                        const int32_t mid = (lo + hi + 1) >> 1;
+                        if (r_off[mid] <= ii) lo = mid;
+                        else hi = mid - 1;
                     }
+                    const int32_t q = ii - r_off[lo];            // touches go from the last block
+                    const int32_t kb = r_Ps[lo] - 1 - q;         // to the first
+                    st[u] = (uint32_t)(stamp0 + r_off[lo] + q);
+                    hoff[u] = (-(int64_t)v[u]) & (r_cbs[lo] + kb);
                 }
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) h[u] = a.chains[hoff[u]];
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    const Slot* g = tk + ((uint64_t)(-(int64_t)v[u]) & home_slot(h[u], smask));
+#pragma unroll
+                    for (int r = 0; r < kWin; ++r) load_slot(g + group_slot(h[u], r), k[u][r], stv[u][r]);
+                }
+                // the key's slot in its first group, or the first empty slot there to claim
+                uint64_t sl[kRU], prev[kRU];
+                int32_t claim[kRU];
 #pragma unroll
                 for (int u = 0; u < kRU; ++u) {
                     const uint64_t s0 = home_slot(h[u], smask);
+                    sl[u] = ~0ull;
+                    claim[u] = -1;
+                    bool later = false, stop = false;
 #pragma unroll
                     for (int r = 0; r < kWin; ++r) {
-                        k[u][r] = kEmpty;
-                        stv[u][r] = 0;
-                        if (h[u] != kEmpty) load_slot(tk + s0 + group_slot(h[u], r), k[u][r], stv[u][r]);
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < kRU; ++u) {
-                    if (h[u] == kEmpty) continue;
-                    const uint64_t s0 = home_slot(h[u], smask);
-                    uint64_t sl = ~0ull;
-                    bool later = false;
-                    int empty = -1;
-#pragma unroll
-                    for (int r = 0; r < kWin; ++r) {
-                        if (sl == ~0ull && empty < 0) {
+                        if (!stop) {
                             if (k[u][r] == h[u]) {
-                                sl = s0 + group_slot(h[u], r);
+                                sl[u] = s0 + group_slot(h[u], r);
                                 later = stv[u][r] > st[u];
+                                stop = true;
                             } else if (k[u][r] == kEmpty) {
-                                empty = r;
+                                claim[u] = r;
+                                stop = true;
                             }
                         }
                     }
-                    if (later) continue;      // a later touch of the block was stamped already
-                    if (sl == ~0ull) {
-                        bool done = false;
-                        if (empty >= 0) {
-                            const uint64_t si = s0 + group_slot(h[u], empty);
-                            uint64_t prev = kEmpty;
-                            if (__hip_atomic_compare_exchange_strong(&tk[si].key, &prev, h[u], __ATOMIC_RELAXED,
-                                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) ||
-                                prev == h[u]) {
-                                sl = si;
-                                done = true;
-                            }
-                        }
-                        if (!done) {
-                            int ins;
-                            sl = insert_or_touch(tk, smask, h[u], ins, a.status);
-                        }
+                    if (!v[u] || later) {         // a later touch of the block was stamped already
+                        sl[u] = ~0ull;
+                        claim[u] = -2;
                     }
-                    if (sl == ~0ull) continue;
-                    __hip_atomic_fetch_max(&tk[sl].stamp, st[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                    tl[st[u] & rmask] = (uint32_t)sl;
+                    prev[u] = kEmpty;
+                }
+                // the claims return the slots' previous keys; nothing reads them before all are issued
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    if (claim[u] >= 0) {
+                        const uint64_t si = home_slot(h[u], smask) + group_slot(h[u], claim[u]);
+                        prev[u] = atomicCAS(reinterpret_cast<unsigned long long*>(&tk[si].key), kEmpty, h[u]);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    if (claim[u] >= 0) {
+                        if (prev[u] == kEmpty || prev[u] == h[u])
+                            sl[u] = home_slot(h[u], smask) + group_slot(h[u], claim[u]);
+                    }
+                    if (claim[u] != -2 && sl[u] == ~0ull) {    // a full first group or a lost claim
+                        int ins;
+                        sl[u] = insert_or_touch(tk, smask, h[u], ins, a.status);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kRU; ++u) {
+                    if (sl[u] == ~0ull) continue;
+                    __hip_atomic_fetch_max(&tk[sl[u]].stamp, st[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    tl[st[u] & rmask] = (uint32_t)sl[u];
                 }
             }
             end = stamp0;
