@@ -107,7 +107,7 @@ struct LeanTag {
 };
 
 struct EpShared {
-    int32_t next_e;
+    int32_t next_e, nlist;
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
     int32_t woff[NW][KR + 1], wst[NW][KR];
     uint32_t new_head, first_kept, adv;
@@ -597,20 +597,66 @@ constexpr int KI = 4;   // searches a thread keeps in flight together
 constexpr int KP = 4;   // batch pairs a thread searches together for their common prefix
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n: item i
-// names a chain, its length and a worker table (info, false for an item
-// this search does not handle), and receives the first chain position
-// missing from the table (put).  Binary search per thread, exact for tables
-// prefix-closed along the chain.  A step loads the probed block's group and
-// the chain hashes of both positions the next step may probe, so a step costs
-// one memory round trip; the KI searches of a thread issue the same loads
-// from addresses chosen by masks (a finished search reads the first group of
-// the slots and the first chain hash again), so that no branch separates
-// them and all are in flight together.
+// names a chain, its length, its hash at block 0 and a worker table (info,
+// false for an item this search does not handle), and receives the first
+// chain position missing from the table (put).  A first probe of every item's
+// block 0 decides the items that miss it (o = 0) and lists the others in
+// `list`; those then run a binary search over [1, P), exact for tables
+// prefix-closed along the chain, several per thread at most.  A step loads
+// the probed block's group and the chain hashes of both positions the next
+// step may probe, so a step costs one memory round trip; the KI searches of a
+// thread issue the same loads from addresses chosen by masks (a finished
+// search reads the first group of the slots and the first chain hash again),
+// so that no branch separates them and all are in flight together.
 template <class Info, class Put>
 __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, const Put& put, const Slot* slots,
-                                                uint64_t S, const uint64_t* chains)
+                                                uint64_t S, const uint64_t* chains, uint16_t* list,
+                                                int32_t* nlist)
 {
     const uint64_t smask = S - 1;
+    {
+        const int lane = threadIdx.x & 63;
+        __syncthreads();           // the list's previous users are done
+        if (threadIdx.x == 0) *nlist = 0;
+        __syncthreads();
+        for (int32_t base = 0; base < n; base += NT * KI) {
+            uint64_t tbo[KI], h0[KI], kw[KI][kWin];
+            uint32_t sw[KI][kWin];
+            bool own[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+                const uint64_t* ch = chains;
+                int32_t P = 0, j = 0;
+                h0[u] = 0ull;
+                own[u] = i < n && info(i, ch, P, j, h0[u]);
+                if (own[u] && P == 0) {
+                    put(i, 0);
+                    own[u] = false;
+                }
+                tbo[u] = (uint64_t)j * S;
+                const Slot* g = slots + ((uint64_t)(-(int64_t)own[u]) & (tbo[u] + home_slot(h0[u], smask)));
+#pragma unroll
+                for (int x = 0; x < kWin; ++x) load_slot(g + group_slot(h0[u], x), kw[u][x], sw[u][x]);
+            }
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+                bool hit = false;
+                if (own[u]) {
+                    hit = finish_lookup(slots + tbo[u], smask, h0[u], home_slot(h0[u], smask), kw[u], sw[u]);
+                    if (!hit) put(i, 0);
+                }
+                const unsigned long long m = __ballot(hit);
+                int32_t wb = 0;
+                if (lane == 0 && m) wb = atomicAdd(nlist, (int32_t)__popcll(m));
+                wb = __builtin_amdgcn_readfirstlane(wb);
+                if (hit) list[wb + __popcll(m & ((1ull << lane) - 1ull))] = (uint16_t)i;
+            }
+        }
+        __syncthreads();
+        n = *nlist;
+    }
     for (int32_t base = 0; base < n; base += NT * KI) {
         int32_t lo[KI], hi[KI];
         int64_t cb[KI];
@@ -618,21 +664,21 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
         bool own[KI];
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
-            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            const int32_t i2 = base + u * NT + (int32_t)threadIdx.x;
             lo[u] = 0;
             hi[u] = 0;
             cb[u] = 0;
             tbo[u] = 0;
             own[u] = false;
-            if (i < n) {
+            if (i2 < n) {
                 const uint64_t* ch = chains;
                 int32_t P, j;
-                own[u] = info(i, ch, P, j);
-                if (own[u]) {
-                    hi[u] = P;
-                    cb[u] = ch - chains;
-                    tbo[u] = (uint64_t)j * S;
-                }
+                uint64_t h0;
+                own[u] = info((int32_t)list[i2], ch, P, j, h0);
+                lo[u] = 1;                 // block 0 is cached
+                hi[u] = P;
+                cb[u] = ch - chains;
+                tbo[u] = (uint64_t)j * S;
             }
         }
         bool act = false;
@@ -680,8 +726,8 @@ __device__ __forceinline__ void prefix_searches(int32_t n, const Info& info, con
         }
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
-            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
-            if (i < n && own[u]) put(i, lo[u]);
+            const int32_t i2 = base + u * NT + (int32_t)threadIdx.x;
+            if (i2 < n && own[u]) put((int32_t)list[i2], lo[u]);
         }
     }
 }
@@ -792,8 +838,10 @@ __device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_
 }
 
 // Longest cached prefix for items i = threadIdx.x, + NT, ... < n on workers
-// without recency; info(i, ch, P, j, h0) as in prefix_searches plus the
-// item's hash at block 0, put as there.  A step of the checkpoint search
+// without recency; info(i, ch, P, j, h0) and put as in prefix_searches.  As
+// there, a first probe of block 0 (checkpoint 0) decides the items that miss
+// it and lists the others, which the full search then takes up from
+// checkpoint 0 again, several per thread at most.  A step of the checkpoint search
 // (CKPT) loads a run pair and the chain hashes at both checkpoints the next
 // step may probe; a step of the walk inside the last interval loads the
 // item's hash at its current block (HASH), a run pair (LOOK), or the two
@@ -802,11 +850,60 @@ __device__ __forceinline__ void run_insert(RunSlot* rt, uint64_t rsmask, uint64_
 // run pair and two chain hashes, from addresses chosen by its mode (an item
 // that needs fewer reads the index's first pair or the first chain hash
 // again), so that no branch separates the KI items' loads and all of them are
-// in flight together.
+// in flight together; a wavefront skips a load that none of its lanes needs.
 template <class Info, class Put>
 __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const Put& put, const RunSlot* rt,
-                                             uint64_t rsmask, const uint64_t* chains)
+                                             uint64_t rsmask, const uint64_t* chains, uint16_t* list,
+                                             int32_t* nlist)
 {
+    // first probe of every item, its block 0 (hash known): a miss decides o = 0, a hit puts the
+    // item on the list that the full search then takes up, several hits per thread at most
+    {
+        const int lane = threadIdx.x & 63;
+        __syncthreads();           // the list's previous users are done
+        if (threadIdx.x == 0) *nlist = 0;
+        __syncthreads();
+        for (int32_t base = 0; base < n; base += NT * KI) {
+            int32_t jw[KI];
+            uint64_t h0[KI], x0[KI], x1[KI], y0[KI], y1[KI];
+            bool own[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+                const uint64_t* ch = chains;
+                int32_t P = 0;
+                jw[u] = 0;
+                h0[u] = 0ull;
+                own[u] = i < n && info(i, ch, P, jw[u], h0[u]);
+                if (own[u] && P == 0) {
+                    put(i, 0);
+                    own[u] = false;
+                }
+                const uint64_t g = (uint64_t)(-(int64_t)own[u]) & run_home(h0[u], jw[u], rsmask);
+                load_run(rt + g, x0[u], y0[u]);
+                x1[u] = y1[u] = 0ull;
+                if constexpr (kRunWin > 1) load_run(rt + g + 1, x1[u], y1[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+                bool hit = false;
+                if (own[u]) {
+                    const uint64_t kk[2] = {x0[u], x1[u]}, vv[2] = {y0[u], y1[u]};
+                    uint64_t val;
+                    hit = run_finish(rt, rsmask, h0[u], jw[u], run_home(h0[u], jw[u], rsmask), kk, vv, val);
+                    if (!hit) put(i, 0);
+                }
+                const unsigned long long m = __ballot(hit);
+                int32_t wb = 0;
+                if (lane == 0 && m) wb = atomicAdd(nlist, (int32_t)__popcll(m));
+                wb = __builtin_amdgcn_readfirstlane(wb);
+                if (hit) list[wb + __popcll(m & ((1ull << lane) - 1ull))] = (uint16_t)i;
+            }
+        }
+        __syncthreads();
+        n = *nlist;
+    }
     enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3, CKPT = 4 };
     for (int32_t base = 0; base < n; base += NT * KI) {
         int64_t cb[KI], rcb[KI];     // chain bases of the item and of the run it follows
@@ -815,7 +912,8 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
         bool own[KI], qok[KI];
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
-            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
+            const int32_t i2 = base + u * NT + (int32_t)threadIdx.x;
+            const int32_t i = i2 < n ? (int32_t)list[i2] : 0;
             const uint64_t* ch = chains;
             P[u] = 0;
             jw[u] = 0;
@@ -823,7 +921,7 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
             hq[u] = 0ull;
             qhi[u] = 0ull;
             qok[u] = false;
-            own[u] = i < n && info(i, ch, P[u], jw[u], hq[u]);
+            own[u] = i2 < n && info(i, ch, P[u], jw[u], hq[u]);
             cb[u] = ch - chains;
             rcb[u] = 0;
             // checkpoints [lo, hi) undecided (those below lo cached, from hi on missing); km is
@@ -857,15 +955,18 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                 const int64_t bc = (int64_t)(mC | mH | mM) & cb[u];
                 const int64_t bd = ((int64_t)mC & cb[u]) | ((int64_t)mM & rcb[u]);
                 const uint64_t g = (uint64_t)(int64_t)mP & run_home(hq[u], jw[u], rsmask);
-                load_run(rt + g, x0[u], y0[u]);
-                load_run(rt + g + 1, x1[u], y1[u]);
-                hc[u] = chains[bc + ic];
-                hd[u] = chains[bd + id];
+                x0[u] = y0[u] = x1[u] = y1[u] = hc[u] = hd[u] = 0ull;
+                if (__ballot(mP != 0)) {
+                    load_run(rt + g, x0[u], y0[u]);
+                    load_run(rt + g + 1, x1[u], y1[u]);
+                }
+                if (__ballot((mC | mH | mM) != 0)) hc[u] = chains[bc + ic];
+                if (__ballot((mC | mM) != 0)) hd[u] = chains[bd + id];
             }
 #pragma unroll
             for (int u = 0; u < KI; ++u) {
                 if (mode[u] == CKPT) {
-                    const uint64_t kk[kRunWin] = {x0[u], x1[u]}, vv[kRunWin] = {y0[u], y1[u]};
+                    const uint64_t kk[2] = {x0[u], x1[u]}, vv[2] = {y0[u], y1[u]};
                     uint64_t val = 0ull;
                     if (run_finish(rt, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
                         rcb[u] = (int64_t)(val >> 24);
@@ -901,7 +1002,7 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
                     hq[u] = hc[u];
                     mode[u] = LOOK;
                 } else if (mode[u] == LOOK) {
-                    const uint64_t kk[kRunWin] = {x0[u], x1[u]}, vv[kRunWin] = {y0[u], y1[u]};
+                    const uint64_t kk[2] = {x0[u], x1[u]}, vv[2] = {y0[u], y1[u]};
                     uint64_t val = 0ull;
                     if (!run_finish(rt, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
                         mode[u] = DONE;
@@ -944,8 +1045,8 @@ __device__ __forceinline__ void run_searches(int32_t n, const Info& info, const 
         }
 #pragma unroll
         for (int u = 0; u < KI; ++u) {
-            const int32_t i = base + u * NT + (int32_t)threadIdx.x;
-            if (own[u]) put(i, o[u]);
+            const int32_t i2 = base + u * NT + (int32_t)threadIdx.x;
+            if (own[u]) put((int32_t)list[i2], o[u]);
         }
     }
 }
@@ -1026,7 +1127,7 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
     uint32_t rcb, rlast, rfirst, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
-        t1, t12, bytes;
+        items, t1, t12, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool tiers)
@@ -1059,6 +1160,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     b.revd = take(nb * 8, 8);
     b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
+    b.items = take(nb * w * 2, 4);
     b.t1 = take(tiers ? nb * w * 2 : 0, 4);
     b.t12 = take(tiers ? nb * w * 2 : 0, 4);
     b.bytes = (o + 15) / 16 * 16;
@@ -1145,6 +1247,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     uint64_t* r_evd = (uint64_t*)(bb + BL.revd);
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
+    uint16_t* l_items = (uint16_t*)(bb + BL.items);        // search items left after a first probe
     uint16_t* t1_tab = (uint16_t*)(bb + BL.t1);            // [b][j] leading blocks in G1 (tiers)
     uint16_t* t12_tab = (uint16_t*)(bb + BL.t12);          // [b][j] leading blocks in G1 u G2 (tiers)
 
@@ -1799,14 +1902,15 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             if (st)
                 prefix_searches(
                     n,
-                    [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj) {
+                    [&](int32_t i, const uint64_t*& ch, int32_t& P, int32_t& jj, uint64_t& h0) {
                         const int32_t b = b_lo + i / per;
                         jj = j < 0 ? i % per : j;
                         ch = a.chains + r_cb[b];
                         P = r_P[b];
+                        h0 = r_first[b];
                         return s_stamped[jj] != 0;
                     },
-                    put, g_slots, S, a.chains);
+                    put, g_slots, S, a.chains, l_items, &sh.nlist);
             if (lz)
                 run_searches(
                     n,
@@ -1818,7 +1922,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         h0 = r_first[b];
                         return s_stamped[jj] == 0;
                     },
-                    put, g_runs, rsmask, a.chains);
+                    put, g_runs, rsmask, a.chains, l_items, &sh.nlist);
         } else {
             for (int32_t b = b_lo + wave; b < nb; b += NW) {
                 const uint64_t* ch = a.chains + r_cb[b];
