@@ -1127,7 +1127,7 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
     uint32_t rcb, rlast, rfirst, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
-        items, t1, t12, bytes;
+        items, pairs, t1, t12, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool tiers)
@@ -1161,6 +1161,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
     b.items = take(nb * w * 2, 4);
+    b.pairs = take(nb * (nb - 1) / 2 * 2 + 2, 4);
     b.t1 = take(tiers ? nb * w * 2 : 0, 4);
     b.t12 = take(tiers ? nb * w * 2 : 0, 4);
     b.bytes = (o + 15) / 16 * 16;
@@ -1248,6 +1249,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
     uint16_t* l_items = (uint16_t*)(bb + BL.items);        // search items left after a first probe
+    uint16_t* l_pairs = (uint16_t*)(bb + BL.pairs);        // batch pairs whose common prefix is searched
     uint16_t* t1_tab = (uint16_t*)(bb + BL.t1);            // [b][j] leading blocks in G1 (tiers)
     uint16_t* t12_tab = (uint16_t*)(bb + BL.t12);          // [b][j] leading blocks in G1 u G2 (tiers)
 
@@ -2080,11 +2082,37 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         // every (request, worker) overlap against the caches as they stand
         search(0, nb, -1);
         if (tiers) tier_search(0, nb, -1);
-        // common prefix of every pair of the batch's chains (prefix mode): a thread's pairs are
-        // searched KP at a time, each group in the depth of one binary search on equal hashes
+        // common prefix of every pair of the batch's chains (prefix mode): pairs whose first
+        // blocks differ (or that have one block in common at most) are decided at once; the
+        // others are listed and searched KP at a time per thread, each group in the depth of one
+        // binary search on equal hashes
         if (!scan) {
             const int32_t npair = nb * (nb - 1) / 2;
-            for (int32_t grp = 0; grp * KP * NT < npair; ++grp) {
+            if (tid == 0) sh.nlist = 0;
+            __syncthreads();
+            for (int32_t q0 = 0; q0 < npair; q0 += NT) {
+                const int32_t q = q0 + tid;
+                bool srch = false;
+                int32_t b = 0, b2 = 0;
+                if (q < npair) {
+                    b = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
+                    while (b > 1 && b * (b - 1) / 2 > q) --b;
+                    while ((b + 1) * b / 2 <= q) ++b;
+                    b2 = q - b * (b - 1) / 2;
+                    const int32_t m = min(r_P[b], r_P[b2]);
+                    const bool same = m > 0 && r_first[b] == r_first[b2];
+                    srch = same && m > 1;
+                    l_lcp[b * NB + b2] = (uint16_t)(same ? 1 : 0);
+                }
+                const unsigned long long mb = __ballot(srch);
+                int32_t wb = 0;
+                if (lane == 0 && mb) wb = atomicAdd(&sh.nlist, (int32_t)__popcll(mb));
+                wb = __builtin_amdgcn_readfirstlane(wb);
+                if (srch) l_pairs[wb + __popcll(mb & ((1ull << lane) - 1ull))] = (uint16_t)(b | (b2 << 8));
+            }
+            __syncthreads();
+            const int32_t nsrch = sh.nlist;
+            for (int32_t grp = 0; grp * KP * NT < nsrch; ++grp) {
             int32_t lo[KP], hi[KP], pp[KP];   // pp: b | b2 << 8, or -1
             int64_t ca[KP], cc[KP];
 #pragma unroll
@@ -2095,19 +2123,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 pp[k] = -1;
                 ca[k] = 0;
                 cc[k] = 0;
-                if (q < npair) {
-                    int32_t b = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
-                    while (b > 1 && b * (b - 1) / 2 > q) --b;
-                    while ((b + 1) * b / 2 <= q) ++b;
-                    const int32_t b2 = q - b * (b - 1) / 2;
-                    pp[k] = b | (b2 << 8);
-                    const int32_t m = min(r_P[b], r_P[b2]);
-                    if (m > 0 && r_first[b] == r_first[b2]) {
-                        lo[k] = 1;
-                        hi[k] = m;
-                        ca[k] = r_cb[b];
-                        cc[k] = r_cb[b2];
-                    }
+                if (q < nsrch) {
+                    pp[k] = l_pairs[q];
+                    const int32_t b = pp[k] & 0xff, b2 = pp[k] >> 8;
+                    lo[k] = 1;                 // block 0 is common
+                    hi[k] = min(r_P[b], r_P[b2]);
+                    ca[k] = r_cb[b];
+                    cc[k] = r_cb[b2];
                 }
             }
             for (;;) {

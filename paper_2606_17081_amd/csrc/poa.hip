@@ -104,30 +104,67 @@ __device__ __forceinline__ double window_sum(int32_t m, const Term& term)
 }
 
 // Dispatch order: windows by descending size class (bit length of m), so the
-// longest windows start first.  One workgroup; the order within a class is
-// whatever the atomics give (it only affects scheduling).
-__global__ __launch_bounds__(1024) void poa_order_kernel(int32_t n_windows, const int64_t* __restrict__ win_off,
-                                                          int32_t* __restrict__ order)
+// longest windows start first.  Three small launches over the whole grid
+// (one workgroup reading a million window offsets alone takes a millisecond):
+// zero the 16 class counters and 16 class cursors; count the windows of each
+// class (a wavefront adds its 64 windows per class with ballots, one atomic
+// per class present); scatter each window to its class's range, the classes
+// laid out from the longest down.  The order within a class is whatever the
+// atomics give (it only affects scheduling).
+__device__ __forceinline__ int32_t window_class(const int64_t* __restrict__ win_off, int32_t w)
 {
-    __shared__ int32_t cnt[16], base[16];
-    const int tid = threadIdx.x;
-    if (tid < 16) cnt[tid] = 0;
-    __syncthreads();
-    auto cls = [&](int32_t w) {
-        const int64_t m = win_off[w + 1] - win_off[w];
-        return m <= 0 ? 0 : (m >= 4096 ? 13 : 64 - __clzll((unsigned long long)m));
-    };
-    for (int32_t w = tid; w < n_windows; w += blockDim.x) atomicAdd(&cnt[cls(w)], 1);
-    __syncthreads();
-    if (tid == 0) {
+    const int64_t m = win_off[w + 1] - win_off[w];
+    return m <= 0 ? 0 : (m >= 4096 ? 13 : 64 - __clzll((unsigned long long)m));
+}
+
+__global__ void poa_order_zero_kernel(int32_t* __restrict__ cls_cnt)
+{
+    if (threadIdx.x < 32) cls_cnt[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(256) void poa_order_count_kernel(int32_t n_windows, const int64_t* __restrict__ win_off,
+                                                               int32_t* __restrict__ cls_cnt)
+{
+    const int lane = threadIdx.x & 63;
+    const int32_t stride = gridDim.x * blockDim.x;
+    for (int32_t w0 = blockIdx.x * blockDim.x + threadIdx.x - lane; w0 < n_windows; w0 += stride) {
+        const int32_t w = w0 + lane;
+        const int32_t c = w < n_windows ? window_class(win_off, w) : -1;
+        for (int32_t k = 0; k < 16; ++k) {
+            const unsigned long long mb = __ballot(c == k);
+            if (lane == 0 && mb) atomicAdd(&cls_cnt[k], (int32_t)__popcll(mb));
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void poa_order_scatter_kernel(int32_t n_windows, const int64_t* __restrict__ win_off,
+                                                                 int32_t* __restrict__ cls_cnt,
+                                                                 int32_t* __restrict__ order)
+{
+    // cls_cnt[0..15]: windows per class; cls_cnt[16..31]: windows of each class placed so far
+    __shared__ int32_t base[16];
+    if (threadIdx.x == 0) {
         int32_t o = 0;
         for (int32_t c = 15; c >= 0; --c) {
             base[c] = o;
-            o += cnt[c];
+            o += cls_cnt[c];
         }
     }
     __syncthreads();
-    for (int32_t w = tid; w < n_windows; w += blockDim.x) order[atomicAdd(&base[cls(w)], 1)] = w;
+    const int lane = threadIdx.x & 63;
+    const int32_t stride = gridDim.x * blockDim.x;
+    for (int32_t w0 = blockIdx.x * blockDim.x + threadIdx.x - lane; w0 < n_windows; w0 += stride) {
+        const int32_t w = w0 + lane;
+        const int32_t c = w < n_windows ? window_class(win_off, w) : -1;
+        for (int32_t k = 0; k < 16; ++k) {
+            const unsigned long long mb = __ballot(c == k);
+            if (!mb) continue;
+            int32_t b0 = 0;
+            if (lane == 0) b0 = base[k] + atomicAdd(&cls_cnt[16 + k], (int32_t)__popcll(mb));
+            b0 = __builtin_amdgcn_readfirstlane(b0);
+            if (c == k) order[b0 + __popcll(mb & ((1ull << lane) - 1ull))] = w;
+        }
+    }
 }
 
 template <bool LDSMAT, int WMAX>
@@ -384,7 +421,7 @@ extern "C" size_t rk_poa_workspace_size(int64_t n_rows, int32_t W)
     if (n_rows < 0 || W < 1) return 0;
     return align_up((size_t)n_rows * (size_t)W * sizeof(float), 256) + 2 * 256 +
            2 * align_up(((size_t)n_rows + 1) * sizeof(double), 256) +
-           align_up(((size_t)n_rows + 1) * sizeof(int32_t), 256);
+           align_up(((size_t)n_rows + 1) * sizeof(int32_t), 256) + 256;
 }
 
 template <bool LDSMAT>
@@ -473,7 +510,13 @@ static int poa_launch(int32_t n_windows, const int64_t* win_off, int32_t n_episo
         a.lds_mat = (uint32_t)o;
         if (lds_mat) o += mat;
         if (order) {
-            hipLaunchKernelGGL(poa_order_kernel, dim3(1), dim3(1024), 0, s, n_windows, win_off, order);
+            int32_t* cls_cnt = (int32_t*)(ws + cm_bytes + 512 + 2 * vec_bytes +
+                                          align_up(((size_t)n_rows + 1) * sizeof(int32_t), 256));
+            const unsigned og = (unsigned)((n_windows + 255) / 256 < 1024 ? (n_windows + 255) / 256 : 1024);
+            hipLaunchKernelGGL(poa_order_zero_kernel, dim3(1), dim3(64), 0, s, cls_cnt);
+            hipLaunchKernelGGL(poa_order_count_kernel, dim3(og), dim3(256), 0, s, n_windows, win_off, cls_cnt);
+            hipLaunchKernelGGL(poa_order_scatter_kernel, dim3(og), dim3(256), 0, s, n_windows, win_off, cls_cnt,
+                               order);
             int rc = hip_check(hipGetLastError(), "rk_poa_estimate order launch");
             if (rc) return rc;
         }
