@@ -456,8 +456,8 @@ int rk_poa_estimate(int32_t n_windows, const int64_t* win_off, int32_t n_episode
  * rk_poa_estimate minus workspace and ws_bytes: its scratch (the frozen
  * matrices, the dispatch order and its class counters and, when selfish_out
  * or coord_out is NULL, the window sums) lives in a static device buffer of
- * RK_POA_NOALLOC_BYTES that
- * the library holds on each device it runs on until the process ends.  The
+ * RK_POA_NOALLOC_BYTES that the library holds on each device it runs on
+ * until the process ends.  The
  * call allocates nothing.  A shape whose rk_poa_workspace_size(n_rows, W)
  * exceeds RK_POA_NOALLOC_BYTES returns RK_EUNSUPPORTED before any launch.
  * Every call on one device shares that device's buffer and leaves its
