@@ -450,6 +450,74 @@ __device__ __forceinline__ uint64_t touch_hinted(Slot* __restrict__ t, uint64_t 
 }
 
 
+// touch_hinted for two keys of a lane at once (act: the key is to be touched;
+// hint as there), the claims (compare-and-swap returning the slot's previous
+// key) and group loads of both issued before either result is used.
+__device__ __forceinline__ void touch_hinted2(Slot* const* t, uint64_t smask, const uint64_t* h, const bool* hint,
+                                              const bool* act, uint64_t* sl, int* ins, int32_t* status)
+{
+    uint64_t s[2], prev[2], k[2][kWin];
+    uint32_t st[2][kWin];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        s[u] = home_slot(h[u], smask);
+        prev[u] = kEmpty;
+        if (act[u] && !hint[u])
+            prev[u] = atomicCAS(reinterpret_cast<unsigned long long*>(&t[u][s[u] + group_slot(h[u], 0)].key), kEmpty,
+                                h[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const Slot* g = t[u] + s[u];
+#pragma unroll
+        for (int r = 0; r < kWin; ++r) load_slot(g + group_slot(h[u], r), k[u][r], st[u][r]);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        sl[u] = ~0ull;
+        ins[u] = 0;
+        if (!act[u]) continue;
+        bool done = false;
+        if (hint[u]) {
+#pragma unroll
+            for (int r = 0; r < kWin; ++r)
+                if (!done && k[u][r] == h[u] && st[u][r] != kTomb) {
+                    sl[u] = s[u] + group_slot(h[u], r);
+                    done = true;
+                }
+        } else if (prev[u] == kEmpty) {
+            sl[u] = s[u] + group_slot(h[u], 0);
+            ins[u] = 1;
+            done = true;
+        } else if (prev[u] != h[u]) {   // the first slot holds another key: look further along the group
+            bool stop = false;
+#pragma unroll
+            for (int r = 1; r < kWin; ++r) {
+                if (done || stop) continue;
+                const uint64_t si = s[u] + group_slot(h[u], r);
+                if (k[u][r] == h[u]) {
+                    if (st[u][r] != kTomb) {
+                        sl[u] = si;
+                        done = true;
+                    }
+                    continue;
+                }
+                if (k[u][r] != kEmpty) continue;
+                uint64_t pi = kEmpty;
+                if (__hip_atomic_compare_exchange_strong(&t[u][si].key, &pi, h[u], __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                    sl[u] = si;
+                    ins[u] = 1;
+                    done = true;
+                } else {
+                    stop = true;   // lost a race for the slot: walk from the start
+                }
+            }
+        }
+        if (!done) sl[u] = insert_or_touch(t[u], smask, h[u], ins[u], status);
+    }
+}
+
 constexpr int kRU = 4;   // touches a thread keeps in flight while a worker's recency is rebuilt
 
 // touch_hinted(t, smask, h[u], false, ...) for kRU keys (kEmpty: none) with the
@@ -1479,36 +1547,73 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 }
                 if (lane == 0) woff[nr] = tot;
                 ep_wave_sync();
-                for (int32_t i = lane; i < tot; i += 64) {
-                    int32_t r = 0;
-                    while (r + 1 < nr && woff[r + 1] <= i) ++r;
-                    const int32_t b = c + r;
-                    const int32_t k = i - woff[r];
-                    const int32_t P = r_P[b], sg = r_sig[b];
-                    if (wst[r] >= 0) {
-                        const int32_t pos = run_entry_pos(wst[r], k);
-                        run_insert(g_runs, rsmask, a.chains[r_cb[b] + pos], sg, run_val(r_cb[b], sg, P), a.status);
-                        continue;
+                // a claim of routes that only add runs: one entry per lane at a time
+                if (__ballot(lane < nr && wst[lane] < 0) == 0ull) {
+                    for (int32_t i = lane; i < tot; i += 64) {
+                        int32_t r = 0;
+                        while (r + 1 < nr && woff[r + 1] <= i) ++r;
+                        const int32_t b = c + r, sg = r_sig[b];
+                        const int32_t pos = run_entry_pos(wst[r], i - woff[r]);
+                        run_insert(g_runs, rsmask, a.chains[r_cb[b] + pos], sg, run_val(r_cb[b], sg, r_P[b]),
+                                   a.status);
                     }
-                    Slot* tk = g_slots + (uint64_t)sg * S;
-                    uint32_t* tl = g_log + (uint64_t)sg * R;
-                    const bool known = k < r_otab[b];
-                    const uint64_t h = a.chains[r_cb[b] + k];
-                    const uint32_t stamp = r_stamp[b] + (uint32_t)(P - 1 - k);
-                    int ins;
-                    const uint64_t sl = touch_hinted(tk, smask, h, known, ins, a.status);
-                    // routes of one worker that share a block touch it concurrently: the latest stamp wins
-                    if (sl != ~0ull) {
-                        const uint32_t old = __hip_atomic_fetch_max(&tk[sl].stamp, stamp, __ATOMIC_RELAXED,
-                                                                    __HIP_MEMORY_SCOPE_WORKGROUP);
-                        if (freq) freq_touch(&tk[sl].fkey, ins != 0, r_ep[b]);
-                        if (tiers && !ins) {       // a hit whose old record lay in a tier's run
-                            my_h1 += old >= s_b1[sg];
-                            my_h2 += old >= s_b2[sg];
+                    ep_wave_sync();
+                    continue;
+                }
+                // otherwise two blocks per lane at a time, their chain hashes, claims and group loads
+                // in flight together
+                for (int32_t i0 = lane; i0 < tot; i0 += 128) {
+                    int32_t bq[2], kq[2], sgq[2];
+                    bool v[2], lazy[2];
+                    int64_t hoff[2];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const int32_t i = i0 + 64 * u;
+                        v[u] = i < tot;
+                        int32_t r = 0;
+                        while (r + 1 < nr && woff[r + 1] <= i) ++r;
+                        bq[u] = c + r;
+                        kq[u] = i - woff[r];
+                        lazy[u] = wst[r] >= 0;
+                        sgq[u] = v[u] ? r_sig[bq[u]] : 0;
+                        const int32_t pos = lazy[u] ? run_entry_pos(wst[r], kq[u]) : kq[u];
+                        hoff[u] = v[u] ? r_cb[bq[u]] + pos : 0;
+                    }
+                    uint64_t h[2];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) h[u] = a.chains[hoff[u]];
+                    Slot* tk[2];
+                    bool hint[2], act[2];
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        if (v[u] && lazy[u])
+                            run_insert(g_runs, rsmask, h[u], sgq[u], run_val(r_cb[bq[u]], sgq[u], r_P[bq[u]]),
+                                       a.status);
+                        tk[u] = g_slots + (uint64_t)sgq[u] * S;
+                        act[u] = v[u] && !lazy[u];
+                        hint[u] = kq[u] < r_otab[bq[u]];
+                    }
+                    uint64_t sl[2];
+                    int ins[2];
+                    touch_hinted2(tk, smask, h, hint, act, sl, ins, a.status);
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        if (!act[u]) continue;
+                        const int32_t b = bq[u], sg = sgq[u];
+                        const uint32_t stamp = r_stamp[b] + (uint32_t)(r_P[b] - 1 - kq[u]);
+                        // routes of one worker that share a block touch it concurrently: the latest stamp wins
+                        if (sl[u] != ~0ull) {
+                            const uint32_t old = __hip_atomic_fetch_max(&tk[u][sl[u]].stamp, stamp, __ATOMIC_RELAXED,
+                                                                        __HIP_MEMORY_SCOPE_WORKGROUP);
+                            if (freq) freq_touch(&tk[u][sl[u]].fkey, ins[u] != 0, r_ep[b]);
+                            if (tiers && !ins[u]) {       // a hit whose old record lay in a tier's run
+                                my_h1 += old >= s_b1[sg];
+                                my_h2 += old >= s_b2[sg];
+                            }
                         }
+                        g_log[(uint64_t)sg * R + (stamp & rmask)] = (uint32_t)sl[u];   // a failed insert logs an out-of-range slot
+                        my_ins += ins[u];
                     }
-                    tl[stamp & rmask] = (uint32_t)sl;    // a failed insert logs an out-of-range slot
-                    my_ins += ins;
                 }
                 ep_wave_sync();
                 continue;
