@@ -93,7 +93,7 @@ struct EpArgs {
     unsigned char* ws;
     EpisodeLayout L;
     int32_t* status;
-    uint32_t lds_w, lds_inflight, lds_u, lds_batch;
+    uint32_t lds_w, lds_inflight, lds_u, lds_roff, lds_batch;
 };
 
 constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
@@ -1294,6 +1294,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     int32_t* s_stc = s_stP + a.max_inflight;               // conversation (| kMoreTurns)
     int32_t* s_stepn = s_stc + a.max_inflight;             // routes per step slot
     int64_t* s_u = (int64_t*)(smem + a.lds_u);             // controller load samples
+    int32_t* s_roff = (int32_t*)(smem + a.lds_roff);       // recency rebuild: first touch of each route
     // the batch
     const BatchLayout BL = batch_layout(NB, W, a.tiers != 0);
     unsigned char* bb = smem + a.lds_batch;
@@ -1688,8 +1689,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         Slot* tk = g_slots + (uint64_t)j * S;
         uint32_t* tl = g_log + (uint64_t)j * R;
         int64_t* r_cbs = (int64_t*)(ws + a.L.off_replay);     // per chunk of routes, the worker's: chain
-        int32_t* r_off = (int32_t*)(r_cbs + NT);              // base, first touch index and P
-        int32_t* r_Ps = r_off + NT;
+        int32_t* r_off = s_roff;                              // base (global), first touch index (LDS)
+                                                              // and P (global)
+        int32_t* r_Ps = (int32_t*)(r_cbs + NT) + NT;
         for (int pass = 0; pass < 2; ++pass) {
             int64_t stamp0 = 0;      // original stamp of the chunk's first touch
             int32_t live = 0;        // pass 2: live records laid down so far
@@ -1792,8 +1794,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         Slot* tk = g_slots + (uint64_t)j * S;
         uint32_t* tl = g_log + (uint64_t)j * R;
         int64_t* r_cbs = (int64_t*)(ws + a.L.off_replay);     // per chunk of routes, the worker's: chain
-        int32_t* r_off = (int32_t*)(r_cbs + NT);              // base, first touch index and P
-        int32_t* r_Ps = r_off + NT;
+        int32_t* r_off = s_roff;                              // base (global), first touch index (LDS)
+                                                              // and P (global)
+        int32_t* r_Ps = (int32_t*)(r_cbs + NT) + NT;
         auto route_of = [&](int32_t r, int32_t& P, int64_t& cb) {
             P = 0;
             cb = 0;
@@ -2793,6 +2796,8 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     o = align_up(o + (size_t)b->max_inflight * 4 * 4, 16);
     a.lds_u = (uint32_t)o;
     o = align_up(o + (size_t)b->max_ctrl_window * 8, 16);
+    a.lds_roff = (uint32_t)o;
+    o = align_up(o + (size_t)kEpisodeThreads * 4, 16);
     a.lds_batch = (uint32_t)o;
     const size_t limit = 60 * 1024;
     int32_t NB = kMaxBatch;
