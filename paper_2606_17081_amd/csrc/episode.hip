@@ -107,7 +107,7 @@ struct LeanTag {
 };
 
 struct EpShared {
-    int32_t next_e, nlist;
+    int32_t next_e, nlist, jn, jsync, jnext, jp, jpnext, jq, jqnext;
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
     int32_t woff[NW][KR + 1], wst[NW][KR];
     uint32_t new_head, first_kept, adv;
@@ -1195,7 +1195,7 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
     uint32_t rcb, rlast, rfirst, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
-        items, pairs, t1, t12, bytes;
+        items, pairs, nxcb, nxfirst, nxP, nxo, lcp2, pval, t1, t12, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool tiers)
@@ -1229,7 +1229,13 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     b.rrnd = take(nb * 8, 4);
     b.lcp = take(nb * nb * 2, 4);
     b.items = take(nb * w * 2, 4);
-    b.pairs = take(nb * (nb - 1) / 2 * 2 + 2, 4);
+    b.pairs = take(nb * nb * 2 + 2, 4);
+    b.nxcb = take(nb * 8, 8);
+    b.nxfirst = take(nb * 8, 8);
+    b.nxP = take(nb * 4, 4);
+    b.nxo = take(nb * w * 4, 4);
+    b.lcp2 = take(nb * nb * 2, 4);
+    b.pval = take(nb * nb * 2 + 2, 4);
     b.t1 = take(tiers ? nb * w * 2 : 0, 4);
     b.t12 = take(tiers ? nb * w * 2 : 0, 4);
     b.bytes = (o + 15) / 16 * 16;
@@ -1317,8 +1323,14 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     uint64_t* r_evd = (uint64_t*)(bb + BL.revd);
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
     uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
+    uint16_t* nx_lcp = (uint16_t*)(bb + BL.lcp2);          //   the same for the next batch (the two swap)
+    uint16_t* l_pval = (uint16_t*)(bb + BL.pval);          // common prefix of each listed pair
     uint16_t* l_items = (uint16_t*)(bb + BL.items);        // search items left after a first probe
     uint16_t* l_pairs = (uint16_t*)(bb + BL.pairs);        // batch pairs whose common prefix is searched
+    int64_t* nx_cb = (int64_t*)(bb + BL.nxcb);             // the next batch, its overlaps computed while
+    uint64_t* nx_first = (uint64_t*)(bb + BL.nxfirst);     //   this batch is decided: chain base, h_0, P
+    int32_t* nx_P = (int32_t*)(bb + BL.nxP);
+    int32_t* nx_o = (int32_t*)(bb + BL.nxo);               //   and [b][j] overlaps
     uint16_t* t1_tab = (uint16_t*)(bb + BL.t1);            // [b][j] leading blocks in G1 (tiers)
     uint16_t* t12_tab = (uint16_t*)(bb + BL.t12);          // [b][j] leading blocks in G1 u G2 (tiers)
 
@@ -2141,32 +2153,455 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     double rg_ewma = 0.0;                          // regime controller: smoothed latency, regime,
     int32_t rg_r = 0, rg_up = 0, rg_down = 0;      // hysteresis counters
 
+    // Longest common prefix of npair pairs of chains (all threads): pair(q, ca, cb, m, b1, b2)
+    // names pair q's chain bases, the lesser length and two indices for store(q, b1, b2, lcp).
+    // Pairs whose first blocks differ (or that have at most one block in common) are stored at
+    // once; the others are listed and searched KP at a time per thread, each group in the depth
+    // of one binary search on equal hashes.  npair <= NB * NB.
+    auto pair_lcps = [&](int32_t npair, const auto& pair, const auto& store) {
+        if (tid == 0) sh.nlist = 0;
+        __syncthreads();
+        for (int32_t q0 = 0; q0 < npair; q0 += NT) {
+            const int32_t q = q0 + tid;
+            bool srch = false;
+            if (q < npair) {
+                int64_t ca, cc;
+                int32_t m, b1, b2;
+                const bool same = pair(q, ca, cc, m, b1, b2);
+                srch = same && m > 1;
+                if (!srch) store(q, b1, b2, same && m > 0 ? 1 : 0);
+            }
+            const unsigned long long mb = __ballot(srch);
+            int32_t wb = 0;
+            if (lane == 0 && mb) wb = atomicAdd(&sh.nlist, (int32_t)__popcll(mb));
+            wb = __builtin_amdgcn_readfirstlane(wb);
+            if (srch) l_pairs[wb + __popcll(mb & ((1ull << lane) - 1ull))] = (uint16_t)q;
+        }
+        __syncthreads();
+        const int32_t nsrch = sh.nlist;
+        for (int32_t grp = 0; grp * KP * NT < nsrch; ++grp) {
+            int32_t lo[KP], hi[KP], qq[KP], p1[KP], p2[KP];
+            int64_t ca[KP], cc[KP];
+#pragma unroll
+            for (int k = 0; k < KP; ++k) {
+                const int32_t i = tid + (grp * KP + k) * NT;
+                lo[k] = 0;
+                hi[k] = 0;
+                qq[k] = -1;
+                ca[k] = 0;
+                cc[k] = 0;
+                p1[k] = p2[k] = 0;
+                if (i < nsrch) {
+                    qq[k] = l_pairs[i];
+                    int32_t m;
+                    pair(qq[k], ca[k], cc[k], m, p1[k], p2[k]);
+                    lo[k] = 1;                 // block 0 is common
+                    hi[k] = m;
+                }
+            }
+            for (;;) {
+                bool any = false;
+#pragma unroll
+                for (int k = 0; k < KP; ++k) any |= lo[k] < hi[k];
+                if (!any) break;
+                // addresses by masks (a closed search reads the first chain hash), so that the KP
+                // pairs' loads are in flight together
+                int32_t mid[KP];
+                uint64_t va[KP], vb[KP];
+#pragma unroll
+                for (int k = 0; k < KP; ++k) {
+                    mid[k] = (lo[k] + hi[k]) >> 1;
+                    const int64_t mk = -(int64_t)(lo[k] < hi[k]);
+                    va[k] = a.chains[mk & (ca[k] + mid[k])];
+                    vb[k] = a.chains[mk & (cc[k] + mid[k])];
+                }
+#pragma unroll
+                for (int k = 0; k < KP; ++k) {
+                    if (lo[k] < hi[k]) {
+                        if (va[k] == vb[k]) lo[k] = mid[k] + 1;
+                        else hi[k] = mid[k];
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < KP; ++k)
+                if (qq[k] >= 0) store(qq[k], p1[k], p2[k], lo[k]);
+        }
+        __syncthreads();
+    };
+    // pair q of the batch: routes b1 > b2 (q = b1 (b1 - 1) / 2 + b2)
+    auto batch_pair = [&](int32_t q, int64_t& ca, int64_t& cc, int32_t& m, int32_t& b1, int32_t& b2) {
+        b1 = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
+        while (b1 > 1 && b1 * (b1 - 1) / 2 > q) --b1;
+        while ((b1 + 1) * b1 / 2 <= q) ++b1;
+        b2 = q - b1 * (b1 - 1) / 2;
+        ca = r_cb[b1];
+        cc = r_cb[b2];
+        m = min(r_P[b1], r_P[b2]);
+        return m > 0 && r_first[b1] == r_first[b2];
+    };
+
+    // the request at queue position qi: conversation, turn, prompt blocks and chain base
+    auto queued = [&](int32_t qi, int32_t& c, int32_t& k, int64_t& turn, int32_t& P, int64_t& cb, bool& more) {
+        c = g_queue[qi >= qcap ? qi - qcap : qi];
+        k = g_next[c];
+        const int64_t g = gc0 + c;
+        const int64_t tb0 = a.turn_off[g], tb1 = a.turn_off[g + 1];
+        turn = tb0 + k;
+        P = a.turn_blocks[turn];
+        cb = a.chain_off[g];
+        const int64_t ce = a.chain_off[g + 1];
+        if (P < 0 || (int64_t)P > ce - cb) {
+            atomicOr(a.status, RK_DEV_SHORT_INPUT);
+            P = P < 0 ? 0 : (int32_t)max((int64_t)0, ce - cb);
+        }
+        if (cb < 0 || cb >= (1ll << 40)) {     // a run keeps 40 bits of its chain's base
+            atomicOr(a.status, RK_DEV_BAD_OFFSETS);
+            P = 0;
+        }
+        if (P > a.max_blocks) {
+            atomicOr(a.status, RK_DEV_TOO_LARGE);
+            P = a.max_blocks;
+        }
+        more = (int64_t)k + 1 < tb1 - tb0;
+    };
+    int32_t nb_cur = 0;            // routes of the batch being decided
+    // Waves 1-3: every (request, worker) overlap of the next batch (all workers add runs), by the
+    // run-index search of run_searches: a first probe of block 0 settles the misses and lists the
+    // rest; once the three waves have listed theirs, the listed items are searched with KI slots
+    // per thread, each slot taking the next listed item when its search ends.
+    auto next_batch_job = [&]() {
+        enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3, CKPT = 4 };
+        constexpr int NJ = NT - 64;                  // the job's threads
+        const int32_t tj = tid - 64;
+        const int32_t n = NB * W;
+        for (int32_t base = 0; base < n; base += NJ * KI) {
+            int32_t jw[KI];
+            uint64_t h0[KI], x0[KI], x1[KI], y0[KI], y1[KI];
+            bool own[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int32_t i = base + u * NJ + tj;
+                const int32_t b = i / W;
+                jw[u] = i - b * W;
+                own[u] = i < n && nx_P[b < NB ? b : 0] > 0;
+                if (i < n && !own[u]) nx_o[i] = 0;
+                h0[u] = own[u] ? nx_first[b] : 0ull;
+                const uint64_t g = (uint64_t)(-(int64_t)own[u]) & run_home(h0[u], jw[u], rsmask);
+                load_run(g_runs + g, x0[u], y0[u]);
+                load_run(g_runs + g + 1, x1[u], y1[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                const int32_t i = base + u * NJ + tj;
+                bool hit = false;
+                if (own[u]) {
+                    const uint64_t kk[2] = {x0[u], x1[u]}, vv[2] = {y0[u], y1[u]};
+                    uint64_t val;
+                    hit = run_finish(g_runs, rsmask, h0[u], jw[u], run_home(h0[u], jw[u], rsmask), kk, vv, val);
+                    if (!hit) nx_o[i] = 0;
+                }
+                const unsigned long long m = __ballot(hit);
+                int32_t wb = 0;
+                if (lane == 0 && m) wb = atomicAdd(&sh.jn, (int32_t)__popcll(m));
+                wb = __builtin_amdgcn_readfirstlane(wb);
+                if (hit) l_items[wb + __popcll(m & ((1ull << lane) - 1ull))] = (uint16_t)i;
+            }
+        }
+        // barrier k of the three job waves (the decision wavefront does not take part)
+        auto job_barrier = [&](int32_t k) {
+            ep_wave_sync();
+            if (lane == 0) __hip_atomic_fetch_add(&sh.jsync, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+            while (__builtin_amdgcn_readfirstlane(
+                       __hip_atomic_load(&sh.jsync, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) < k * (NW - 1))
+                __builtin_amdgcn_s_sleep(1);
+        };
+        job_barrier(1);            // the three waves' lists are complete
+        const int32_t n2 = __hip_atomic_load(&sh.jn, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const uint64_t* chains = a.chains;
+        int64_t cb[KI], rcb[KI];
+        int32_t P[KI], jw[KI], o[KI], lo[KI], hi[KI], mode[KI], km[KI], lim[KI], item[KI];
+        uint64_t hq[KI], qhi[KI];
+        bool qok[KI];
+        // slot u takes listed item idx (or none)
+        auto take = [&](int u, int32_t idx) {
+            item[u] = -1;
+            mode[u] = DONE;
+            if (idx >= n2) return;
+            const int32_t i = l_items[idx];
+            const int32_t b = i / W;
+            item[u] = i;
+            jw[u] = i - b * W;
+            cb[u] = nx_cb[b];
+            P[u] = nx_P[b];
+            hq[u] = nx_first[b];
+            rcb[u] = 0;
+            o[u] = 0;
+            qhi[u] = 0ull;
+            qok[u] = false;
+            lo[u] = 0;
+            hi[u] = (P[u] + kCkpt - 1) >> kCkptLog;
+            km[u] = 0;
+            lim[u] = P[u];
+            mode[u] = CKPT;
+        };
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            cb[u] = rcb[u] = 0;
+            P[u] = jw[u] = o[u] = lo[u] = hi[u] = km[u] = lim[u] = 0;
+            hq[u] = qhi[u] = 0ull;
+            qok[u] = false;
+            take(u, atomicAdd(&sh.jnext, 1));
+        }
+        for (;;) {
+            bool any = false;
+#pragma unroll
+            for (int u = 0; u < KI; ++u) any |= mode[u] != DONE;
+            if (!any) break;
+            uint64_t x0[KI], x1[KI], y0[KI], y1[KI], hc[KI], hd[KI];
+            int32_t mid[KI];
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                mid[u] = (lo[u] + hi[u]) >> 1;
+                const int32_t md = mode[u];
+                const int32_t mC = -(int32_t)(md == CKPT), mH = -(int32_t)(md == HASH), mM = -(int32_t)(md == CMP);
+                const int32_t mP = -(int32_t)(md == CKPT || md == LOOK);
+                const int32_t mh = km[u] + 1 < hi[u] ? (km[u] + 1 + hi[u]) >> 1 : 0;
+                const int32_t mm = lo[u] < km[u] ? (lo[u] + km[u]) >> 1 : 0;
+                const int32_t ic = (mC & (mh << kCkptLog)) | (mH & o[u]) | (mM & mid[u]);
+                const int32_t id = (mC & (mm << kCkptLog)) | (mM & mid[u]);
+                const int64_t bc = (int64_t)(mC | mH | mM) & cb[u];
+                const int64_t bd = ((int64_t)mC & cb[u]) | ((int64_t)mM & rcb[u]);
+                const uint64_t g = (uint64_t)(int64_t)mP & run_home(hq[u], jw[u], rsmask);
+                x0[u] = y0[u] = x1[u] = y1[u] = hc[u] = hd[u] = 0ull;
+                if (__ballot(mP != 0)) {
+                    load_run(g_runs + g, x0[u], y0[u]);
+                    load_run(g_runs + g + 1, x1[u], y1[u]);
+                }
+                if (__ballot((mC | mH | mM) != 0)) hc[u] = chains[bc + ic];
+                if (__ballot((mC | mM) != 0)) hd[u] = chains[bd + id];
+            }
+#pragma unroll
+            for (int u = 0; u < KI; ++u) {
+                if (mode[u] == CKPT) {
+                    const uint64_t kk[2] = {x0[u], x1[u]}, vv[2] = {y0[u], y1[u]};
+                    uint64_t val = 0ull;
+                    if (run_finish(g_runs, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
+                        rcb[u] = (int64_t)(val >> 24);
+                        o[u] = (int32_t)(val & 0xFFFFu);
+                        lo[u] = km[u] + 1;
+                        hq[u] = hc[u];
+                    } else {
+                        hi[u] = km[u];
+                        hq[u] = hd[u];
+                    }
+                    km[u] = (lo[u] + hi[u]) >> 1;
+                    if (lo[u] >= hi[u]) {
+                        if (lo[u] == 0) {
+                            mode[u] = DONE;
+                        } else {
+                            const int32_t c = (lo[u] - 1) << kCkptLog;
+                            lim[u] = min(P[u], lo[u] << kCkptLog);
+                            const int32_t m = min(lim[u], o[u]);
+                            lo[u] = c + 1;
+                            hi[u] = m;
+                            qok[u] = false;
+                            if (lo[u] >= hi[u]) {
+                                o[u] = m;
+                                mode[u] = o[u] < lim[u] ? HASH : DONE;
+                            } else {
+                                mode[u] = CMP;
+                            }
+                        }
+                    }
+                } else if (mode[u] == HASH) {
+                    hq[u] = hc[u];
+                    mode[u] = LOOK;
+                } else if (mode[u] == LOOK) {
+                    const uint64_t kk[2] = {x0[u], x1[u]}, vv[2] = {y0[u], y1[u]};
+                    uint64_t val = 0ull;
+                    if (!run_finish(g_runs, rsmask, hq[u], jw[u], run_home(hq[u], jw[u], rsmask), kk, vv, val)) {
+                        mode[u] = DONE;
+                    } else {
+                        rcb[u] = (int64_t)(val >> 24);
+                        const int32_t m = min(lim[u], (int32_t)(val & 0xFFFFu));
+                        lo[u] = o[u] + 1;
+                        hi[u] = m;
+                        qok[u] = false;
+                        if (lo[u] >= hi[u]) {
+                            o[u] = m;
+                            mode[u] = o[u] < lim[u] ? HASH : DONE;
+                        } else {
+                            mode[u] = CMP;
+                        }
+                    }
+                } else if (mode[u] == CMP) {
+                    if (hc[u] == hd[u]) {
+                        lo[u] = mid[u] + 1;
+                    } else {
+                        hi[u] = mid[u];
+                        qhi[u] = hc[u];
+                        qok[u] = true;
+                    }
+                    if (lo[u] >= hi[u]) {
+                        o[u] = lo[u];
+                        if (o[u] >= lim[u]) {
+                            mode[u] = DONE;
+                        } else if (qok[u]) {
+                            hq[u] = qhi[u];
+                            mode[u] = LOOK;
+                        } else {
+                            mode[u] = HASH;
+                        }
+                    }
+                }
+                if (mode[u] == DONE && item[u] >= 0) {
+                    nx_o[item[u]] = o[u];
+                    take(u, atomicAdd(&sh.jnext, 1));
+                }
+            }
+        }
+        // ---- common prefixes of pairs (pair(q, ...) as for pair_lcps): direct(q, b1, b2, same, m)
+        //      stores a pair's prefix at once or returns true to list the pair; the listed pairs are
+        //      searched with KP slots per thread, each taking the next listed pair when its search
+        //      ends, store(listed index, q, prefix)
+        auto job_pairs = [&](int32_t npair, int32_t* cnt, int32_t* next, int32_t bar, const auto& pair,
+                             const auto& direct, const auto& store) {
+            for (int32_t q0 = 0; q0 < npair; q0 += NJ) {
+                const int32_t q = q0 + tj;
+                bool lst = false;
+                if (q < npair) {
+                    int64_t ca, cc;
+                    int32_t m, b1, b2;
+                    const bool same = pair(q, ca, cc, m, b1, b2);
+                    lst = direct(q, b1, b2, same, m);
+                }
+                const unsigned long long mb = __ballot(lst);
+                int32_t wb = 0;
+                if (lane == 0 && mb) wb = atomicAdd(cnt, (int32_t)__popcll(mb));
+                wb = __builtin_amdgcn_readfirstlane(wb);
+                if (lst) l_pairs[wb + __popcll(mb & ((1ull << lane) - 1ull))] = (uint16_t)q;
+            }
+            job_barrier(bar);
+            const int32_t nl = __hip_atomic_load(cnt, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            int32_t lo[KP], hi[KP], it[KP];
+            int64_t ca[KP], cc[KP];
+            auto takep = [&](int k, int32_t idx) {
+                it[k] = -1;
+                lo[k] = hi[k] = 0;
+                ca[k] = cc[k] = 0;
+                if (idx >= nl) return;
+                int32_t m, b1, b2;
+                it[k] = idx;
+                pair(l_pairs[idx], ca[k], cc[k], m, b1, b2);
+                lo[k] = 1;                 // block 0 is common
+                hi[k] = m;
+            };
+#pragma unroll
+            for (int k = 0; k < KP; ++k) takep(k, atomicAdd(next, 1));
+            for (;;) {
+                bool any = false;
+#pragma unroll
+                for (int k = 0; k < KP; ++k) any |= it[k] >= 0;
+                if (!any) break;
+                int32_t mid[KP];
+                uint64_t va[KP], vb[KP];
+#pragma unroll
+                for (int k = 0; k < KP; ++k) {
+                    mid[k] = (lo[k] + hi[k]) >> 1;
+                    const int64_t mk = -(int64_t)(lo[k] < hi[k]);
+                    va[k] = a.chains[mk & (ca[k] + mid[k])];
+                    vb[k] = a.chains[mk & (cc[k] + mid[k])];
+                }
+#pragma unroll
+                for (int k = 0; k < KP; ++k) {
+                    if (lo[k] < hi[k]) {
+                        if (va[k] == vb[k]) lo[k] = mid[k] + 1;
+                        else hi[k] = mid[k];
+                    }
+                    if (it[k] >= 0 && lo[k] >= hi[k]) {
+                        store(it[k], (int32_t)l_pairs[it[k]], lo[k]);
+                        takep(k, atomicAdd(next, 1));
+                    }
+                }
+            }
+        };
+        // within the next batch, into nx_lcp
+        job_pairs(
+            NB * (NB - 1) / 2, &sh.jp, &sh.jpnext, 2,
+            [&](int32_t q, int64_t& ca, int64_t& cc, int32_t& m, int32_t& b1, int32_t& b2) {
+                b1 = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
+                while (b1 > 1 && b1 * (b1 - 1) / 2 > q) --b1;
+                while ((b1 + 1) * b1 / 2 <= q) ++b1;
+                b2 = q - b1 * (b1 - 1) / 2;
+                ca = nx_cb[b1];
+                cc = nx_cb[b2];
+                m = min(nx_P[b1], nx_P[b2]);
+                return m > 0 && nx_first[b1] == nx_first[b2];
+            },
+            [&](int32_t q, int32_t b1, int32_t b2, bool same, int32_t m) {
+                if (same && m > 1) return true;
+                nx_lcp[b1 * NB + b2] = (uint16_t)(same && m > 0 ? 1 : 0);
+                return false;
+            },
+            [&](int32_t idx, int32_t q, int32_t l) {
+                int32_t b1 = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
+                while (b1 > 1 && b1 * (b1 - 1) / 2 > q) --b1;
+                while ((b1 + 1) * b1 / 2 <= q) ++b1;
+                nx_lcp[b1 * NB + (q - b1 * (b1 - 1) / 2)] = (uint16_t)l;
+            });
+        job_barrier(3);            // the within-batch list is no longer read
+        // between the next batch's routes and this batch's (nb routes), every pair whose first
+        // blocks agree listed, its prefix in l_pval: the overlaps rise by them at the next batch
+        const int32_t nbc = nb_cur;
+        job_pairs(
+            NB * nbc, &sh.jq, &sh.jqnext, 4,
+            [&](int32_t q, int64_t& ca, int64_t& cc, int32_t& m, int32_t& b1, int32_t& b2) {
+                b1 = q / nbc;
+                b2 = q - b1 * nbc;
+                ca = nx_cb[b1];
+                cc = r_cb[b2];
+                m = min(nx_P[b1], r_P[b2]);
+                return m > 0 && nx_first[b1] == r_first[b2];
+            },
+            [&](int32_t q, int32_t b1, int32_t b2, bool same, int32_t m) { return same; },
+            [&](int32_t idx, int32_t q, int32_t l) { l_pval[idx] = (uint16_t)l; });
+    };
+
+    // the next batch's overlaps, computed by waves 1-3 while wavefront 0 decides this batch
+    // (run-index searches against the caches as this batch found them); nx_ready: they are
+    // complete and this batch had no eviction, compaction or epoch stop, so the caches grew by
+    // this batch's chains only
+    bool nx_ready = false;
+    int32_t nb_prev = 0;
     for (;;) {
         // ---- A. the batch: the next nb queued requests (queue order is routing order)
         const int32_t qh0 = sh.qhead;
         const int32_t tb0 = sh.tdone;        // routes decided before this batch
         int32_t nb = min(NB, sh.qsize);
+        const bool pre = nx_ready && nb == NB;
+        if (pre) {
+            // the precomputed batch's common prefixes become the batch's; a route of the batch just
+            // decided added its chain to its worker's cache, so the precomputed overlap of a next
+            // route on that worker rises to their common prefix (the decided batch's arrays are
+            // still in place)
+            uint16_t* tl = l_lcp;
+            l_lcp = nx_lcp;
+            nx_lcp = tl;
+            const int32_t nxl = sh.jq;
+            for (int32_t i = tid; i < nxl; i += NT) {
+                const int32_t q = l_pairs[i], l = l_pval[i];
+                const int32_t b1 = q / nb_prev, b2 = q - b1 * nb_prev;
+                if (l > 0) atomicMax(&nx_o[b1 * W + r_sig[b2]], l);
+            }
+            __syncthreads();
+        }
         for (int32_t b = tid; b < nb; b += NT) {
-            const int32_t c = g_queue[qh0 + b >= qcap ? qh0 + b - qcap : qh0 + b];
-            const int32_t k = g_next[c];
-            const int64_t g = gc0 + c;
-            const int64_t tb0 = a.turn_off[g], tb1 = a.turn_off[g + 1];
-            const int64_t turn = tb0 + k;
-            int32_t P = a.turn_blocks[turn];
-            const int64_t cb = a.chain_off[g], ce = a.chain_off[g + 1];
-            if (P < 0 || (int64_t)P > ce - cb) {
-                atomicOr(a.status, RK_DEV_SHORT_INPUT);
-                P = P < 0 ? 0 : (int32_t)max((int64_t)0, ce - cb);
-            }
-            if (cb < 0 || cb >= (1ll << 40)) {     // a run keeps 40 bits of its chain's base
-                atomicOr(a.status, RK_DEV_BAD_OFFSETS);
-                P = 0;
-            }
-            if (P > a.max_blocks) {
-                atomicOr(a.status, RK_DEV_TOO_LARGE);
-                P = a.max_blocks;
-            }
-            r_c[b] = c | ((int64_t)k + 1 < tb1 - tb0 ? kMoreTurns : 0);
+            int32_t c, k, P;
+            int64_t turn, cb;
+            bool more;
+            queued(qh0 + b, c, k, turn, P, cb, more);
+            r_c[b] = c | (more ? kMoreTurns : 0);
             r_k[b] = k;
             r_turn[b] = (int32_t)turn;
             r_P[b] = P;
@@ -2187,86 +2622,45 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         }
         __syncthreads();
         nb = sh.nb;
-        // every (request, worker) overlap against the caches as they stand
-        search(0, nb, -1);
-        if (tiers) tier_search(0, nb, -1);
-        // common prefix of every pair of the batch's chains (prefix mode): pairs whose first
-        // blocks differ (or that have one block in common at most) are decided at once; the
-        // others are listed and searched KP at a time per thread, each group in the depth of one
-        // binary search on equal hashes
-        if (!scan) {
-            const int32_t npair = nb * (nb - 1) / 2;
-            if (tid == 0) sh.nlist = 0;
+        if (pre) {
+            // the overlaps computed during the previous batch, raised above
+            for (int32_t i = tid; i < nb * W; i += NT) o_tab[i] = o_cur[i] = nx_o[i];
             __syncthreads();
-            for (int32_t q0 = 0; q0 < npair; q0 += NT) {
-                const int32_t q = q0 + tid;
-                bool srch = false;
-                int32_t b = 0, b2 = 0;
-                if (q < npair) {
-                    b = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
-                    while (b > 1 && b * (b - 1) / 2 > q) --b;
-                    while ((b + 1) * b / 2 <= q) ++b;
-                    b2 = q - b * (b - 1) / 2;
-                    const int32_t m = min(r_P[b], r_P[b2]);
-                    const bool same = m > 0 && r_first[b] == r_first[b2];
-                    srch = same && m > 1;
-                    l_lcp[b * NB + b2] = (uint16_t)(same ? 1 : 0);
-                }
-                const unsigned long long mb = __ballot(srch);
-                int32_t wb = 0;
-                if (lane == 0 && mb) wb = atomicAdd(&sh.nlist, (int32_t)__popcll(mb));
-                wb = __builtin_amdgcn_readfirstlane(wb);
-                if (srch) l_pairs[wb + __popcll(mb & ((1ull << lane) - 1ull))] = (uint16_t)(b | (b2 << 8));
+        } else {
+            // every (request, worker) overlap against the caches as they stand
+            search(0, nb, -1);
+            if (tiers) tier_search(0, nb, -1);
+            if (!scan) pair_lcps(nb * (nb - 1) / 2, batch_pair, [&](int32_t q, int32_t b1, int32_t b2, int32_t l) {
+                l_lcp[b1 * NB + b2] = (uint16_t)l;
+            });
+        }
+        // the next batch is searched during this batch's decisions when every worker still adds
+        // runs (no recency kept: the run index is all the searches read) and the queue already
+        // holds all of the next batch
+        bool job = false;
+        if (lean || lean_ctrl) {
+            bool stamped_any = false;
+            for (int32_t j = 0; j < W; ++j) stamped_any |= s_stamped[j] != 0;
+            job = !stamped_any && sh.qsize >= nb + NB;
+        }
+        if (job) {
+            for (int32_t b = tid; b < NB; b += NT) {
+                int32_t c, k, P;
+                int64_t turn, cb;
+                bool more;
+                queued(qh0 + nb + b, c, k, turn, P, cb, more);
+                nx_cb[b] = cb;
+                nx_P[b] = P;
+                nx_first[b] = P > 0 ? a.chains[cb] : 0ull;
             }
-            __syncthreads();
-            const int32_t nsrch = sh.nlist;
-            for (int32_t grp = 0; grp * KP * NT < nsrch; ++grp) {
-            int32_t lo[KP], hi[KP], pp[KP];   // pp: b | b2 << 8, or -1
-            int64_t ca[KP], cc[KP];
-#pragma unroll
-            for (int k = 0; k < KP; ++k) {
-                const int32_t q = tid + (grp * KP + k) * NT;
-                lo[k] = 0;
-                hi[k] = 0;
-                pp[k] = -1;
-                ca[k] = 0;
-                cc[k] = 0;
-                if (q < nsrch) {
-                    pp[k] = l_pairs[q];
-                    const int32_t b = pp[k] & 0xff, b2 = pp[k] >> 8;
-                    lo[k] = 1;                 // block 0 is common
-                    hi[k] = min(r_P[b], r_P[b2]);
-                    ca[k] = r_cb[b];
-                    cc[k] = r_cb[b2];
-                }
-            }
-            for (;;) {
-                bool any = false;
-#pragma unroll
-                for (int k = 0; k < KP; ++k) any |= lo[k] < hi[k];
-                if (!any) break;
-                // addresses by masks (a closed search reads the first chain hash), so that the KP
-                // pairs' loads are in flight together
-                int32_t mid[KP];
-                uint64_t va[KP], vb[KP];
-#pragma unroll
-                for (int k = 0; k < KP; ++k) {
-                    mid[k] = (lo[k] + hi[k]) >> 1;
-                    const int64_t m = -(int64_t)(lo[k] < hi[k]);
-                    va[k] = a.chains[m & (ca[k] + mid[k])];
-                    vb[k] = a.chains[m & (cc[k] + mid[k])];
-                }
-#pragma unroll
-                for (int k = 0; k < KP; ++k) {
-                    if (lo[k] < hi[k]) {
-                        if (va[k] == vb[k]) lo[k] = mid[k] + 1;
-                        else hi[k] = mid[k];
-                    }
-                }
-            }
-#pragma unroll
-            for (int k = 0; k < KP; ++k)
-                if (pp[k] >= 0) l_lcp[(pp[k] & 0xff) * NB + (pp[k] >> 8)] = (uint16_t)lo[k];
+            if (tid == 0) {
+                sh.jn = 0;
+                sh.jsync = 0;
+                sh.jnext = 0;
+                sh.jp = 0;
+                sh.jpnext = 0;
+                sh.jq = 0;
+                sh.jqnext = 0;
             }
             __syncthreads();
         }
@@ -2588,16 +2982,23 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 __hip_atomic_store(&sh.stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
         };
+        nb_cur = nb;
+        bool had_stop = false;      // an eviction, compaction or epoch stop in this batch
+        bool job_ran = false;
         for (;;) {
             if (wave == 0) {
                 if (lean) decide(LeanTag<1>{});
                 else if (lean_ctrl) decide(LeanTag<2>{});
                 else decide(LeanTag<0>{});
             } else {
+                if (job) next_batch_job();
                 writer();
             }
+            job_ran = job_ran || job;
+            job = false;
             __syncthreads();
             event = sh.event;
+            if (event != EV_BATCH && event != EV_DONE) had_stop = true;
             if (event == EV_ROOM) {
                 // every decided route's writes are in: compact the route's worker, then decide on
                 rebuild(sh.ev_b);
@@ -2690,6 +3091,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         }
         if (tid == 0) sh.ins = 0;
         __syncthreads();
+        nx_ready = job_ran && !had_stop && event == EV_BATCH;
+        nb_prev = nb;
         if (event == EV_DONE) break;
     }
     if (tid == 0 && a.out.totals) {
@@ -2788,7 +3191,7 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.L = L;
     a.status = st;
     // LDS: worker state, in-flight routes, controller window, then the batch arrays of the largest
-    // batch that fits in 60 KiB (two episodes can then share a CU)
+    // batch that fits in 76 KiB (two episodes can then share a CU)
     size_t o = 0;
     a.lds_w = 0;
     o = align_up(o + (size_t)b->W * 11 * 4, 16);
@@ -2799,12 +3202,12 @@ extern "C" int rk_simulate_episodes(const rk_episode_batch* b, const rk_episode_
     a.lds_roff = (uint32_t)o;
     o = align_up(o + (size_t)kEpisodeThreads * 4, 16);
     a.lds_batch = (uint32_t)o;
-    const size_t limit = 60 * 1024;
+    const size_t limit = 76 * 1024;
     int32_t NB = kMaxBatch;
     const bool tiers = b->tiers != 0;
     while (NB > 1 && o + batch_layout(NB, b->W, tiers).bytes > limit) NB /= 2;
     if (o + batch_layout(NB, b->W, tiers).bytes > limit)
-        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 60 KiB",
+        return fail(RK_EUNSUPPORTED, "rk_simulate_episodes: %zu bytes of LDS per episode exceed 76 KiB",
                     o + (size_t)batch_layout(NB, b->W, tiers).bytes);
     a.NB = NB;
     const size_t lds = o + batch_layout(NB, b->W, tiers).bytes;
