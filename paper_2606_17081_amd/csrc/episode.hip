@@ -2990,6 +2990,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 if (lean) decide(LeanTag<1>{});
                 else if (lean_ctrl) decide(LeanTag<2>{});
                 else decide(LeanTag<0>{});
+                writer();           // the decided routes not yet claimed
             } else {
                 if (job) next_batch_job();
                 writer();
