@@ -96,7 +96,6 @@ struct EpArgs {
     uint32_t lds_w, lds_inflight, lds_u, lds_roff, lds_batch;
 };
 
-constexpr int KR = 4;      // decided routes a writer wavefront claims at a time
 
 // Which copy of the decision loop runs: 0 the full one, 1 the lean one (prefix
 // mode, argmin, LRU, no tiers, no controller), 2 the lean one with the load
@@ -109,7 +108,6 @@ struct LeanTag {
 struct EpShared {
     int32_t next_e, nlist, jn, jsync, jnext, jp, jpnext, jq, jqnext;
     int32_t qhead, qsize, nb, event, ev_b, ins, remaining, ev, decided, claimed, stop, tdone, h1, h2;
-    int32_t woff[NW][KR + 1], wst[NW][KR];
     uint32_t new_head, first_kept, adv;
     int64_t ev_row, ev_total;
     unsigned long long digest, rb_mask;
@@ -1195,7 +1193,7 @@ __device__ __forceinline__ void tier_searches(int32_t n, bool bsearch, const Inf
 // Offsets of the batch arrays in LDS (bytes), shared by the launch and the kernel.
 struct BatchLayout {
     uint32_t rcb, rlast, rfirst, o_cur, o_tab, rc, rk, rturn, rP, rsig, rotab, rstamp, rep, rstep, rreg, revc, revd, rrnd, lcp,
-        items, pairs, nxcb, nxfirst, nxP, nxo, lcp2, pval, t1, t12, bytes;
+        items, pairs, nxcb, nxfirst, nxP, nxo, lcp2, pval, wend, t1, t12, bytes;
 };
 
 __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool tiers)
@@ -1234,6 +1232,7 @@ __host__ __device__ inline BatchLayout batch_layout(int32_t NB, int32_t W, bool 
     b.nxfirst = take(nb * 8, 8);
     b.nxP = take(nb * 4, 4);
     b.nxo = take(nb * w * 4, 4);
+    b.wend = take(nb * 4, 4);
     b.lcp2 = take(nb * nb * 2, 4);
     b.pval = take(nb * nb * 2 + 2, 4);
     b.t1 = take(tiers ? nb * w * 2 : 0, 4);
@@ -1331,6 +1330,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     uint64_t* nx_first = (uint64_t*)(bb + BL.nxfirst);     //   this batch is decided: chain base, h_0, P
     int32_t* nx_P = (int32_t*)(bb + BL.nxP);
     int32_t* nx_o = (int32_t*)(bb + BL.nxo);               //   and [b][j] overlaps
+    int32_t* r_wend = (int32_t*)(bb + BL.wend);            // writes of the batch's routes up to b, inclusive
     uint16_t* t1_tab = (uint16_t*)(bb + BL.t1);            // [b][j] leading blocks in G1 (tiers)
     uint16_t* t12_tab = (uint16_t*)(bb + BL.t12);          // [b][j] leading blocks in G1 u G2 (tiers)
 
@@ -1513,21 +1513,26 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         __syncthreads();
     };
 
-    // ---- waves 1-3 while wavefront 0 decides: claim up to KR decided routes at a time (sh.claimed,
-    //      compare-and-swap) and apply their cache writes with the wave's 64 lanes, the claimed
-    //      routes' blocks numbered consecutively; stop once wavefront 0 has stopped and every
-    //      decided route is claimed.  sh.decided and sh.claimed only grow until the workgroup
-    //      synchronizes.
+    // ---- waves 1-3 while wavefront 0 decides (and wavefront 0 once it stops): claim the next
+    //      128 writes of the decided routes (sh.claimed counts writes, r_wend numbers them; a
+    //      compare-and-swap) and apply them with the wave's 64 lanes, two each; stop once
+    //      wavefront 0 has stopped and every decided write is claimed.  sh.decided and
+    //      sh.claimed only grow until the workgroup synchronizes.
     auto writer = [&]() {
-        int32_t* woff = sh.woff[wave];
         int my_ins = 0, my_h1 = 0, my_h2 = 0;
         for (;;) {
             const int32_t c = __builtin_amdgcn_readfirstlane(
                 __hip_atomic_load(&sh.claimed, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
             const int32_t d = __builtin_amdgcn_readfirstlane(
                 __hip_atomic_load(&sh.decided, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
-            if (c < d) {
-                const int32_t hi = min(d, c + KR);
+            const int32_t wd = d > 0 ? __builtin_amdgcn_readfirstlane(r_wend[d - 1]) : 0;
+            if (c < wd) {
+                // work items [c, hi): the decided routes' writes numbered in order, route b's
+                // [r_wend[b - 1], r_wend[b]).  A route on a worker that keeps no recency yet adds
+                // the entries of one run to the run index (the blocks past its decided overlap,
+                // which counts the common prefixes with the batch's earlier routes on that
+                // worker); a route on a worker that keeps recency touches all of its blocks.
+                const int32_t hi = min(wd, c + 128);
                 int32_t won = 0;
                 if (lane == 0) {
                     int32_t expect = c;
@@ -1535,100 +1540,66 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 }
                 if (!__builtin_amdgcn_readfirstlane(won)) continue;
-                // routes [c, hi).  A route on a worker that keeps no recency yet adds one run to
-                // the run index: the blocks past its decided overlap, which counts the common
-                // prefixes with the batch's earlier routes on that worker.  A route on a worker
-                // that keeps recency touches all of its blocks, numbered consecutively over the
-                // claimed routes.
-                int32_t* wst = sh.wst[wave];
-                const int32_t nr = hi - c;
-                int32_t tot = 0, pr = 0, st = -1;
-                if (lane < nr) {
-                    const int32_t bl = c + lane, sgl = r_sig[bl], Pl = r_P[bl];
-                    if (s_stamped[sgl]) {
-                        pr = Pl;
-                    } else {
-                        st = o_cur[bl * W + sgl];
-                        pr = st < Pl ? run_entries(st, Pl) : 0;
-                    }
+                int32_t b0 = 0, bh = d - 1;    // the route of item c
+                while (b0 < bh) {
+                    const int32_t mid = (b0 + bh) >> 1;
+                    if (r_wend[mid] > c) bh = mid;
+                    else b0 = mid + 1;
                 }
-                const int32_t off = wave_excl_sum_dpp(pr, tot);
-                if (tot == 0) continue;
-                if (lane < nr) {
-                    woff[lane] = off;
-                    wst[lane] = st;         // a run's first block, or -1 for a route that touches every block
+                // two items per lane, their chain hashes, claims and group loads in flight together
+                int32_t bq[2], kq[2], sgq[2], stq[2];
+                bool v[2], lazy[2];
+                int64_t hoff[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int32_t w = c + lane + 64 * u;
+                    v[u] = w < hi;
+                    int32_t b = b0;
+                    while (v[u] && r_wend[b] <= w) ++b;
+                    bq[u] = b;
+                    kq[u] = w - (b > 0 ? r_wend[b - 1] : 0);
+                    sgq[u] = v[u] ? r_sig[b] : 0;
+                    lazy[u] = v[u] && !s_stamped[sgq[u]];
+                    stq[u] = lazy[u] ? o_cur[b * W + sgq[u]] : 0;
+                    const int32_t pos = lazy[u] ? run_entry_pos(stq[u], kq[u]) : kq[u];
+                    hoff[u] = v[u] ? r_cb[b] + pos : 0;
                 }
-                if (lane == 0) woff[nr] = tot;
-                ep_wave_sync();
-                // a claim of routes that only add runs: one entry per lane at a time
-                if (__ballot(lane < nr && wst[lane] < 0) == 0ull) {
-                    for (int32_t i = lane; i < tot; i += 64) {
-                        int32_t r = 0;
-                        while (r + 1 < nr && woff[r + 1] <= i) ++r;
-                        const int32_t b = c + r, sg = r_sig[b];
-                        const int32_t pos = run_entry_pos(wst[r], i - woff[r]);
-                        run_insert(g_runs, rsmask, a.chains[r_cb[b] + pos], sg, run_val(r_cb[b], sg, r_P[b]),
+                uint64_t h[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) h[u] = a.chains[hoff[u]];
+                Slot* tk[2];
+                bool hint[2], act[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    if (lazy[u])
+                        run_insert(g_runs, rsmask, h[u], sgq[u], run_val(r_cb[bq[u]], sgq[u], r_P[bq[u]]),
                                    a.status);
-                    }
-                    ep_wave_sync();
-                    continue;
+                    tk[u] = g_slots + (uint64_t)sgq[u] * S;
+                    act[u] = v[u] && !lazy[u];
+                    hint[u] = kq[u] < r_otab[bq[u]];
                 }
-                // otherwise two blocks per lane at a time, their chain hashes, claims and group loads
-                // in flight together
-                for (int32_t i0 = lane; i0 < tot; i0 += 128) {
-                    int32_t bq[2], kq[2], sgq[2];
-                    bool v[2], lazy[2];
-                    int64_t hoff[2];
+                if (__ballot(act[0] || act[1]) == 0ull) continue;
+                uint64_t sl[2];
+                int ins[2];
+                touch_hinted2(tk, smask, h, hint, act, sl, ins, a.status);
 #pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        const int32_t i = i0 + 64 * u;
-                        v[u] = i < tot;
-                        int32_t r = 0;
-                        while (r + 1 < nr && woff[r + 1] <= i) ++r;
-                        bq[u] = c + r;
-                        kq[u] = i - woff[r];
-                        lazy[u] = wst[r] >= 0;
-                        sgq[u] = v[u] ? r_sig[bq[u]] : 0;
-                        const int32_t pos = lazy[u] ? run_entry_pos(wst[r], kq[u]) : kq[u];
-                        hoff[u] = v[u] ? r_cb[bq[u]] + pos : 0;
-                    }
-                    uint64_t h[2];
-#pragma unroll
-                    for (int u = 0; u < 2; ++u) h[u] = a.chains[hoff[u]];
-                    Slot* tk[2];
-                    bool hint[2], act[2];
-#pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        if (v[u] && lazy[u])
-                            run_insert(g_runs, rsmask, h[u], sgq[u], run_val(r_cb[bq[u]], sgq[u], r_P[bq[u]]),
-                                       a.status);
-                        tk[u] = g_slots + (uint64_t)sgq[u] * S;
-                        act[u] = v[u] && !lazy[u];
-                        hint[u] = kq[u] < r_otab[bq[u]];
-                    }
-                    uint64_t sl[2];
-                    int ins[2];
-                    touch_hinted2(tk, smask, h, hint, act, sl, ins, a.status);
-#pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        if (!act[u]) continue;
-                        const int32_t b = bq[u], sg = sgq[u];
-                        const uint32_t stamp = r_stamp[b] + (uint32_t)(r_P[b] - 1 - kq[u]);
-                        // routes of one worker that share a block touch it concurrently: the latest stamp wins
-                        if (sl[u] != ~0ull) {
-                            const uint32_t old = __hip_atomic_fetch_max(&tk[u][sl[u]].stamp, stamp, __ATOMIC_RELAXED,
-                                                                        __HIP_MEMORY_SCOPE_WORKGROUP);
-                            if (freq) freq_touch(&tk[u][sl[u]].fkey, ins[u] != 0, r_ep[b]);
-                            if (tiers && !ins[u]) {       // a hit whose old record lay in a tier's run
-                                my_h1 += old >= s_b1[sg];
-                                my_h2 += old >= s_b2[sg];
-                            }
+                for (int u = 0; u < 2; ++u) {
+                    if (!act[u]) continue;
+                    const int32_t b = bq[u], sg = sgq[u];
+                    const uint32_t stamp = r_stamp[b] + (uint32_t)(r_P[b] - 1 - kq[u]);
+                    // routes of one worker that share a block touch it concurrently: the latest stamp wins
+                    if (sl[u] != ~0ull) {
+                        const uint32_t old = __hip_atomic_fetch_max(&tk[u][sl[u]].stamp, stamp, __ATOMIC_RELAXED,
+                                                                    __HIP_MEMORY_SCOPE_WORKGROUP);
+                        if (freq) freq_touch(&tk[u][sl[u]].fkey, ins[u] != 0, r_ep[b]);
+                        if (tiers && !ins[u]) {       // a hit whose old record lay in a tier's run
+                            my_h1 += old >= s_b1[sg];
+                            my_h2 += old >= s_b2[sg];
                         }
-                        g_log[(uint64_t)sg * R + (stamp & rmask)] = (uint32_t)sl[u];   // a failed insert logs an out-of-range slot
-                        my_ins += ins[u];
                     }
+                    g_log[(uint64_t)sg * R + (stamp & rmask)] = (uint32_t)sl[u];   // a failed insert logs an out-of-range slot
+                    my_ins += ins[u];
                 }
-                ep_wave_sync();
                 continue;
             }
             if (__builtin_amdgcn_readfirstlane(
@@ -1637,7 +1608,8 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     __hip_atomic_load(&sh.claimed, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
                 const int32_t d2 = __builtin_amdgcn_readfirstlane(
                     __hip_atomic_load(&sh.decided, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
-                if (c2 >= d2) break;
+                const int32_t wd2 = d2 > 0 ? __builtin_amdgcn_readfirstlane(r_wend[d2 - 1]) : 0;
+                if (c2 >= wd2) break;
                 continue;
             }
             __builtin_amdgcn_s_sleep(2);
@@ -2694,6 +2666,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             }
             // workers that keep recency (write log records)
             const unsigned long long stamped_mask = __ballot(lane < W && s_stamped[lane] != 0);
+            // writes of the batch's routes decided so far (run-index entries or touches; the
+            // decisions go on in the same batch after a stop)
+            int32_t rwork = t > t0 ? r_wend[t - t0 - 1] : 0;
             for (;;) {
                 if (!step_open) {
                     // release the routes of step s - H; queue their conversations' next turns
@@ -2878,8 +2853,10 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                         rused += P - osg;
                     }
                 }
+                rwork += ((stamped_mask >> sg) & 1ull) ? P : (osg < P ? run_entries(osg, P) : 0);
                 if (lane == 0) {
                     r_sig[b] = sg;
+                    r_wend[b] = rwork;
                     r_stamp[b] = base;
                     r_ep[b] = freq_d ? (uint32_t)run_ep : 0u;
                     g_hist[2 * t] = rc & ~kMoreTurns;
