@@ -2242,9 +2242,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     // run-index search of run_searches: a first probe of block 0 settles the misses and lists the
     // rest; once the three waves have listed theirs, the listed items are searched with KI slots
     // per thread, each slot taking the next listed item when its search ends.
-    auto next_batch_job = [&]() {
+    auto job_search_part = [&]() {
         enum : int32_t { DONE = 0, HASH = 1, LOOK = 2, CMP = 3, CKPT = 4 };
-        constexpr int NJ = NT - 64;                  // the job's threads
+        constexpr int NJ = NT - 128;                 // the searching threads
         const int32_t tj = tid - 64;
         const int32_t n = NB * W;
         for (int32_t base = 0; base < n; base += NJ * KI) {
@@ -2280,15 +2280,12 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 if (hit) l_items[wb + __popcll(m & ((1ull << lane) - 1ull))] = (uint16_t)i;
             }
         }
-        // barrier k of the three job waves (the decision wavefront does not take part)
-        auto job_barrier = [&](int32_t k) {
-            ep_wave_sync();
-            if (lane == 0) __hip_atomic_fetch_add(&sh.jsync, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-            while (__builtin_amdgcn_readfirstlane(
-                       __hip_atomic_load(&sh.jsync, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) < k * (NW - 1))
-                __builtin_amdgcn_s_sleep(1);
-        };
-        job_barrier(1);            // the three waves' lists are complete
+        // barrier of the searching waves: their lists are complete
+        ep_wave_sync();
+        if (lane == 0) __hip_atomic_fetch_add(&sh.jsync, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+        while (__builtin_amdgcn_readfirstlane(
+                   __hip_atomic_load(&sh.jsync, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) < NW - 2)
+            __builtin_amdgcn_s_sleep(1);
         const int32_t n2 = __hip_atomic_load(&sh.jn, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
         const uint64_t* chains = a.chains;
         int64_t cb[KI], rcb[KI];
@@ -2433,14 +2430,16 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 }
             }
         }
+    };
+    auto job_pair_part = [&]() {
         // ---- common prefixes of pairs (pair(q, ...) as for pair_lcps): direct(q, b1, b2, same, m)
         //      stores a pair's prefix at once or returns true to list the pair; the listed pairs are
         //      searched with KP slots per thread, each taking the next listed pair when its search
         //      ends, store(listed index, q, prefix)
-        auto job_pairs = [&](int32_t npair, int32_t* cnt, int32_t* next, int32_t bar, const auto& pair,
-                             const auto& direct, const auto& store) {
-            for (int32_t q0 = 0; q0 < npair; q0 += NJ) {
-                const int32_t q = q0 + tj;
+        auto job_pairs = [&](int32_t npair, int32_t* cnt, int32_t* next, const auto& pair, const auto& direct,
+                             const auto& store) {
+            for (int32_t q0 = 0; q0 < npair; q0 += 64) {
+                const int32_t q = q0 + lane;
                 bool lst = false;
                 if (q < npair) {
                     int64_t ca, cc;
@@ -2454,8 +2453,9 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 wb = __builtin_amdgcn_readfirstlane(wb);
                 if (lst) l_pairs[wb + __popcll(mb & ((1ull << lane) - 1ull))] = (uint16_t)q;
             }
-            job_barrier(bar);
-            const int32_t nl = __hip_atomic_load(cnt, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            ep_wave_sync();
+            const int32_t nl = __builtin_amdgcn_readfirstlane(
+                __hip_atomic_load(cnt, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
             int32_t lo[KP], hi[KP], it[KP];
             int64_t ca[KP], cc[KP];
             auto takep = [&](int k, int32_t idx) {
@@ -2500,7 +2500,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         };
         // within the next batch, into nx_lcp
         job_pairs(
-            NB * (NB - 1) / 2, &sh.jp, &sh.jpnext, 2,
+            NB * (NB - 1) / 2, &sh.jp, &sh.jpnext,
             [&](int32_t q, int64_t& ca, int64_t& cc, int32_t& m, int32_t& b1, int32_t& b2) {
                 b1 = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
                 while (b1 > 1 && b1 * (b1 - 1) / 2 > q) --b1;
@@ -2522,12 +2522,12 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 while ((b1 + 1) * b1 / 2 <= q) ++b1;
                 nx_lcp[b1 * NB + (q - b1 * (b1 - 1) / 2)] = (uint16_t)l;
             });
-        job_barrier(3);            // the within-batch list is no longer read
+        ep_wave_sync();            // the within-batch list is no longer read
         // between the next batch's routes and this batch's (nb routes), every pair whose first
         // blocks agree listed, its prefix in l_pval: the overlaps rise by them at the next batch
         const int32_t nbc = nb_cur;
         job_pairs(
-            NB * nbc, &sh.jq, &sh.jqnext, 4,
+            NB * nbc, &sh.jq, &sh.jqnext,
             [&](int32_t q, int64_t& ca, int64_t& cc, int32_t& m, int32_t& b1, int32_t& b2) {
                 b1 = q / nbc;
                 b2 = q - b1 * nbc;
@@ -2538,6 +2538,12 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             },
             [&](int32_t q, int32_t b1, int32_t b2, bool same, int32_t m) { return same; },
             [&](int32_t idx, int32_t q, int32_t l) { l_pval[idx] = (uint16_t)l; });
+    };
+    // The job's two parts run side by side: waves 1 .. NW-2 search the run index, the last wave
+    // takes the common prefixes of the batch pairs.
+    auto next_batch_job = [&]() {
+        if (wave == NW - 1) job_pair_part();
+        else job_search_part();
     };
 
     // the next batch's overlaps, computed by waves 1-3 while wavefront 0 decides this batch
