@@ -2970,9 +2970,12 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         bool job_ran = false;
         for (;;) {
             if (wave == 0) {
+                // the serial chain of decisions goes first on its SIMD
+                __builtin_amdgcn_s_setprio(3);
                 if (lean) decide(LeanTag<1>{});
                 else if (lean_ctrl) decide(LeanTag<2>{});
                 else decide(LeanTag<0>{});
+                __builtin_amdgcn_s_setprio(0);
                 writer();           // the decided routes not yet claimed
             } else {
                 if (job) next_batch_job();
