@@ -258,6 +258,10 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
         for (int32_t pq = tid; pq < W * W; pq += PT) s_er[pq] = -1;
         __syncthreads();
         const bool wl = tid < W;
+        // lanes that share the recomputation of one edge: a power of two up to a row of 16 lanes,
+        // so that DPP moves within rows combine them
+        int32_t G = 1;
+        while (G < 16 && 2 * G * W <= PT) G *= 2;
         int32_t cnt = 0;   // lane y: rows on worker y in the partial optimum
         bool placed_all = true;
         for (int32_t i = 0; i < m; ++i) {
@@ -349,27 +353,64 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             }
             __syncthreads();
             // ---- edge maintenance, e[x][z] = min over rows r on x of c[r][z] - c[r][x]:
-            // an edge whose argmin row left x is recomputed over x's rows (all
-            // lanes scan, then a wavefront argmin); a gained row is folded in.
+            // the edges whose argmin row left x are recomputed over x's rows together
+            // (lane G z + g scans x's rows g, g + G, ... for edge x -> z; the G lanes of
+            // an edge then take the least (value, row) pair); a gained row is folded in.
             for (int32_t h = 0; h < hops; ++h) {
                 const int32_t x = __builtin_amdgcn_readlane(hx, h), r = __builtin_amdgcn_readlane(hr, h);
                 if (x < 0) continue;
-                uint64_t lost = __ballot(wl && tid != x && s_er[x * W + tid] == r);
+                const bool lz = wl && tid != x && s_er[x * W + tid] == r;
+                const uint64_t lost = __ballot(lz);
+                if (lost == 0ull) continue;
                 const int32_t cx = __builtin_amdgcn_readlane(cnt, x);
-                while (lost) {
-                    const int32_t z = __ffsll((unsigned long long)lost) - 1;
-                    lost &= lost - 1;
+                if ((lost & (lost - 1)) == 0ull) {
+                    // a single edge: every lane scans rows for it, then a wavefront argmin
+                    const int32_t z1 = __ffsll((unsigned long long)lost) - 1;
                     double best = dinf();
                     int32_t brow = 0x7fffffff;
                     for (int32_t k = tid; k < cx; k += PT) {
                         const int32_t q = s_mem[x * a.kmax + k];
-                        pick(best, brow, (double)cm[(int64_t)q * W + z] - (double)cm[(int64_t)q * W + x], q);
+                        pick(best, brow, (double)cm[(int64_t)q * W + z1] - (double)cm[(int64_t)q * W + x], q);
                     }
                     wave_argmin_f64(best, brow);
                     if (tid == 0) {
-                        s_e[x * W + z] = best;
-                        s_er[x * W + z] = (int16_t)(brow == 0x7fffffff ? -1 : brow);
+                        s_e[x * W + z1] = best;
+                        s_er[x * W + z1] = (int16_t)(brow == 0x7fffffff ? -1 : brow);
                     }
+                    continue;
+                }
+                const int32_t z = tid / G, g = tid % G;
+                const bool mine = z < W && z != x && s_er[x * W + z] == r;
+                double best = dinf();
+                int32_t brow = 0x7fffffff;
+                if (mine) {
+                    // four rows per lane at a time, their loads issued before any is used
+                    for (int32_t k0 = g; k0 < cx; k0 += 4 * G) {
+                        int32_t q[4];
+                        float cz[4], cxv[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const int32_t k = k0 + u * G;
+                            q[u] = k < cx ? s_mem[x * a.kmax + k] : -1;
+                        }
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const int64_t row = q[u] >= 0 ? (int64_t)q[u] * W : 0;
+                            cz[u] = cm[row + z];
+                            cxv[u] = cm[row + x];
+                        }
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            if (q[u] >= 0) pick(best, brow, (double)cz[u] - (double)cxv[u], q[u]);
+                    }
+                }
+                if (G >= 2) argmin_dpp_step<0xB1>(best, brow);    // quad_perm [1,0,3,2]
+                if (G >= 4) argmin_dpp_step<0x4E>(best, brow);    // quad_perm [2,3,0,1]
+                if (G >= 8) argmin_dpp_step<0x141>(best, brow);   // row_half_mirror
+                if (G >= 16) argmin_dpp_step<0x140>(best, brow);  // row_mirror
+                if (g == 0 && mine) {
+                    s_e[x * W + z] = best;
+                    s_er[x * W + z] = (int16_t)(brow == 0x7fffffff ? -1 : brow);
                 }
             }
             for (int32_t h = 0; h < hops; ++h) {
