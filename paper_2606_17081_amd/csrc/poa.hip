@@ -272,12 +272,16 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             for (int32_t x = 0; x < WMAX; ++x) ecol[x] = (x < W && wl) ? s_e[x * W + tid] : dinf();
             double dist = wl ? (double)cm[(int64_t)i * W + tid] : dinf();
             int32_t pred = -1;
+            // workers to relax from: all in the first round, then those whose distance fell in
+            // the round before (from any other worker every candidate was tried already with
+            // the same distance, and a tie never replaces a distance or a predecessor)
+            uint64_t relax = ~0ull;
             for (int32_t round = 0;; ++round) {
                 double nd = dist;
                 int32_t pb = pred;
 #pragma unroll
                 for (int32_t x = 0; x < WMAX; ++x) {
-                    if (x < W) {
+                    if (x < W && ((relax >> x) & 1ull)) {
                         const double v = lane_f64(dist, x) + ecol[x];
                         if (wl && v < nd) {
                             nd = v;
@@ -285,10 +289,11 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                         }
                     }
                 }
-                const bool changed = __ballot(nd != dist || pb != pred) != 0ull;
+                const uint64_t fell = __ballot(nd != dist);
                 dist = nd;
                 pred = pb;
-                if (!changed) break;
+                if (fell == 0ull) break;
+                relax = fell;
                 if (round > W + 1) {
                     if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
                     break;
