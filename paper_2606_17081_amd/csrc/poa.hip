@@ -72,6 +72,20 @@ __device__ __forceinline__ void argmin_dpp_step(double& v, int32_t& j)
     pick(v, j, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)), oj);
 }
 
+// One candidate of the row-parallel relaxation: the distance at position P of the lane's row of
+// 16 (the halves lo, hi of a double), plus the edge weight e, against the best (bv, bx) so far.
+template <int P>
+__device__ __forceinline__ void relax_from_row(int32_t lo, int32_t hi, double e, int32_t x, double& bv, int32_t& bx)
+{
+    const uint32_t l = (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, 0x150 + P, 0xF, 0xF, false);   // row_newbcast:P
+    const uint32_t h = (uint32_t)__builtin_amdgcn_update_dpp(hi, hi, 0x150 + P, 0xF, 0xF, false);
+    const double v = __longlong_as_double((long long)(((uint64_t)h << 32) | l)) + e;
+    if (v < bv) {
+        bv = v;
+        bx = x;
+    }
+}
+
 // Least (value, index) pair over the 64 lanes, by value and then by index;
 // every lane receives it.  Swaps within quads, then the mirrored half row and
 // row, leave each row of 16 lanes holding its minimum; the four rows are then
@@ -265,38 +279,90 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
         int32_t cnt = 0;   // lane y: rows on worker y in the partial optimum
         bool placed_all = true;
         for (int32_t i = 0; i < m; ++i) {
-            // Bellman-Ford over the workers (Jacobi rounds): lane y keeps dist[y]
-            // and pred[y]; lane y's column of edge weights sits in registers
-            double ecol[WMAX];
-#pragma unroll
-            for (int32_t x = 0; x < WMAX; ++x) ecol[x] = (x < W && wl) ? s_e[x * W + tid] : dinf();
-            double dist = wl ? (double)cm[(int64_t)i * W + tid] : dinf();
+            double dist;
             int32_t pred = -1;
-            // workers to relax from: all in the first round, then those whose distance fell in
-            // the round before (from any other worker every candidate was tried already with
-            // the same distance, and a tie never replaces a distance or a predecessor)
-            uint64_t relax = ~0ull;
-            for (int32_t round = 0;; ++round) {
-                double nd = dist;
-                int32_t pb = pred;
+            if constexpr (WMAX <= 16) {
+                // Bellman-Ford over the workers (Jacobi rounds), the wavefront as four rows of 16
+                // lanes (W <= 16): every row keeps dist[y] at position y, row g relaxes from
+                // workers 4g .. 4g + 3 (lane (g, y) keeps the weights e[4g + p][y] in registers),
+                // and the rows' least (distance, worker) pairs are merged; worker order breaks ties
+                // as in a relaxation from every worker in turn
+                const int32_t g = tid >> 4, y = tid & 15;
+                const bool wy = y < W;
+                double ec[4];
 #pragma unroll
-                for (int32_t x = 0; x < WMAX; ++x) {
-                    if (x < W && ((relax >> x) & 1ull)) {
-                        const double v = lane_f64(dist, x) + ecol[x];
-                        if (wl && v < nd) {
-                            nd = v;
-                            pb = x;
-                        }
+                for (int32_t p = 0; p < 4; ++p) {
+                    const int32_t x = 4 * g + p;
+                    ec[p] = (x < W && wy) ? s_e[x * W + y] : dinf();
+                }
+                dist = wy ? (double)cm[(int64_t)i * W + y] : dinf();
+                const int32_t src = (tid & ~15) | (4 * g + (tid & 3));   // position p < 4 of row g: dist[4g + p]
+                for (int32_t round = 0;; ++round) {
+                    const long long db = __double_as_longlong(dist);
+                    const int32_t rlo = __shfl((int)(uint32_t)db, src);
+                    const int32_t rhi = __shfl((int)(uint32_t)(db >> 32), src);
+                    double bv = dinf();
+                    int32_t bx = 0x7fffffff;
+                    relax_from_row<0>(rlo, rhi, ec[0], 4 * g, bv, bx);
+                    relax_from_row<1>(rlo, rhi, ec[1], 4 * g + 1, bv, bx);
+                    relax_from_row<2>(rlo, rhi, ec[2], 4 * g + 2, bv, bx);
+                    relax_from_row<3>(rlo, rhi, ec[3], 4 * g + 3, bv, bx);
+#pragma unroll
+                    for (int32_t sft = 16; sft < 64; sft <<= 1) {
+                        const long long bb = __double_as_longlong(bv);
+                        const uint32_t olo = (uint32_t)__shfl_xor((int)(uint32_t)bb, sft);
+                        const uint32_t ohi = (uint32_t)__shfl_xor((int)(uint32_t)(bb >> 32), sft);
+                        const int32_t ox = __shfl_xor(bx, sft);
+                        pick(bv, bx, __longlong_as_double((long long)(((uint64_t)ohi << 32) | olo)), ox);
+                    }
+                    double nd = dist;
+                    int32_t pb = pred;
+                    if (wy && bv < nd) {
+                        nd = bv;
+                        pb = bx;
+                    }
+                    const uint64_t fell = __ballot(nd != dist);
+                    dist = nd;
+                    pred = pb;
+                    if (fell == 0ull) break;
+                    if (round > W + 1) {
+                        if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
+                        break;
                     }
                 }
-                const uint64_t fell = __ballot(nd != dist);
-                dist = nd;
-                pred = pb;
-                if (fell == 0ull) break;
-                relax = fell;
-                if (round > W + 1) {
-                    if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
-                    break;
+            } else {
+                // Bellman-Ford over the workers (Jacobi rounds): lane y keeps dist[y]
+                // and pred[y]; lane y's column of edge weights sits in registers
+                double ecol[WMAX];
+#pragma unroll
+                for (int32_t x = 0; x < WMAX; ++x) ecol[x] = (x < W && wl) ? s_e[x * W + tid] : dinf();
+                dist = wl ? (double)cm[(int64_t)i * W + tid] : dinf();
+                // workers to relax from: all in the first round, then those whose distance fell in
+                // the round before (from any other worker every candidate was tried already with
+                // the same distance, and a tie never replaces a distance or a predecessor)
+                uint64_t relax = ~0ull;
+                for (int32_t round = 0;; ++round) {
+                    double nd = dist;
+                    int32_t pb = pred;
+#pragma unroll
+                    for (int32_t x = 0; x < WMAX; ++x) {
+                        if (x < W && ((relax >> x) & 1ull)) {
+                            const double v = lane_f64(dist, x) + ecol[x];
+                            if (wl && v < nd) {
+                                nd = v;
+                                pb = x;
+                            }
+                        }
+                    }
+                    const uint64_t fell = __ballot(nd != dist);
+                    dist = nd;
+                    pred = pb;
+                    if (fell == 0ull) break;
+                    relax = fell;
+                    if (round > W + 1) {
+                        if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
+                        break;
+                    }
                 }
             }
             // target: least distance among workers with spare capacity (lowest index on ties)
