@@ -281,6 +281,7 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
         for (int32_t i = 0; i < m; ++i) {
             double dist;
             int32_t pred = -1;
+            float c_row;   // lane y < W (row 0): the new row's cost on worker y
             if constexpr (WMAX <= 16) {
                 // Bellman-Ford over the workers (Jacobi rounds), the wavefront as four rows of 16
                 // lanes (W <= 16): every row keeps dist[y] at position y, row g relaxes from
@@ -295,7 +296,8 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                     const int32_t x = 4 * g + p;
                     ec[p] = (x < W && wy) ? s_e[x * W + y] : dinf();
                 }
-                dist = wy ? (double)cm[(int64_t)i * W + y] : dinf();
+                c_row = wy ? cm[(int64_t)i * W + y] : 0.0f;
+                dist = wy ? (double)c_row : dinf();
                 const int32_t src = (tid & ~15) | (4 * g + (tid & 3));   // position p < 4 of row g: dist[4g + p]
                 for (int32_t round = 0;; ++round) {
                     const long long db = __double_as_longlong(dist);
@@ -336,7 +338,8 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                 double ecol[WMAX];
 #pragma unroll
                 for (int32_t x = 0; x < WMAX; ++x) ecol[x] = (x < W && wl) ? s_e[x * W + tid] : dinf();
-                dist = wl ? (double)cm[(int64_t)i * W + tid] : dinf();
+                c_row = wl ? cm[(int64_t)i * W + tid] : 0.0f;
+                dist = wl ? (double)c_row : dinf();
                 // workers to relax from: all in the first round, then those whose distance fell in
                 // the round before (from any other worker every candidate was tried already with
                 // the same distance, and a tie never replaces a distance or a predecessor)
@@ -486,8 +489,11 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             }
             for (int32_t h = 0; h < hops; ++h) {
                 const int32_t yg = __builtin_amdgcn_readlane(hy, h), r = __builtin_amdgcn_readlane(hr, h);
+                // the new row's costs are in registers already
+                const float cg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c_row), yg));
                 if (wl && tid != yg) {
-                    const double v = (double)cm[(int64_t)r * W + tid] - (double)cm[(int64_t)r * W + yg];
+                    const double v = r == i ? (double)c_row - (double)cg
+                                            : (double)cm[(int64_t)r * W + tid] - (double)cm[(int64_t)r * W + yg];
                     if (v < s_e[yg * W + tid]) {
                         s_e[yg * W + tid] = v;
                         s_er[yg * W + tid] = (int16_t)r;
