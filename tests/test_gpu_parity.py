@@ -404,6 +404,43 @@ def test_snapshot_poa(gpu, orc):
     assert float(hat[0]) == pytest.approx(sel.sum() / coo.sum(), rel=1e-12)
 
 
+@pytest.mark.parametrize("W", [1, 2, 5, 8, 9, 12, 15, 16, 17, 24, 32, 40, 64])
+def test_poa_worker_counts(gpu, orc, W):
+    """Windows of 1..160 rows at worker counts on both sides of the kernel's lane layouts (rows of
+    16 lanes for W <= 16, one lane per worker above), with overlaps from a few levels so that many
+    costs tie and a moved row often held several edge minima; every window against the oracle."""
+    torch, rk = gpu
+    rng = np.random.default_rng(1000 + W)
+    sizes = [1, 2, 3, W, W + 1, 2 * W, 5 * W + 3] + [int(x) for x in rng.integers(1, 161, 12)]
+    sizes = [m for m in sizes if m >= 1]
+    win = np.zeros(len(sizes) + 1, np.int64)
+    np.cumsum(sizes, out=win[1:])
+    n = int(win[-1])
+    P = rng.integers(1, 300, n).astype(np.int32)
+    am = rng.integers(0, W, n).astype(np.int32)
+    lev = rng.choice([0.0, 0.25, 0.5, 1.0], size=(n, W), p=[0.4, 0.2, 0.2, 0.2])
+    ov = np.floor(lev * P[:, None]).astype(np.int32)
+    up = rk.to_device
+    sel = torch.zeros(len(sizes), dtype=torch.float64, device="cuda")
+    coo = torch.zeros_like(sel)
+    hat = torch.zeros(1, dtype=torch.float64, device="cuda")
+    pp = dict(wl.POA_PARAMS)
+    params = rk.PoaParams(pp["a"], pp["b"], pp["d"], pp["beta"], pp["C_cap"], pp["w_c"], 0)
+    mw = max(sizes)
+    ws = torch.empty(rk.poa_workspace_size(n, W), dtype=torch.uint8, device="cuda")
+    say("PoA parity, W", W, "windows", len(sizes), "rows", n)
+    rk.poa_estimate(up(win), up(np.array([0, len(sizes)], np.int64)), n, mw, W, up(am), up(ov), up(P),
+                    params, sel, coo, hat, ws)
+    torch.cuda.synchronize()
+    _status_clean(rk)
+    sel, coo = sel.cpu().numpy(), coo.cpu().numpy()
+    for w in range(len(sizes)):
+        r0, r1 = int(win[w]), int(win[w + 1])
+        s, c, _ = orc.poa_window(am[r0:r1], ov[r0:r1], P[r0:r1], W, **pp)
+        assert sel[w] == pytest.approx(s, rel=REL), (W, w, sizes[w])
+        assert coo[w] == pytest.approx(c, rel=REL), (W, w, sizes[w])
+
+
 def test_lazy_recency_late_first_eviction(gpu, orc):
     """1P/5D-shaped traces with caches that fill only late in the episode (under LRU the kernel
     keeps no recency until a worker first evicts, then rebuilds it from the whole history of
