@@ -332,6 +332,66 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                         break;
                     }
                 }
+            } else if constexpr (WMAX == 32) {
+                // the same with two halves of 32 lanes (16 < W <= 32): every half keeps dist[y] at
+                // position y, half h relaxes from workers 16h .. 16h + 15, each row of the half
+                // reading them through a copy that holds dist[16h + q] at position q
+                const int32_t hh = tid >> 5, y = tid & 31;
+                const bool wy = y < W;
+                double ec[16];
+#pragma unroll
+                for (int32_t p = 0; p < 16; ++p) {
+                    const int32_t x = 16 * hh + p;
+                    ec[p] = (x < W && wy) ? s_e[x * W + y] : dinf();
+                }
+                c_row = wy ? cm[(int64_t)i * W + y] : 0.0f;
+                dist = wy ? (double)c_row : dinf();
+                const int32_t src = 48 * hh + (tid & 15);
+                for (int32_t round = 0;; ++round) {
+                    const long long db = __double_as_longlong(dist);
+                    const int32_t rlo = __shfl((int)(uint32_t)db, src);
+                    const int32_t rhi = __shfl((int)(uint32_t)(db >> 32), src);
+                    double bv = dinf();
+                    int32_t bx = 0x7fffffff;
+                    const int32_t x0 = 16 * hh;
+                    relax_from_row<0>(rlo, rhi, ec[0], x0, bv, bx);
+                    relax_from_row<1>(rlo, rhi, ec[1], x0 + 1, bv, bx);
+                    relax_from_row<2>(rlo, rhi, ec[2], x0 + 2, bv, bx);
+                    relax_from_row<3>(rlo, rhi, ec[3], x0 + 3, bv, bx);
+                    relax_from_row<4>(rlo, rhi, ec[4], x0 + 4, bv, bx);
+                    relax_from_row<5>(rlo, rhi, ec[5], x0 + 5, bv, bx);
+                    relax_from_row<6>(rlo, rhi, ec[6], x0 + 6, bv, bx);
+                    relax_from_row<7>(rlo, rhi, ec[7], x0 + 7, bv, bx);
+                    relax_from_row<8>(rlo, rhi, ec[8], x0 + 8, bv, bx);
+                    relax_from_row<9>(rlo, rhi, ec[9], x0 + 9, bv, bx);
+                    relax_from_row<10>(rlo, rhi, ec[10], x0 + 10, bv, bx);
+                    relax_from_row<11>(rlo, rhi, ec[11], x0 + 11, bv, bx);
+                    relax_from_row<12>(rlo, rhi, ec[12], x0 + 12, bv, bx);
+                    relax_from_row<13>(rlo, rhi, ec[13], x0 + 13, bv, bx);
+                    relax_from_row<14>(rlo, rhi, ec[14], x0 + 14, bv, bx);
+                    relax_from_row<15>(rlo, rhi, ec[15], x0 + 15, bv, bx);
+                    {
+                        const long long bb = __double_as_longlong(bv);
+                        const uint32_t olo = (uint32_t)__shfl_xor((int)(uint32_t)bb, 32);
+                        const uint32_t ohi = (uint32_t)__shfl_xor((int)(uint32_t)(bb >> 32), 32);
+                        const int32_t ox = __shfl_xor(bx, 32);
+                        pick(bv, bx, __longlong_as_double((long long)(((uint64_t)ohi << 32) | olo)), ox);
+                    }
+                    double nd = dist;
+                    int32_t pb = pred;
+                    if (wy && bv < nd) {
+                        nd = bv;
+                        pb = bx;
+                    }
+                    const uint64_t fell = __ballot(nd != dist);
+                    dist = nd;
+                    pred = pb;
+                    if (fell == 0ull) break;
+                    if (round > W + 1) {
+                        if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
+                        break;
+                    }
+                }
             } else {
                 // Bellman-Ford over the workers (Jacobi rounds): lane y keeps dist[y]
                 // and pred[y]; lane y's column of edge weights sits in registers
