@@ -90,6 +90,8 @@ __device__ __forceinline__ void relax_from_row(int32_t lo, int32_t hi, double e,
 // every lane receives it.  Swaps within quads, then the mirrored half row and
 // row, leave each row of 16 lanes holding its minimum; the four rows are then
 // combined in a fixed order.
+// ROWS: the rows of 16 lanes that can hold a candidate (the others hold +inf).
+template <int ROWS = 4>
 __device__ __forceinline__ void wave_argmin_f64(double& v, int32_t& j)
 {
     argmin_dpp_step<0xB1>(v, j);    // quad_perm [1,0,3,2]
@@ -98,7 +100,8 @@ __device__ __forceinline__ void wave_argmin_f64(double& v, int32_t& j)
     argmin_dpp_step<0x140>(v, j);   // row_mirror
     double bv = lane_f64(v, 0);
     int32_t bj = __builtin_amdgcn_readlane(j, 0);
-    for (int32_t r = 16; r < 64; r += 16) pick(bv, bj, lane_f64(v, r), __builtin_amdgcn_readlane(j, r));
+#pragma unroll
+    for (int32_t r = 16; r < 16 * ROWS; r += 16) pick(bv, bj, lane_f64(v, r), __builtin_amdgcn_readlane(j, r));
     v = bv;
     j = bj;
 }
@@ -431,7 +434,7 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
             // target: least distance among workers with spare capacity (lowest index on ties)
             double bd = wl && cnt < K ? dist : dinf();
             int32_t t = wl && cnt < K ? tid : 0x7fffffff;
-            wave_argmin_f64(bd, t);
+            wave_argmin_f64<WMAX <= 16 ? 1 : WMAX <= 32 ? 2 : 4>(bd, t);
             if (t < 0 || t >= W) {   // no worker with spare capacity: impossible when K * W >= m
                 if (tid == 0) atomicOr(a.status, RK_DEV_NO_CONVERGE);
                 placed_all = false;
