@@ -73,13 +73,11 @@ __device__ __forceinline__ void argmin_dpp_step(double& v, int32_t& j)
 }
 
 // One candidate of the row-parallel relaxation: the distance at position P of the lane's row of
-// 16 (the halves lo, hi of a double), plus the edge weight e, against the best (bv, bx) so far.
+// 16, plus the edge weight e, against the best (bv, bx) so far.
 template <int P>
-__device__ __forceinline__ void relax_from_row(int32_t lo, int32_t hi, double e, int32_t x, double& bv, int32_t& bx)
+__device__ __forceinline__ void relax_from_row(double rot, double e, int32_t x, double& bv, int32_t& bx)
 {
-    const uint32_t l = (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, 0x150 + P, 0xF, 0xF, false);   // row_newbcast:P
-    const uint32_t h = (uint32_t)__builtin_amdgcn_update_dpp(hi, hi, 0x150 + P, 0xF, 0xF, false);
-    const double v = __longlong_as_double((long long)(((uint64_t)h << 32) | l)) + e;
+    const double v = __builtin_amdgcn_update_dpp(rot, rot, 0x150 + P, 0xF, 0xF, false) + e;   // row_newbcast:P
     if (v < bv) {
         bv = v;
         bx = x;
@@ -304,14 +302,15 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                 const int32_t src = (tid & ~15) | (4 * g + (tid & 3));   // position p < 4 of row g: dist[4g + p]
                 for (int32_t round = 0;; ++round) {
                     const long long db = __double_as_longlong(dist);
-                    const int32_t rlo = __shfl((int)(uint32_t)db, src);
-                    const int32_t rhi = __shfl((int)(uint32_t)(db >> 32), src);
+                    const uint32_t rlo = (uint32_t)__shfl((int)(uint32_t)db, src);
+                    const uint32_t rhi = (uint32_t)__shfl((int)(uint32_t)(db >> 32), src);
+                    const double rot = __longlong_as_double((long long)(((uint64_t)rhi << 32) | rlo));
                     double bv = dinf();
                     int32_t bx = 0x7fffffff;
-                    relax_from_row<0>(rlo, rhi, ec[0], 4 * g, bv, bx);
-                    relax_from_row<1>(rlo, rhi, ec[1], 4 * g + 1, bv, bx);
-                    relax_from_row<2>(rlo, rhi, ec[2], 4 * g + 2, bv, bx);
-                    relax_from_row<3>(rlo, rhi, ec[3], 4 * g + 3, bv, bx);
+                    relax_from_row<0>(rot, ec[0], 4 * g, bv, bx);
+                    relax_from_row<1>(rot, ec[1], 4 * g + 1, bv, bx);
+                    relax_from_row<2>(rot, ec[2], 4 * g + 2, bv, bx);
+                    relax_from_row<3>(rot, ec[3], 4 * g + 3, bv, bx);
 #pragma unroll
                     for (int32_t sft = 16; sft < 64; sft <<= 1) {
                         const long long bb = __double_as_longlong(bv);
@@ -352,27 +351,28 @@ __global__ __launch_bounds__(PT) void poa_window_kernel(PoaArgs a)
                 const int32_t src = 48 * hh + (tid & 15);
                 for (int32_t round = 0;; ++round) {
                     const long long db = __double_as_longlong(dist);
-                    const int32_t rlo = __shfl((int)(uint32_t)db, src);
-                    const int32_t rhi = __shfl((int)(uint32_t)(db >> 32), src);
+                    const uint32_t rlo = (uint32_t)__shfl((int)(uint32_t)db, src);
+                    const uint32_t rhi = (uint32_t)__shfl((int)(uint32_t)(db >> 32), src);
+                    const double rot = __longlong_as_double((long long)(((uint64_t)rhi << 32) | rlo));
                     double bv = dinf();
                     int32_t bx = 0x7fffffff;
                     const int32_t x0 = 16 * hh;
-                    relax_from_row<0>(rlo, rhi, ec[0], x0, bv, bx);
-                    relax_from_row<1>(rlo, rhi, ec[1], x0 + 1, bv, bx);
-                    relax_from_row<2>(rlo, rhi, ec[2], x0 + 2, bv, bx);
-                    relax_from_row<3>(rlo, rhi, ec[3], x0 + 3, bv, bx);
-                    relax_from_row<4>(rlo, rhi, ec[4], x0 + 4, bv, bx);
-                    relax_from_row<5>(rlo, rhi, ec[5], x0 + 5, bv, bx);
-                    relax_from_row<6>(rlo, rhi, ec[6], x0 + 6, bv, bx);
-                    relax_from_row<7>(rlo, rhi, ec[7], x0 + 7, bv, bx);
-                    relax_from_row<8>(rlo, rhi, ec[8], x0 + 8, bv, bx);
-                    relax_from_row<9>(rlo, rhi, ec[9], x0 + 9, bv, bx);
-                    relax_from_row<10>(rlo, rhi, ec[10], x0 + 10, bv, bx);
-                    relax_from_row<11>(rlo, rhi, ec[11], x0 + 11, bv, bx);
-                    relax_from_row<12>(rlo, rhi, ec[12], x0 + 12, bv, bx);
-                    relax_from_row<13>(rlo, rhi, ec[13], x0 + 13, bv, bx);
-                    relax_from_row<14>(rlo, rhi, ec[14], x0 + 14, bv, bx);
-                    relax_from_row<15>(rlo, rhi, ec[15], x0 + 15, bv, bx);
+                    relax_from_row<0>(rot, ec[0], x0, bv, bx);
+                    relax_from_row<1>(rot, ec[1], x0 + 1, bv, bx);
+                    relax_from_row<2>(rot, ec[2], x0 + 2, bv, bx);
+                    relax_from_row<3>(rot, ec[3], x0 + 3, bv, bx);
+                    relax_from_row<4>(rot, ec[4], x0 + 4, bv, bx);
+                    relax_from_row<5>(rot, ec[5], x0 + 5, bv, bx);
+                    relax_from_row<6>(rot, ec[6], x0 + 6, bv, bx);
+                    relax_from_row<7>(rot, ec[7], x0 + 7, bv, bx);
+                    relax_from_row<8>(rot, ec[8], x0 + 8, bv, bx);
+                    relax_from_row<9>(rot, ec[9], x0 + 9, bv, bx);
+                    relax_from_row<10>(rot, ec[10], x0 + 10, bv, bx);
+                    relax_from_row<11>(rot, ec[11], x0 + 11, bv, bx);
+                    relax_from_row<12>(rot, ec[12], x0 + 12, bv, bx);
+                    relax_from_row<13>(rot, ec[13], x0 + 13, bv, bx);
+                    relax_from_row<14>(rot, ec[14], x0 + 14, bv, bx);
+                    relax_from_row<15>(rot, ec[15], x0 + 15, bv, bx);
                     {
                         const long long bb = __double_as_longlong(bv);
                         const uint32_t olo = (uint32_t)__shfl_xor((int)(uint32_t)bb, 32);
