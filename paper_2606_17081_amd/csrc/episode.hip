@@ -1256,6 +1256,324 @@ __global__ void episode_queue_init(int32_t* __restrict__ q)
 // The queued loop is a kernel of its own (Queued = true): a loop around the
 // episode keeps more values live across it, and the one-episode kernel keeps
 // its register allocation.
+// ------------------------------------------------- the lean decision loop
+// Pointers into LDS and global memory with their address spaces spelled out, for code outside
+// the kernel body (a 32-bit LDS address, a global address).
+template <typename T>
+using lds_p = __attribute__((address_space(3))) T*;
+template <typename T>
+using glb_p = __attribute__((address_space(1))) T*;
+
+template <typename T>
+__device__ __forceinline__ lds_p<T> lds_at(uint32_t off)
+{
+    return (lds_p<T>)off;
+}
+template <typename T>
+__device__ __forceinline__ uint32_t lds_off(T* p)
+{
+    return (uint32_t)(uintptr_t)(lds_p<T>)p;
+}
+
+// v, the same in every lane, as a wave-uniform value (every 32-bit word through readfirstlane):
+// the arguments of a function arrive in vector registers.
+template <typename T>
+__device__ __forceinline__ T wave_uniform(const T& v)
+{
+    static_assert(sizeof(T) % 4 == 0, "32-bit words");
+    T r;
+    const int32_t* src = reinterpret_cast<const int32_t*>(&v);
+    int32_t* dst = reinterpret_cast<int32_t*>(&r);
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(T) / 4); ++i) dst[i] = __builtin_amdgcn_readfirstlane(src[i]);
+    return r;
+}
+
+// What the lean decision loop reads: LDS addresses of the episode's arrays, global arrays and
+// the episode's parameters.
+struct LeanCtx {
+    uint32_t sh, s_A, s_N, s_tail, s_live, s_used, s_head, s_stamped, s_stw, s_stP, s_stc, s_stepn, s_u;
+    uint32_t r_P, r_c, r_k, o_cur, o_tab, lcp, r_sig, r_wend, r_stamp, r_ep, r_otab, r_step, r_reg, r_evc, r_evd;
+    glb_p<int32_t> g_hist;
+    glb_p<int32_t> g_next;
+    glb_p<int32_t> g_queue;
+    glb_p<float> out_cost;
+    glb_p<int32_t> status;
+    int64_t out_base, ctrl_thr;
+    uint64_t used_limit, R;
+    int32_t W, NB, nb, t0, H, rps, qcap, cache, ctrl_window, ctrl_den, cap_blocks;
+    float w_ov, w_act, w_sat, ctrl_w_ov, inv_cap;
+};
+
+// The routing sequence's state, carried from one call to the next.
+struct LeanState {
+    int32_t t, s, r_in_step, n_step, s_slot, c_pos, room_b, step_open, prev_active;
+    int64_t u_sum, u_tot;
+    int64_t tot[8];
+};
+
+// The decisions of wavefront 0 for an episode in prefix mode, routed by argmin under LRU,
+// without memory tiers, frequency decay or the regime controller (LC: with the load
+// controller), from route t up to the batch's end or a stop, as the general loop of the kernel
+// takes them: the same routes, outputs and state.  It is a function of its own so that its
+// registers are its own and not those of the whole episode kernel, which keeps the serial
+// chain of decisions short: the batch's per-route inputs sit in registers (lane b holds route
+// b's), the load release of a step is applied in registers, and the next route's overlaps are
+// read from LDS while the current route's outputs are written.
+template <bool LC>
+__device__ __noinline__ void lean_decide(const LeanCtx c_arg, LeanState* st_arg)
+{
+    const int lane = (int)(threadIdx.x & 63);
+    const LeanCtx c = wave_uniform(c_arg);
+    LeanState* const st = wave_uniform(st_arg);
+    const LeanState st0 = wave_uniform(*st);
+    const lds_p<EpShared> sh = lds_at<EpShared>(c.sh);
+    const lds_p<int32_t> s_A = lds_at<int32_t>(c.s_A), s_N = lds_at<int32_t>(c.s_N);
+    const lds_p<uint32_t> s_tail = lds_at<uint32_t>(c.s_tail), s_head = lds_at<uint32_t>(c.s_head);
+    const lds_p<int32_t> s_live = lds_at<int32_t>(c.s_live), s_used = lds_at<int32_t>(c.s_used);
+    const lds_p<int32_t> s_stamped = lds_at<int32_t>(c.s_stamped);
+    const lds_p<int32_t> s_stw = lds_at<int32_t>(c.s_stw), s_stP = lds_at<int32_t>(c.s_stP);
+    const lds_p<int32_t> s_stc = lds_at<int32_t>(c.s_stc), s_stepn = lds_at<int32_t>(c.s_stepn);
+    const lds_p<int64_t> s_u = lds_at<int64_t>(c.s_u);
+    const lds_p<int32_t> r_P = lds_at<int32_t>(c.r_P), r_c = lds_at<int32_t>(c.r_c), r_k = lds_at<int32_t>(c.r_k);
+    const lds_p<int32_t> o_cur = lds_at<int32_t>(c.o_cur), o_tab = lds_at<int32_t>(c.o_tab);
+    const lds_p<uint16_t> l_lcp = lds_at<uint16_t>(c.lcp);
+    const lds_p<int32_t> r_sig = lds_at<int32_t>(c.r_sig), r_wend = lds_at<int32_t>(c.r_wend);
+    const lds_p<uint32_t> r_stamp = lds_at<uint32_t>(c.r_stamp), r_ep = lds_at<uint32_t>(c.r_ep);
+    const lds_p<int32_t> r_otab = lds_at<int32_t>(c.r_otab), r_step = lds_at<int32_t>(c.r_step);
+    const lds_p<int32_t> r_reg = lds_at<int32_t>(c.r_reg), r_evc = lds_at<int32_t>(c.r_evc);
+    const lds_p<uint64_t> r_evd = lds_at<uint64_t>(c.r_evd);
+    const int32_t W = c.W, NB = c.NB, nb = c.nb, t0 = c.t0, H = c.H, rps = c.rps;
+
+    int32_t t = st0.t, s = st0.s, r_in_step = st0.r_in_step, n_step = st0.n_step, s_slot = st0.s_slot;
+    int32_t c_pos = st0.c_pos, room_b = st0.room_b;
+    bool step_open = st0.step_open != 0, prev_active = st0.prev_active != 0;
+    int64_t u_sum = st0.u_sum, u_tot = st0.u_tot;
+    int64_t tot0 = st0.tot[0], tot2 = st0.tot[2], tot3 = st0.tot[3], tot4 = st0.tot[4], tot5 = st0.tot[5],
+            tot6 = st0.tot[6];
+    int32_t event = EV_BATCH;
+
+    // lane j < W keeps worker j's load, log tail and block counts; lane b < nb route b's inputs
+    int32_t rA = 0, rlive = 0, rused = 0, rN = 0;
+    uint32_t rtail = 0;
+    int32_t q_head = __builtin_amdgcn_readfirstlane(sh->qhead), q_size = __builtin_amdgcn_readfirstlane(sh->qsize);
+    if (lane < W) {
+        rA = s_A[lane];
+        rN = s_N[lane];
+        rtail = s_tail[lane];
+        rlive = s_live[lane];
+        rused = s_used[lane];
+    }
+    const unsigned long long stamped_mask = __ballot(lane < W && s_stamped[lane] != 0);
+    const int32_t b_start = t - t0;
+    int32_t rwork = b_start > 0 ? __builtin_amdgcn_readfirstlane(r_wend[b_start - 1]) : 0;
+    int32_t vP = 0, vc = 0, vk = 0;
+    if (lane < nb) {
+        vP = r_P[lane];
+        vc = r_c[lane];
+        vk = r_k[lane];
+    }
+    if (lane >= b_start && lane < nb) {
+        r_ep[lane] = 0u;
+        r_reg[lane] = 0;
+        r_evc[lane] = 0;
+        r_evd[lane] = 0ull;
+    }
+    // the overlaps of the next route (all earlier routes' raises are in)
+    int32_t oj = lane < W && b_start < nb ? o_cur[b_start * W + lane] : 0;
+    for (;;) {
+        if (!step_open) {
+            // release the routes of step s - H (their loads, in registers); queue their
+            // conversations' next turns
+            const int32_t slot = s_slot, sb = slot * rps;
+            if (s >= H) {
+                const int32_t nprev = __builtin_amdgcn_readfirstlane(s_stepn[slot]);
+                const int32_t qtail = q_head + q_size;
+                int32_t pushed = 0;
+                int64_t rel = 0;
+                for (int32_t base = 0; base < nprev; base += 64) {
+                    const int32_t r = base + lane;
+                    int32_t wr = 0, pr = 0, cr = 0;
+                    if (r < nprev) {
+                        wr = s_stw[sb + r];
+                        pr = s_stP[sb + r];
+                        cr = s_stc[sb + r];
+                    }
+                    const bool more = r < nprev && (cr & kMoreTurns) != 0;
+                    const unsigned long long mb = __ballot(more);
+                    if (more) {
+                        const int32_t qi = qtail + pushed + __popcll(mb & ((1ull << lane) - 1ull));
+                        c.g_queue[qi >= c.qcap ? qi - c.qcap : qi] = cr & ~kMoreTurns;
+                    }
+                    pushed += __popcll(mb);
+                    const int32_t m = min(64, nprev - base);
+                    for (int32_t k = 0; k < m; ++k) {
+                        const int32_t wk = __builtin_amdgcn_readlane(wr, k), pk = __builtin_amdgcn_readlane(pr, k);
+                        rel += pk;
+                        if (lane == wk) {
+                            rA -= pk;
+                            rN -= 1;
+                        }
+                    }
+                }
+                u_tot -= rel;
+                q_size += pushed;
+            }
+            int32_t inflight = 0;
+            for (int32_t k = 1; k < H && k <= s; ++k)
+                inflight += __builtin_amdgcn_readfirstlane(s_stepn[s_slot >= k ? s_slot - k : s_slot - k + H]);
+            if (q_size == 0 && inflight == 0) {
+                event = EV_DONE;
+                break;
+            }
+            n_step = min(rps, q_size);
+            if (lane == 0) s_stepn[slot] = n_step;
+            if (n_step > 0) tot5 = s + 1;
+            r_in_step = 0;
+            step_open = true;
+        }
+        if (r_in_step >= n_step) {
+            ++s;
+            s_slot = s_slot + 1 == H ? 0 : s_slot + 1;
+            step_open = false;
+            continue;
+        }
+        const int32_t b = t - t0;
+        if (b >= nb) break;
+        // one route: controller, cost of every worker, argmin
+        const int32_t sb = s_slot * rps;
+        bool active = false;
+        if (LC && t >= c.ctrl_window) active = (int64_t)c.ctrl_den * u_sum > c.ctrl_thr;
+        const float w = active ? fminf(c.w_ov, c.ctrl_w_ov) : c.w_ov;
+        const int32_t P = __builtin_amdgcn_readlane(vP, b);
+        const int64_t row = c.out_base + (int64_t)t;
+        uint32_t bits = 0xFFFFFFFFu;
+        if (lane < W) {
+            const float cj = route_cost_ep(w, c.w_act, c.w_sat, c.cap_blocks, c.inv_cap, P, oj, rA);
+            if (c.out_cost) c.out_cost[row * W + lane] = cj;
+            bits = __float_as_uint(__fadd_rn(cj, 0.0f));
+        }
+        const uint32_t mn = ep_wave_min_u32(bits);
+        const int32_t sg = __ffsll(__ballot(lane < W && bits == mn)) - 1;
+        const int32_t osg = __builtin_amdgcn_readlane(oj, sg);
+        const int32_t live_after = __builtin_amdgcn_readlane(rlive, sg) + P - osg;
+        const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)rtail, sg);
+        const bool flush = live_after > c.cache;
+        const bool stamped = ((stamped_mask >> sg) & 1ull) != 0;
+        // a worker that keeps recency needs log records for the route's P touches and slots for
+        // its new blocks: without room, stop before the route and compact that worker
+        if (__builtin_expect(stamped, 0)) {
+            const uint32_t head = __builtin_amdgcn_readfirstlane(s_head[sg]);
+            const uint64_t add = (uint64_t)(P - osg);
+            if ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(rused, sg) + add > c.used_limit ||
+                (uint64_t)(base - head) + (uint64_t)P > c.R || (uint64_t)base + (uint64_t)P > 0x40000000u) {
+                if (room_b == t) {
+                    if (lane == 0) atomicOr((int32_t*)c.status, RK_DEV_TABLE_FULL);
+                } else {
+                    room_b = t;
+                    if (lane == 0) sh->ev_b = sg;
+                    event = EV_ROOM;
+                    break;
+                }
+            }
+        }
+        if (active) {
+            tot3 += 1;
+            if (!prev_active) tot4 += 1;
+        }
+        prev_active = active;
+        const int32_t rc = __builtin_amdgcn_readlane(vc, b);
+        if (lane == sg) {
+            rA += P;
+            rN += 1;
+            rtail = base + (uint32_t)P;
+            rlive = live_after;
+            rused += P - osg;
+        }
+        rwork += stamped ? P : (osg < P ? run_entries(osg, P) : 0);
+        // later requests of the batch now find this chain on sg; then the next route's overlaps
+        const int32_t b2 = b + 1 + lane;
+        if (b2 < nb) {
+            const int32_t l = l_lcp[b2 * NB + b];
+            if (l > o_cur[b2 * W + sg]) o_cur[b2 * W + sg] = l;
+        }
+        oj = lane < W && b + 1 < nb ? o_cur[(b + 1) * W + lane] : 0;
+        if (lane == 0) {
+            r_sig[b] = sg;
+            r_wend[b] = rwork;
+            r_stamp[b] = base;
+            r_otab[b] = o_tab[b * W + sg];
+            s_stw[sb + r_in_step] = sg;
+            s_stP[sb + r_in_step] = P;
+            s_stc[sb + r_in_step] = rc;
+            r_step[b] = s;
+            c.g_hist[2 * t] = rc & ~kMoreTurns;
+            c.g_hist[2 * t + 1] = P | (sg << 16);
+            c.g_next[rc & ~kMoreTurns] = __builtin_amdgcn_readlane(vk, b) + 1;
+            if (flush) {
+                sh->ev_b = b;
+                sh->ev_row = row;
+            }
+        }
+        u_tot += P;
+        q_head = q_head + 1 == c.qcap ? 0 : q_head + 1;
+        q_size -= 1;
+        if (LC) {
+            const int32_t pos = c_pos;
+            c_pos = c_pos + 1 == c.ctrl_window ? 0 : c_pos + 1;
+            if (t >= c.ctrl_window) {
+                const int64_t old = s_u[pos];
+                u_sum -= (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int32_t)(old >> 32)) << 32) |
+                                   (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)old));
+            }
+            if (lane == 0) s_u[pos] = u_tot;
+            u_sum += u_tot;
+        }
+        tot0 += P - osg;
+        tot2 += P;
+        tot6 += osg;
+        ++t;
+        ++r_in_step;
+        ep_wave_sync();
+        if (lane == 0) __hip_atomic_store(&sh->decided, b + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (__builtin_expect(flush, 0)) {
+            event = EV_FLUSH;
+            break;
+        }
+    }
+    if (lane < W) {
+        s_A[lane] = rA;
+        s_N[lane] = rN;
+        s_tail[lane] = rtail;
+        s_live[lane] = rlive;
+        s_used[lane] = rused;
+    }
+    if (lane == 0) {
+        sh->qhead = q_head;
+        sh->qsize = q_size;
+        sh->event = event;
+        sh->tdone = t;
+        __hip_atomic_store(&sh->stop, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    st->t = t;
+    st->s = s;
+    st->r_in_step = r_in_step;
+    st->n_step = n_step;
+    st->s_slot = s_slot;
+    st->c_pos = c_pos;
+    st->room_b = room_b;
+    st->step_open = step_open;
+    st->prev_active = prev_active;
+    st->u_sum = u_sum;
+    st->u_tot = u_tot;
+    st->tot[0] = tot0;
+    st->tot[2] = tot2;
+    st->tot[3] = tot3;
+    st->tot[4] = tot4;
+    st->tot[5] = tot5;
+    st->tot[6] = tot6;
+}
+
 template <bool Queued>
 __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
 {
@@ -2972,9 +3290,98 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             if (wave == 0) {
                 // the serial chain of decisions goes first on its SIMD
                 __builtin_amdgcn_s_setprio(3);
-                if (lean) decide(LeanTag<1>{});
-                else if (lean_ctrl) decide(LeanTag<2>{});
-                else decide(LeanTag<0>{});
+                if (!Queued && (lean || lean_ctrl) && t == t0) {
+                    // a batch's first decisions in the one-episode kernel: the lean loop as a function
+                    // of its own (the queued kernel, and the decisions after a stop, keep the copy
+                    // inside the kernel and spare the call's register saves)
+                    LeanCtx lc;
+                    lc.sh = lds_off(&sh);
+                    lc.s_A = lds_off(s_A);
+                    lc.s_N = lds_off(s_N);
+                    lc.s_tail = lds_off(s_tail);
+                    lc.s_live = lds_off(s_live);
+                    lc.s_used = lds_off(s_used);
+                    lc.s_head = lds_off(s_head);
+                    lc.s_stamped = lds_off(s_stamped);
+                    lc.s_stw = lds_off(s_stw);
+                    lc.s_stP = lds_off(s_stP);
+                    lc.s_stc = lds_off(s_stc);
+                    lc.s_stepn = lds_off(s_stepn);
+                    lc.s_u = lds_off(s_u);
+                    lc.r_P = lds_off(r_P);
+                    lc.r_c = lds_off(r_c);
+                    lc.r_k = lds_off(r_k);
+                    lc.o_cur = lds_off(o_cur);
+                    lc.o_tab = lds_off(o_tab);
+                    lc.lcp = lds_off(l_lcp);
+                    lc.r_sig = lds_off(r_sig);
+                    lc.r_wend = lds_off(r_wend);
+                    lc.r_stamp = lds_off(r_stamp);
+                    lc.r_ep = lds_off(r_ep);
+                    lc.r_otab = lds_off(r_otab);
+                    lc.r_step = lds_off(r_step);
+                    lc.r_reg = lds_off(r_reg);
+                    lc.r_evc = lds_off(r_evc);
+                    lc.r_evd = lds_off(r_evd);
+                    lc.g_hist = (glb_p<int32_t>)g_hist;
+                    lc.g_next = (glb_p<int32_t>)g_next;
+                    lc.g_queue = (glb_p<int32_t>)g_queue;
+                    lc.out_cost = (glb_p<float>)a.out.cost;
+                    lc.status = (glb_p<int32_t>)a.status;
+                    lc.out_base = prm.out_base;
+                    lc.ctrl_thr = (int64_t)prm.ctrl_num * prm.ctrl_window * W * (int64_t)prm.cap_blocks;
+                    lc.used_limit = used_limit;
+                    lc.R = R;
+                    lc.W = W;
+                    lc.NB = NB;
+                    lc.nb = nb;
+                    lc.t0 = t0;
+                    lc.H = H;
+                    lc.rps = rps;
+                    lc.qcap = qcap;
+                    lc.cache = a.cache;
+                    lc.ctrl_window = prm.ctrl_window;
+                    lc.ctrl_den = prm.ctrl_den;
+                    lc.cap_blocks = prm.cap_blocks;
+                    lc.w_ov = prm.w_ov;
+                    lc.w_act = prm.w_act;
+                    lc.w_sat = prm.w_sat;
+                    lc.ctrl_w_ov = prm.ctrl_w_ov;
+                    lc.inv_cap = inv_cap;
+                    LeanState ls;
+                    ls.t = t;
+                    ls.s = s;
+                    ls.r_in_step = r_in_step;
+                    ls.n_step = n_step;
+                    ls.s_slot = s_slot;
+                    ls.c_pos = c_pos;
+                    ls.room_b = room_b;
+                    ls.step_open = step_open;
+                    ls.prev_active = prev_active;
+                    ls.u_sum = u_sum;
+                    ls.u_tot = u_tot;
+                    for (int k = 0; k < 8; ++k) ls.tot[k] = tot[k];
+                    if (lean_ctrl) lean_decide<true>(lc, &ls);
+                    else lean_decide<false>(lc, &ls);
+                    t = ls.t;
+                    s = ls.s;
+                    r_in_step = ls.r_in_step;
+                    n_step = ls.n_step;
+                    s_slot = ls.s_slot;
+                    c_pos = ls.c_pos;
+                    room_b = ls.room_b;
+                    step_open = ls.step_open != 0;
+                    prev_active = ls.prev_active != 0;
+                    u_sum = ls.u_sum;
+                    u_tot = ls.u_tot;
+                    for (int k = 0; k < 8; ++k) tot[k] = ls.tot[k];
+                } else if (lean) {
+                    decide(LeanTag<1>{});
+                } else if (lean_ctrl) {
+                    decide(LeanTag<2>{});
+                } else {
+                    decide(LeanTag<0>{});
+                }
                 __builtin_amdgcn_s_setprio(0);
                 writer();           // the decided routes not yet claimed
             } else {
