@@ -118,6 +118,8 @@ __global__ __launch_bounds__(256) void block_fnv_kernel(int64_t n_seq, const int
 // stores that block's final value), which keeps every memory instruction
 // unconditional.
 constexpr int kChainChunk = 16;
+// two chained values, 8-byte aligned (a 16-byte access needs only the element alignment)
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2), aligned(8)));
 constexpr int kChainWG = 1024;
 constexpr int kChainClasses = 32;
 
@@ -166,20 +168,43 @@ __global__ __launch_bounds__(kChainWG) void chain_kernel(int64_t n_seq, const in
     if (n <= 0) return;
     const int64_t last = c0 + n - 1;
     uint64_t cur[kChainChunk], nxt[kChainChunk];
+    // whole chunks move as pairs of values (16-byte accesses); a chunk that reaches past the
+    // sequence's last block moves value by value, clamped to it
+    auto load_chunk = [&](int64_t k, uint64_t* v) {
+        if (k + kChainChunk - 1 <= last - c0) {
 #pragma unroll
-    for (int u = 0; u < kChainChunk; ++u) cur[u] = chains[min(c0 + u, last)];
+            for (int u = 0; u < kChainChunk; u += 2) {
+                const u64x2 q = *reinterpret_cast<const u64x2*>(chains + c0 + k + u);
+                v[u] = q.x;
+                v[u + 1] = q.y;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kChainChunk; ++u) v[u] = chains[min(c0 + k + u, last)];
+        }
+    };
+    load_chunk(0, cur);
     uint64_t h = 0;
     for (int64_t k0 = 0; k0 < n; k0 += kChainChunk) {
-#pragma unroll
-        for (int u = 0; u < kChainChunk; ++u) nxt[u] = chains[min(c0 + k0 + kChainChunk + u, last)];
+        load_chunk(k0 + kChainChunk, nxt);
 #pragma unroll
         for (int u = 0; u < kChainChunk; ++u) {
             const uint64_t hn = chain_next(h, cur[u]);
             h = k0 + u < n ? hn : h;
             cur[u] = h;
         }
+        if (k0 + kChainChunk - 1 <= last - c0) {
 #pragma unroll
-        for (int u = 0; u < kChainChunk; ++u) chains[min(c0 + k0 + u, last)] = cur[u];
+            for (int u = 0; u < kChainChunk; u += 2) {
+                u64x2 q;
+                q.x = cur[u];
+                q.y = cur[u + 1];
+                *reinterpret_cast<u64x2*>(chains + c0 + k0 + u) = q;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kChainChunk; ++u) chains[min(c0 + k0 + u, last)] = cur[u];
+        }
 #pragma unroll
         for (int u = 0; u < kChainChunk; ++u) cur[u] = nxt[u];
     }
