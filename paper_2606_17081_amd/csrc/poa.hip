@@ -14,8 +14,12 @@
 // window's matrix lives in LDS when it fits, else in the workspace.  Lane y
 // keeps worker y's distance, predecessor and row count in registers, values
 // move between lanes by readlane and DPP, and the path is walked by the whole
-// wavefront in lockstep.  Windows are dispatched longest first (a bucket sort
-// by size class), since the longest ones set the length of the launch.
+// wavefront in lockstep.  With few workers the idle lanes share the work: for
+// W <= 16 (W <= 32) the rows (halves) of the wavefront each relax from a part
+// of the workers, and the edges that lost their argmin row are recomputed by
+// groups of lanes side by side.  Windows are dispatched longest first (a
+// bucket sort by size class), since the longest ones set the length of the
+// launch.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
