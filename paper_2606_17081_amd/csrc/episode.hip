@@ -2860,8 +2860,13 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     // The job's two parts run side by side: waves 1 .. NW-2 search the run index, the last wave
     // takes the common prefixes of the batch pairs.
     auto next_batch_job = [&]() {
-        if (wave == NW - 1) job_pair_part();
-        else job_search_part();
+        if (wave == NW - 1) {
+            job_pair_part();
+        } else {
+            __builtin_amdgcn_s_setprio(2);   // the searches end the job: ahead of writers and pairs
+            job_search_part();
+            __builtin_amdgcn_s_setprio(0);
+        }
     };
 
     // the next batch's overlaps, computed by waves 1-3 while wavefront 0 decides this batch
