@@ -657,8 +657,10 @@ static int poa_launch(int32_t n_windows, const int64_t* win_off, int32_t n_episo
     double* selfish = selfish_out ? selfish_out : (double*)(ws + cm_bytes + 256);
     double* coord = coord_out ? coord_out : (double*)(ws + cm_bytes + 512 + vec_bytes);
     // the dispatch order has room for n_rows + 1 windows; beyond that (many
-    // empty windows) the windows run in index order
-    int32_t* order = (n_windows > 1 && (size_t)n_windows <= (size_t)n_rows + 1)
+    // empty windows) the windows run in index order, and so do up to 256
+    // windows (each starts at once on a CU of its own, so no order shortens
+    // the launch, and the three ordering launches are saved)
+    int32_t* order = (n_windows > 256 && (size_t)n_windows <= (size_t)n_rows + 1)
                          ? (int32_t*)(ws + cm_bytes + 512 + 2 * vec_bytes) : nullptr;
     if (n_episodes > 0 && (!selfish_out || !coord_out) && (size_t)n_windows > (size_t)n_rows + 1)
         return fail(RK_EINVAL, "rk_poa_estimate: pass selfish_out and coord_out when windows exceed rows");
