@@ -1267,7 +1267,7 @@ using glb_p = __attribute__((address_space(1))) T*;
 template <typename T>
 __device__ __forceinline__ lds_p<T> lds_at(uint32_t off)
 {
-    return (lds_p<T>)off;
+    return (lds_p<T>)(uintptr_t)off;
 }
 template <typename T>
 __device__ __forceinline__ uint32_t lds_off(T* p)
@@ -1494,7 +1494,7 @@ __device__ __noinline__ void lean_decide(const LeanCtx c_arg, LeanState* st_arg)
         // later requests of the batch now find this chain on sg; then the next route's overlaps
         const int32_t b2 = b + 1 + lane;
         if (b2 < nb) {
-            const int32_t l = l_lcp[b2 * NB + b];
+            const int32_t l = l_lcp[b * NB + b2];
             if (l > o_cur[b2 * W + sg]) o_cur[b2 * W + sg] = l;
         }
         oj = lane < W && b + 1 < nb ? o_cur[(b + 1) * W + lane] : 0;
@@ -1639,7 +1639,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     int32_t* r_evc = (int32_t*)(bb + BL.revc);             //   and their digest
     uint64_t* r_evd = (uint64_t*)(bb + BL.revd);
     uint32_t* r_rnd = (uint32_t*)(bb + BL.rrnd);           // the route's two random words
-    uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b][b2], b2 < b: common prefix
+    uint16_t* l_lcp = (uint16_t*)(bb + BL.lcp);            // [b2][b], b2 < b: common prefix (a row per earlier route)
     uint16_t* nx_lcp = (uint16_t*)(bb + BL.lcp2);          //   the same for the next batch (the two swap)
     uint16_t* l_pval = (uint16_t*)(bb + BL.pval);          // common prefix of each listed pair
     uint16_t* l_items = (uint16_t*)(bb + BL.items);        // search items left after a first probe
@@ -2831,14 +2831,14 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             },
             [&](int32_t q, int32_t b1, int32_t b2, bool same, int32_t m) {
                 if (same && m > 1) return true;
-                nx_lcp[b1 * NB + b2] = (uint16_t)(same && m > 0 ? 1 : 0);
+                nx_lcp[b2 * NB + b1] = (uint16_t)(same && m > 0 ? 1 : 0);
                 return false;
             },
             [&](int32_t idx, int32_t q, int32_t l) {
                 int32_t b1 = (int32_t)((1.0f + sqrtf(1.0f + 8.0f * (float)q)) * 0.5f);
                 while (b1 > 1 && b1 * (b1 - 1) / 2 > q) --b1;
                 while ((b1 + 1) * b1 / 2 <= q) ++b1;
-                nx_lcp[b1 * NB + (q - b1 * (b1 - 1) / 2)] = (uint16_t)l;
+                nx_lcp[(q - b1 * (b1 - 1) / 2) * NB + b1] = (uint16_t)l;
             });
         ep_wave_sync();            // the within-batch list is no longer read
         // between the next batch's routes and this batch's (nb routes), every pair whose first
@@ -2932,7 +2932,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
             search(0, nb, -1);
             if (tiers) tier_search(0, nb, -1);
             if (!scan) pair_lcps(nb * (nb - 1) / 2, batch_pair, [&](int32_t q, int32_t b1, int32_t b2, int32_t l) {
-                l_lcp[b1 * NB + b2] = (uint16_t)l;
+                l_lcp[b2 * NB + b1] = (uint16_t)l;
             });
         }
         // the next batch is searched during this batch's decisions when every worker still adds
@@ -3259,7 +3259,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                 if (!scan_d) {
                     const int32_t b2 = b + 1 + lane;
                     if (b2 < nb) {
-                        const int32_t l = l_lcp[b2 * NB + b];
+                        const int32_t l = l_lcp[b * NB + b2];
                         if (l > o_cur[b2 * W + sg]) o_cur[b2 * W + sg] = l;
                     }
                 }
