@@ -67,6 +67,7 @@ EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks
     L.off_next = o;    o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);
     L.off_hist = o;    o = align_up(o + ((size_t)max_routes + 1) * 2 * sizeof(int32_t), 256);
     L.off_replay = o;  o = align_up(o + (size_t)kEpisodeThreads * 16, 256);
+    L.off_later = o;   o = align_up(o + ((size_t)max_conv + 1) * sizeof(int32_t), 256);
     L.off_ctl = o;     o = align_up(o + 256, 256);     // launch control (episode queue counter)
     L.off_runs = o;    o = align_up(o + L.runs * sizeof(RunSlot), 256);
     L.per_episode = o;

@@ -1745,18 +1745,21 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     }
     for (int32_t i = tid; i < a.max_inflight; i += NT) s_stepn[i] = 0;
     int32_t qn = 0;
+    int32_t turns2 = 0;   // some conversation of the episode has a second turn
     for (int32_t base = 0; base < n_conv; base += NT) {
         const int32_t c = base + tid;
         bool has = false;
         if (c < n_conv) {
             g_next[c] = 0;
             has = a.turn_off[gc0 + c + 1] > a.turn_off[gc0 + c];
+            turns2 |= a.turn_off[gc0 + c + 1] - a.turn_off[gc0 + c] > 1 ? 1 : 0;
         }
         int32_t total;
         const int32_t rank = block_scan(has, sh.wtot, total);
         if (has) g_queue[qn + rank] = c;
         qn += total;
     }
+    const bool multi_turn = __syncthreads_or(turns2) != 0;
     if (tid == 0) {
         sh.qhead = 0;
         sh.qsize = qn;
@@ -2091,30 +2094,41 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
     //      writes its record there and raises the block's stamp to its own, and a record is live
     //      iff the block's stamp is its position, as in the eager upkeep.  The log positions of
     //      all touches are cleared first.  Routes go newest first, so a touch that finds its
-    //      block already stamped by a later touch does nothing more.
+    //      block already stamped by a later touch does nothing more.  Every turn of a
+    //      conversation reads the leading blocks of the conversation's one chain, so the first
+    //      D blocks of a route are touched again by any later route of its conversation on j
+    //      with D blocks: those touches are skipped outright (their log positions stay clear,
+    //      as a record that is not live), and only the route's last P - min(P, D) blocks are
+    //      looked up, D the most blocks of such a route in the chunks done before (any D up to
+    //      the most blocks of a later route gives the same result; the skips need none).
     auto materialize = [&](int32_t j, int32_t t_end) -> bool {
         Slot* tk = g_slots + (uint64_t)j * S;
         uint32_t* tl = g_log + (uint64_t)j * R;
-        int64_t* r_cbs = (int64_t*)(ws + a.L.off_replay);     // per chunk of routes, the worker's: chain
-        int32_t* r_off = s_roff;                              // base (global), first touch index (LDS)
-                                                              // and P (global)
-        int32_t* r_Ps = (int32_t*)(r_cbs + NT) + NT;
-        auto route_of = [&](int32_t r, int32_t& P, int64_t& cb) {
+        int64_t* r_cbs = (int64_t*)(ws + a.L.off_replay);     // per chunk, the routes on j: chain base,
+        int32_t* r_sb = (int32_t*)(r_cbs + NT);               //   stamp of the route's last block within
+        int32_t* r_Ps = r_sb + NT;                            //   the chunk, P (global) and the first of
+        int32_t* r_off = s_roff;                              //   its looked-up touches (LDS)
+        int32_t* m_P = (int32_t*)(ws + a.L.off_later);        // per conversation: most blocks of a route
+        if (multi_turn)                                       //   on j in the chunks done so far
+            for (int32_t c = tid; c < n_conv; c += NT) m_P[c] = 0;
+        auto route_of = [&](int32_t r, int32_t& P, int64_t& cb, int32_t& cv) {
             P = 0;
             cb = 0;
+            cv = 0;
             if (r < t_end) {
                 const int32_t pw = g_hist[2 * r + 1];
                 if ((pw >> 16) == j) {
                     P = pw & 0xFFFF;
-                    cb = a.chain_off[gc0 + g_hist[2 * r]];
+                    cv = g_hist[2 * r];
+                    cb = a.chain_off[gc0 + cv];
                 }
             }
         };
         int64_t T = 0;     // touches of the worker's routes
         for (int32_t base = 0; base < t_end; base += NT) {
-            int32_t P;
+            int32_t P, cv;
             int64_t cb;
-            route_of(base + tid, P, cb);
+            route_of(base + tid, P, cb, cv);
             int32_t ptot;
             block_excl_sum(P, sh.wtot, ptot);
             T += ptot;
@@ -2125,41 +2139,47 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
         int64_t end = T;   // stamp after the last touch of the chunks done so far
         const int32_t nchunk = (t_end + NT - 1) / NT;
         for (int32_t c = nchunk - 1; c >= 0; --c) {
-            int32_t P;
+            int32_t P, cv;
             int64_t cb;
-            route_of(c * NT + tid, P, cb);
-            int32_t n_r, ptot;
+            route_of(c * NT + tid, P, cb, cv);
+            int32_t n_r, ptot, ltot;
             const int32_t rank = block_scan(P > 0, sh.wtot, n_r);
+            const int32_t D = multi_turn && P > 0 ? m_P[cv] : 0;   // blocks touched again later
             const int32_t off = block_excl_sum(P, sh.wtot, ptot);
+            int32_t loff = off;
+            ltot = ptot;
+            if (multi_turn) loff = block_excl_sum(P - min(P, D), sh.wtot, ltot);
             if (P > 0) {
-                r_off[rank] = off;
+                r_off[rank] = loff;
                 r_cbs[rank] = cb;
+                r_sb[rank] = off;
                 r_Ps[rank] = P;
             }
             __syncthreads();
             const int64_t stamp0 = end - ptot;
-            // kRU touches per thread, each step's memory operations issued for all of them before
-            // any result is used (addresses by masks: an empty touch reads chain hash 0 and the
-            // table's first group)
-            for (int32_t i0 = 0; i0 < ptot; i0 += NT * kRU) {
+            // kRU looked-up touches per thread, each step's memory operations issued for all of
+            // them before any result is used (addresses by masks: an empty touch reads chain hash
+            // 0 and the table's first group).  A route's looked-up touches are its last blocks, so
+            // the q-th of them is the route's q-th touch.
+            for (int32_t i0 = 0; i0 < ltot; i0 += NT * kRU) {
                 uint64_t h[kRU], k[kRU][kWin];
                 uint32_t st[kRU], stv[kRU][kWin];
                 int64_t hoff[kRU];
                 bool v[kRU];
 #pragma unroll
                 for (int u = 0; u < kRU; ++u) {
-                    const int32_t i = ptot - 1 - (i0 + u * NT + tid);    // the chunk's newest touches first
+                    const int32_t i = ltot - 1 - (i0 + u * NT + tid);    // the chunk's newest touches first
                     v[u] = i >= 0;
                     const int32_t ii = v[u] ? i : 0;
-                    int32_t lo = 0, hi = n_r - 1;     // the route holding touch ii
-                    while (lo < hi) {
+                    int32_t lo = 0, hi = n_r - 1;     // the route holding touch ii (the last of equal
+                    while (lo < hi) {                 // offsets: a route with none shares the next's)
                         const int32_t mid = (lo + hi + 1) >> 1;
                         if (r_off[mid] <= ii) lo = mid;
                         else hi = mid - 1;
                     }
                     const int32_t q = ii - r_off[lo];            // touches go from the last block
                     const int32_t kb = r_Ps[lo] - 1 - q;         // to the first
-                    st[u] = (uint32_t)(stamp0 + r_off[lo] + q);
+                    st[u] = (uint32_t)(stamp0 + r_sb[lo] + q);
                     hoff[u] = (-(int64_t)v[u]) & (r_cbs[lo] + kb);
                 }
 #pragma unroll
@@ -2167,8 +2187,21 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
 #pragma unroll
                 for (int u = 0; u < kRU; ++u) {
                     const Slot* g = tk + ((uint64_t)(-(int64_t)v[u]) & home_slot(h[u], smask));
+                    load_slot(g + group_slot(h[u], 0), k[u][0], stv[u][0]);
+                }
 #pragma unroll
-                    for (int r = 0; r < kWin; ++r) load_slot(g + group_slot(h[u], r), k[u][r], stv[u][r]);
+                for (int u = 0; u < kRU; ++u) {
+                    const bool more = v[u] && k[u][0] != h[u] && k[u][0] != kEmpty;
+#pragma unroll
+                    for (int r = 1; r < kWin; ++r) {
+                        k[u][r] = kEmpty;
+                        stv[u][r] = 0;
+                    }
+                    if (more) {
+                        const Slot* g = tk + home_slot(h[u], smask);
+#pragma unroll
+                        for (int r = 1; r < kWin; ++r) load_slot(g + group_slot(h[u], r), k[u][r], stv[u][r]);
+                    }
                 }
                 // the key's slot in its first group, or the first empty slot there to claim
                 uint64_t sl[kRU], prev[kRU];
@@ -2224,6 +2257,7 @@ __global__ __launch_bounds__(NT, 2) void episode_kernel(EpArgs a)
                     tl[st[u] & rmask] = (uint32_t)sl[u];
                 }
             }
+            if (multi_turn && P > 0) atomicMax(&m_P[cv], P);     // later routes for the chunks before
             end = stamp0;
             __syncthreads();
         }

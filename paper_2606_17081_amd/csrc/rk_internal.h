@@ -275,8 +275,8 @@ struct EpisodeLayout {
     uint64_t slots;        // table slots per worker (power of two)
     uint64_t ring;         // LRU log records per worker (power of two)
     uint64_t runs;         // run slots of the episode's prefix index (power of two)
-    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next, off_hist, off_replay, off_ctl,
-        off_runs;
+    size_t off_slots, off_log, off_scratch, off_scratch_f, off_queue, off_next, off_hist, off_replay, off_later,
+        off_ctl, off_runs;
     size_t per_episode;
 };
 EpisodeLayout episode_layout(int32_t W, int32_t cache_blocks, int32_t max_blocks, int32_t max_conv,
