@@ -460,6 +460,71 @@ def test_lazy_recency_late_first_eviction(gpu, orc):
     assert late >= 8
 
 
+def _repeated_turns_case(rng, n_conv, monotone):
+    """Prefix-closed conversations of 1-5 turns; each turn reads the first turn_blocks of its
+    conversation's chain, growing from turn to turn (monotone) or in any order."""
+    chains, turn_blocks, turn_off, prefix_id = [], [], [0], {}
+    for _ in range(n_conv):
+        L = int(rng.integers(4, 48))
+        path = tuple(int(x) for x in rng.integers(0, 3, size=L))
+        chains.append([prefix_id.setdefault(path[:k], len(prefix_id) + 1) for k in range(1, L + 1)])
+        tb = [int(x) for x in rng.integers(1, L + 1, size=int(rng.integers(1, 6)))]
+        if monotone:
+            tb.sort()
+        turn_blocks.extend(tb)
+        turn_off.append(len(turn_blocks))
+    return chains, np.array(turn_off, np.int64), np.array(turn_blocks, np.int32)
+
+
+def test_recency_rebuild_repeated_turns(gpu, orc):
+    """Multi-turn episodes whose workers first evict after hundreds of routes, so the recency
+    rebuilt from a worker's history spans several chunks of 256 routes, with later turns of a
+    conversation on the same worker rereading its chain (the rebuild skips the touches they
+    repeat), turn lengths growing or in any order: every route, overlap, eviction count and
+    digest against the oracle."""
+    rng = np.random.default_rng(2024)
+    W = 3
+    traces, all_chains = {}, {}
+    for seed in range(6):
+        chains, turn_off, turn_blocks = _repeated_turns_case(rng, 600, monotone=seed % 2 == 0)
+        lens = np.array([len(c) for c in chains], np.int32)
+        chain_off = np.zeros(len(chains) + 1, np.int64)
+        np.cumsum(lens, out=chain_off[1:])
+        traces[seed] = wl.Trace(seed=seed, tokens=np.zeros(16, np.int32), tok_off=chain_off * 0,
+                                chain_blocks=lens, chain_off=chain_off, turn_off=turn_off,
+                                turn_blocks=turn_blocks, group=np.zeros(len(chains), np.int32),
+                                shared=np.zeros(len(chains), np.int32))
+        all_chains[seed] = np.array([k for c in chains for k in c], np.uint64)
+    flat = np.concatenate([all_chains[s] for s in sorted(traces)])
+    specs = [wl.EpisodeSpec(seed=s, concurrency=8, hold_steps=2, w_ov=w, w_act=0.5, w_sat=4.0, cap=200)
+             for s in sorted(traces) for w in (1.0, 2.0)]
+    spanned = 0
+    for cache in (1200, 2400):
+        work = wl.Workload("repeated-turns", W=W, cache_blocks=cache, traces=traces, episodes=specs)
+        say("repeated-turn episodes with", cache, "-block caches")
+        r = _run(gpu, work, chains=flat)
+        for e, sp in enumerate(specs):
+            tr = traces[sp.seed]
+            o = orc.simulate_episode(W, cache, sp, tr.turn_off, tr.turn_blocks, tr.chain_off, all_chains[sp.seed])
+            _compare_episode(r.episode_results(e), o, W, window=sp.concurrency, label=f"cache {cache} e{e}")
+            # routes before their worker's first eviction whose conversation comes back to that
+            # worker in a later chunk of 256 routes, also before it
+            rw = np.asarray(o["route_worker"])
+            conv = np.searchsorted(tr.turn_off, np.asarray(o["route_turn"]), side="right") - 1
+            ev = np.nonzero(o["evict_count"])[0]
+            for j in range(W):
+                evj = ev[rw[ev] == j]
+                t_end = int(evj[0]) if evj.size else 0
+                last = {}
+                for t in range(t_end - 1, -1, -1):
+                    if rw[t] != j:
+                        continue
+                    if conv[t] in last and last[conv[t]] // 256 != t // 256:
+                        spanned += 1
+                    last.setdefault(conv[t], t)
+    assert spanned >= 100, spanned
+
+
 def test_workspace_contents_never_read(gpu, orc):
     """An episode clears the parts of its workspace it uses (the run index at
     its start; a worker's block table at its start under frequency eviction,
