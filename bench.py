@@ -827,7 +827,8 @@ def main():
                "sample": f"{len(specs)} of the 10240 saturation episodes (seeds 0..{args.cpu_seeds - 1}, every C "
                          f"and w_ov) incl. hashing their traces and the PoA-hat windows; {routes} routes in "
                          f"{dt:.2f} s",
-               "extrapolated": True, "full_config_seconds_extrapolated": round(full_s, 1),
+               "extrapolated": len(specs) < len(r4.episodes),
+               "full_config_seconds_extrapolated": round(full_s, 1),
                "episodes_per_s": len(specs) / dt, "seconds": round(dt, 3)}
         cpu.update(cpu_info(threads))
         log(f"oracle: {cpu['value']:.4g} scorings/s ({len(specs)} episodes in {dt:.2f} s); parity "
