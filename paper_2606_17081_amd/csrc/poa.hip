@@ -692,8 +692,12 @@ static int poa_launch(int32_t n_windows, const int64_t* win_off, int32_t n_episo
         const size_t limit = 60 * 1024;
         if (o > limit)
             return fail(RK_EUNSUPPORTED, "rk_poa_estimate: %zu bytes of LDS per window exceed 60 KiB", o);
+        // the frozen matrix goes to LDS only while a window's whole LDS stays within 20 KiB, so that
+        // at least eight windows share a CU; a larger matrix is read from the workspace instead
+        // (the solver's steps are latency-bound and need the waves: multi-turn windows of 256
+        // rows x 32 workers, 43 KiB with the matrix, take half the time from the workspace)
         const size_t mat = (size_t)max_window * (size_t)W * sizeof(float);
-        const bool lds_mat = o + mat <= limit;
+        const bool lds_mat = o + mat <= 20 * 1024;
         a.lds_mat = (uint32_t)o;
         if (lds_mat) o += mat;
         if (order) {
